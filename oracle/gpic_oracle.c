@@ -1,0 +1,521 @@
+/*
+ * gpic_oracle.c -- the oracle for Power Iteration Clustering (PIC) as the
+ * GPIC paper (arXiv 1604.02700) states it.
+ *
+ * TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the tests, the smoke check and
+ * the benchmark's CPU-baseline leg load this library.  The GPU library never
+ * links, includes or calls it, and this file includes nothing of the GPU
+ * library: the two share no code.
+ *
+ * Everything is plain float64 C, written for a reader to check against the
+ * paper by eye.  OpenMP only splits independent rows between threads; every
+ * row's sum runs sequentially in ascending column order on one thread, and
+ * every cross-row reduction (sum of degrees, the L1 norm, the max of the stop
+ * statistic) runs serially in ascending row order, so results are bitwise
+ * independent of the thread count.
+ *
+ * What each function follows:
+ *   orc_affinity_rows      affinity matrix A of the graph G (section
+ *                          "Spectral Cluster"); Gaussian kernel with a zero
+ *                          diagonal, the reading taken because the paper
+ *                          never writes its kernel down (its Experiment I
+ *                          used cosine similarity, Table 2 caption).
+ *   orc_degree_normalize   d_ii = sum_j a_ij and W = D^-1 A ("Spectral
+ *                          Cluster"); v0 = D / sum(D) (Algorithm 2, the
+ *                          Reduction and Norm steps before the loop).
+ *   orc_power_iterate_*    Algorithm 1: delta_0 = v_0; each step
+ *                          v_{t+1} = W v_t / ||W v_t||_1 (the update
+ *                          equation of section "PIC: an overview"),
+ *                          delta_{t+1} = |v_{t+1} - v_t|, stop when
+ *                          |delta_{t+1} - delta_t| <= eps for every entry.
+ *   orc_kmeans1d           "k-means of v" (Algorithm 1, last step), read as
+ *                          the exact minimum within-cluster sum of squares
+ *                          partition of the scalars v_i (plain O(k n^2)
+ *                          dynamic programme, or the same programme with the
+ *                          divide-and-conquer argmin search for large n).
+ *
+ * Pins: every function is checked by the CPU tests against invariants,
+ * closed forms, library routines or brute force (row sums, uniform and
+ * block-diagonal fixed points, the eigendecomposition closed form, a
+ * hand-derived two-node trace, scipy's distance routine, exhaustive
+ * partition search).  No function here is "parity unpinned".
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+int32_t orc_num_threads(void)
+{
+#ifdef _OPENMP
+    return (int32_t)omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------ */
+/* Affinity                                                            */
+/* ------------------------------------------------------------------ */
+
+/* a_ij = exp(-||x_i - x_j||^2 / (2 sigma^2)) for i != j, a_ii = 0.
+ * The squared distance is summed from the coordinate differences (not from
+ * norms and dot products), every coordinate promoted exactly to float64. */
+static double gauss_affinity(const float *X, int32_t d, int64_t i, int64_t j,
+                             double two_sigma2)
+{
+    if (i == j)
+        return 0.0;
+    const float *xi = X + i * (int64_t)d;
+    const float *xj = X + j * (int64_t)d;
+    double dist2 = 0.0;
+    for (int32_t c = 0; c < d; ++c) {
+        double diff = (double)xi[c] - (double)xj[c];
+        dist2 += diff * diff;
+    }
+    return exp(-dist2 / two_sigma2);
+}
+
+/* Rows row0 .. row0+nrows-1 of A, written to out[r * n + j]. */
+void orc_affinity_rows(const float *X, int64_t n, int32_t d, double sigma,
+                       int64_t row0, int64_t nrows, double *out)
+{
+    const double two_sigma2 = 2.0 * sigma * sigma;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < nrows; ++r)
+        for (int64_t j = 0; j < n; ++j)
+            out[r * n + j] = gauss_affinity(X, d, row0 + r, j, two_sigma2);
+}
+
+/* Degrees of the listed rows, d_i = sum_j a_ij, with A recomputed. */
+void orc_degree_rows(const float *X, int64_t n, int32_t d, double sigma,
+                     const int64_t *rows, int64_t nrows, double *deg)
+{
+    const double two_sigma2 = 2.0 * sigma * sigma;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < nrows; ++r) {
+        double s = 0.0;
+        for (int64_t j = 0; j < n; ++j)
+            s += gauss_affinity(X, d, rows[r], j, two_sigma2);
+        deg[r] = s;
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Degree, W = D^-1 A and v0 = D / sum(D)                               */
+/* ------------------------------------------------------------------ */
+
+/* v0_i = d_i / sum_j d_j; returns the number of zero-degree rows, or -1
+ * when the degrees sum to zero (v0 undefined). */
+static int64_t start_vector(const double *degree, int64_t n, double *v0)
+{
+    double total = 0.0;
+    int64_t nzero = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        total += degree[i];
+        if (degree[i] == 0.0)
+            ++nzero;
+    }
+    if (!(total > 0.0) || !isfinite(total))
+        return -1;
+    for (int64_t i = 0; i < n; ++i)
+        v0[i] = degree[i] / total;
+    return nzero;
+}
+
+/* Dense: A (n x n, row-major) is overwritten by W.  A zero-degree row stays
+ * a zero row.  Returns the zero-row count, or -1 if sum(D) is not positive. */
+int64_t orc_degree_normalize(double *A, int64_t n, double *degree, double *v0)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double s = 0.0;
+        for (int64_t j = 0; j < n; ++j)
+            s += A[i * n + j];
+        degree[i] = s;
+        for (int64_t j = 0; j < n; ++j)
+            A[i * n + j] = (s == 0.0) ? 0.0 : A[i * n + j] / s;
+    }
+    return start_vector(degree, n, v0);
+}
+
+/* CSR: w = D^-1 a over the stored entries (columns ascending per row). */
+int64_t orc_degree_normalize_csr(const int64_t *row_ptr, const int32_t *col,
+                                 const double *a, int64_t n, double *w,
+                                 double *degree, double *v0)
+{
+    (void)col;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double s = 0.0;
+        for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p)
+            s += a[p];
+        degree[i] = s;
+        for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p)
+            w[p] = (s == 0.0) ? 0.0 : a[p] / s;
+    }
+    return start_vector(degree, n, v0);
+}
+
+/* Degrees of every row with A recomputed (the on-the-fly operator). */
+int64_t orc_degree_onthefly(const float *X, int64_t n, int32_t d, double sigma,
+                            double *degree, double *v0)
+{
+    const double two_sigma2 = 2.0 * sigma * sigma;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double s = 0.0;
+        for (int64_t j = 0; j < n; ++j)
+            s += gauss_affinity(X, d, i, j, two_sigma2);
+        degree[i] = s;
+    }
+    return start_vector(degree, n, v0);
+}
+
+/* ------------------------------------------------------------------ */
+/* The operator y = W v in its three storage forms                      */
+/* ------------------------------------------------------------------ */
+
+enum { OP_DENSE = 0, OP_CSR = 1, OP_ONTHEFLY = 2 };
+
+typedef struct {
+    int kind;
+    int64_t n;
+    /* dense */
+    const double *W;
+    /* csr */
+    const int64_t *row_ptr;
+    const int32_t *col;
+    const double *w;
+    /* on the fly: W_ij = a_ij / d_i with a_ij recomputed from X */
+    const float *X;
+    int32_t d;
+    double sigma;
+    const double *degree;
+} orc_op;
+
+static double op_row(const orc_op *op, int64_t i, const double *v)
+{
+    double y = 0.0;
+    switch (op->kind) {
+    case OP_DENSE:
+        for (int64_t j = 0; j < op->n; ++j)
+            y += op->W[i * op->n + j] * v[j];
+        break;
+    case OP_CSR:
+        for (int64_t p = op->row_ptr[i]; p < op->row_ptr[i + 1]; ++p)
+            y += op->w[p] * v[op->col[p]];
+        break;
+    default: {
+        const double two_sigma2 = 2.0 * op->sigma * op->sigma;
+        const double di = op->degree[i];
+        if (di == 0.0)
+            return 0.0;
+        for (int64_t j = 0; j < op->n; ++j)
+            y += (gauss_affinity(op->X, op->d, i, j, two_sigma2) / di) * v[j];
+    }
+    }
+    return y;
+}
+
+static void op_apply(const orc_op *op, const double *v, double *y)
+{
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t i = 0; i < op->n; ++i)
+        y[i] = op_row(op, i, v);
+}
+
+/* ------------------------------------------------------------------ */
+/* Algorithm 1                                                          */
+/* ------------------------------------------------------------------ */
+
+/* mode 0: run exactly max_iter updates and record the statistic;
+ * mode 1: stop at the first t with max_i |delta_{t+1,i} - delta_{t,i}| <= eps.
+ * v (in: v_t, out: the newest iterate) and delta (in: delta_t, out: the
+ * newest velocity) carry the state, so a run can be resumed.  stats[t]
+ * receives the statistic of update t.  Returns the number of matrix-vector
+ * products performed, or -1 when ||W v||_1 is zero or not finite. */
+static int32_t power_iterate(const orc_op *op, int32_t mode, int32_t max_iter,
+                             double eps, double *v, double *delta,
+                             double *stats, int32_t *converged)
+{
+    const int64_t n = op->n;
+    double *y = (double *)malloc((size_t)n * sizeof(double));
+    *converged = 0;
+    int32_t done = max_iter;
+    for (int32_t t = 0; t < max_iter; ++t) {
+        op_apply(op, v, y);                            /* W v_t            */
+        double tau = 0.0;                              /* ||W v_t||_1      */
+        for (int64_t i = 0; i < n; ++i)
+            tau += fabs(y[i]);
+        if (!(tau > 0.0) || !isfinite(tau)) {
+            done = -1;
+            break;
+        }
+        double s = 0.0;
+        for (int64_t i = 0; i < n; ++i) {
+            double v_next = y[i] / tau;                /* v_{t+1}          */
+            double d_next = fabs(v_next - v[i]);       /* delta_{t+1}      */
+            double acc = fabs(d_next - delta[i]);      /* |d_{t+1} - d_t|  */
+            if (acc > s)
+                s = acc;
+            v[i] = v_next;
+            delta[i] = d_next;
+        }
+        if (stats)
+            stats[t] = s;
+        if (mode == 1 && s <= eps) {
+            *converged = 1;
+            done = t + 1;
+            break;
+        }
+    }
+    free(y);
+    return done;
+}
+
+int32_t orc_power_iterate_dense(const double *W, int64_t n, int32_t mode,
+                                int32_t max_iter, double eps, double *v,
+                                double *delta, double *stats,
+                                int32_t *converged)
+{
+    orc_op op = {0};
+    op.kind = OP_DENSE;
+    op.n = n;
+    op.W = W;
+    return power_iterate(&op, mode, max_iter, eps, v, delta, stats, converged);
+}
+
+int32_t orc_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
+                              const double *w, int64_t n, int32_t mode,
+                              int32_t max_iter, double eps, double *v,
+                              double *delta, double *stats, int32_t *converged)
+{
+    orc_op op = {0};
+    op.kind = OP_CSR;
+    op.n = n;
+    op.row_ptr = row_ptr;
+    op.col = col;
+    op.w = w;
+    return power_iterate(&op, mode, max_iter, eps, v, delta, stats, converged);
+}
+
+int32_t orc_power_iterate_onthefly(const float *X, int64_t n, int32_t d,
+                                   double sigma, const double *degree,
+                                   int32_t mode, int32_t max_iter, double eps,
+                                   double *v, double *delta, double *stats,
+                                   int32_t *converged)
+{
+    orc_op op = {0};
+    op.kind = OP_ONTHEFLY;
+    op.n = n;
+    op.X = X;
+    op.d = d;
+    op.sigma = sigma;
+    op.degree = degree;
+    return power_iterate(&op, mode, max_iter, eps, v, delta, stats, converged);
+}
+
+/* One product y_i = (W v)_i for the listed rows only, W recomputed. */
+void orc_matvec_onthefly_rows(const float *X, int64_t n, int32_t d,
+                              double sigma, const double *degree,
+                              const double *v, const int64_t *rows,
+                              int64_t nrows, double *y)
+{
+    orc_op op = {0};
+    op.kind = OP_ONTHEFLY;
+    op.n = n;
+    op.X = X;
+    op.d = d;
+    op.sigma = sigma;
+    op.degree = degree;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < nrows; ++r)
+        y[r] = op_row(&op, rows[r], v);
+}
+
+/* ------------------------------------------------------------------ */
+/* Exact 1-D k-means                                                    */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    double value;
+    int64_t index;
+} keyed;
+
+static int cmp_keyed(const void *a, const void *b)
+{
+    const keyed *x = (const keyed *)a, *y = (const keyed *)b;
+    if (x->value < y->value) return -1;
+    if (x->value > y->value) return 1;
+    return (x->index < y->index) ? -1 : (x->index > y->index);
+}
+
+typedef struct {
+    int64_t n;
+    const double *S1; /* S1[p] = sum_{q<p} u_q   (length n+1) */
+    const double *S2; /* S2[p] = sum_{q<p} u_q^2 (length n+1) */
+} prefix_t;
+
+/* Within-cluster sum of squares of sorted positions j..i (inclusive),
+ * from the prefix sums of the centred values; clamped at zero. */
+static double seg_cost(const prefix_t *P, int64_t j, int64_t i)
+{
+    double m = (double)(i - j + 1);
+    double s1 = P->S1[i + 1] - P->S1[j];
+    double s2 = P->S2[i + 1] - P->S2[j];
+    double c = s2 - s1 * s1 / m;
+    return c > 0.0 ? c : 0.0;
+}
+
+/* Leftmost argmin over allowed split points j in [lo, hi] of
+ * prev[j-1] + cost(j, i); j must start a run of equal values. */
+static void best_split(const prefix_t *P, const unsigned char *run_start,
+                       const double *prev, int64_t i, int64_t lo, int64_t hi,
+                       double *best, int64_t *arg)
+{
+    double b = INFINITY;
+    int64_t a = -1;
+    for (int64_t j = lo; j <= hi; ++j) {
+        if (!run_start[j])
+            continue;
+        double c = prev[j - 1] + seg_cost(P, j, i);
+        if (c < b) {
+            b = c;
+            a = j;
+        }
+    }
+    *best = b;
+    *arg = a;
+}
+
+/* divide and conquer over rows lo..hi whose leftmost argmins lie in
+ * [olo, ohi] (monotone optimal split points, see the quadrangle inequality
+ * of the within-cluster sum of squares in 1-D) */
+static void dc_layer(const prefix_t *P, const unsigned char *run_start,
+                     const double *prev, double *cur, int64_t *opt,
+                     int64_t lo, int64_t hi, int64_t olo, int64_t ohi)
+{
+    while (lo <= hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        int64_t a_lo = olo < 1 ? 1 : olo;
+        int64_t a_hi = ohi < mid ? ohi : mid;
+        double b;
+        int64_t a;
+        best_split(P, run_start, prev, mid, a_lo, a_hi, &b, &a);
+        cur[mid] = b;
+        opt[mid] = (a < 0) ? a_lo : a;
+        /* left half recursively, right half in this loop */
+        if (lo <= mid - 1)
+            dc_layer(P, run_start, prev, cur, opt, lo, mid - 1, olo, opt[mid]);
+        lo = mid + 1;
+        olo = opt[mid];
+    }
+}
+
+/* method 0: plain O(k n^2) programme; method 1: divide-and-conquer search.
+ * labels[i] in 0..k_eff-1 by ascending centroid; centroids[c] is the mean
+ * of cluster c; *cost_out the total within-cluster sum of squares, both
+ * computed directly from the members.  Returns 0, or -1 on bad input. */
+int32_t orc_kmeans1d(const double *v, int64_t n, int32_t k, int32_t method,
+                     int32_t *labels, double *centroids, int32_t *k_eff,
+                     double *cost_out)
+{
+    if (n < 1 || k < 1)
+        return -1;
+    keyed *kv = (keyed *)malloc((size_t)n * sizeof(keyed));
+    for (int64_t i = 0; i < n; ++i) {
+        kv[i].value = v[i];
+        kv[i].index = i;
+    }
+    qsort(kv, (size_t)n, sizeof(keyed), cmp_keyed);
+
+    unsigned char *run_start = (unsigned char *)malloc((size_t)n);
+    int64_t distinct = 0;
+    for (int64_t p = 0; p < n; ++p) {
+        run_start[p] = (p == 0 || kv[p].value != kv[p - 1].value);
+        distinct += run_start[p];
+    }
+    int32_t ke = (int64_t)k < distinct ? k : (int32_t)distinct;
+
+    double mean = 0.0;
+    for (int64_t p = 0; p < n; ++p)
+        mean += kv[p].value;
+    mean /= (double)n;
+    double *S1 = (double *)malloc((size_t)(n + 1) * sizeof(double));
+    double *S2 = (double *)malloc((size_t)(n + 1) * sizeof(double));
+    S1[0] = S2[0] = 0.0;
+    for (int64_t p = 0; p < n; ++p) {
+        double u = kv[p].value - mean;
+        S1[p + 1] = S1[p] + u;
+        S2[p + 1] = S2[p] + u * u;
+    }
+    prefix_t P = {n, S1, S2};
+
+    /* D[c][i]: best cost of sorted positions 0..i in c+1 clusters */
+    double *prev = (double *)malloc((size_t)n * sizeof(double));
+    double *cur = (double *)malloc((size_t)n * sizeof(double));
+    int64_t *opt = (int64_t *)malloc((size_t)ke * (size_t)n * sizeof(int64_t));
+    for (int64_t i = 0; i < n; ++i) {
+        prev[i] = seg_cost(&P, 0, i);
+        opt[i] = 0;
+    }
+    for (int32_t c = 1; c < ke; ++c) {
+        int64_t *oc = opt + (int64_t)c * n;
+        if (method == 0) {
+#pragma omp parallel for schedule(dynamic, 64)
+            for (int64_t i = 0; i < n; ++i) {
+                double b;
+                int64_t a;
+                best_split(&P, run_start, prev, i, 1, i, &b, &a);
+                cur[i] = b;
+                oc[i] = (a < 0) ? 1 : a;
+            }
+        } else {
+            dc_layer(&P, run_start, prev, cur, oc, 0, n - 1, 1, n - 1);
+        }
+        double *tmp = prev;
+        prev = cur;
+        cur = tmp;
+    }
+
+    /* backtrack from the last position */
+    int64_t *first = (int64_t *)malloc((size_t)ke * sizeof(int64_t));
+    int64_t i = n - 1;
+    for (int32_t c = ke - 1; c >= 0; --c) {
+        int64_t j = opt[(int64_t)c * n + i];
+        first[c] = j;
+        i = j - 1;
+    }
+    int32_t status = (i == -1 && first[0] == 0) ? 0 : -1;
+
+    double total = 0.0;
+    for (int32_t c = 0; c < ke && status == 0; ++c) {
+        int64_t b = first[c], e = (c + 1 < ke) ? first[c + 1] - 1 : n - 1;
+        double s = 0.0;
+        for (int64_t p = b; p <= e; ++p)
+            s += kv[p].value;
+        double mu = s / (double)(e - b + 1);
+        centroids[c] = mu;
+        for (int64_t p = b; p <= e; ++p) {
+            labels[kv[p].index] = c;
+            total += (kv[p].value - mu) * (kv[p].value - mu);
+        }
+    }
+    *k_eff = ke;
+    if (cost_out)
+        *cost_out = total;
+
+    free(first);
+    free(opt);
+    free(cur);
+    free(prev);
+    free(S2);
+    free(S1);
+    free(run_start);
+    free(kv);
+    return status;
+}
