@@ -1,0 +1,218 @@
+"""Benchmark of the PIC hot path on one MI355X.
+
+One step = the whole path on the 16-D blob workload (n = 50,000, d = 16,
+10 Dirichlet(5)-sized blobs, sigma = median pair distance of a 1,000-point
+sample): Gaussian affinity (dense float32 W of 2.5e9 entries, 10 GB),
+degrees and W = D^-1 A in place, v0, T = 50 power-iteration updates and the
+exact 1-D k-means with k = 10.  Inputs are resident in HBM before the timed
+region.
+
+Prints one JSON line.  `value` is the power-iteration rate in GB/s of W
+streamed (4 bytes per stored entry, 50 updates per step, divided by the
+power-iteration time); `ms_per_step` is the end-to-end step.  The roofline
+object is for the dominant kernel (the dense product), timed with HIP events
+on the library's stream; cpu_baseline is the float64 oracle on a bounded
+sample of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_traffic_blobs16d_n50000.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(os.path.join(ROOT, "paper_1604_02700_amd", "csrc", "power.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per product launch from the committed rocprofv3 counter
+    runs, if they were taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("power_hip_sha") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(w, n_sample, T):
+    """The oracle on the first n_sample points of the same workload."""
+    import oracle
+    X = w.X[:n_sample]
+    t0 = time.perf_counter()
+    W = oracle.affinity(X, w.sigma)
+    W, deg, v0, _ = oracle.degree_normalize(W, copy=False)
+    t1 = time.perf_counter()
+    pi = oracle.power_iterate_dense(W, v0, "fixed", T)
+    t2 = time.perf_counter()
+    oracle.kmeans1d(pi.v, w.k)
+    t3 = time.perf_counter()
+    gbs = T * 4.0 * n_sample * n_sample / (t2 - t1) / 1e9
+    return {"value": round(gbs, 3), "unit": "GB/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"first {n_sample} of the {w.n} points, dense W (float64 in "
+                      f"the oracle, counted at 4 B/entry like the GPU), T = {T}",
+            "phases_s": {"affinity_normalise": round(t1 - t0, 3),
+                         "power_iteration": round(t2 - t1, 3),
+                         "kmeans": round(t3 - t2, 3)}}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--n", type=int, default=50000)
+    ap.add_argument("--T", type=int, default=50)
+    ap.add_argument("--gemv-reps", type=int, default=20)
+    ap.add_argument("--cpu-sample", type=int, default=40000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-converge", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU "
+              "path; N > 1 is not supported.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_1604_02700_amd as g
+    import workloads
+
+    dev = torch.device("cuda:0")
+    w = workloads.make("blobs16d", n=args.n if args.n != 50000 else None)
+    n, d, T, k = w.n, w.d, args.T, w.k
+    log(f"bench: workload blobs16d n={n} d={d} sigma={float(w.sigma):.6g} T={T} k={k}")
+
+    X = torch.from_numpy(w.X).to(dev)
+    lda = g.padded_ld(n)
+    A = torch.empty((n, lda), dtype=torch.float32, device=dev)
+    v = torch.empty(n, dtype=torch.float64, device=dev)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    wbytes = 4.0 * n * n
+
+    def step(record):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        ev[0].record(stream)
+        A_, deg = g.gpic_affinity(X, w.sigma, A)
+        ev[1].record(stream)
+        W, deg, v0, nz = g.gpic_degree_normalize(A_, n, deg, degree_given=True)
+        v.copy_(v0)
+        ev[2].record(stream)
+        pi = g.gpic_power_iterate_dense(W, v, None, "fixed", T, record_stats=False, n=n)
+        ev[3].record(stream)
+        km = g.gpic_kmeans1d(v, k)
+        ev[4].record(stream)
+        if record is not None:
+            torch.cuda.synchronize()
+            record.append([ev[i].elapsed_time(ev[i + 1]) for i in range(4)])
+        return pi, km
+
+    for i in range(args.warmup):
+        step(None)
+        log(f"bench: warmup step {i + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+
+    phases = []
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        pi, km = step(phases)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log(f"bench: {args.steps} timed steps done in {wall:.3f} s")
+    ph = np.array(phases)                     # ms per phase per step
+    ms_step = wall * 1e3 / args.steps
+    pi_ms = float(ph[:, 2].mean())
+    value = T * wbytes / (pi_ms * 1e-3) / 1e9
+
+    # dominant kernel: the dense product alone, on the same stream
+    W = A
+    y = torch.empty(n, dtype=torch.float64, device=dev)
+    g.gpic_matvec_dense(W, v, y, n=n)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.gemv_reps):
+        g.gpic_matvec_dense(W, v, y, n=n)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gemv_ms = e0.elapsed_time(e1) / args.gemv_reps
+    alg_bytes = wbytes + 16.0 * n            # W once, v read, y written
+    achieved = alg_bytes / (gemv_ms * 1e-3) / 1e9
+    log(f"bench: product {gemv_ms:.4f} ms/launch, {achieved:.1f} GB/s")
+
+    conv = None
+    if not args.no_converge:
+        tc0 = time.perf_counter()
+        out = g.pic_dense(X, w.sigma, k, "converge", 1000, w.eps, A=A)
+        torch.cuda.synchronize()
+        tc = time.perf_counter() - tc0
+        conv = {"e2e_s": round(tc, 5), "iterations": out.pi.iterations,
+                "converged": out.pi.converged, "eps": w.eps}
+        log(f"bench: to convergence {out.pi.iterations} updates, {tc:.4f} s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"bench: cpu baseline (oracle) on {args.cpu_sample} points ...")
+        cpu = cpu_baseline(w, min(args.cpu_sample, n), T)
+        log(f"bench: cpu baseline {cpu['value']} GB/s on {cpu['cores']} threads")
+
+    traffic = measured_traffic()
+    line = {
+        "metric": "power-iteration GB/s of W streamed (% HBM peak); end-to-end "
+                  "PIC seconds, n=50k",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": f"blobs16d: n={n}, d={d}, 10 Dirichlet(5) Gaussian "
+                               f"blobs, sigma=median pair distance, dense float32 W, "
+                               f"T={T} fixed updates, exact 1-D k-means k={k}",
+                   "n": n, "d": d, "T": T, "k": k, "storage": "f32",
+                   "accumulate": "f64", "parallelism": "single GPU"},
+        "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "e2e_fixed_T_s": round(ms_step / 1e3, 5),
+        "phases_ms": {"affinity": round(float(ph[:, 0].mean()), 4),
+                      "degree_normalise_v0": round(float(ph[:, 1].mean()), 4),
+                      "power_iteration": round(pi_ms, 4),
+                      "kmeans": round(float(ph[:, 3].mean()), 4)},
+        "to_convergence": conv,
+        "roofline": {"bound": "hbm", "kernel": "gemv_kernel",
+                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "avg_launch_ms": round(gemv_ms, 5),
+                     "bytes_per_launch": alg_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,229 @@
+/*
+ * gpic.h -- C ABI of libgpic, Power Iteration Clustering (PIC) on one
+ * AMD Instinct MI355X (gfx950), following the GPIC paper (arXiv 1604.02700).
+ *
+ * The library covers the data-parallel hot path of the method:
+ *   1. the affinity matrix A of the data graph (section "Spectral Cluster";
+ *      the AffinityMatrix step of Algorithm 2),
+ *   2. the degrees d_ii = sum_j a_ij, W = D^-1 A and v0 = D / sum(D)
+ *      ("Spectral Cluster"; the RowSum, NormMat, Reduction and Norm steps
+ *      of Algorithm 2),
+ *   3. the power iteration v_{t+1} = W v_t / ||W v_t||_1 (update equation of
+ *      section "Power Iteration Clustering: An Overview") with the
+ *      acceleration stop of Algorithm 1 -- delta_0 = v_0,
+ *      delta_{t+1} = |v_{t+1} - v_t|, stop when |delta_{t+1} - delta_t| <= eps
+ *      in every entry -- over three storages of W: a dense matrix, an
+ *      on-the-fly (fused) recomputation from the points, and a CSR graph,
+ *   4. the final k-means of the one-dimensional embedding v (last step of
+ *      Algorithms 1 and 2), computed exactly.
+ *
+ * Conventions (all entry points):
+ *   - Pointers are DEVICE pointers owned by the caller unless marked "host".
+ *     The library never allocates or frees device memory; scratch space comes
+ *     from the caller through (ws, ws_bytes), sized by gpic_workspace_bytes.
+ *     Workspace must be 256-byte aligned.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Calls are asynchronous unless stated otherwise.
+ *   - Every call returns a gpic_status; no C++ exception crosses the ABI.
+ *     Arguments are validated on the host before any launch.  On an error
+ *     the outputs are unspecified; gpic_last_error() gives the text
+ *     (thread-local).
+ *   - Layouts: points X are float32 [n x d] row-major (16-byte aligned);
+ *     dense A / W are float32 [n x lda] row-major, only the first n columns
+ *     of each row are read or written, lda % 4 == 0, base 16-byte aligned.
+ *     Vectors v, delta, degree, v0 are float64 [n], 16-byte aligned.
+ *     CSR graphs: row_ptr int64 [n+1], col int32 [nnz], val float32 [nnz].
+ *   - Floating point: stored matrices and points are float32; every
+ *     accumulation and all iteration state (v, delta, the L1 norm, the stop
+ *     statistic, degrees) are float64.  Reductions are deterministic (fixed
+ *     order, no floating-point atomics): two runs give identical bits.
+ */
+#ifndef GPIC_H
+#define GPIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GPIC_ABI_VERSION 1
+
+typedef enum gpic_status {
+    GPIC_OK = 0,
+    GPIC_ERR_INVALID_ARG = 1, /* null pointer, bad size, bad alignment, ... */
+    GPIC_ERR_WORKSPACE = 2,   /* ws_bytes smaller than gpic_workspace_bytes */
+    GPIC_ERR_HIP = 3,         /* a HIP launch or runtime call failed        */
+    GPIC_ERR_NUMERIC = 4,     /* ||W v||_1 or sum(D) zero or not finite     */
+    GPIC_ERR_UNSUPPORTED = 5  /* valid request this build does not handle   */
+} gpic_status;
+
+/* Operation codes for gpic_workspace_bytes. */
+enum {
+    GPIC_OP_AFFINITY = 0,
+    GPIC_OP_DEGREE_NORMALIZE = 1,
+    GPIC_OP_DEGREE_NORMALIZE_CSR = 2,
+    GPIC_OP_DEGREE_FUSED = 3,
+    GPIC_OP_PI_DENSE = 4,
+    GPIC_OP_PI_FUSED = 5,
+    GPIC_OP_PI_CSR = 6,
+    GPIC_OP_KMEANS1D = 7
+};
+
+/* Power-iteration modes. */
+enum {
+    GPIC_MODE_FIXED = 0,   /* exactly max_iter updates; the statistic is recorded */
+    GPIC_MODE_CONVERGE = 1 /* stop at the first update whose statistic <= eps */
+};
+
+typedef struct gpic_pi_params {
+    int32_t mode;        /* GPIC_MODE_FIXED or GPIC_MODE_CONVERGE                  */
+    int32_t max_iter;    /* T in FIXED mode, the cap in CONVERGE mode (>= 0)       */
+    double eps;          /* stop precision (>= 0); the paper uses 1e-5 / n         */
+    int32_t check_every; /* CONVERGE: the host reads the stop state every this
+                            many updates (0 = default 16); results do not depend
+                            on it, only the number of empty launches after a stop */
+    int32_t reserved;    /* must be 0                                              */
+    double *stats_host;  /* host, nullable: receives the statistic
+                            s_t = max_i |delta_{t+1,i} - delta_{t,i}| of every
+                            update performed (room for max_iter values)            */
+} gpic_pi_params;
+
+typedef struct gpic_pi_result {
+    int32_t iterations;  /* matrix-vector products performed                       */
+    int32_t converged;   /* 1 if the stop test held, else 0 (not an error)         */
+    double last_stat;    /* statistic of the last update (0 if none)               */
+} gpic_pi_result;
+
+/* ---------------------------------------------------------------- helpers */
+
+int32_t gpic_abi_version(void);
+const char *gpic_status_string(gpic_status s);
+/* Text of the last error raised on the calling thread ("" if none). */
+const char *gpic_last_error(void);
+/* Workspace bytes an operation needs for n rows, nnz stored entries (CSR)
+ * and k clusters (k-means); arguments an operation does not use are
+ * ignored.  0 means the operation needs none.  Returns 0 for an unknown op
+ * or negative sizes. */
+size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k);
+
+/* ------------------------------------------------------- 1. affinity (A) */
+
+/* Dense Gaussian affinity, the reading taken for the affinity of section
+ * "Spectral Cluster" (the paper does not write its kernel down):
+ *   A_ij = exp(-||x_i - x_j||^2 / (2 sigma^2)) for i != j,  A_ii = 0.
+ * X: float32 [n x d]; A: float32 [n x lda], written in columns 0..n-1 only.
+ * d < 16 or d > 128 uses direct coordinate differences; 16 <= d <= 128
+ * forms the squared distance from norms and an fp32 matrix-core Gram
+ * product (clamped at 0).  degree (nullable) receives d_i = sum_j A_ij of the
+ * stored float32 values, accumulated in float64.
+ * Errors: INVALID_ARG for null X/A, n < 2, d < 1, sigma <= 0 or not finite,
+ * lda < n, lda % 4 != 0, misaligned pointers.  Asynchronous. */
+gpic_status gpic_affinity(const float *X, int64_t n, int32_t d, float sigma,
+                          float *A, int64_t lda, double *degree, void *stream);
+
+/* --------------------------------- 2. degrees, W = D^-1 A, v0 = D / sum D */
+
+/* Dense, in place: A becomes W (row i scaled by 1/d_i).  If degree_given
+ * is non-zero, degree holds d (e.g. written by gpic_affinity) and is read;
+ * otherwise it is computed here from A and written.  v0_i = d_i / sum_j d_j.
+ * A zero-degree row stays a zero row, gets v0_i = 0 and is counted in
+ * *n_zero_rows (device int64, nullable).  If sum(D) is zero or not finite,
+ * v0 is left unwritten and the call returns GPIC_ERR_NUMERIC (this check
+ * synchronises the stream).  ws: gpic_workspace_bytes(GPIC_OP_DEGREE_NORMALIZE, n, 0, 0). */
+gpic_status gpic_degree_normalize(float *A, int64_t n, int64_t lda,
+                                  double *degree, int32_t degree_given,
+                                  double *v0, int64_t *n_zero_rows, void *ws,
+                                  size_t ws_bytes, void *stream);
+
+/* CSR, in place over val (rows sorted or not; entries summed in storage
+ * order).  Same outputs and errors as the dense version.
+ * ws: gpic_workspace_bytes(GPIC_OP_DEGREE_NORMALIZE_CSR, n, nnz, 0). */
+gpic_status gpic_degree_normalize_csr(const int64_t *row_ptr,
+                                      const int32_t *col, float *val,
+                                      int64_t n, int64_t nnz, double *degree,
+                                      double *v0, int64_t *n_zero_rows,
+                                      void *ws, size_t ws_bytes, void *stream);
+
+/* Fused (W never stored): d_i = sum_{j != i} A_ij with A recomputed from the
+ * points as in gpic_affinity, and v0 = D / sum D.  Nothing of size n^2 is
+ * written.  ws: gpic_workspace_bytes(GPIC_OP_DEGREE_FUSED, n, 0, 0). */
+gpic_status gpic_degree_fused(const float *X, int64_t n, int32_t d,
+                              float sigma, double *degree, double *v0,
+                              int64_t *n_zero_rows, void *ws, size_t ws_bytes,
+                              void *stream);
+
+/* ------------------------------------------ 3. the operator y = W v alone */
+
+/* One product y = W v over dense float32 W [n x ldw] (Multiply step of
+ * Algorithm 2), accumulated in float64.  No normalisation.  Asynchronous. */
+gpic_status gpic_matvec_dense(const float *W, int64_t n, int64_t ldw,
+                              const double *v, double *y, void *stream);
+
+/* One product over a CSR W.  Asynchronous. */
+gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
+                            const float *val, int64_t n, int64_t nnz,
+                            const double *v, double *y, void *stream);
+
+/* One product y_i = (sum_{j != i} A_ij v_j) / d_i with A recomputed from X
+ * (the fused operator; W = D^-1 A is never stored).  A zero-degree row gives
+ * y_i = 0.  Asynchronous. */
+gpic_status gpic_matvec_fused(const float *X, int64_t n, int32_t d,
+                              float sigma, const double *degree,
+                              const double *v, double *y, void *stream);
+
+/* ------------------------------------------------- 3+4. power iteration */
+
+/* Algorithm 1's loop over dense W.  v (in: v_t, usually v0; out: the newest
+ * iterate) and delta (in: delta_t; out: the newest velocity) carry the whole
+ * state, so a run can be resumed; delta == NULL means delta_0 = v_0 (kept
+ * in the workspace).  Each update: y = W v, tau = sum_i |y_i|,
+ * v <- y / tau, delta' = |v_new - v_old|, s_t = max_i |delta' - delta|.
+ * Synchronises the stream at the end (and every check_every updates in
+ * CONVERGE mode); *res (host) receives the counts.  GPIC_ERR_NUMERIC if
+ * tau is zero or not finite; reaching max_iter without the stop is not an
+ * error (converged = 0).  ws: gpic_workspace_bytes(GPIC_OP_PI_DENSE, n, 0, 0). */
+gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
+                                     const gpic_pi_params *params, double *v,
+                                     double *delta, void *ws, size_t ws_bytes,
+                                     gpic_pi_result *res, void *stream);
+
+/* The same loop with the fused operator (A recomputed every update from X,
+ * sigma, and the degrees from gpic_degree_fused).
+ * ws: gpic_workspace_bytes(GPIC_OP_PI_FUSED, n, 0, 0). */
+gpic_status gpic_power_iterate_fused(const float *X, int64_t n, int32_t d,
+                                     float sigma, const double *degree,
+                                     const gpic_pi_params *params, double *v,
+                                     double *delta, void *ws, size_t ws_bytes,
+                                     gpic_pi_result *res, void *stream);
+
+/* The same loop over a CSR W (values already normalised by
+ * gpic_degree_normalize_csr).  ws: gpic_workspace_bytes(GPIC_OP_PI_CSR, n, nnz, 0). */
+gpic_status gpic_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
+                                   const float *val, int64_t n, int64_t nnz,
+                                   const gpic_pi_params *params, double *v,
+                                   double *delta, void *ws, size_t ws_bytes,
+                                   gpic_pi_result *res, void *stream);
+
+/* ------------------------------------------------------- 5. 1-D k-means */
+
+/* "k-means of v" read as the exact minimum within-cluster sum of squares
+ * partition of the n scalars v_i into k clusters (the paper leaves the
+ * variant open).  Equal values are never split: with fewer than k distinct
+ * values, *k_eff (host) < k.  labels (int32 [n]) are 0..k_eff-1 by
+ * ascending centroid; centroids (float64 [k]) get the k_eff cluster means;
+ * *cost (host, nullable) the total within-cluster sum of squares.  Split
+ * ties go to the smallest sorted position.  Synchronises the stream.
+ * Errors: INVALID_ARG for n < 1, k < 1, k > n, null pointers; values must
+ * be finite.  ws: gpic_workspace_bytes(GPIC_OP_KMEANS1D, n, 0, k). */
+gpic_status gpic_kmeans1d(const double *v, int64_t n, int32_t k,
+                          int32_t *labels, double *centroids, int32_t *k_eff,
+                          double *cost, void *ws, size_t ws_bytes,
+                          void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GPIC_H */

@@ -116,9 +116,10 @@ def degree_rows(X, sigma, rows) -> np.ndarray:
 
 
 # ------------------------------------------------------- degree / normalise
-def degree_normalize(A):
-    """Returns (W, degree, v0, n_zero_rows); A itself is not modified."""
-    W = np.array(A, dtype=np.float64, order="C", copy=True)
+def degree_normalize(A, copy=True):
+    """Returns (W, degree, v0, n_zero_rows); with copy=False a float64
+    C-contiguous A is overwritten by W."""
+    W = np.array(A, dtype=np.float64, order="C", copy=copy)
     n = W.shape[0]
     deg = np.empty(n)
     v0 = np.empty(n)

@@ -1,0 +1,392 @@
+"""Python binding of libgpic: Power Iteration Clustering on an MI355X.
+
+A thin ctypes layer over the C ABI declared in include/gpic.h.  Every
+function here has the name of a C entry point and only marshals arguments:
+it checks dtypes and devices, allocates caller-owned outputs and workspace
+as torch tensors (PyTorch is used for device memory and streams only),
+passes raw pointers and the current HIP stream, and raises GpicError on a
+non-OK status.  All computation happens in the library's HIP kernels.
+
+There is no fallback: if libgpic.so is missing or cannot be loaded, every
+call raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgpic.so")
+
+GPIC_OK = 0
+STATUS = {0: "GPIC_OK", 1: "GPIC_ERR_INVALID_ARG", 2: "GPIC_ERR_WORKSPACE",
+          3: "GPIC_ERR_HIP", 4: "GPIC_ERR_NUMERIC", 5: "GPIC_ERR_UNSUPPORTED"}
+OP = {"affinity": 0, "degree_normalize": 1, "degree_normalize_csr": 2,
+      "degree_fused": 3, "pi_dense": 4, "pi_fused": 5, "pi_csr": 6,
+      "kmeans1d": 7}
+MODES = {"fixed": 0, "converge": 1}
+
+# C entry points declared in include/gpic.h (checked by the tests)
+EXPORTS = (
+    "gpic_abi_version", "gpic_status_string", "gpic_last_error",
+    "gpic_workspace_bytes", "gpic_affinity", "gpic_degree_normalize",
+    "gpic_degree_normalize_csr", "gpic_degree_fused", "gpic_matvec_dense",
+    "gpic_matvec_csr", "gpic_matvec_fused", "gpic_power_iterate_dense",
+    "gpic_power_iterate_fused", "gpic_power_iterate_csr", "gpic_kmeans1d",
+)
+
+
+class GpicError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class PiParams(C.Structure):
+    _fields_ = [("mode", C.c_int32), ("max_iter", C.c_int32), ("eps", C.c_double),
+                ("check_every", C.c_int32), ("reserved", C.c_int32),
+                ("stats_host", C.POINTER(C.c_double))]
+
+
+class PiResult(C.Structure):
+    _fields_ = [("iterations", C.c_int32), ("converged", C.c_int32),
+                ("last_stat", C.c_double)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """The loaded libgpic (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() "
+                              "or python paper_1604_02700_amd/build.py")
+        L = C.CDLL(LIB_PATH)
+        p, i64, i32, f32, sz = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_size_t
+        L.gpic_abi_version.restype = i32
+        L.gpic_status_string.restype = C.c_char_p
+        L.gpic_status_string.argtypes = [C.c_int]
+        L.gpic_last_error.restype = C.c_char_p
+        L.gpic_workspace_bytes.restype = sz
+        L.gpic_workspace_bytes.argtypes = [i32, i64, i64, i32]
+        sigs = {
+            "gpic_affinity": [p, i64, i32, f32, p, i64, p, p],
+            "gpic_degree_normalize": [p, i64, i64, p, i32, p, p, p, sz, p],
+            "gpic_degree_normalize_csr": [p, p, p, i64, i64, p, p, p, p, sz, p],
+            "gpic_degree_fused": [p, i64, i32, f32, p, p, p, p, sz, p],
+            "gpic_matvec_dense": [p, i64, i64, p, p, p],
+            "gpic_matvec_csr": [p, p, p, i64, i64, p, p, p],
+            "gpic_matvec_fused": [p, i64, i32, f32, p, p, p, p],
+            "gpic_power_iterate_dense": [p, i64, i64, C.POINTER(PiParams), p, p, p,
+                                         sz, C.POINTER(PiResult), p],
+            "gpic_power_iterate_fused": [p, i64, i32, f32, p, C.POINTER(PiParams),
+                                         p, p, p, sz, C.POINTER(PiResult), p],
+            "gpic_power_iterate_csr": [p, p, p, i64, i64, C.POINTER(PiParams), p, p,
+                                       p, sz, C.POINTER(PiResult), p],
+            "gpic_kmeans1d": [p, i64, i32, p, p, C.POINTER(i32), C.POINTER(C.c_double),
+                              p, sz, p],
+        }
+        for name, args in sigs.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _check(st: int):
+    if st != GPIC_OK:
+        raise GpicError(st, lib().gpic_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> C.c_void_p:
+    return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dev(t: torch.Tensor, dtype, name):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _vec(t, n, name, device):
+    if t is None:
+        return torch.empty(n, dtype=torch.float64, device=device)
+    _dev(t, torch.float64, name)
+    if not t.is_contiguous() or t.numel() != n:
+        raise ValueError(f"{name} must be contiguous with {n} elements")
+    return t
+
+
+def workspace_bytes(op: str, n: int, nnz: int = 0, k: int = 0) -> int:
+    return int(lib().gpic_workspace_bytes(OP[op], int(n), int(nnz), int(k)))
+
+
+def workspace(op: str, n: int, nnz: int = 0, k: int = 0, device="cuda"):
+    """A 256-byte aligned uint8 workspace tensor for `op` (plus its size)."""
+    nbytes = workspace_bytes(op, n, nnz, k)
+    if nbytes == 0:
+        return None, 0
+    buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + nbytes], nbytes
+
+
+def padded_ld(n: int) -> int:
+    """Row stride (in floats) used for dense n x n storage: 128-byte rows."""
+    return (n + 31) // 32 * 32
+
+
+# ------------------------------------------------------------- 1. affinity
+def gpic_affinity(X: torch.Tensor, sigma: float, A: Optional[torch.Tensor] = None,
+                  want_degree: bool = True):
+    """A (float32 [n, lda], first n columns valid) and optional float64 degrees."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    if A is None:
+        A = torch.empty((n, padded_ld(n)), dtype=torch.float32, device=X.device)
+    _dev(A, torch.float32, "A")
+    if A.dim() != 2 or A.shape[0] != n or A.stride(1) != 1 or A.shape[1] < n:
+        raise ValueError("A must be [n, >= n] with unit column stride")
+    deg = torch.empty(n, dtype=torch.float64, device=X.device) if want_degree else None
+    _check(lib().gpic_affinity(_ptr(X), n, d, float(sigma), _ptr(A), A.stride(0),
+                               _ptr(deg), _stream(X.device)))
+    return A, deg
+
+
+# ----------------------------------------------- 2. degrees, W and v0
+def gpic_degree_normalize(A: torch.Tensor, n: Optional[int] = None,
+                          degree: Optional[torch.Tensor] = None,
+                          degree_given: bool = False):
+    """A -> W in place; returns (A, degree, v0, n_zero_rows tensor)."""
+    _dev(A, torch.float32, "A")
+    n = A.shape[0] if n is None else n
+    dev = A.device
+    degree = _vec(degree, n, "degree", dev)
+    v0 = torch.empty(n, dtype=torch.float64, device=dev)
+    nz = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws, nb = workspace("degree_normalize", n, device=dev)
+    _check(lib().gpic_degree_normalize(_ptr(A), n, A.stride(0), _ptr(degree),
+                                       1 if degree_given else 0, _ptr(v0), _ptr(nz),
+                                       _ptr(ws), nb, _stream(dev)))
+    return A, degree, v0, nz
+
+
+def gpic_degree_normalize_csr(row_ptr, col, val):
+    """val -> normalised in place; returns (val, degree, v0, n_zero_rows)."""
+    _dev(row_ptr, torch.int64, "row_ptr")
+    _dev(col, torch.int32, "col")
+    _dev(val, torch.float32, "val")
+    n = row_ptr.numel() - 1
+    nnz = val.numel()
+    dev = val.device
+    degree = torch.empty(n, dtype=torch.float64, device=dev)
+    v0 = torch.empty(n, dtype=torch.float64, device=dev)
+    nz = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws, nb = workspace("degree_normalize_csr", n, nnz, device=dev)
+    _check(lib().gpic_degree_normalize_csr(_ptr(row_ptr), _ptr(col), _ptr(val), n, nnz,
+                                           _ptr(degree), _ptr(v0), _ptr(nz), _ptr(ws),
+                                           nb, _stream(dev)))
+    return val, degree, v0, nz
+
+
+def gpic_degree_fused(X: torch.Tensor, sigma: float):
+    """Degrees and v0 with A recomputed and never stored."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    dev = X.device
+    degree = torch.empty(n, dtype=torch.float64, device=dev)
+    v0 = torch.empty(n, dtype=torch.float64, device=dev)
+    nz = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws, nb = workspace("degree_fused", n, device=dev)
+    _check(lib().gpic_degree_fused(_ptr(X), n, d, float(sigma), _ptr(degree), _ptr(v0),
+                                   _ptr(nz), _ptr(ws), nb, _stream(dev)))
+    return degree, v0, nz
+
+
+# --------------------------------------------------- 3. one product y = W v
+def gpic_matvec_dense(W: torch.Tensor, v: torch.Tensor, y=None, n=None):
+    _dev(W, torch.float32, "W")
+    n = W.shape[0] if n is None else n
+    y = _vec(y, n, "y", W.device)
+    _dev(v, torch.float64, "v")
+    _check(lib().gpic_matvec_dense(_ptr(W), n, W.stride(0), _ptr(v), _ptr(y),
+                                   _stream(W.device)))
+    return y
+
+
+def gpic_matvec_csr(row_ptr, col, val, v, y=None):
+    n = row_ptr.numel() - 1
+    y = _vec(y, n, "y", val.device)
+    _dev(v, torch.float64, "v")
+    _check(lib().gpic_matvec_csr(_ptr(row_ptr), _ptr(col), _ptr(val), n, val.numel(),
+                                 _ptr(v), _ptr(y), _stream(val.device)))
+    return y
+
+
+def gpic_matvec_fused(X, sigma, degree, v, y=None):
+    _dev(X, torch.float32, "X")
+    n, d = X.shape
+    y = _vec(y, n, "y", X.device)
+    _check(lib().gpic_matvec_fused(_ptr(X), n, d, float(sigma), _ptr(degree), _ptr(v),
+                                   _ptr(y), _stream(X.device)))
+    return y
+
+
+# ------------------------------------------------------- 3+4. iteration
+@dataclasses.dataclass
+class PIOut:
+    v: torch.Tensor
+    delta: Optional[torch.Tensor]
+    iterations: int
+    converged: bool
+    last_stat: float
+    stats: np.ndarray
+
+
+def _params(mode, max_iter, eps, check_every, stats_buf):
+    p = PiParams()
+    p.mode = MODES[mode]
+    p.max_iter = int(max_iter)
+    p.eps = float(eps)
+    p.check_every = int(check_every)
+    p.reserved = 0
+    p.stats_host = (stats_buf.ctypes.data_as(C.POINTER(C.c_double))
+                    if stats_buf is not None else None)
+    return p
+
+
+def _run_pi(fn, head, n, dev, v, delta, mode, max_iter, eps, check_every,
+            record_stats, op, nnz=0):
+    stats = np.zeros(max(int(max_iter), 1)) if record_stats else None
+    p = _params(mode, max_iter, eps, check_every, stats)
+    r = PiResult()
+    ws, nb = workspace(op, n, nnz, device=dev)
+    _check(fn(*head, C.byref(p), _ptr(v), _ptr(delta), _ptr(ws), nb, C.byref(r),
+              _stream(dev)))
+    st = stats[: r.iterations].copy() if record_stats else np.zeros(0)
+    return PIOut(v, delta, int(r.iterations), bool(r.converged), float(r.last_stat), st)
+
+
+def gpic_power_iterate_dense(W, v, delta=None, mode="converge", max_iter=1000, eps=0.0,
+                             check_every=0, record_stats=True, n=None):
+    """Algorithm 1's loop over dense W; v (and delta, if given) are updated in place."""
+    _dev(W, torch.float32, "W")
+    n = W.shape[0] if n is None else n
+    _vec(v, n, "v", W.device)
+    if delta is not None:
+        _vec(delta, n, "delta", W.device)
+    return _run_pi(lib().gpic_power_iterate_dense, (_ptr(W), n, W.stride(0)), n,
+                   W.device, v, delta, mode, max_iter, eps, check_every, record_stats,
+                   "pi_dense")
+
+
+def gpic_power_iterate_fused(X, sigma, degree, v, delta=None, mode="fixed", max_iter=30,
+                             eps=0.0, check_every=0, record_stats=True):
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    _vec(v, n, "v", X.device)
+    _vec(degree, n, "degree", X.device)
+    if delta is not None:
+        _vec(delta, n, "delta", X.device)
+    return _run_pi(lib().gpic_power_iterate_fused,
+                   (_ptr(X), n, d, float(sigma), _ptr(degree)), n, X.device, v, delta,
+                   mode, max_iter, eps, check_every, record_stats, "pi_fused")
+
+
+def gpic_power_iterate_csr(row_ptr, col, val, v, delta=None, mode="converge",
+                           max_iter=1000, eps=0.0, check_every=0, record_stats=True):
+    _dev(row_ptr, torch.int64, "row_ptr")
+    _dev(col, torch.int32, "col")
+    _dev(val, torch.float32, "val")
+    n = row_ptr.numel() - 1
+    nnz = val.numel()
+    _vec(v, n, "v", val.device)
+    if delta is not None:
+        _vec(delta, n, "delta", val.device)
+    return _run_pi(lib().gpic_power_iterate_csr,
+                   (_ptr(row_ptr), _ptr(col), _ptr(val), n, nnz), n, val.device, v,
+                   delta, mode, max_iter, eps, check_every, record_stats, "pi_csr",
+                   nnz)
+
+
+# ------------------------------------------------------------ 5. k-means
+@dataclasses.dataclass
+class KMOut:
+    labels: torch.Tensor        # int32 [n]
+    centroids: torch.Tensor     # float64 [k_eff]
+    k_eff: int
+    cost: float
+
+
+def gpic_kmeans1d(v: torch.Tensor, k: int) -> KMOut:
+    _dev(v, torch.float64, "v")
+    n = v.numel()
+    dev = v.device
+    labels = torch.empty(n, dtype=torch.int32, device=dev)
+    cent = torch.empty(max(int(k), 1), dtype=torch.float64, device=dev)
+    ke = C.c_int32(0)
+    cost = C.c_double(0.0)
+    ws, nb = workspace("kmeans1d", n, 0, k, device=dev)
+    _check(lib().gpic_kmeans1d(_ptr(v), n, int(k), _ptr(labels), _ptr(cent),
+                               C.byref(ke), C.byref(cost), _ptr(ws), nb, _stream(dev)))
+    return KMOut(labels, cent[: ke.value], int(ke.value), float(cost.value))
+
+
+# ----------------------------------------------- whole paths (call chains)
+@dataclasses.dataclass
+class PICOut:
+    degree: torch.Tensor
+    v0: torch.Tensor
+    pi: PIOut
+    km: KMOut
+    n_zero_rows: int
+
+
+def pic_dense(X, sigma, k, mode="converge", max_iter=1000, eps=0.0, check_every=0,
+              A: Optional[torch.Tensor] = None) -> PICOut:
+    """Affinity, degrees, W = D^-1 A, v0, the power iteration and k-means,
+    over a materialised dense W (n^2 float32)."""
+    n = X.shape[0]
+    A, deg = gpic_affinity(X, sigma, A)
+    W, deg, v0, nz = gpic_degree_normalize(A, n, deg, degree_given=True)
+    v = v0.clone()
+    pi = gpic_power_iterate_dense(W, v, None, mode, max_iter, eps, check_every, n=n)
+    km = gpic_kmeans1d(pi.v, k)
+    return PICOut(deg, v0, pi, km, int(nz.item()))
+
+
+def pic_fused(X, sigma, k, mode="fixed", max_iter=30, eps=0.0, check_every=0) -> PICOut:
+    """The same path with W never stored (affinity recomputed every sweep)."""
+    deg, v0, nz = gpic_degree_fused(X, sigma)
+    v = v0.clone()
+    pi = gpic_power_iterate_fused(X, sigma, deg, v, None, mode, max_iter, eps, check_every)
+    km = gpic_kmeans1d(pi.v, k)
+    return PICOut(deg, v0, pi, km, int(nz.item()))
+
+
+def pic_csr(row_ptr, col, val, k, mode="converge", max_iter=1000, eps=0.0,
+            check_every=0) -> PICOut:
+    """The same path over a CSR affinity graph (val normalised in place)."""
+    val, deg, v0, nz = gpic_degree_normalize_csr(row_ptr, col, val)
+    v = v0.clone()
+    pi = gpic_power_iterate_csr(row_ptr, col, val, v, None, mode, max_iter, eps,
+                                check_every)
+    km = gpic_kmeans1d(pi.v, k)
+    return PICOut(deg, v0, pi, km, int(nz.item()))

@@ -1,0 +1,587 @@
+// libgpic C ABI: host-side validation, workspace layout and the
+// power-iteration driver (Algorithm 1's loop) over the kernels of the other
+// translation units.  Nothing here computes on the host; every step of the
+// method runs in the HIP kernels.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/gpic.h"
+#include "common.h"
+
+namespace gpic {
+
+namespace {
+thread_local std::string g_last_error;
+} // namespace
+
+const char *last_error_text() { return g_last_error.c_str(); }
+
+void set_error(const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+}
+
+} // namespace gpic
+
+using namespace gpic;
+
+namespace {
+
+constexpr int64_t kMaxN = 2147483647LL;     // indices are int32 in places
+constexpr int64_t kRing = 1024;             // statistic slots on the device
+constexpr size_t kCtlBytes = 256;           // err @0, tau @8, csr flag @16
+
+inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline bool aligned(const void *p, size_t a)
+{
+    return ((uintptr_t)p % a) == 0;
+}
+
+gpic_status fail(gpic_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    set_error("%s", buf);
+    return st;
+}
+
+gpic_status hip_fail(hipError_t e, const char *where)
+{
+    return fail(GPIC_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define CHECK_ARG(cond, ...)                                                   \
+    do {                                                                       \
+        if (!(cond))                                                           \
+            return fail(GPIC_ERR_INVALID_ARG, __VA_ARGS__);                    \
+    } while (0)
+
+#define CHECK_HIP(expr, where)                                                 \
+    do {                                                                       \
+        hipError_t e_ = (expr);                                                \
+        if (e_ != hipSuccess)                                                  \
+            return hip_fail(e_, where);                                        \
+    } while (0)
+
+size_t start_ws(int64_t n) { return al(start_vector_ws(n)); }
+
+size_t pi_ws(int64_t n, int64_t nb)
+{
+    return kCtlBytes + al(kRing * 8) + al((size_t)nb * 8) + 2 * al((size_t)n * 8);
+}
+
+int64_t fused_nb_bound(int64_t n) { return (n + 7) / 8; }
+
+// exp(-x / (2 sigma^2)) = exp2(-c x) with c = log2(e) / (2 sigma^2)
+bool gauss_coefficient(float sigma, float *c)
+{
+    const double s = (double)sigma;
+    const double cc = 1.4426950408889634074 / (2.0 * s * s);
+    *c = (float)cc;
+    return isfinite(*c) && *c > 0.0f;
+}
+
+gpic_status check_points(const float *X, int64_t n, int32_t d, float sigma)
+{
+    CHECK_ARG(X != nullptr, "X is null");
+    CHECK_ARG(aligned(X, 4), "X must be 4-byte aligned");
+    CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range [2, 2^31-1]", (long long)n);
+    CHECK_ARG(d >= 1, "d = %d must be >= 1", d);
+    CHECK_ARG(isfinite(sigma) && sigma > 0.0f, "sigma must be finite and > 0");
+    float c;
+    CHECK_ARG(gauss_coefficient(sigma, &c), "sigma too small (1/(2 sigma^2) overflows)");
+    return GPIC_OK;
+}
+
+gpic_status check_vec(const void *p, const char *name, bool nullable = false)
+{
+    if (p == nullptr) {
+        if (nullable)
+            return GPIC_OK;
+        return fail(GPIC_ERR_INVALID_ARG, "%s is null", name);
+    }
+    if (!aligned(p, 16))
+        return fail(GPIC_ERR_INVALID_ARG, "%s must be 16-byte aligned", name);
+    return GPIC_OK;
+}
+
+gpic_status check_ws(void *ws, size_t have, size_t need)
+{
+    if (need == 0)
+        return GPIC_OK;
+    if (ws == nullptr || have < need)
+        return fail(GPIC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given",
+                    need, ws == nullptr ? (size_t)0 : have);
+    if (!aligned(ws, 256))
+        return fail(GPIC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    return GPIC_OK;
+}
+
+gpic_status check_params(const gpic_pi_params *p)
+{
+    CHECK_ARG(p != nullptr, "params is null");
+    CHECK_ARG(p->mode == GPIC_MODE_FIXED || p->mode == GPIC_MODE_CONVERGE,
+              "mode %d is not FIXED (0) or CONVERGE (1)", p->mode);
+    CHECK_ARG(p->max_iter >= 0, "max_iter must be >= 0");
+    CHECK_ARG(!(p->eps < 0.0) && !isnan(p->eps), "eps must be >= 0");
+    CHECK_ARG(p->check_every >= 0, "check_every must be >= 0");
+    CHECK_ARG(p->reserved == 0, "reserved must be 0");
+    return GPIC_OK;
+}
+
+gpic_status check_csr(const int64_t *row_ptr, const int32_t *col,
+                      const void *val, int64_t n, int64_t nnz)
+{
+    CHECK_ARG(row_ptr != nullptr && col != nullptr && val != nullptr,
+              "CSR arrays must not be null");
+    CHECK_ARG(aligned(row_ptr, 8) && aligned(col, 4) && aligned(val, 4),
+              "CSR arrays misaligned");
+    CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range", (long long)n);
+    CHECK_ARG(nnz >= 0, "nnz must be >= 0");
+    return GPIC_OK;
+}
+
+// Device-side structural check of a CSR graph (row_ptr monotone from 0 to
+// nnz, columns in range) before any kernel indexes through it.
+gpic_status verify_csr(const int64_t *row_ptr, const int32_t *col, int64_t n,
+                       int64_t nnz, void *ws, hipStream_t s)
+{
+    int *flag = reinterpret_cast<int *>(static_cast<char *>(ws) + 16);
+    int bad = 0;
+    CHECK_HIP(launch_csr_check(row_ptr, col, n, nnz, flag, s, &bad), "csr check");
+    if (bad)
+        return fail(GPIC_ERR_INVALID_ARG,
+                    "CSR structure invalid (row_ptr not monotone from 0 to nnz, "
+                    "or a column outside [0, n))");
+    return GPIC_OK;
+}
+
+// The product of one update: y = W v, with per-block partial |y| sums.
+struct Product {
+    virtual ~Product() {}
+    virtual int64_t blocks() const = 0;
+    virtual hipError_t launch(const double *v, double *y, double *partial,
+                              StopCtl ctl, hipStream_t s) const = 0;
+};
+
+struct DenseProduct : Product {
+    const float *W;
+    int64_t n, ldw;
+    int64_t blocks() const override { return gemv_blocks(n); }
+    hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
+                      hipStream_t s) const override
+    {
+        return launch_gemv(W, n, ldw, v, y, partial, ctl, true, s);
+    }
+};
+
+struct CsrProduct : Product {
+    const int64_t *row_ptr;
+    const int32_t *col;
+    const float *val;
+    int64_t n;
+    int64_t blocks() const override { return spmv_blocks(n); }
+    hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
+                      hipStream_t s) const override
+    {
+        return launch_spmv(row_ptr, col, val, n, v, y, partial, ctl, true, s);
+    }
+};
+
+struct FusedProduct : Product {
+    const float *X;
+    int64_t n;
+    int d;
+    float c;
+    const double *degree;
+    int64_t blocks() const override { return fused_blocks(n, d); }
+    hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
+                      hipStream_t s) const override
+    {
+        return launch_fused_apply(X, n, d, c, v, degree, y, partial, ctl, true, s);
+    }
+};
+
+// Algorithm 1's loop on the device; the host only batches launches and
+// reads the statistic slots back every chunk.
+gpic_status run_power_iteration(const Product &op, int64_t n,
+                                const gpic_pi_params *p, double *v,
+                                double *delta_user, void *ws,
+                                gpic_pi_result *res, hipStream_t s)
+{
+    char *w = static_cast<char *>(ws);
+    int *err = reinterpret_cast<int *>(w);
+    double *tau = reinterpret_cast<double *>(w + 8);
+    size_t o = kCtlBytes;
+    double *ring = reinterpret_cast<double *>(w + o);
+    o += al(kRing * 8);
+    double *partial = reinterpret_cast<double *>(w + o);
+    o += al((size_t)op.blocks() * 8);
+    double *y = reinterpret_cast<double *>(w + o);
+    o += al((size_t)n * 8);
+    double *delta = delta_user ? delta_user : reinterpret_cast<double *>(w + o);
+
+    res->iterations = 0;
+    res->converged = 0;
+    res->last_stat = 0.0;
+    CHECK_HIP(launch_init_state(ring, kRing, err, v, delta, n, delta_user == nullptr, s),
+              "init");
+    const bool conv = p->mode == GPIC_MODE_CONVERGE;
+    const double eps = conv ? p->eps : -1.0;
+    int64_t chunk = kRing;
+    if (conv)
+        chunk = p->check_every > 0 ? (p->check_every < kRing ? p->check_every : kRing)
+                                   : 16;
+    std::vector<double> hstat((size_t)chunk);
+    const int64_t T = p->max_iter;
+    int64_t t = 0;
+    bool stopped = false;
+    while (t < T && !stopped) {
+        const int64_t te = (t + chunk < T) ? t + chunk : T;
+        for (int64_t u = t; u < te; ++u) {
+            StopCtl ctl;
+            ctl.prev_stat = (conv && u > 0) ? ring + ((u - 1) % kRing) : nullptr;
+            ctl.cur_stat = ring + (u % kRing);
+            ctl.eps = eps;
+            ctl.err = err;
+            CHECK_HIP(op.launch(v, y, partial, ctl, s), "product");
+            CHECK_HIP(launch_reduce_tau(partial, op.blocks(), tau, ctl, s), "tau");
+            CHECK_HIP(launch_update(y, tau, v, delta, n, ctl, s), "update");
+        }
+        const int64_t m = te - t;
+        const int64_t a = t % kRing;
+        const int64_t first = (a + m <= kRing) ? m : kRing - a;
+        CHECK_HIP(hipMemcpyAsync(hstat.data(), ring + a, first * 8,
+                                 hipMemcpyDeviceToHost, s), "stat copy");
+        if (first < m)
+            CHECK_HIP(hipMemcpyAsync(hstat.data() + first, ring, (m - first) * 8,
+                                     hipMemcpyDeviceToHost, s), "stat copy");
+        int herr = 0;
+        CHECK_HIP(hipMemcpyAsync(&herr, err, sizeof(int), hipMemcpyDeviceToHost, s),
+                  "flag copy");
+        CHECK_HIP(hipStreamSynchronize(s), "synchronize");
+        if (herr)
+            return fail(GPIC_ERR_NUMERIC, "||W v||_1 is zero or not finite");
+        for (int64_t u = t; u < te; ++u) {
+            const double su = hstat[(size_t)(u - t)];
+            if (p->stats_host)
+                p->stats_host[u] = su;
+            res->last_stat = su;
+            res->iterations = (int32_t)(u + 1);
+            if (conv && su <= p->eps) {
+                res->converged = 1;
+                stopped = true;
+                break;
+            }
+        }
+        t = te;
+    }
+    if (T == 0)
+        CHECK_HIP(hipStreamSynchronize(s), "synchronize");
+    return GPIC_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+int32_t gpic_abi_version(void) { return GPIC_ABI_VERSION; }
+
+const char *gpic_status_string(gpic_status st)
+{
+    switch (st) {
+    case GPIC_OK: return "GPIC_OK";
+    case GPIC_ERR_INVALID_ARG: return "GPIC_ERR_INVALID_ARG";
+    case GPIC_ERR_WORKSPACE: return "GPIC_ERR_WORKSPACE";
+    case GPIC_ERR_HIP: return "GPIC_ERR_HIP";
+    case GPIC_ERR_NUMERIC: return "GPIC_ERR_NUMERIC";
+    case GPIC_ERR_UNSUPPORTED: return "GPIC_ERR_UNSUPPORTED";
+    }
+    return "unknown gpic_status";
+}
+
+const char *gpic_last_error(void) { return gpic::last_error_text(); }
+
+size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
+{
+    if (n < 0 || nnz < 0 || k < 0)
+        return 0;
+    switch (op) {
+    case GPIC_OP_AFFINITY: return 0;
+    case GPIC_OP_DEGREE_NORMALIZE: return start_ws(n);
+    case GPIC_OP_DEGREE_NORMALIZE_CSR: return kCtlBytes + start_ws(n);
+    case GPIC_OP_DEGREE_FUSED: return start_ws(n);
+    case GPIC_OP_PI_DENSE: return pi_ws(n, gemv_blocks(n));
+    case GPIC_OP_PI_FUSED: return pi_ws(n, fused_nb_bound(n));
+    case GPIC_OP_PI_CSR: return pi_ws(n, spmv_blocks(n));
+    case GPIC_OP_KMEANS1D: return kmeans_ws(n, k < 1 ? 1 : k);
+    default: return 0;
+    }
+}
+
+gpic_status gpic_affinity(const float *X, int64_t n, int32_t d, float sigma,
+                          float *A, int64_t lda, double *degree, void *stream)
+{
+    gpic_status st = check_points(X, n, d, sigma);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(A != nullptr, "A is null");
+    CHECK_ARG(aligned(A, 16), "A must be 16-byte aligned");
+    CHECK_ARG(lda >= n && lda % 4 == 0, "lda = %lld must be >= n and a multiple of 4",
+              (long long)lda);
+    if ((st = check_vec(degree, "degree", true)) != GPIC_OK)
+        return st;
+    float c;
+    gauss_coefficient(sigma, &c);
+    CHECK_HIP(launch_affinity(X, n, d, c, A, lda, degree, (hipStream_t)stream),
+              "affinity");
+    return GPIC_OK;
+}
+
+gpic_status gpic_degree_normalize(float *A, int64_t n, int64_t lda, double *degree,
+                                  int32_t degree_given, double *v0,
+                                  int64_t *n_zero_rows, void *ws, size_t ws_bytes,
+                                  void *stream)
+{
+    CHECK_ARG(A != nullptr && aligned(A, 16), "A is null or not 16-byte aligned");
+    CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range", (long long)n);
+    CHECK_ARG(lda >= n && lda % 4 == 0, "lda must be >= n and a multiple of 4");
+    gpic_status st;
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v0, "v0")) != GPIC_OK)
+        return st;
+    CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
+              "n_zero_rows misaligned");
+    if ((st = check_ws(ws, ws_bytes, start_ws(n))) != GPIC_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    if (!degree_given)
+        CHECK_HIP(launch_dense_degree(A, n, lda, degree, s), "degree");
+    CHECK_HIP(launch_dense_scale(A, n, lda, degree, s), "normalise");
+    int bad = 0;
+    CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
+    if (bad)
+        return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
+    return GPIC_OK;
+}
+
+gpic_status gpic_degree_normalize_csr(const int64_t *row_ptr, const int32_t *col,
+                                      float *val, int64_t n, int64_t nnz,
+                                      double *degree, double *v0,
+                                      int64_t *n_zero_rows, void *ws,
+                                      size_t ws_bytes, void *stream)
+{
+    gpic_status st = check_csr(row_ptr, col, val, n, nnz);
+    if (st != GPIC_OK)
+        return st;
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v0, "v0")) != GPIC_OK)
+        return st;
+    CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
+              "n_zero_rows misaligned");
+    if ((st = check_ws(ws, ws_bytes, kCtlBytes + start_ws(n))) != GPIC_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    if ((st = verify_csr(row_ptr, col, n, nnz, ws, s)) != GPIC_OK)
+        return st;
+    CHECK_HIP(launch_csr_degree_scale(row_ptr, val, n, degree, s), "csr normalise");
+    int bad = 0;
+    CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows,
+                                  static_cast<char *>(ws) + kCtlBytes, s, &bad),
+              "v0");
+    if (bad)
+        return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
+    return GPIC_OK;
+}
+
+gpic_status gpic_degree_fused(const float *X, int64_t n, int32_t d, float sigma,
+                              double *degree, double *v0, int64_t *n_zero_rows,
+                              void *ws, size_t ws_bytes, void *stream)
+{
+    gpic_status st = check_points(X, n, d, sigma);
+    if (st != GPIC_OK)
+        return st;
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v0, "v0")) != GPIC_OK)
+        return st;
+    CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
+              "n_zero_rows misaligned");
+    if ((st = check_ws(ws, ws_bytes, start_ws(n))) != GPIC_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    float c;
+    gauss_coefficient(sigma, &c);
+    CHECK_HIP(launch_fused_degree(X, n, d, c, degree, s), "fused degree");
+    int bad = 0;
+    CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
+    if (bad)
+        return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
+    return GPIC_OK;
+}
+
+gpic_status gpic_matvec_dense(const float *W, int64_t n, int64_t ldw,
+                              const double *v, double *y, void *stream)
+{
+    CHECK_ARG(W != nullptr && aligned(W, 16), "W is null or not 16-byte aligned");
+    CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range", (long long)n);
+    CHECK_ARG(ldw >= n && ldw % 4 == 0, "ldw must be >= n and a multiple of 4");
+    gpic_status st;
+    if ((st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
+        return st;
+    StopCtl none{};
+    CHECK_HIP(launch_gemv(W, n, ldw, v, y, nullptr, none, false, (hipStream_t)stream),
+              "gemv");
+    return GPIC_OK;
+}
+
+gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
+                            const float *val, int64_t n, int64_t nnz,
+                            const double *v, double *y, void *stream)
+{
+    gpic_status st = check_csr(row_ptr, col, val, n, nnz);
+    if (st != GPIC_OK)
+        return st;
+    if ((st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
+        return st;
+    StopCtl none{};
+    CHECK_HIP(launch_spmv(row_ptr, col, val, n, v, y, nullptr, none, false,
+                          (hipStream_t)stream),
+              "spmv");
+    return GPIC_OK;
+}
+
+gpic_status gpic_matvec_fused(const float *X, int64_t n, int32_t d, float sigma,
+                              const double *degree, const double *v, double *y,
+                              void *stream)
+{
+    gpic_status st = check_points(X, n, d, sigma);
+    if (st != GPIC_OK)
+        return st;
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
+        return st;
+    float c;
+    gauss_coefficient(sigma, &c);
+    StopCtl none{};
+    CHECK_HIP(launch_fused_apply(X, n, d, c, v, degree, y, nullptr, none, false,
+                                 (hipStream_t)stream),
+              "fused product");
+    return GPIC_OK;
+}
+
+static gpic_status check_pi_common(int64_t n, const gpic_pi_params *params,
+                                   double *v, double *delta, gpic_pi_result *res)
+{
+    CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range", (long long)n);
+    gpic_status st;
+    if ((st = check_params(params)) != GPIC_OK)
+        return st;
+    if ((st = check_vec(v, "v")) != GPIC_OK ||
+        (st = check_vec(delta, "delta", true)) != GPIC_OK)
+        return st;
+    CHECK_ARG(res != nullptr, "res is null");
+    return GPIC_OK;
+}
+
+gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
+                                     const gpic_pi_params *params, double *v,
+                                     double *delta, void *ws, size_t ws_bytes,
+                                     gpic_pi_result *res, void *stream)
+{
+    CHECK_ARG(W != nullptr && aligned(W, 16), "W is null or not 16-byte aligned");
+    gpic_status st = check_pi_common(n, params, v, delta, res);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(ldw >= n && ldw % 4 == 0, "ldw must be >= n and a multiple of 4");
+    if ((st = check_ws(ws, ws_bytes, pi_ws(n, gemv_blocks(n)))) != GPIC_OK)
+        return st;
+    DenseProduct op;
+    op.W = W;
+    op.n = n;
+    op.ldw = ldw;
+    return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
+}
+
+gpic_status gpic_power_iterate_fused(const float *X, int64_t n, int32_t d,
+                                     float sigma, const double *degree,
+                                     const gpic_pi_params *params, double *v,
+                                     double *delta, void *ws, size_t ws_bytes,
+                                     gpic_pi_result *res, void *stream)
+{
+    gpic_status st = check_points(X, n, d, sigma);
+    if (st != GPIC_OK)
+        return st;
+    if ((st = check_vec(degree, "degree")) != GPIC_OK)
+        return st;
+    if ((st = check_pi_common(n, params, v, delta, res)) != GPIC_OK)
+        return st;
+    if ((st = check_ws(ws, ws_bytes, pi_ws(n, fused_nb_bound(n)))) != GPIC_OK)
+        return st;
+    FusedProduct op;
+    op.X = X;
+    op.n = n;
+    op.d = d;
+    gauss_coefficient(sigma, &op.c);
+    op.degree = degree;
+    return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
+}
+
+gpic_status gpic_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
+                                   const float *val, int64_t n, int64_t nnz,
+                                   const gpic_pi_params *params, double *v,
+                                   double *delta, void *ws, size_t ws_bytes,
+                                   gpic_pi_result *res, void *stream)
+{
+    gpic_status st = check_csr(row_ptr, col, val, n, nnz);
+    if (st != GPIC_OK)
+        return st;
+    if ((st = check_pi_common(n, params, v, delta, res)) != GPIC_OK)
+        return st;
+    if ((st = check_ws(ws, ws_bytes, pi_ws(n, spmv_blocks(n)))) != GPIC_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    if ((st = verify_csr(row_ptr, col, n, nnz, ws, s)) != GPIC_OK)
+        return st;
+    CsrProduct op;
+    op.row_ptr = row_ptr;
+    op.col = col;
+    op.val = val;
+    op.n = n;
+    return run_power_iteration(op, n, params, v, delta, ws, res, s);
+}
+
+gpic_status gpic_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
+                          double *centroids, int32_t *k_eff, double *cost, void *ws,
+                          size_t ws_bytes, void *stream)
+{
+    CHECK_ARG(n >= 1 && n <= kMaxN, "n = %lld out of range [1, 2^31-1]", (long long)n);
+    CHECK_ARG(k >= 1 && (int64_t)k <= n, "k = %d must be in [1, n]", k);
+    gpic_status st;
+    if ((st = check_vec(v, "v")) != GPIC_OK ||
+        (st = check_vec(centroids, "centroids")) != GPIC_OK)
+        return st;
+    CHECK_ARG(labels != nullptr && aligned(labels, 4), "labels null or misaligned");
+    CHECK_ARG(k_eff != nullptr, "k_eff is null");
+    if ((st = check_ws(ws, ws_bytes, kmeans_ws(n, k))) != GPIC_OK)
+        return st;
+    CHECK_HIP(run_kmeans1d(v, n, k, labels, centroids, k_eff, cost, ws,
+                           (hipStream_t)stream),
+              "kmeans1d");
+    return GPIC_OK;
+}
+
+} // extern "C"

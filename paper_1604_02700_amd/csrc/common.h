@@ -1,0 +1,166 @@
+// Internal helpers shared by the libgpic HIP translation units (not part of
+// the C ABI).  Written for gfx950: 64-lane wavefronts, float64 shuffles
+// through two 32-bit lane exchanges, no floating-point atomics anywhere.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gpic {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- errors
+// Records the text of the last error on the calling thread.
+void set_error(const char *fmt, ...);
+
+// ------------------------------------------------------ wave reductions
+// Butterfly reductions: lane l combines with lane l ^ o.  Because a + b and
+// b + a round identically, every lane ends with bit-identical results and
+// the result does not depend on scheduling.
+__device__ __forceinline__ double wave_sum(double x)
+{
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1)
+        x += __shfl_xor(x, o, kWave);
+    return x;
+}
+
+__device__ __forceinline__ double wave_max(double x)
+{
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1)
+        x = fmax(x, __shfl_xor(x, o, kWave));
+    return x;
+}
+
+// Sum over groups of `width` consecutive lanes (width a power of two <= 64).
+template <int width>
+__device__ __forceinline__ double group_sum(double x)
+{
+#pragma unroll
+    for (int o = width / 2; o > 0; o >>= 1)
+        x += __shfl_xor(x, o, kWave);
+    return x;
+}
+
+// Block sum for a block of NT threads; result valid in every thread.
+// `scratch` must hold NT / 64 doubles.  Order: wave butterflies, then the
+// wave partials in ascending wave order.
+template <int NT>
+__device__ __forceinline__ double block_sum(double x, double *scratch)
+{
+    constexpr int nw = NT / kWave;
+    x = wave_sum(x);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x % kWave) == 0)
+        scratch[w] = x;
+    __syncthreads();
+    double t = 0.0;
+#pragma unroll
+    for (int i = 0; i < nw; ++i)
+        t += scratch[i];
+    __syncthreads();
+    return t;
+}
+
+template <int NT>
+__device__ __forceinline__ double block_max(double x, double *scratch)
+{
+    constexpr int nw = NT / kWave;
+    x = wave_max(x);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x % kWave) == 0)
+        scratch[w] = x;
+    __syncthreads();
+    double t = scratch[0];
+#pragma unroll
+    for (int i = 1; i < nw; ++i)
+        t = fmax(t, scratch[i]);
+    __syncthreads();
+    return t;
+}
+
+// ---------------------------------------------------- power-iteration state
+// Device-side stop control shared by the product, reduction and update
+// kernels of one update t.  The statistic of update t lives in
+// stat_ring[t % ring]; the product kernel of update t clears that slot
+// (block 0) and every kernel of update t is skipped when the statistic of
+// update t-1 already satisfied the stop test, or a numeric error was
+// flagged.  Skipped updates leave their slot at 0, so the chain of skips
+// continues to the end of the launched batch.
+struct StopCtl {
+    const double *prev_stat; // slot of update t-1, or nullptr (no test)
+    double *cur_stat;        // slot of update t
+    double eps;              // stop precision (< 0 in FIXED mode: never)
+    int *err;                // numeric error flag (tau zero / not finite)
+};
+
+__device__ __forceinline__ bool stop_reached(const StopCtl &c)
+{
+    if (*c.err != 0)
+        return true;
+    return c.prev_stat != nullptr && *c.prev_stat <= c.eps;
+}
+
+// --------------------------------------------------------------- launchers
+// Host-side launch wrappers implemented in the kernel translation units.
+// Each returns hipSuccess or the launch error.
+const char *last_error_text();
+
+// affinity.hip
+hipError_t launch_affinity(const float *X, int64_t n, int d, float c_log2,
+                           float *A, int64_t lda, double *degree,
+                           hipStream_t s);
+hipError_t launch_fused_degree(const float *X, int64_t n, int d, float c_log2,
+                               double *degree, hipStream_t s);
+hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c_log2,
+                              const double *v, const double *degree, double *y,
+                              double *partial, StopCtl ctl, bool use_ctl,
+                              hipStream_t s);
+int64_t fused_blocks(int64_t n, int d);
+
+// normalize.hip
+hipError_t launch_dense_degree(const float *A, int64_t n, int64_t lda,
+                               double *degree, hipStream_t s);
+hipError_t launch_dense_scale(float *A, int64_t n, int64_t lda,
+                              const double *degree, hipStream_t s);
+hipError_t launch_csr_degree_scale(const int64_t *row_ptr, float *val,
+                                   int64_t n, double *degree, hipStream_t s);
+size_t start_vector_ws(int64_t n);
+// Sum of degrees, zero-row count and v0 = d / sum(d); synchronises the
+// stream and reports a zero / non-finite sum through *bad_host.
+hipError_t launch_start_vector(const double *degree, int64_t n, double *v0,
+                               int64_t *n_zero, void *ws, hipStream_t s,
+                               int *bad_host);
+// Structural check of a CSR graph; synchronises, *bad_host = 1 if invalid.
+hipError_t launch_csr_check(const int64_t *row_ptr, const int32_t *col,
+                            int64_t n, int64_t nnz, int *flag, hipStream_t s,
+                            int *bad_host);
+
+// power.hip
+int64_t gemv_blocks(int64_t n);
+int64_t spmv_blocks(int64_t n);
+hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
+                       double *y, double *partial, StopCtl ctl, bool use_ctl,
+                       hipStream_t s);
+hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
+                       const float *val, int64_t n, const double *v, double *y,
+                       double *partial, StopCtl ctl, bool use_ctl,
+                       hipStream_t s);
+hipError_t launch_reduce_tau(const double *partial, int64_t nb, double *tau,
+                             StopCtl ctl, hipStream_t s);
+hipError_t launch_update(const double *y, const double *tau, double *v,
+                         double *delta, int64_t n, StopCtl ctl, hipStream_t s);
+hipError_t launch_init_state(double *ring, int64_t ring_len, int *err,
+                             const double *v, double *delta, int64_t n,
+                             bool copy_delta, hipStream_t s);
+
+// kmeans.hip
+size_t kmeans_ws(int64_t n, int32_t k);
+// Runs the whole exact 1-D k-means; synchronises the stream.
+hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
+                        double *centroids, int32_t *k_eff, double *cost,
+                        void *ws, hipStream_t s);
+
+} // namespace gpic

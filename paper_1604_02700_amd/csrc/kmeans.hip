@@ -1,0 +1,634 @@
+// Exact one-dimensional k-means for gfx950: the "k-means of v" step that
+// ends Algorithms 1 and 2, read as the minimum within-cluster sum of
+// squares partition of the scalars v_i.
+//
+// Steps (all deterministic):
+//   1. order-preserving 64-bit keys of v, stable LSD radix sort (8 passes of
+//      8 bits) of (key, index) pairs: tile histograms, one exclusive scan,
+//      stable scatter with in-wave ranks from ballots;
+//   2. run starts of equal values (a cluster never splits equal values),
+//      their count, the mean, and float64 prefix sums S1, S2 of the centred
+//      values u = v_sorted - mean;
+//   3. dynamic programme over layers c = 1..k_eff-1:
+//        D_c(i) = min_{j <= i, j starts a run} D_{c-1}(j-1) + cost(j, i),
+//        cost(j, i) = max(0, (S2[i+1]-S2[j]) - (S1[i+1]-S1[j])^2 / (i-j+1)),
+//      with the leftmost argmin; split points are monotone in i (quadrangle
+//      inequality of the 1-D within-cluster sum of squares), so each layer
+//      is solved by divide and conquer, one launch per recursion level;
+//   4. backtrack, per-cluster means and sums of squares, labels by
+//      ascending centroid.
+#include "common.h"
+
+namespace gpic {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kItems = 16;
+constexpr int kTile = kThreads * kItems;   // elements per sort / scan tile
+constexpr int kRadix = 256;
+
+__host__ __device__ inline int64_t tiles(int64_t n) { return (n + kTile - 1) / kTile; }
+
+__device__ __forceinline__ uint64_t to_key(double x)
+{
+    if (x == 0.0)
+        x = 0.0;                       // -0 and +0 are equal values
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+
+__device__ __forceinline__ double from_key(uint64_t k)
+{
+    const uint64_t b = (k >> 63) ? (k & 0x7fffffffffffffffull) : ~k;
+    return __longlong_as_double((long long)b);
+}
+
+__global__ __launch_bounds__(kThreads) void make_keys_kernel(
+    const double *__restrict__ v, int64_t n, uint64_t *__restrict__ key,
+    int32_t *__restrict__ idx)
+{
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) {
+        key[i] = to_key(v[i]);
+        idx[i] = (int32_t)i;
+    }
+}
+
+// hist[digit * ntiles + tile]
+__global__ __launch_bounds__(kThreads) void radix_hist_kernel(
+    const uint64_t *__restrict__ key, int64_t n, int shift,
+    uint32_t *__restrict__ hist)
+{
+    __shared__ uint32_t h[kRadix];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kTile;
+    for (int it = 0; it < kItems; ++it) {
+        const int64_t i = base + it * kThreads + threadIdx.x;
+        if (i < n)
+            atomicAdd(&h[(key[i] >> shift) & 0xff], 1u);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * gridDim.x + blockIdx.x] = h[threadIdx.x];
+}
+
+// Exclusive scan of m uint32 counts, in place, by one workgroup of 1024.
+__global__ __launch_bounds__(1024) void scan_counts_kernel(uint32_t *__restrict__ a,
+                                                           int64_t m)
+{
+    __shared__ uint32_t s[1024];
+    const int64_t per = (m + 1023) / 1024;
+    const int64_t b = threadIdx.x * per;
+    const int64_t e = (b + per < m) ? b + per : m;
+    uint32_t tot = 0;
+    for (int64_t i = b; i < e; ++i)
+        tot += a[i];
+    s[threadIdx.x] = tot;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+        const uint32_t x = (threadIdx.x >= (unsigned)o) ? s[threadIdx.x - o] : 0u;
+        __syncthreads();
+        s[threadIdx.x] += x;
+        __syncthreads();
+    }
+    uint32_t run = s[threadIdx.x] - tot;
+    for (int64_t i = b; i < e; ++i) {
+        const uint32_t x = a[i];
+        a[i] = run;
+        run += x;
+    }
+}
+
+// Stable scatter of one tile.  Element order inside a tile is
+// (item, thread); for every item the 256 elements are ranked inside their
+// wave with ballots over the 8 digit bits, and across waves with per-wave
+// digit counts in LDS.
+__global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
+    const uint64_t *__restrict__ kin, const int32_t *__restrict__ iin,
+    uint64_t *__restrict__ kout, int32_t *__restrict__ iout, int64_t n,
+    int shift, const uint32_t *__restrict__ offs)
+{
+    constexpr int nw = kThreads / kWave;
+    __shared__ uint32_t base[kRadix];
+    __shared__ uint32_t wc[nw][kRadix];
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    base[threadIdx.x] = offs[(int64_t)threadIdx.x * gridDim.x + blockIdx.x];
+    for (int w = 0; w < nw; ++w)
+        wc[w][threadIdx.x] = 0;
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int64_t tb = (int64_t)blockIdx.x * kTile;
+    for (int it = 0; it < kItems; ++it) {
+        const int64_t i = tb + it * kThreads + threadIdx.x;
+        const bool live = i < n;
+        uint64_t k = 0;
+        int32_t ix = 0;
+        int dg = 0;
+        if (live) {
+            k = kin[i];
+            ix = iin[i];
+            dg = (int)((k >> shift) & 0xff);
+        }
+        uint64_t peers = __ballot(live);
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+            const uint64_t bb = __ballot((dg >> bit) & 1);
+            peers &= ((dg >> bit) & 1) ? bb : ~bb;
+        }
+        const uint32_t rank = (uint32_t)__popcll(peers & lt);
+        const uint32_t cnt = (uint32_t)__popcll(peers);
+        const bool leader = live && (peers & lt) == 0;
+        if (leader)
+            wc[wave][dg] = cnt;
+        __syncthreads();
+        if (live) {
+            uint32_t pos = base[dg] + rank;
+            for (int w = 0; w < wave; ++w)
+                pos += wc[w][dg];
+            kout[pos] = k;
+            iout[pos] = ix;
+        }
+        __syncthreads();
+        uint32_t add = 0;
+        for (int w = 0; w < nw; ++w) {
+            add += wc[w][threadIdx.x];
+            wc[w][threadIdx.x] = 0;
+        }
+        base[threadIdx.x] += add;
+        __syncthreads();
+    }
+}
+
+// Sorted values, run starts, and per-tile sums of values and run starts.
+__global__ __launch_bounds__(kThreads) void decode_kernel(
+    const uint64_t *__restrict__ key, int64_t n, double *__restrict__ sv,
+    int32_t *__restrict__ run, double *__restrict__ tsum,
+    double *__restrict__ truns)
+{
+    __shared__ double red[kThreads / kWave];
+    const int64_t tb = (int64_t)blockIdx.x * kTile;
+    double s = 0.0, r = 0.0;
+    for (int it = 0; it < kItems; ++it) {
+        const int64_t i = tb + it * kThreads + threadIdx.x;
+        if (i < n) {
+            const uint64_t k = key[i];
+            const double x = from_key(k);
+            sv[i] = x;
+            const int st = (i == 0) || (key[i - 1] != k);
+            run[i] = st;
+            s += x;
+            r += st;
+        }
+    }
+    const double ts = block_sum<kThreads>(s, red);
+    const double tr = block_sum<kThreads>(r, red);
+    if (threadIdx.x == 0) {
+        tsum[blockIdx.x] = ts;
+        truns[blockIdx.x] = tr;
+    }
+}
+
+struct KmScalars {
+    double mean;
+    double distinct;
+};
+
+__global__ __launch_bounds__(1024) void totals_kernel(
+    const double *__restrict__ tsum, const double *__restrict__ truns,
+    int64_t nt, int64_t n, KmScalars *__restrict__ sc)
+{
+    __shared__ double red[1024 / kWave];
+    double s = 0.0, r = 0.0;
+    for (int64_t b = threadIdx.x; b < nt; b += 1024) {
+        s += tsum[b];
+        r += truns[b];
+    }
+    const double ts = block_sum<1024>(s, red);
+    const double tr = block_sum<1024>(r, red);
+    if (threadIdx.x == 0) {
+        sc->mean = ts / (double)n;
+        sc->distinct = tr;
+    }
+}
+
+// Per-tile totals of u and u^2 (u = value - mean), each thread summing its
+// kItems consecutive elements.
+__global__ __launch_bounds__(kThreads) void tile_moments_kernel(
+    const double *__restrict__ sv, int64_t n, const KmScalars *__restrict__ sc,
+    double *__restrict__ t1, double *__restrict__ t2)
+{
+    __shared__ double red[kThreads / kWave];
+    const double mu = sc->mean;
+    const int64_t b = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+    double s1 = 0.0, s2 = 0.0;
+    for (int it = 0; it < kItems; ++it) {
+        const int64_t i = b + it;
+        if (i < n) {
+            const double u = sv[i] - mu;
+            s1 += u;
+            s2 += u * u;
+        }
+    }
+    // thread totals in thread order: serial over the block's 256 totals
+    __shared__ double a1[kThreads], a2[kThreads];
+    a1[threadIdx.x] = s1;
+    a2[threadIdx.x] = s2;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double x1 = 0.0, x2 = 0.0;
+        for (int t = 0; t < kThreads; ++t) {
+            x1 += a1[t];
+            x2 += a2[t];
+        }
+        t1[blockIdx.x] = x1;
+        t2[blockIdx.x] = x2;
+    }
+    (void)red;
+}
+
+// Exclusive scan of the tile totals (serial: there are few tiles).
+__global__ void scan_tiles_kernel(double *__restrict__ t1, double *__restrict__ t2,
+                                  int64_t nt)
+{
+    if (threadIdx.x != 0)
+        return;
+    double r1 = 0.0, r2 = 0.0;
+    for (int64_t b = 0; b < nt; ++b) {
+        const double x1 = t1[b], x2 = t2[b];
+        t1[b] = r1;
+        t2[b] = r2;
+        r1 += x1;
+        r2 += x2;
+    }
+}
+
+// S1[i+1], S2[i+1] = tile offset + in-tile running sums (each thread walks
+// its kItems elements after an exclusive scan of the thread totals).
+__global__ __launch_bounds__(kThreads) void prefix_kernel(
+    const double *__restrict__ sv, int64_t n, const KmScalars *__restrict__ sc,
+    const double *__restrict__ o1, const double *__restrict__ o2,
+    double *__restrict__ S1, double *__restrict__ S2)
+{
+    __shared__ double a1[kThreads], a2[kThreads];
+    const double mu = sc->mean;
+    const int64_t b = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+    double s1 = 0.0, s2 = 0.0;
+    for (int it = 0; it < kItems; ++it) {
+        const int64_t i = b + it;
+        if (i < n) {
+            const double u = sv[i] - mu;
+            s1 += u;
+            s2 += u * u;
+        }
+    }
+    a1[threadIdx.x] = s1;
+    a2[threadIdx.x] = s2;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double r1 = o1[blockIdx.x], r2 = o2[blockIdx.x];
+        for (int t = 0; t < kThreads; ++t) {
+            const double x1 = a1[t], x2 = a2[t];
+            a1[t] = r1;
+            a2[t] = r2;
+            r1 += x1;
+            r2 += x2;
+        }
+    }
+    __syncthreads();
+    double r1 = a1[threadIdx.x], r2 = a2[threadIdx.x];
+    for (int it = 0; it < kItems; ++it) {
+        const int64_t i = b + it;
+        if (i < n) {
+            const double u = sv[i] - mu;
+            r1 += u;
+            r2 += u * u;
+            S1[i + 1] = r1;
+            S2[i + 1] = r2;
+        }
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        S1[0] = 0.0;
+        S2[0] = 0.0;
+    }
+}
+
+__device__ __forceinline__ double seg_cost(const double *__restrict__ S1,
+                                           const double *__restrict__ S2,
+                                           int64_t j, int64_t i)
+{
+    const double m = (double)(i - j + 1);
+    const double s1 = S1[i + 1] - S1[j];
+    const double s2 = S2[i + 1] - S2[j];
+    const double c = s2 - s1 * s1 / m;
+    return c > 0.0 ? c : 0.0;
+}
+
+__global__ __launch_bounds__(kThreads) void first_layer_kernel(
+    const double *__restrict__ S1, const double *__restrict__ S2, int64_t n,
+    double *__restrict__ D)
+{
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n)
+        D[i] = seg_cost(S1, S2, 0, i);
+}
+
+// Node q of recursion level L over rows [0, n-1]: returns false if empty.
+__device__ __forceinline__ bool dc_node(int64_t n, int L, int64_t q, int64_t &lo,
+                                        int64_t &hi)
+{
+    lo = 0;
+    hi = n - 1;
+    for (int b = L - 1; b >= 0; --b) {
+        if (lo > hi)
+            return false;
+        const int64_t mid = lo + (hi - lo) / 2;
+        if ((q >> b) & 1)
+            lo = mid + 1;
+        else
+            hi = mid - 1;
+    }
+    return lo <= hi;
+}
+
+// Leftmost-argmin merge of (value, index) pairs.
+__device__ __forceinline__ void amin_merge(double &b, int64_t &a, double ob,
+                                           int64_t oa)
+{
+    if (ob < b || (ob == b && oa < a)) {
+        b = ob;
+        a = oa;
+    }
+}
+
+// One recursion level of one layer.  G threads per node (G = 256: one
+// workgroup per node; G = 64: one wave per node).
+template <int G>
+__global__ __launch_bounds__(kThreads) void dc_level_kernel(
+    const double *__restrict__ S1, const double *__restrict__ S2,
+    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
+    double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
+    int64_t nodes)
+{
+    constexpr int per_block = kThreads / G;
+    __shared__ double rb[kThreads / kWave];
+    __shared__ int64_t ra[kThreads / kWave];
+    const int64_t q = (int64_t)blockIdx.x * per_block + threadIdx.x / G;
+    const int t = threadIdx.x % G;
+    int64_t lo = 0, hi = -1;
+    const bool live = q < nodes && dc_node(n, L, q, lo, hi);
+    double best = INFINITY;
+    int64_t arg = INT64_MAX;
+    int64_t mid = 0, alo = 1;
+    if (live) {
+        mid = lo + (hi - lo) / 2;
+        const int64_t olo = (lo > 0) ? (int64_t)opt[lo - 1] : 1;
+        const int64_t ohi = (hi < n - 1) ? (int64_t)opt[hi + 1] : n - 1;
+        alo = olo < 1 ? 1 : olo;
+        const int64_t ahi = ohi < mid ? ohi : mid;
+        for (int64_t j = alo + t; j <= ahi; j += G) {
+            if (!run[j])
+                continue;
+            const double c = Dprev[j - 1] + seg_cost(S1, S2, j, mid);
+            if (c < best) {
+                best = c;
+                arg = j;
+            }
+        }
+    }
+    // reduce within the node's group of G lanes
+#pragma unroll
+    for (int o = (G < kWave ? G : kWave) / 2; o > 0; o >>= 1) {
+        const double ob = __shfl_xor(best, o, kWave);
+        const int64_t oa = __shfl_xor(arg, o, kWave);
+        amin_merge(best, arg, ob, oa);
+    }
+    if (G > kWave) {
+        const int w = threadIdx.x / kWave;
+        if ((threadIdx.x % kWave) == 0) {
+            rb[w] = best;
+            ra[w] = arg;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            for (int i = 1; i < kThreads / kWave; ++i)
+                amin_merge(best, arg, rb[i], ra[i]);
+        }
+    }
+    if (live && t == 0) {
+        Dcur[mid] = best;
+        opt[mid] = (int32_t)((arg == INT64_MAX) ? alo : arg);
+    }
+}
+
+__global__ void backtrack_kernel(const int32_t *__restrict__ opt, int64_t n,
+                                 int ke, int64_t *__restrict__ first)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0)
+        return;
+    int64_t i = n - 1;
+    for (int c = ke - 1; c >= 1; --c) {
+        const int64_t j = opt[(int64_t)c * n + i];
+        first[c] = j;
+        i = j - 1;
+    }
+    first[0] = 0;
+    first[ke] = n;
+}
+
+// One workgroup per cluster: mean (sum in a fixed order / count) and the
+// sum of squared deviations from it.
+__global__ __launch_bounds__(kThreads) void cluster_stats_kernel(
+    const double *__restrict__ sv, const int64_t *__restrict__ first,
+    double *__restrict__ centroids, double *__restrict__ costs)
+{
+    __shared__ double red[kThreads / kWave];
+    const int c = blockIdx.x;
+    const int64_t b = first[c], e = first[c + 1];
+    double s = 0.0;
+    for (int64_t p = b + threadIdx.x; p < e; p += kThreads)
+        s += sv[p];
+    const double mu = block_sum<kThreads>(s, red) / (double)(e - b);
+    double q = 0.0;
+    for (int64_t p = b + threadIdx.x; p < e; p += kThreads)
+        q += (sv[p] - mu) * (sv[p] - mu);
+    const double tq = block_sum<kThreads>(q, red);
+    if (threadIdx.x == 0) {
+        centroids[c] = mu;
+        costs[c] = tq;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void labels_kernel(
+    const int32_t *__restrict__ idx, int64_t n, const int64_t *__restrict__ first,
+    int ke, int32_t *__restrict__ labels)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= n)
+        return;
+    int lo = 0, hi = ke - 1;        // last c with first[c] <= p
+    while (lo < hi) {
+        const int m = (lo + hi + 1) / 2;
+        if (first[m] <= p)
+            lo = m;
+        else
+            hi = m - 1;
+    }
+    labels[idx[p]] = lo;
+}
+
+inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct KmLayout {
+    size_t keyA, keyB, idxA, idxB, hist, sv, run, t1, t2, S1, S2, Da, Db, opt,
+        sc, first, costs, total;
+};
+
+KmLayout layout(int64_t n, int32_t k)
+{
+    KmLayout L{};
+    const int64_t nt = tiles(n);
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += al(bytes);
+        return at;
+    };
+    L.keyA = take(n * 8);
+    L.keyB = take(n * 8);
+    L.idxA = take(n * 4);
+    L.idxB = take(n * 4);
+    L.hist = take((size_t)kRadix * nt * 4);
+    L.sv = take(n * 8);
+    L.run = take(n * 4);
+    L.t1 = take(nt * 8);
+    L.t2 = take(nt * 8);
+    L.S1 = take((n + 1) * 8);
+    L.S2 = take((n + 1) * 8);
+    L.Da = take(n * 8);
+    L.Db = take(n * 8);
+    L.opt = take((size_t)k * n * 4);
+    L.sc = take(sizeof(KmScalars));
+    L.first = take((size_t)(k + 1) * 8);
+    L.costs = take((size_t)k * 8);
+    L.total = o;
+    return L;
+}
+
+unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
+
+} // namespace
+
+size_t kmeans_ws(int64_t n, int32_t k) { return layout(n, k).total; }
+
+#define GPIC_TRY(x)                                                            \
+    do {                                                                       \
+        hipError_t e_ = (x);                                                   \
+        if (e_ != hipSuccess)                                                  \
+            return e_;                                                         \
+    } while (0)
+
+hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
+                        double *centroids, int32_t *k_eff, double *cost,
+                        void *ws, hipStream_t s)
+{
+    const KmLayout L = layout(n, k);
+    char *w = static_cast<char *>(ws);
+    uint64_t *keyA = (uint64_t *)(w + L.keyA), *keyB = (uint64_t *)(w + L.keyB);
+    int32_t *idxA = (int32_t *)(w + L.idxA), *idxB = (int32_t *)(w + L.idxB);
+    uint32_t *hist = (uint32_t *)(w + L.hist);
+    double *sv = (double *)(w + L.sv);
+    int32_t *run = (int32_t *)(w + L.run);
+    double *t1 = (double *)(w + L.t1), *t2 = (double *)(w + L.t2);
+    double *S1 = (double *)(w + L.S1), *S2 = (double *)(w + L.S2);
+    double *Da = (double *)(w + L.Da), *Db = (double *)(w + L.Db);
+    int32_t *opt = (int32_t *)(w + L.opt);
+    KmScalars *sc = (KmScalars *)(w + L.sc);
+    int64_t *first = (int64_t *)(w + L.first);
+    double *costs = (double *)(w + L.costs);
+    const int64_t nt = tiles(n);
+
+    // 1. radix sort
+    hipLaunchKernelGGL(make_keys_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
+                       v, n, keyA, idxA);
+    for (int pass = 0; pass < 8; ++pass) {
+        const int shift = 8 * pass;
+        hipLaunchKernelGGL(radix_hist_kernel, dim3((unsigned)nt), dim3(kThreads), 0,
+                           s, keyA, n, shift, hist);
+        hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(1024), 0, s, hist,
+                           (int64_t)kRadix * nt);
+        hipLaunchKernelGGL(radix_scatter_kernel, dim3((unsigned)nt), dim3(kThreads),
+                           0, s, keyA, idxA, keyB, idxB, n, shift, hist);
+        uint64_t *tk = keyA; keyA = keyB; keyB = tk;
+        int32_t *ti = idxA; idxA = idxB; idxB = ti;
+    }
+    GPIC_TRY(hipGetLastError());
+
+    // 2. values, runs, mean, prefix sums
+    hipLaunchKernelGGL(decode_kernel, dim3((unsigned)nt), dim3(kThreads), 0, s, keyA,
+                       n, sv, run, t1, t2);
+    hipLaunchKernelGGL(totals_kernel, dim3(1), dim3(1024), 0, s, t1, t2, nt, n, sc);
+    hipLaunchKernelGGL(tile_moments_kernel, dim3((unsigned)nt), dim3(kThreads), 0, s,
+                       sv, n, sc, t1, t2);
+    hipLaunchKernelGGL(scan_tiles_kernel, dim3(1), dim3(64), 0, s, t1, t2, nt);
+    hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)nt), dim3(kThreads), 0, s, sv,
+                       n, sc, t1, t2, S1, S2);
+    GPIC_TRY(hipGetLastError());
+    KmScalars hsc{};
+    GPIC_TRY(hipMemcpyAsync(&hsc, sc, sizeof(hsc), hipMemcpyDeviceToHost, s));
+    GPIC_TRY(hipStreamSynchronize(s));
+    const int64_t distinct = (int64_t)hsc.distinct;
+    const int ke = (int)((int64_t)k < distinct ? k : distinct);
+
+    // 3. layers
+    hipLaunchKernelGGL(first_layer_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
+                       S1, S2, n, Da);
+    int levels = 0;
+    while (levels < 63 && ((int64_t)1 << levels) <= n)
+        ++levels;
+    double *Dprev = Da, *Dcur = Db;
+    for (int c = 1; c < ke; ++c) {
+        int32_t *oc = opt + (int64_t)c * n;
+        for (int Lv = 0; Lv < levels; ++Lv) {
+            const int64_t nodes = (int64_t)1 << Lv;
+            if (nodes <= 2048) {
+                hipLaunchKernelGGL(dc_level_kernel<kThreads>, dim3((unsigned)nodes),
+                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur,
+                                   oc, n, Lv, nodes);
+            } else {
+                const int64_t per = kThreads / kWave;
+                hipLaunchKernelGGL(dc_level_kernel<kWave>,
+                                   dim3((unsigned)((nodes + per - 1) / per)),
+                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur,
+                                   oc, n, Lv, nodes);
+            }
+        }
+        double *tmp = Dprev; Dprev = Dcur; Dcur = tmp;
+    }
+    GPIC_TRY(hipGetLastError());
+
+    // 4. boundaries, cluster statistics, labels
+    hipLaunchKernelGGL(backtrack_kernel, dim3(1), dim3(64), 0, s, opt, n, ke, first);
+    hipLaunchKernelGGL(cluster_stats_kernel, dim3((unsigned)ke), dim3(kThreads), 0, s,
+                       sv, first, centroids, costs);
+    hipLaunchKernelGGL(labels_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, idxA,
+                       n, first, ke, labels);
+    GPIC_TRY(hipGetLastError());
+    double hc[1024];
+    double total = 0.0;
+    for (int c0 = 0; c0 < ke; c0 += 1024) {
+        const int m = (ke - c0 < 1024) ? ke - c0 : 1024;
+        GPIC_TRY(hipMemcpyAsync(hc, costs + c0, m * sizeof(double),
+                                hipMemcpyDeviceToHost, s));
+        GPIC_TRY(hipStreamSynchronize(s));
+        for (int c = 0; c < m; ++c)
+            total += hc[c];
+    }
+    GPIC_TRY(hipStreamSynchronize(s));
+    *k_eff = ke;
+    if (cost != nullptr)
+        *cost = total;
+    return hipSuccess;
+}
+
+} // namespace gpic

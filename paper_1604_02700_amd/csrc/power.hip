@@ -1,0 +1,269 @@
+// Power-iteration kernels for gfx950: the product y = W v (dense, CSR),
+// the L1 norm tau = sum_i |y_i|, and the update
+//   v_{t+1} = y / tau,  delta_{t+1} = |v_{t+1} - v_t|,
+//   s_t = max_i |delta_{t+1,i} - delta_{t,i}|
+// of Algorithm 1 (update equation of section "Power Iteration Clustering:
+// An Overview"; the Multiply, Reduction and Norm steps of Algorithm 2's loop
+// and its stop test).
+//
+// One update is three launches on the caller's stream: product (writes y and
+// per-block partial sums of |y_i|), tau (one workgroup sums the partials in
+// ascending block order), update (grid-wide; block maxima of the statistic
+// are combined with an integer atomic max on the bit pattern of the
+// non-negative float64, which is order-free and therefore deterministic).
+#include "common.h"
+
+namespace gpic {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kGemvRows = 8;        // rows per workgroup of the dense product
+constexpr int kSpmvLanes = 16;      // lanes per CSR row
+constexpr int kSpmvRows = 128;      // rows per workgroup of the CSR product
+
+// Dense product.  A workgroup owns kGemvRows consecutive rows; every thread
+// takes float4 column groups c, c + 256, ... and keeps one float64
+// accumulator per row, so each 32-byte slice of v it loads is reused across
+// all rows of the block.  Rows past n are clamped for loading and never
+// written.
+template <int R>
+__global__ __launch_bounds__(kThreads) void gemv_kernel(
+    const float *__restrict__ W, int64_t n, int64_t ldw,
+    const double *__restrict__ v, double *__restrict__ y,
+    double *__restrict__ partial, StopCtl ctl, int use_ctl)
+{
+    __shared__ double red[R][kThreads / kWave];
+    if (use_ctl) {
+        if (blockIdx.x == 0 && threadIdx.x == 0)
+            *ctl.cur_stat = 0.0;
+        if (stop_reached(ctl))
+            return;
+    }
+    const int64_t row0 = (int64_t)blockIdx.x * R;
+    const float4 *rp[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t i = (row0 + r < n) ? row0 + r : n - 1;
+        rp[r] = reinterpret_cast<const float4 *>(W + i * ldw);
+    }
+    double acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        acc[r] = 0.0;
+
+    const int64_t n4 = n >> 2;
+    const double2 *v2 = reinterpret_cast<const double2 *>(v);
+#pragma unroll 2
+    for (int64_t c = threadIdx.x; c < n4; c += kThreads) {
+        float4 w[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            w[r] = rp[r][c];
+        const double2 va = v2[2 * c];
+        const double2 vb = v2[2 * c + 1];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            acc[r] = fma((double)w[r].x, va.x, acc[r]);
+            acc[r] = fma((double)w[r].y, va.y, acc[r]);
+            acc[r] = fma((double)w[r].z, vb.x, acc[r]);
+            acc[r] = fma((double)w[r].w, vb.y, acc[r]);
+        }
+    }
+    const int64_t tail = n - (n4 << 2);
+    if (threadIdx.x < tail) {
+        const int64_t j = (n4 << 2) + threadIdx.x;
+        const double vj = v[j];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const float *row = reinterpret_cast<const float *>(rp[r]);
+            acc[r] = fma((double)row[j], vj, acc[r]);
+        }
+    }
+    const int wave = threadIdx.x / kWave;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const double t = wave_sum(acc[r]);
+        if ((threadIdx.x % kWave) == 0)
+            red[r][wave] = t;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double part = 0.0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            double t = 0.0;
+#pragma unroll
+            for (int w = 0; w < kThreads / kWave; ++w)
+                t += red[r][w];
+            if (row0 + r < n) {
+                y[row0 + r] = t;
+                part += fabs(t);
+            }
+        }
+        if (partial != nullptr)
+            partial[blockIdx.x] = part;
+    }
+}
+
+// CSR product: 16 lanes per row, lane-strided over the row's entries, a
+// 16-lane butterfly per row; a workgroup walks kSpmvRows rows in passes of
+// 16.
+__global__ __launch_bounds__(kThreads) void spmv_kernel(
+    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    const float *__restrict__ val, int64_t n, const double *__restrict__ v,
+    double *__restrict__ y, double *__restrict__ partial, StopCtl ctl,
+    int use_ctl)
+{
+    __shared__ double red[kThreads / kWave];
+    if (use_ctl) {
+        if (blockIdx.x == 0 && threadIdx.x == 0)
+            *ctl.cur_stat = 0.0;
+        if (stop_reached(ctl))
+            return;
+    }
+    const int sl = threadIdx.x % kSpmvLanes;
+    const int grp = threadIdx.x / kSpmvLanes;
+    constexpr int groups = kThreads / kSpmvLanes;
+    double part = 0.0;
+    for (int pass = 0; pass < kSpmvRows / groups; ++pass) {
+        const int64_t i = (int64_t)blockIdx.x * kSpmvRows + pass * groups + grp;
+        double s = 0.0;
+        if (i < n) {
+            const int64_t b = row_ptr[i], e = row_ptr[i + 1];
+            for (int64_t p = b + sl; p < e; p += kSpmvLanes)
+                s = fma((double)val[p], v[col[p]], s);
+        }
+        s = group_sum<kSpmvLanes>(s);
+        if (i < n && sl == 0) {
+            y[i] = s;
+            part += fabs(s);
+        }
+    }
+    const double t = block_sum<kThreads>(part, red);
+    if (threadIdx.x == 0 && partial != nullptr)
+        partial[blockIdx.x] = t;
+}
+
+// tau = sum of the block partials, by one workgroup in a fixed order.
+__global__ __launch_bounds__(1024) void reduce_tau_kernel(
+    const double *__restrict__ partial, int64_t nb, double *__restrict__ tau,
+    StopCtl ctl)
+{
+    __shared__ double red[1024 / kWave];
+    if (stop_reached(ctl))
+        return;
+    double s = 0.0;
+    for (int64_t b = threadIdx.x; b < nb; b += 1024)
+        s += partial[b];
+    const double t = block_sum<1024>(s, red);
+    if (threadIdx.x == 0) {
+        *tau = t;
+        if (!(t > 0.0) || !isfinite(t))
+            *ctl.err = 1;
+    }
+}
+
+// v <- y / tau, delta <- |v_new - v_old|, statistic = max |delta_new - delta|.
+__global__ __launch_bounds__(kThreads) void update_kernel(
+    const double *__restrict__ y, const double *__restrict__ tau,
+    double *__restrict__ v, double *__restrict__ delta, int64_t n, StopCtl ctl)
+{
+    __shared__ double red[kThreads / kWave];
+    if (stop_reached(ctl))
+        return;
+    const double t = *tau;
+    double s = 0.0;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+         i += stride) {
+        const double vn = y[i] / t;
+        const double dn = fabs(vn - v[i]);
+        s = fmax(s, fabs(dn - delta[i]));
+        v[i] = vn;
+        delta[i] = dn;
+    }
+    const double m = block_max<kThreads>(s, red);
+    if (threadIdx.x == 0)
+        atomicMax(reinterpret_cast<unsigned long long *>(ctl.cur_stat),
+                  (unsigned long long)__double_as_longlong(m));
+}
+
+__global__ __launch_bounds__(kThreads) void init_state_kernel(
+    double *__restrict__ ring, int64_t ring_len, int *__restrict__ err,
+    const double *__restrict__ v, double *__restrict__ delta, int64_t n,
+    int copy_delta)
+{
+    const int64_t t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    if (t0 == 0)
+        *err = 0;
+    for (int64_t i = t0; i < ring_len; i += stride)
+        ring[i] = 0.0;
+    if (copy_delta)
+        for (int64_t i = t0; i < n; i += stride)
+            delta[i] = v[i];
+}
+
+unsigned grid_for(int64_t n, int64_t cap)
+{
+    int64_t b = (n + kThreads - 1) / kThreads;
+    if (b > cap)
+        b = cap;
+    if (b < 1)
+        b = 1;
+    return (unsigned)b;
+}
+
+} // namespace
+
+int64_t gemv_blocks(int64_t n) { return (n + kGemvRows - 1) / kGemvRows; }
+int64_t spmv_blocks(int64_t n) { return (n + kSpmvRows - 1) / kSpmvRows; }
+
+hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
+                       double *y, double *partial, StopCtl ctl, bool use_ctl,
+                       hipStream_t s)
+{
+    hipLaunchKernelGGL(gemv_kernel<kGemvRows>, dim3((unsigned)gemv_blocks(n)),
+                       dim3(kThreads), 0, s, W, n, ldw, v, y, partial, ctl,
+                       use_ctl ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
+                       const float *val, int64_t n, const double *v, double *y,
+                       double *partial, StopCtl ctl, bool use_ctl, hipStream_t s)
+{
+    hipLaunchKernelGGL(spmv_kernel, dim3((unsigned)spmv_blocks(n)),
+                       dim3(kThreads), 0, s, row_ptr, col, val, n, v, y, partial,
+                       ctl, use_ctl ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_tau(const double *partial, int64_t nb, double *tau,
+                             StopCtl ctl, hipStream_t s)
+{
+    hipLaunchKernelGGL(reduce_tau_kernel, dim3(1), dim3(1024), 0, s, partial, nb,
+                       tau, ctl);
+    return hipGetLastError();
+}
+
+hipError_t launch_update(const double *y, const double *tau, double *v,
+                         double *delta, int64_t n, StopCtl ctl, hipStream_t s)
+{
+    hipLaunchKernelGGL(update_kernel, dim3(grid_for(n, 2048)), dim3(kThreads), 0,
+                       s, y, tau, v, delta, n, ctl);
+    return hipGetLastError();
+}
+
+hipError_t launch_init_state(double *ring, int64_t ring_len, int *err,
+                             const double *v, double *delta, int64_t n,
+                             bool copy_delta, hipStream_t s)
+{
+    const int64_t m = copy_delta ? (n > ring_len ? n : ring_len) : ring_len;
+    hipLaunchKernelGGL(init_state_kernel, dim3(grid_for(m, 2048)), dim3(kThreads),
+                       0, s, ring, ring_len, err, v, delta, n,
+                       copy_delta ? 1 : 0);
+    return hipGetLastError();
+}
+
+} // namespace gpic

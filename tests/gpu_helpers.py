@@ -1,0 +1,67 @@
+"""Shared helpers for the GPU parity tests (comparison metrics only)."""
+import numpy as np
+from scipy.optimize import linear_sum_assignment
+
+EPS32 = float(np.finfo(np.float32).eps)
+
+
+def rel_l1(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.abs(a - b).sum() / np.abs(b).sum())
+
+
+def matched_agreement(a, b) -> float:
+    """Label agreement after the best one-to-one matching of label ids."""
+    a = np.asarray(a)
+    b = np.asarray(b)
+    ka, kb = a.max() + 1, b.max() + 1
+    M = np.zeros((ka, kb))
+    np.add.at(M, (a, b), 1)
+    r, c = linear_sum_assignment(-M)
+    return float(M[r, c].sum() / a.shape[0])
+
+
+def separation_ok(v_oracle, v_gpu, labels_oracle, factor=100.0) -> bool:
+    """Every gap between consecutive clusters of the oracle's sorted v is at
+    least `factor` times the largest |v_gpu - v_oracle| (the guard under
+    which label agreement is a parity criterion)."""
+    v = np.asarray(v_oracle)
+    err = float(np.abs(np.asarray(v_gpu) - v).max())
+    k = labels_oracle.max() + 1
+    lo = np.array([v[labels_oracle == c].min() for c in range(k)])
+    hi = np.array([v[labels_oracle == c].max() for c in range(k)])
+    gaps = lo[1:] - hi[:-1]
+    return bool(np.all(gaps >= factor * err))
+
+
+def stop_margin(stats, eps, t_star) -> float:
+    """min over t in {t*-1, t*} (0-based update indices) of |s_t - eps| / eps."""
+    ts = [t for t in (t_star - 2, t_star - 1) if 0 <= t < len(stats)]
+    return float(min(abs(stats[t] - eps) / eps for t in ts))
+
+
+def affinity_tolerance(X, sigma, A_ref, gram: bool):
+    """Per-entry bound on |A_gpu - A_ref| from the float32 arithmetic.
+
+    Direct differences: each squared distance carries a relative error of a
+    few float32 ulps.  Gram form: |x_i|^2 + |x_j|^2 - 2 x_i.x_j carries an
+    absolute error up to about (d + 4) eps32 (|x_i|^2 + |x_j|^2), from the
+    norms and the length-d dot product.  Either error e in dist2 moves
+    A = exp(-dist2 / (2 sigma^2)) by A e / (2 sigma^2); exp2 and the final
+    rounding add a few ulps of A.
+    """
+    X64 = np.asarray(X, dtype=np.float64)
+    d = X64.shape[1]
+    s2 = 2.0 * float(sigma) ** 2
+    nrm = (X64 * X64).sum(1)
+    with np.errstate(divide="ignore"):
+        dist2 = -np.log(np.where(A_ref > 0, A_ref, 1.0)) * s2
+    if gram:
+        e = (d + 4) * EPS32 * (nrm[:, None] + nrm[None, :])
+    else:
+        e = (d + 4) * EPS32 * dist2
+    # the exponent itself is formed in float32: c * dist2 rounds once more
+    e = e + 4 * EPS32 * dist2
+    # float32 underflow: values below the smallest normal may flush to 0
+    return A_ref * e / s2 + 8 * EPS32 * A_ref + 2.4e-38

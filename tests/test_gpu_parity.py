@@ -1,0 +1,344 @@
+"""GPU parity: the HIP path through the C ABI against the oracle.
+
+Every comparison runs the same seeded inputs through both sides.  The GPU
+stores X, A and W in float32 and keeps every accumulation and the iteration
+state in float64; the oracle is float64 throughout.
+"""
+import numpy as np
+import pytest
+
+from gpu_helpers import (EPS32, affinity_tolerance, matched_agreement, rel_l1,
+                         separation_ok, stop_margin)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def g():
+    import paper_1604_02700_amd as g
+    g.lib()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return g
+
+
+DEV = "cuda:0"
+
+
+def _pts(n, d, seed, scale=1.0):
+    rng = np.random.default_rng(seed)
+    return (scale * rng.standard_normal((n, d))).astype(np.float32)
+
+
+def _t(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+# --------------------------------------------------------------- affinity
+@pytest.mark.parametrize("n,d", [(2, 2), (3, 1), (63, 2), (64, 3), (65, 15),
+                                 (1000, 2), (1023, 5), (130, 16), (257, 17),
+                                 (200, 64), (129, 40), (77, 130)])
+def test_affinity_parity(g, orc, n, d):
+    X = _pts(n, d, 1000 + n + d, scale=2.0)
+    sigma = np.float32(1.5 * np.sqrt(d))
+    print(f"affinity n={n} d={d}", flush=True)
+    A, deg = g.gpic_affinity(_t(X), sigma)
+    torch.cuda.synchronize()
+    Ag = A[:, :n].cpu().numpy().astype(np.float64)
+    Ar = orc.affinity(X, sigma)
+    gram = 16 <= d <= 128
+    tol = affinity_tolerance(X, sigma, Ar, gram)
+    err = np.abs(Ag - Ar)
+    assert np.all(np.diag(Ag) == 0.0)
+    assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
+    # degrees are the float64 sums of the stored float32 values
+    np.testing.assert_allclose(deg.cpu().numpy(), Ag.sum(1), rtol=1e-13)
+
+
+def test_affinity_padding_untouched(g):
+    n, d = 37, 2
+    X = _pts(n, d, 5)
+    A = torch.full((n, 44), -7.0, dtype=torch.float32, device=DEV)
+    g.gpic_affinity(_t(X), 1.0, A)
+    torch.cuda.synchronize()
+    assert torch.all(A[:, n:] == -7.0)
+
+
+# ------------------------------------------------------- degree / normalise
+@pytest.mark.parametrize("given", [False, True])
+def test_degree_normalize_parity(g, orc, given):
+    n, d = 777, 3
+    X = _pts(n, d, 7)
+    sigma = np.float32(1.1)
+    A, deg = g.gpic_affinity(_t(X), sigma)
+    Ag = A[:, :n].cpu().numpy().astype(np.float64)
+    W, degree, v0, nz = g.gpic_degree_normalize(A, n, deg if given else None, given)
+    torch.cuda.synchronize()
+    Wg = W[:, :n].cpu().numpy().astype(np.float64)
+    Wr, dr, v0r, nzr = orc.degree_normalize(orc.affinity(X, sigma))
+    # against the oracle's float64 chain
+    np.testing.assert_allclose(degree.cpu().numpy(), dr, rtol=2e-6)
+    np.testing.assert_allclose(v0.cpu().numpy(), v0r, rtol=4e-6)
+    np.testing.assert_allclose(Wg, Wr, rtol=4e-6, atol=1e-37)
+    # exactly what this stage computes from the stored float32 A
+    np.testing.assert_allclose(degree.cpu().numpy(), Ag.sum(1), rtol=1e-13)
+    np.testing.assert_allclose(Wg, Ag / Ag.sum(1)[:, None], rtol=2 * EPS32, atol=1e-38)
+    np.testing.assert_allclose(Wg.sum(1), 1.0, atol=n * EPS32)       # pin P1
+    assert int(nz.item()) == nzr == 0
+
+
+def test_zero_degree_rows_and_numeric_error(g):
+    X = np.array([[0, 0], [0.1, 0], [1000, 1000], [0.2, 0.1]], dtype=np.float32)
+    A, deg = g.gpic_affinity(_t(X), 0.05)
+    W, degree, v0, nz = g.gpic_degree_normalize(A, 4, deg, True)
+    torch.cuda.synchronize()
+    assert int(nz.item()) == 1 and float(v0[2]) == 0.0
+    assert torch.all(W[2, :4] == 0)
+    Z = torch.zeros((4, 4), dtype=torch.float32, device=DEV)
+    with pytest.raises(g.GpicError) as ei:
+        g.gpic_degree_normalize(Z, 4)
+    assert ei.value.status == 4
+
+
+# -------------------------------------------------------- power iteration
+def _oracle_on_fp32_W(orc, X, sigma):
+    """The oracle's W rounded once to float32 (stage isolation input)."""
+    W, deg, v0, _ = orc.degree_normalize(orc.affinity(X, sigma))
+    W32 = W.astype(np.float32)
+    return W32, v0
+
+
+@pytest.mark.parametrize("n", [5, 64, 513, 2050])
+def test_power_iteration_stage_isolation(g, orc, n):
+    """Same float32 W into both sides: only summation order differs."""
+    X = _pts(n, 2, 20 + n)
+    W32, v0 = _oracle_on_fp32_W(orc, X, 0.7)
+    Wd = torch.zeros((n, g.padded_ld(n)), dtype=torch.float32, device=DEV)
+    Wd[:, :n] = _t(W32)
+    v = _t(v0.copy())
+    out = g.gpic_power_iterate_dense(Wd, v, None, "fixed", 25, n=n)
+    ref = orc.power_iterate_dense(W32.astype(np.float64), v0, "fixed", 25)
+    assert out.iterations == 25
+    np.testing.assert_allclose(v.cpu().numpy(), ref.v, rtol=1e-11, atol=1e-300)
+    np.testing.assert_allclose(out.stats, ref.stats, rtol=1e-6, atol=1e-15)
+    # a single product
+    y = g.gpic_matvec_dense(Wd, _t(v0), n=n)
+    np.testing.assert_allclose(y.cpu().numpy(), W32.astype(np.float64) @ v0,
+                               rtol=1e-12)
+
+
+def test_power_iteration_uniform_fixed_point(g, orc):
+    """Pin P3 on the GPU: v = 1/n stops after exactly 2 products."""
+    n = 300
+    X = _pts(n, 2, 31)
+    A, deg = g.gpic_affinity(_t(X), 1.0)
+    W, _, _, _ = g.gpic_degree_normalize(A, n, deg, True)
+    v = torch.full((n,), 1.0 / n, dtype=torch.float64, device=DEV)
+    out = g.gpic_power_iterate_dense(W, v, None, "converge", 100, 1e-9, n=n)
+    assert out.converged and out.iterations == 2
+    np.testing.assert_allclose(v.cpu().numpy(), 1.0 / n, rtol=1e-6)
+    assert out.stats[0] == pytest.approx(1.0 / n, rel=1e-6)
+
+
+def test_power_iteration_resume_and_determinism(g):
+    n = 1500
+    X = _pts(n, 2, 32)
+    A, deg = g.gpic_affinity(_t(X), 0.5)
+    W, _, v0, _ = g.gpic_degree_normalize(A, n, deg, True)
+    a = v0.clone()
+    da = v0.clone()
+    r1 = g.gpic_power_iterate_dense(W, a, da, "fixed", 7, n=n)
+    r2 = g.gpic_power_iterate_dense(W, a, da, "fixed", 5, n=n)
+    b = v0.clone()
+    db = v0.clone()
+    r3 = g.gpic_power_iterate_dense(W, b, db, "fixed", 12, n=n)
+    assert torch.equal(a, b) and torch.equal(da, db)                   # P11
+    assert np.array_equal(np.concatenate([r1.stats, r2.stats]), r3.stats)
+    c = v0.clone()
+    r4 = g.gpic_power_iterate_dense(W, c, None, "fixed", 12, n=n)
+    assert torch.equal(b, c) and np.array_equal(r3.stats, r4.stats)   # bitwise repeat
+
+
+def test_power_iteration_zero_and_one_update(g):
+    n = 100
+    X = _pts(n, 2, 33)
+    A, deg = g.gpic_affinity(_t(X), 1.0)
+    W, _, v0, _ = g.gpic_degree_normalize(A, n, deg, True)
+    v = v0.clone()
+    out = g.gpic_power_iterate_dense(W, v, None, "fixed", 0, n=n)
+    assert out.iterations == 0 and torch.equal(v, v0)
+    Wn = W[:, :n].double().cpu().numpy()
+    out = g.gpic_power_iterate_dense(W, v, None, "fixed", 1, n=n)
+    y = Wn @ v0.cpu().numpy()
+    np.testing.assert_allclose(v.cpu().numpy(), y / np.abs(y).sum(), rtol=1e-12)
+
+
+def test_power_iteration_numeric_error(g):
+    n = 8
+    W = torch.zeros((n, 8), dtype=torch.float32, device=DEV)
+    v = torch.full((n,), 1.0 / n, dtype=torch.float64, device=DEV)
+    with pytest.raises(g.GpicError) as ei:
+        g.gpic_power_iterate_dense(W, v, None, "fixed", 3, n=n)
+    assert ei.value.status == 4
+
+
+# ------------------------------------------------------ end-to-end (dense)
+@pytest.mark.parametrize("name", ["blobs2d", "rings2d"])
+def test_pic_dense_converge_parity(g, orc, name):
+    import workloads
+    w = workloads.make(name)
+    print(f"pic_dense {name} n={w.n} eps={w.eps}", flush=True)
+    out = g.pic_dense(_t(w.X), w.sigma, w.k, "converge", w.max_iter, w.eps)
+    torch.cuda.synchronize()
+    ref = orc.pic_dense(w.X, w.sigma, w.k, "converge", w.max_iter, w.eps)
+    v = out.pi.v.cpu().numpy()
+    mu = stop_margin(ref.pi.stats, w.eps, ref.pi.iterations)
+    print(f"  iterations gpu={out.pi.iterations} oracle={ref.pi.iterations} "
+          f"margin={mu:.3g} rel_l1={rel_l1(v, ref.pi.v):.3e}", flush=True)
+    assert out.pi.converged and ref.pi.converged
+    assert out.pi.iterations == ref.pi.iterations
+    assert rel_l1(v, ref.pi.v) <= 1e-4
+    np.testing.assert_allclose(out.pi.stats, ref.pi.stats, rtol=1e-3, atol=1e-3 * w.eps)
+    lab = out.km.labels.cpu().numpy()
+    assert out.km.k_eff == ref.km.k_eff == w.k
+    if separation_ok(ref.pi.v, v, ref.km.labels):
+        assert matched_agreement(lab, ref.km.labels) >= 0.999
+
+
+@pytest.mark.parametrize("n", [3000, 4099])
+def test_pic_dense_fixed_T_parity_16d(g, orc, n):
+    """The 16-D blob shape (matrix-core Gram path) at reduced n, T = 50."""
+    import workloads
+    w = workloads.make("blobs16d", n=n)
+    out = g.pic_dense(_t(w.X), w.sigma, w.k, "fixed", 50)
+    torch.cuda.synchronize()
+    ref = orc.pic_dense(w.X, w.sigma, w.k, "fixed", 50)
+    v = out.pi.v.cpu().numpy()
+    assert out.pi.iterations == 50
+    assert rel_l1(v, ref.pi.v) <= 1e-4
+    np.testing.assert_allclose(out.degree.cpu().numpy(), ref.A_degree, rtol=1e-5)
+    # the statistic only matters against eps = 1e-5/n: agree to 1e-3 relative
+    # or 1e-3 eps absolute (below that it is rounding noise of v)
+    np.testing.assert_allclose(out.pi.stats, ref.pi.stats, rtol=1e-3, atol=1e-3 * w.eps)
+
+
+# ------------------------------------------------------------------ k-means
+def _partition_cost(v, labels, k_eff):
+    """Within-cluster sum of squares of a labelling, from its members."""
+    return float(sum(((v[labels == c] - v[labels == c].mean()) ** 2).sum()
+                     for c in range(k_eff)))
+
+
+def _check_kmeans(v, out, ref):
+    """Unique: k_eff and the optimal cost.  The labels must equal the
+    oracle's, or (exact cost ties) form an equally optimal partition into
+    contiguous runs of the sorted values, numbered by ascending centroid,
+    that never splits equal values."""
+    assert out.k_eff == ref.k_eff
+    assert out.cost == pytest.approx(ref.cost, rel=1e-9, abs=1e-12)
+    lab = out.labels.cpu().numpy()
+    if np.array_equal(lab, ref.labels):
+        np.testing.assert_allclose(out.centroids.cpu().numpy(), ref.centroids,
+                                   rtol=1e-10, atol=1e-300)
+        return
+    order = np.argsort(v, kind="stable")
+    ls = lab[order]
+    assert np.all(np.diff(ls) >= 0) and set(ls) == set(range(out.k_eff))
+    vs = v[order]
+    same = vs[1:] == vs[:-1]
+    assert np.all(ls[1:][same] == ls[:-1][same])
+    assert _partition_cost(v, lab, out.k_eff) == pytest.approx(ref.cost, rel=1e-9,
+                                                                abs=1e-12)
+
+
+@pytest.mark.parametrize("n,k,dup", [(1, 1, False), (2, 2, False), (5, 3, False),
+                                     (1000, 4, False), (4097, 10, False),
+                                     (4097, 10, True), (50000, 10, False),
+                                     (20000, 50, True)])
+def test_kmeans1d_parity(g, orc, n, k, dup):
+    rng = np.random.default_rng(n + k)
+    m = max(1, min(k, n))
+    centres = np.sort(rng.uniform(0, 100, size=m))
+    v = centres[rng.integers(0, m, size=n)] + rng.standard_normal(n) * 0.5
+    if dup:
+        v = np.round(v, 0)
+    out = g.gpic_kmeans1d(_t(v), k)
+    ref = orc.kmeans1d(v, k, "dc" if n > 2000 else "plain")
+    _check_kmeans(v, out, ref)
+
+
+def test_kmeans1d_special_values(g, orc):
+    v = np.array([3.0, -0.0, 0.0, -2.5, 1e-300, -40.0, 7.0, 3.0])
+    for k in (1, 3, 6, 8):
+        out = g.gpic_kmeans1d(_t(v), k)
+        ref = orc.kmeans1d(v, k, "plain")
+        _check_kmeans(v, out, ref)
+
+
+# -------------------------------------------------------------- fused path
+@pytest.mark.parametrize("n,d", [(300, 2), (1000, 64), (1025, 16)])
+def test_fused_parity(g, orc, n, d):
+    X = _pts(n, d, 40 + d, scale=1.5)
+    sigma = np.float32(np.sqrt(d))
+    deg, v0, nz = g.gpic_degree_fused(_t(X), sigma)
+    v = v0.clone()
+    out = g.gpic_power_iterate_fused(_t(X), sigma, deg, v, None, "fixed", 10)
+    torch.cuda.synchronize()
+    dr, v0r, _ = orc.degree_onthefly(X, sigma)
+    ref = orc.power_iterate_onthefly(X, sigma, dr, v0r, "fixed", 10)
+    np.testing.assert_allclose(deg.cpu().numpy(), dr, rtol=1e-5)
+    assert rel_l1(v.cpu().numpy(), ref.v) <= 1e-4
+    assert out.iterations == 10
+    # the fused operator equals the dense one built from the same X
+    A, degd = g.gpic_affinity(_t(X), sigma)
+    W, _, v0d, _ = g.gpic_degree_normalize(A, n, degd, True)
+    vd = v0d.clone()
+    g.gpic_power_iterate_dense(W, vd, None, "fixed", 10, n=n)
+    assert rel_l1(v.cpu().numpy(), vd.cpu().numpy()) <= 1e-6
+
+
+# ---------------------------------------------------------------- CSR path
+def test_csr_parity_knn(g, orc):
+    import workloads
+    w = workloads.make("knn8d", n=4000)
+    rp, col, val = w.row_ptr, w.col, w.val
+    out = g.pic_csr(_t(rp), _t(col), _t(val.copy()), w.k, "converge", 1000, w.eps)
+    torch.cuda.synchronize()
+    wr, dr, v0r, _ = orc.degree_normalize_csr(rp, col, val)
+    ref = orc.power_iterate_csr(rp, col, wr, v0r, "converge", 1000, w.eps)
+    np.testing.assert_allclose(out.degree.cpu().numpy(), dr, rtol=1e-12)
+    v = out.pi.v.cpu().numpy()
+    assert out.pi.iterations == ref.iterations
+    assert rel_l1(v, ref.v) <= 1e-4
+
+
+def test_csr_full_pattern_equals_dense(g):
+    n = 300
+    X = _pts(n, 2, 50)
+    A, deg = g.gpic_affinity(_t(X), 1.0)
+    An = A[:, :n].contiguous()
+    rp = torch.arange(0, n * n + 1, n, dtype=torch.int64, device=DEV)
+    col = torch.arange(n, dtype=torch.int32, device=DEV).repeat(n)
+    val = An.reshape(-1).clone()
+    _, dcsr, v0c, _ = g.gpic_degree_normalize_csr(rp, col, val)
+    W, ddense, v0d, _ = g.gpic_degree_normalize(A, n, deg, True)
+    np.testing.assert_allclose(dcsr.cpu().numpy(), ddense.cpu().numpy(), rtol=1e-13)
+    vc, vd = v0c.clone(), v0d.clone()
+    g.gpic_power_iterate_csr(rp, col, val, vc, None, "fixed", 20)
+    g.gpic_power_iterate_dense(W, vd, None, "fixed", 20, n=n)
+    np.testing.assert_allclose(vc.cpu().numpy(), vd.cpu().numpy(), rtol=1e-10)
+
+
+def test_csr_invalid_structure_rejected(g):
+    n = 4
+    rp = torch.tensor([0, 2, 1, 3, 4], dtype=torch.int64, device=DEV)   # not monotone
+    col = torch.tensor([1, 2, 0, 3], dtype=torch.int32, device=DEV)
+    val = torch.ones(4, dtype=torch.float32, device=DEV)
+    with pytest.raises(g.GpicError) as ei:
+        g.gpic_degree_normalize_csr(rp, col, val)
+    assert ei.value.status == 1
+    rp = torch.tensor([0, 1, 2, 3, 4], dtype=torch.int64, device=DEV)
+    col = torch.tensor([1, 2, 0, 9], dtype=torch.int32, device=DEV)      # column >= n
+    with pytest.raises(g.GpicError):
+        g.gpic_degree_normalize_csr(rp, col, val)
