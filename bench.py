@@ -2,9 +2,9 @@
 
 One step = the whole path on the 16-D blob workload (n = 50,000, d = 16,
 10 Dirichlet(5)-sized blobs, sigma = median pair distance of a 1,000-point
-sample): Gaussian affinity (dense float32 W of 2.5e9 entries, 10 GB),
-degrees and W = D^-1 A in place, v0, T = 50 power-iteration updates and the
-exact 1-D k-means with k = 10.  Inputs are resident in HBM before the timed
+sample): Gaussian affinity and degrees, W = D^-1 A written directly (dense
+float32 W of 2.5e9 entries, 10 GB), v0, T = 50 power-iteration updates and
+the exact 1-D k-means with k = 10.  Inputs are resident in HBM before the timed
 region.
 
 Prints one JSON line.  `value` is the power-iteration rate in GB/s of W
@@ -69,8 +69,11 @@ def cpu_baseline(w, n_sample, T):
     gbs = T * 4.0 * n_sample * n_sample / (t2 - t1) / 1e9
     return {"value": round(gbs, 3), "unit": "GB/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"first {n_sample} of the {w.n} points, dense W (float64 in "
-                      f"the oracle, counted at 4 B/entry like the GPU), T = {T}",
+            "sample": (f"first {n_sample} of the {w.n} points" if n_sample < w.n
+                       else f"the whole workload ({w.n} points)")
+                      + f", dense W (float64 in the oracle, counted at 4 B/entry "
+                        f"like the GPU), T = {T}, affinity to k-means",
+            "e2e_s": round(t3 - t0, 3),
             "phases_s": {"affinity_normalise": round(t1 - t0, 3),
                          "power_iteration": round(t2 - t1, 3),
                          "kmeans": round(t3 - t2, 3)}}
@@ -84,9 +87,16 @@ def main():
     ap.add_argument("--n", type=int, default=50000)
     ap.add_argument("--T", type=int, default=50)
     ap.add_argument("--gemv-reps", type=int, default=20)
-    ap.add_argument("--cpu-sample", type=int, default=40000)
+    ap.add_argument("--cpu-sample", type=int, default=50000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-converge", action="store_true")
+    ap.add_argument("--workload", default="blobs16d",
+                    choices=["blobs16d", "blobs64d", "knn8d", "rings2d", "blobs2d"],
+                    help="blobs16d is the headline line; the others measure the "
+                         "fused, CSR and small dense paths")
+    ap.add_argument("--copy-ref-gib", type=float, default=0.0,
+                    help="also time a plain torch copy of this many GiB (the "
+                         "reference kernel for counter scaling)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -97,6 +107,9 @@ def main():
     import torch
     import paper_1604_02700_amd as g
     import workloads
+
+    if args.workload != "blobs16d":
+        return other_workload(args)
 
     dev = torch.device("cuda:0")
     w = workloads.make("blobs16d", n=args.n if args.n != 50000 else None)
@@ -114,9 +127,8 @@ def main():
     def step(record):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
         ev[0].record(stream)
-        A_, deg = g.gpic_affinity(X, w.sigma, A)
         ev[1].record(stream)
-        W, deg, v0, nz = g.gpic_degree_normalize(A_, n, deg, degree_given=True)
+        W, deg, v0, nz = g.gpic_affinity_normalized(X, w.sigma, A)
         v.copy_(v0)
         ev[2].record(stream)
         pi = g.gpic_power_iterate_dense(W, v, None, "fixed", T, record_stats=False, n=n)
@@ -177,6 +189,25 @@ def main():
         cpu = cpu_baseline(w, min(args.cpu_sample, n), T)
         log(f"bench: cpu baseline {cpu['value']} GB/s on {cpu['cores']} threads")
 
+    copy_ref = None
+    if args.copy_ref_gib > 0:
+        m = int(args.copy_ref_gib * (1 << 30)) // 4
+        src = torch.ones(m, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        c0 = torch.cuda.Event(enable_timing=True)
+        c1 = torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        for _ in range(5):
+            dst.copy_(src)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        cms = c0.elapsed_time(c1) / 5
+        copy_ref = {"bytes_read": 4 * m, "bytes_written": 4 * m,
+                    "ms": round(cms, 5), "gbs_read_plus_write": round(8 * m / cms / 1e6, 1)}
+        log(f"bench: copy reference {copy_ref}")
+        del src, dst
+
     traffic = measured_traffic()
     line = {
         "metric": "power-iteration GB/s of W streamed (% HBM peak); end-to-end "
@@ -199,8 +230,7 @@ def main():
                    "accumulate": "f64", "parallelism": "single GPU"},
         "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "e2e_fixed_T_s": round(ms_step / 1e3, 5),
-        "phases_ms": {"affinity": round(float(ph[:, 0].mean()), 4),
-                      "degree_normalise_v0": round(float(ph[:, 1].mean()), 4),
+        "phases_ms": {"affinity_degree_normalise_v0": round(float(ph[:, 1].mean()), 4),
                       "power_iteration": round(pi_ms, 4),
                       "kmeans": round(float(ph[:, 3].mean()), 4)},
         "to_convergence": conv,
@@ -210,7 +240,102 @@ def main():
                      "traffic": traffic, "avg_launch_ms": round(gemv_ms, 5),
                      "bytes_per_launch": alg_bytes},
         "cpu_baseline": cpu,
+        "copy_reference": copy_ref,
     }
+    print(json.dumps(line), flush=True)
+
+
+def other_workload(args):
+    """Fused (blobs64d), CSR (knn8d) and small dense workloads: one JSON line
+    with the path's own rate; not the headline line."""
+    import torch
+    import paper_1604_02700_amd as g
+    import workloads
+
+    dev = torch.device("cuda:0")
+    cache = os.path.join(ROOT, ".cache")
+    w = workloads.make(args.workload, cache_dir=cache)
+    log(f"bench: workload {w.name} n={w.n} d={w.d} path={w.path} mode={w.mode}")
+    stream = torch.cuda.current_stream(dev)
+    X = torch.from_numpy(w.X).to(dev)
+    T = w.max_iter if w.mode == "fixed" else 1000
+    extra = {}
+    if w.path == "csr":
+        rp = torch.from_numpy(w.row_ptr).to(dev)
+        col = torch.from_numpy(w.col).to(dev)
+        val0 = torch.from_numpy(w.val).to(dev)
+        nnz = int(val0.numel())
+        extra["nnz"] = nnz
+
+        def step():
+            val = val0.clone()
+            return g.pic_csr(rp, col, val, w.k, w.mode, T, w.eps)
+    elif w.path == "fused":
+        def step():
+            return g.pic_fused(X, w.sigma, w.k, w.mode, T, w.eps)
+    else:
+        A = torch.empty((w.n, g.padded_ld(w.n)), dtype=torch.float32, device=dev)
+
+        def step():
+            return g.pic_dense(X, w.sigma, w.k, w.mode, T, w.eps, A=A)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out = step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    it = out.pi.iterations
+    # the power-iteration loop alone, from the same start
+    v = out.v0.clone()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    if w.path == "csr":
+        valn = val0.clone()
+        valn, _, _, _ = g.gpic_degree_normalize_csr(rp, col, valn)
+        e0.record(stream)
+        g.gpic_power_iterate_csr(rp, col, valn, v, None, "fixed", it, record_stats=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pi_ms = e0.elapsed_time(e1)
+        bytes_it = 8.0 * nnz + 8.0 * (w.n + 1) + 16.0 * w.n
+        rate = {"unit": "GB/s", "value": it * bytes_it / (pi_ms * 1e-3) / 1e9,
+                "bytes_per_update": bytes_it, "bound": "hbm", "peak": HBM_PEAK_GBS}
+    elif w.path == "fused":
+        e0.record(stream)
+        g.gpic_power_iterate_fused(X, w.sigma, out.degree, v, None, "fixed", it,
+                                   record_stats=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pi_ms = e0.elapsed_time(e1)
+        flops = 2.0 * w.n * w.n * w.d
+        rate = {"unit": "TFLOP/s", "value": it * flops / (pi_ms * 1e-3) / 1e12,
+                "flops_per_sweep": flops, "bound": "mfma", "peak": 157.3}
+    else:
+        W = A
+        e0.record(stream)
+        g.gpic_power_iterate_dense(W, v, None, "fixed", it, record_stats=False, n=w.n)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pi_ms = e0.elapsed_time(e1)
+        bytes_it = 4.0 * w.n * w.n
+        rate = {"unit": "GB/s", "value": it * bytes_it / (pi_ms * 1e-3) / 1e9,
+                "bytes_per_update": bytes_it, "bound": "hbm", "peak": HBM_PEAK_GBS}
+    rate["value"] = round(rate["value"], 3)
+    rate["frac"] = round(rate["value"] / rate["peak"], 4)
+    line = {"metric": f"{w.name}: power-iteration rate ({w.path} operator); "
+                      f"end-to-end PIC seconds",
+            "value": rate["value"], "unit": rate["unit"], "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "f64", "data": "synthetic",
+            "config": {"workload": w.name, "n": w.n, "d": w.d, "path": w.path,
+                       "mode": w.mode, "T_or_cap": T, "k": w.k, **extra},
+            "iterations": it, "converged": out.pi.converged,
+            "pi_ms": round(pi_ms, 4), "ms_per_update": round(pi_ms / max(it, 1), 5),
+            "rate": rate}
     print(json.dumps(line), flush=True)
 
 

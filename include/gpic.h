@@ -68,7 +68,9 @@ enum {
     GPIC_OP_PI_DENSE = 4,
     GPIC_OP_PI_FUSED = 5,
     GPIC_OP_PI_CSR = 6,
-    GPIC_OP_KMEANS1D = 7
+    GPIC_OP_KMEANS1D = 7,
+    GPIC_OP_AFFINITY_NORMALIZED = 8,
+    GPIC_OP_MATVEC_FUSED = 9
 };
 
 /* Power-iteration modes. */
@@ -115,17 +117,36 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k);
  *   A_ij = exp(-||x_i - x_j||^2 / (2 sigma^2)) for i != j,  A_ii = 0.
  * X: float32 [n x d]; A: float32 [n x lda], written in columns 0..n-1 only.
  * d < 16 or d > 128 uses direct coordinate differences; 16 <= d <= 128
- * forms the squared distance from norms and an fp32 matrix-core Gram
- * product (clamped at 0).  degree (nullable) receives d_i = sum_j A_ij of the
- * stored float32 values, accumulated in float64.
+ * forms c * squared distance on the fp32 matrix cores from augmented points
+ * [x_j, |x_j|^2, 1] . [-2c x_i, c, c |x_i|^2] (c = log2(e) / (2 sigma^2),
+ * clamped at 0).  degree (nullable) receives d_i = sum_j A_ij of the stored
+ * float32 values, accumulated in float64 in a fixed order.
+ * ws: gpic_workspace_bytes(GPIC_OP_AFFINITY, n, 0, 0) bytes (squared norms
+ * and per-chunk row sums).
  * Errors: INVALID_ARG for null X/A, n < 2, d < 1, sigma <= 0 or not finite,
  * lda < n, lda % 4 != 0, misaligned pointers.  Asynchronous. */
 gpic_status gpic_affinity(const float *X, int64_t n, int32_t d, float sigma,
-                          float *A, int64_t lda, double *degree, void *stream);
+                          float *A, int64_t lda, double *degree, void *ws,
+                          size_t ws_bytes, void *stream);
+
+/* Steps 1 and 2 in one call, A never stored: a first sweep forms the
+ * degrees d_i = sum_{j != i} A_ij of the float32 affinities (as
+ * gpic_affinity's row sums), then v0 = D / sum D and the zero-degree count,
+ * and a second sweep recomputes A and writes W_ij = A_ij * r_i with
+ * r_i = float32(1 / d_i) into W [n x ldw].  Bit for bit the
+ * same W, degree and v0 as gpic_affinity followed by gpic_degree_normalize
+ * with degree_given = 1, with 4 n^2 bytes of HBM traffic instead of 12 n^2.
+ * Same argument rules as those two calls; synchronises the stream (sum(D)
+ * check).  ws: gpic_workspace_bytes(GPIC_OP_AFFINITY_NORMALIZED, n, 0, 0). */
+gpic_status gpic_affinity_normalized(const float *X, int64_t n, int32_t d,
+                                     float sigma, float *W, int64_t ldw,
+                                     double *degree, double *v0,
+                                     int64_t *n_zero_rows, void *ws,
+                                     size_t ws_bytes, void *stream);
 
 /* --------------------------------- 2. degrees, W = D^-1 A, v0 = D / sum D */
 
-/* Dense, in place: A becomes W (row i scaled by 1/d_i).  If degree_given
+/* Dense, in place: A becomes W (row i times r_i = float32(1 / d_i)).  If degree_given
  * is non-zero, degree holds d (e.g. written by gpic_affinity) and is read;
  * otherwise it is computed here from A and written.  v0_i = d_i / sum_j d_j.
  * A zero-degree row stays a zero row, gets v0_i = 0 and is counted in
@@ -168,10 +189,12 @@ gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
 
 /* One product y_i = (sum_{j != i} A_ij v_j) / d_i with A recomputed from X
  * (the fused operator; W = D^-1 A is never stored).  A zero-degree row gives
- * y_i = 0.  Asynchronous. */
+ * y_i = 0.  ws: gpic_workspace_bytes(GPIC_OP_MATVEC_FUSED, n, 0, 0).
+ * Asynchronous. */
 gpic_status gpic_matvec_fused(const float *X, int64_t n, int32_t d,
                               float sigma, const double *degree,
-                              const double *v, double *y, void *stream);
+                              const double *v, double *y, void *ws,
+                              size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------- 3+4. power iteration */
 

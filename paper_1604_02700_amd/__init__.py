@@ -28,13 +28,14 @@ STATUS = {0: "GPIC_OK", 1: "GPIC_ERR_INVALID_ARG", 2: "GPIC_ERR_WORKSPACE",
           3: "GPIC_ERR_HIP", 4: "GPIC_ERR_NUMERIC", 5: "GPIC_ERR_UNSUPPORTED"}
 OP = {"affinity": 0, "degree_normalize": 1, "degree_normalize_csr": 2,
       "degree_fused": 3, "pi_dense": 4, "pi_fused": 5, "pi_csr": 6,
-      "kmeans1d": 7}
+      "kmeans1d": 7, "affinity_normalized": 8, "matvec_fused": 9}
 MODES = {"fixed": 0, "converge": 1}
 
 # C entry points declared in include/gpic.h (checked by the tests)
 EXPORTS = (
     "gpic_abi_version", "gpic_status_string", "gpic_last_error",
-    "gpic_workspace_bytes", "gpic_affinity", "gpic_degree_normalize",
+    "gpic_workspace_bytes", "gpic_affinity", "gpic_affinity_normalized",
+    "gpic_degree_normalize",
     "gpic_degree_normalize_csr", "gpic_degree_fused", "gpic_matvec_dense",
     "gpic_matvec_csr", "gpic_matvec_fused", "gpic_power_iterate_dense",
     "gpic_power_iterate_fused", "gpic_power_iterate_csr", "gpic_kmeans1d",
@@ -78,13 +79,14 @@ def lib() -> C.CDLL:
         L.gpic_workspace_bytes.restype = sz
         L.gpic_workspace_bytes.argtypes = [i32, i64, i64, i32]
         sigs = {
-            "gpic_affinity": [p, i64, i32, f32, p, i64, p, p],
+            "gpic_affinity": [p, i64, i32, f32, p, i64, p, p, sz, p],
+            "gpic_affinity_normalized": [p, i64, i32, f32, p, i64, p, p, p, p, sz, p],
             "gpic_degree_normalize": [p, i64, i64, p, i32, p, p, p, sz, p],
             "gpic_degree_normalize_csr": [p, p, p, i64, i64, p, p, p, p, sz, p],
             "gpic_degree_fused": [p, i64, i32, f32, p, p, p, p, sz, p],
             "gpic_matvec_dense": [p, i64, i64, p, p, p],
             "gpic_matvec_csr": [p, p, p, i64, i64, p, p, p],
-            "gpic_matvec_fused": [p, i64, i32, f32, p, p, p, p],
+            "gpic_matvec_fused": [p, i64, i32, f32, p, p, p, p, sz, p],
             "gpic_power_iterate_dense": [p, i64, i64, C.POINTER(PiParams), p, p, p,
                                          sz, C.POINTER(PiResult), p],
             "gpic_power_iterate_fused": [p, i64, i32, f32, p, C.POINTER(PiParams),
@@ -163,9 +165,33 @@ def gpic_affinity(X: torch.Tensor, sigma: float, A: Optional[torch.Tensor] = Non
     if A.dim() != 2 or A.shape[0] != n or A.stride(1) != 1 or A.shape[1] < n:
         raise ValueError("A must be [n, >= n] with unit column stride")
     deg = torch.empty(n, dtype=torch.float64, device=X.device) if want_degree else None
+    ws, nb = workspace("affinity", n, device=X.device)
     _check(lib().gpic_affinity(_ptr(X), n, d, float(sigma), _ptr(A), A.stride(0),
-                               _ptr(deg), _stream(X.device)))
+                               _ptr(deg), _ptr(ws), nb, _stream(X.device)))
     return A, deg
+
+
+def gpic_affinity_normalized(X: torch.Tensor, sigma: float,
+                             W: Optional[torch.Tensor] = None):
+    """W = D^-1 A written directly (A never stored); returns
+    (W, degree, v0, n_zero_rows tensor)."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    dev = X.device
+    if W is None:
+        W = torch.empty((n, padded_ld(n)), dtype=torch.float32, device=dev)
+    _dev(W, torch.float32, "W")
+    if W.dim() != 2 or W.shape[0] != n or W.stride(1) != 1 or W.shape[1] < n:
+        raise ValueError("W must be [n, >= n] with unit column stride")
+    degree = torch.empty(n, dtype=torch.float64, device=dev)
+    v0 = torch.empty(n, dtype=torch.float64, device=dev)
+    nz = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws, nb = workspace("affinity_normalized", n, device=dev)
+    _check(lib().gpic_affinity_normalized(_ptr(X), n, d, float(sigma), _ptr(W),
+                                          W.stride(0), _ptr(degree), _ptr(v0),
+                                          _ptr(nz), _ptr(ws), nb, _stream(dev)))
+    return W, degree, v0, nz
 
 
 # ----------------------------------------------- 2. degrees, W and v0
@@ -243,8 +269,9 @@ def gpic_matvec_fused(X, sigma, degree, v, y=None):
     _dev(X, torch.float32, "X")
     n, d = X.shape
     y = _vec(y, n, "y", X.device)
+    ws, nb = workspace("matvec_fused", n, device=X.device)
     _check(lib().gpic_matvec_fused(_ptr(X), n, d, float(sigma), _ptr(degree), _ptr(v),
-                                   _ptr(y), _stream(X.device)))
+                                   _ptr(y), _ptr(ws), nb, _stream(X.device)))
     return y
 
 
@@ -360,12 +387,17 @@ class PICOut:
 
 
 def pic_dense(X, sigma, k, mode="converge", max_iter=1000, eps=0.0, check_every=0,
-              A: Optional[torch.Tensor] = None) -> PICOut:
+              A: Optional[torch.Tensor] = None, fused_normalize: bool = True) -> PICOut:
     """Affinity, degrees, W = D^-1 A, v0, the power iteration and k-means,
-    over a materialised dense W (n^2 float32)."""
+    over a materialised dense W (n^2 float32).  fused_normalize writes W in
+    one call (gpic_affinity_normalized); otherwise A is written, then scaled
+    in place (gpic_affinity + gpic_degree_normalize)."""
     n = X.shape[0]
-    A, deg = gpic_affinity(X, sigma, A)
-    W, deg, v0, nz = gpic_degree_normalize(A, n, deg, degree_given=True)
+    if fused_normalize:
+        W, deg, v0, nz = gpic_affinity_normalized(X, sigma, A)
+    else:
+        A, deg = gpic_affinity(X, sigma, A)
+        W, deg, v0, nz = gpic_degree_normalize(A, n, deg, degree_given=True)
     v = v0.clone()
     pi = gpic_power_iterate_dense(W, v, None, mode, max_iter, eps, check_every, n=n)
     km = gpic_kmeans1d(pi.v, k)

@@ -6,32 +6,332 @@
 // evaluated as exp2(-c * dist2) with c = log2(e) / (2 sigma^2), formed in
 // float64 on the host and rounded once to float32.
 //
-// Two tile engines share one outer structure (a workgroup owns a block of
-// rows and walks every column, so row sums are complete inside it):
-//   * VALU, d < 16: squared distances from coordinate differences.
-//   * MFMA, d >= 16: dist2 = |x_i|^2 + |x_j|^2 - 2 x_i.x_j with the Gram
-//     product on the fp32 matrix cores (v_mfma_f32_16x16x4f32), clamped at 0.
-// Three epilogues (template MODE):
-//   kStore : write A (float32) and optionally the float64 row sums,
-//   kApply : y_i = (sum_j A_ij v_j) / d_i, W = D^-1 A never stored (the
-//            Multiply step with the affinity recomputed), plus per-block
-//            partial sums of |y_i| for the L1 norm,
+// Two tile engines:
+//   * MFMA, 16 <= d <= 128.  The matrix cores produce c * dist2 directly:
+//     column operands are the augmented points [x_j, |x_j|^2, 1] and row
+//     operands [-2c x_i, c, c |x_i|^2], so one fp32 Gram product gives
+//     c (|x_i|^2 + |x_j|^2 - 2 x_i.x_j); it is clamped at 0 before exp2.
+//     A prologue kernel writes both augmented operand arrays once per call
+//     (squared norms as float64 sums rounded to float32, rows padded with
+//     zeros to a multiple of 64), so staging a column tile is a contiguous
+//     16-byte copy.
+//   * VALU, other d: squared distances from coordinate differences.
+// A workgroup owns a block of rows and a range of columns (a chunk); when
+// the rows alone would not fill the chip the columns are split in chunks,
+// and the per-chunk row sums are added in chunk order by a second kernel,
+// so results do not depend on scheduling.
+//
+// Four epilogues (template MODE):
+//   kStore : write A (float32) and, if requested, the float64 row sums,
+//   kStoreW: write W_ij = A_ij * r_i, r_i = float32(1 / d_i), given d,
+//   kApply : y_i = (sum_j A_ij v_j) / d_i (the Multiply step with the
+//            affinity recomputed; W = D^-1 A is never stored),
 //   kDegree: d_i = sum_j A_ij with nothing of size n^2 written.
+// Every mode evaluates the same float32 A_ij and sums rows in the same
+// order, so kDegree reproduces kStore's degrees bit for bit and kStoreW
+// writes exactly what kStore followed by the row scaling writes.
 #include "common.h"
 
 namespace gpic {
 namespace {
 
-enum { kStore = 0, kApply = 1, kDegree = 2 };
+enum { kStore = 0, kApply = 1, kDegree = 2, kStoreW = 3 };
 
 constexpr int kThreads = 256;
+constexpr int kMaxChunks = 16;
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// exp2 on the transcendental unit (1 ulp; results below the smallest
+// normal float flush to zero, far below anything a row sum can notice)
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Plain (cached) stores: measured on MI355X, non-temporal stores of this
+// 16-rows-by-64-bytes pattern reach only about 60 % of the bandwidth of
+// ordinary ones.
+__device__ __forceinline__ void store4(float *dst, float a, float b, float c, float d)
+{
+    floatx4 t = {a, b, c, d};
+    *reinterpret_cast<floatx4 *>(dst) = t;
+}
+
+// ------------------------------------------------------------ prologue
+
+// Augmented operands, KP floats per point (KP = 4 KS >= d + 2):
+//   xa[p] = [x_p, |x_p|^2, 1, 0...]          (column operand)
+//   xb[p] = [-2c x_p, c, c |x_p|^2, 0...]    (row operand)
+// |x_p|^2 is a float64 sum rounded once to float32.  Points n .. np-1
+// (padding up to a multiple of the column tile) are all zeros.
+__global__ __launch_bounds__(kThreads) void augment_kernel(
+    const float *__restrict__ X, int64_t n, int64_t np, int d, int KP, float c,
+    float *__restrict__ xa, float *__restrict__ xb)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= np)
+        return;
+    float *a = xa + p * KP;
+    float *b = xb + p * KP;
+    if (p >= n) {
+        for (int k = 0; k < KP; ++k) {
+            a[k] = 0.0f;
+            b[k] = 0.0f;
+        }
+        return;
+    }
+    double s = 0.0;
+    for (int k = 0; k < d; ++k) {
+        const double x = (double)X[p * d + k];
+        s = fma(x, x, s);
+    }
+    const float nrm = (float)s;
+    for (int k = 0; k < KP; ++k) {
+        if (k < d) {
+            const float x = X[p * d + k];
+            a[k] = x;
+            b[k] = -2.0f * c * x;
+        } else if (k == d) {
+            a[k] = nrm;
+            b[k] = c;
+        } else if (k == d + 1) {
+            a[k] = 1.0f;
+            b[k] = c * nrm;
+        } else {
+            a[k] = 0.0f;
+            b[k] = 0.0f;
+        }
+    }
+}
+
+// ---------------------------------------------------- chunk row-sum reduce
+
+// out_i = sum over chunks of part[c][i] (chunk order); kApply divides by
+// d_i and writes per-workgroup partial sums of |y_i| for the L1 norm.
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void chunk_reduce_kernel(
+    const double *__restrict__ part, int nchunks, int64_t n,
+    const double *__restrict__ degree_in, double *__restrict__ out,
+    double *__restrict__ partial, StopCtl ctl, int use_ctl)
+{
+    __shared__ double red[kThreads / kWave];
+    if (MODE == kApply && use_ctl && stop_reached(ctl))
+        return;
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    double yabs = 0.0;
+    if (i < n) {
+        double s = 0.0;
+        for (int c = 0; c < nchunks; ++c)
+            s += part[(int64_t)c * n + i];
+        if (MODE == kApply) {
+            const double di = degree_in[i];
+            const double yi = (di == 0.0) ? 0.0 : s / di;
+            out[i] = yi;
+            yabs = fabs(yi);
+        } else {
+            out[i] = s;
+        }
+    }
+    if (MODE == kApply && partial != nullptr) {
+        const double t = block_sum<kThreads>(yabs, red);
+        if (threadIdx.x == 0)
+            partial[blockIdx.x] = t;
+    }
+}
+
+// ------------------------------------------------------------------ MFMA
+
+// Workgroup: 4 waves x 16 rows = 64 rows; columns [c0, c1) of its chunk in
+// tiles of 64 staged through double-buffered LDS.
+//
+// v_mfma_f32_16x16x4f32 operand layout (lane l, g = l / 16, m = l % 16):
+//   A operand : element (row m,  k = g)
+//   B operand : element (k = g,  column m)
+//   result    : elements (row 4g + r, column m), r = 0..3
+// The A operand carries 16 affinity columns j and the B operand the wave's
+// 16 rows i, so every lane ends with one row i and four consecutive
+// columns: one 16-byte store per lane.  K-step s, slot g holds augmented
+// coordinate 4 s + g.
+constexpr int kRowsPerWave = 16;
+constexpr int kRowsPerGroup = 4 * kRowsPerWave;
+constexpr int kTileCols = 64;
+
+template <int KS, int MODE>
+__global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
+    const float *__restrict__ xa, const float *__restrict__ xb, int64_t n,
+    int64_t chunk_cols, float *__restrict__ A, int64_t lda,
+    const double *__restrict__ v, const double *__restrict__ degree_in,
+    double *__restrict__ out, double *__restrict__ part,
+    double *__restrict__ partial, StopCtl ctl, int use_ctl)
+{
+    constexpr int KP = 4 * KS;   // augmented, padded dimension
+    constexpr int LS = KP + 1;   // LDS row stride (odd: no bank conflicts)
+    __shared__ float xs[2][kTileCols * LS];
+    __shared__ double vs[2][kTileCols];
+    __shared__ double red[kThreads / kWave];
+
+    if (MODE == kApply && use_ctl) {
+        if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+            *ctl.cur_stat = 0.0;
+        if (stop_reached(ctl))
+            return;
+    }
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    const int g = lane >> 4;
+    const int m = lane & 15;
+    const int64_t wrow0 = (int64_t)blockIdx.x * kRowsPerGroup + wave * kRowsPerWave;
+    const int64_t i = wrow0 + m;
+    const bool row_ok = i < n;
+    const int64_t ic = row_ok ? i : n - 1;
+    const int64_t c0 = (int64_t)blockIdx.y * chunk_cols;
+    const int64_t c1 = (c0 + chunk_cols < n) ? c0 + chunk_cols : n;
+
+    // B operand: augmented row coordinates 4 s + g of [-2c x_i, c, c |x_i|^2]
+    float bop[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+        bop[s] = xb[ic * KP + 4 * s + g];
+    float rs = 0.0f;
+    if (MODE == kStoreW) {
+        const double di = degree_in[ic];
+        rs = (di == 0.0) ? 0.0f : (float)(1.0 / di);
+    }
+
+    // staging: the tile is 64 * KP contiguous floats of xa (rows padded to
+    // a multiple of 64), copied as 16-byte pieces: piece f holds column
+    // f / KS, coordinates 4 (f % KS) .. + 3
+    constexpr int kPieces = kTileCols * KS;
+    constexpr int kPer = (kPieces + kThreads - 1) / kThreads;
+    floatx4 stage[kPer];
+    double vstage = 0.0;
+    auto fetch = [&](int64_t jt) {
+        const floatx4 *src = reinterpret_cast<const floatx4 *>(xa + jt * KP);
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int f = threadIdx.x + u * kThreads;
+            if (kPieces % kThreads == 0 || f < kPieces)
+                stage[u] = src[f];
+        }
+        if (MODE == kApply && threadIdx.x < kTileCols) {
+            const int64_t j = jt + threadIdx.x;
+            vstage = (j < c1) ? v[j] : 0.0;
+        }
+    };
+    auto commit = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int f = threadIdx.x + u * kThreads;
+            if (kPieces % kThreads == 0 || f < kPieces) {
+                float *dst = xs[buf] + (f / KS) * LS + 4 * (f % KS);
+                dst[0] = stage[u][0];
+                dst[1] = stage[u][1];
+                dst[2] = stage[u][2];
+                dst[3] = stage[u][3];
+            }
+        }
+        if (MODE == kApply && threadIdx.x < kTileCols)
+            vs[buf][threadIdx.x] = vstage;
+    };
+
+    double acc = 0.0;
+    const int64_t ntiles = (c1 - c0 + kTileCols - 1) / kTileCols;
+    fetch(c0);
+    commit(0);
+    __syncthreads();
+    for (int64_t t = 0; t < ntiles; ++t) {
+        const int buf = (int)(t & 1);
+        const int64_t jt = c0 + t * kTileCols;
+        if (t + 1 < ntiles)
+            fetch(jt + kTileCols);                  // in flight during compute
+        const bool diag = (wrow0 >= jt) && (wrow0 < jt + kTileCols);
+        const bool tail = jt + kTileCols > c1;
+        const float *xb = xs[buf];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            floatx4 cacc = {0.0f, 0.0f, 0.0f, 0.0f};
+            const float *ap = xb + (q * 16 + m) * LS + g;
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                cacc = __builtin_amdgcn_mfma_f32_16x16x4f32(ap[4 * s], bop[s], cacc,
+                                                            0, 0, 0);
+            float a[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                a[r] = exp2_fast(-fmaxf(cacc[r], 0.0f));
+            const int64_t j0 = jt + 16 * q + 4 * g;    // this lane's columns
+            if (diag || tail) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (j0 + r == i || j0 + r >= c1)
+                        a[r] = 0.0f;
+            }
+            if (MODE == kStore || MODE == kStoreW) {
+                float o[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    o[r] = (MODE == kStoreW) ? a[r] * rs : a[r];
+                if (row_ok) {
+                    float *dst = A + i * lda + j0;
+                    if (!tail || j0 + 3 < c1) {
+                        store4(dst, o[0], o[1], o[2], o[3]);
+                    } else {
+                        for (int r = 0; r < 4 && j0 + r < c1; ++r)
+                            dst[r] = o[r];
+                    }
+                }
+            }
+            if (MODE == kStore || MODE == kDegree) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    acc += (double)a[r];
+            } else if (MODE == kApply) {
+                const double *vp = vs[buf] + q * 16 + 4 * g;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    acc = fma((double)a[r], vp[r], acc);
+            }
+        }
+        if (t + 1 < ntiles) {
+            // the barrier ending the previous iteration ordered every wave's
+            // reads of buffer buf ^ 1 before this write; this one orders the
+            // write before the next tile's reads
+            commit(buf ^ 1);
+            __syncthreads();
+        }
+    }
+
+    if (MODE == kStoreW)
+        return;
+    // the four lanes sharing a row (g = 0..3) hold disjoint columns
+    acc += __shfl_xor(acc, 16, kWave);
+    acc += __shfl_xor(acc, 32, kWave);
+    if (part != nullptr) {
+        // chunk partial, reduced in chunk order by chunk_reduce_kernel
+        if (g == 0 && row_ok)
+            part[(int64_t)blockIdx.y * n + i] = acc;
+        return;
+    }
+    double yabs = 0.0;
+    if (g == 0 && row_ok) {
+        if (MODE == kApply) {
+            const double di = degree_in[i];
+            const double yi = (di == 0.0) ? 0.0 : acc / di;
+            out[i] = yi;
+            yabs = fabs(yi);
+        } else if (out != nullptr) {
+            out[i] = acc;
+        }
+    }
+    if (MODE == kApply && partial != nullptr) {
+        const double sum = block_sum<kThreads>(yabs, red);
+        if (threadIdx.x == 0)
+            partial[blockIdx.x] = sum;
+    }
+}
 
 // ------------------------------------------------------------------ VALU
 
 // Block: 256 threads, RB rows; each thread takes groups of 4 consecutive
-// columns (one float4 store per row), stepping by 1024 columns.
+// columns (one 16-byte store per row), stepping by 1024 columns.
 template <int D, int RB, int MODE>
 __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
     const float *__restrict__ X, int64_t n, int dyn_d, float c,
@@ -60,13 +360,21 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
         }
     }
     double acc[RB];
+    float rs[RB];
 #pragma unroll
-    for (int r = 0; r < RB; ++r)
+    for (int r = 0; r < RB; ++r) {
         acc[r] = 0.0;
+        rs[r] = 0.0f;
+        if (MODE == kStoreW) {
+            const int64_t i = (row0 + r < n) ? row0 + r : n - 1;
+            const double di = degree_in[i];
+            rs[r] = (di == 0.0) ? 0.0f : (float)(1.0 / di);
+        }
+    }
 
     const int64_t ngroups = (n + 3) >> 2;
-    for (int64_t g = threadIdx.x; g < ngroups; g += kThreads) {
-        const int64_t j0 = g << 2;
+    for (int64_t gi = threadIdx.x; gi < ngroups; gi += kThreads) {
+        const int64_t j0 = gi << 2;
         float a[RB][4];
         if (D > 0) {
             float xj[4][DR];
@@ -87,7 +395,7 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
                         const float df = xi[r][k] - xj[q][k];
                         s = fmaf(df, df, s);
                     }
-                    a[r][q] = exp2f(-c * s);
+                    a[r][q] = exp2_fast(-c * s);
                 }
         } else {
             // any d (used above the matrix-core range): coordinates re-read
@@ -102,7 +410,7 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
                         const float df = X[i * d + k] - X[j * d + k];
                         s = fmaf(df, df, s);
                     }
-                    a[r][q] = exp2f(-c * s);
+                    a[r][q] = exp2_fast(-c * s);
                 }
             }
         }
@@ -119,22 +427,29 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
             for (int q = 0; q < 4; ++q)
                 if (i == j0 + q || j0 + q >= n)
                     a[r][q] = 0.0f;
-            if (MODE == kStore && i < n) {
+            if ((MODE == kStore || MODE == kStoreW) && i < n) {
+                float o[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    o[q] = (MODE == kStoreW) ? a[r][q] * rs[r] : a[r][q];
                 float *dst = A + i * lda + j0;
                 if (j0 + 3 < n) {
-                    *reinterpret_cast<float4 *>(dst) =
-                        make_float4(a[r][0], a[r][1], a[r][2], a[r][3]);
+                    store4(dst, o[0], o[1], o[2], o[3]);
                 } else {
                     for (int q = 0; q < 4 && j0 + q < n; ++q)
-                        dst[q] = a[r][q];
+                        dst[q] = o[q];
                 }
             }
+            if (MODE != kStoreW) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                acc[r] = fma((double)a[r][q], vj[q], acc[r]);
+                for (int q = 0; q < 4; ++q)
+                    acc[r] = fma((double)a[r][q], vj[q], acc[r]);
+            }
         }
     }
 
+    if (MODE == kStoreW)
+        return;
     double part = 0.0;
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
@@ -160,185 +475,110 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
         partial[blockIdx.x] = part;
 }
 
-// ------------------------------------------------------------------ MFMA
+// ------------------------------------------------------------- dispatch
 
-// Block: 4 waves x 16 rows = 64 rows.  The block walks the columns in
-// tiles of 64 staged in LDS (points, their squared norms and, for kApply,
-// v); every wave forms four 16x16 Gram sub-tiles per column tile.
-//
-// v_mfma_f32_16x16x4f32 operand layout (lane l, g = l / 16):
-//   A operand : element (m = l % 16, k = g)
-//   B operand : element (k = g,      n = l % 16)
-//   result    : elements (m = 4 g + r, n = l % 16), r = 0..3
-// The A operand carries 16 columns j of the affinity and the B operand the
-// wave's 16 rows i, so the result gives every lane one row i and four
-// consecutive columns: one float4 store per lane.  The k slot g of K-step s
-// holds coordinate g * KS + s, so each lane reads KS consecutive
-// coordinates of a point (vector loads from LDS and HBM).
-constexpr int kRowsPerWave = 16;
-constexpr int kTileCols = 64;
+bool use_mfma(int d) { return d >= 16 && d <= 128; }
 
-template <int KS, int MODE>
-__global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
-    const float *__restrict__ X, int64_t n, int d, float c,
-    float *__restrict__ A, int64_t lda, const double *__restrict__ v,
-    const double *__restrict__ degree_in, double *__restrict__ out,
-    double *__restrict__ partial, StopCtl ctl, int use_ctl)
+int ks_for(int d)
 {
-    constexpr int DP = 4 * KS;       // padded dimension
-    constexpr int LS = DP + 4;       // LDS row stride (floats), 16 B aligned
-    __shared__ __attribute__((aligned(16))) float xs[kTileCols * LS];
-    __shared__ __attribute__((aligned(16))) float ns[kTileCols];
-    __shared__ __attribute__((aligned(16))) double vs[kTileCols];
-    __shared__ double red[kThreads / kWave];
+    const int need = (d + 2 + 3) / 4;          // augmented dimension / 4
+    static const int sizes[] = {5, 6, 8, 10, 12, 14, 17, 20, 24, 28, 33};
+    for (int s : sizes)
+        if (s >= need)
+            return s;
+    return 33;
+}
 
-    if (MODE == kApply && use_ctl) {
-        if (blockIdx.x == 0 && threadIdx.x == 0)
-            *ctl.cur_stat = 0.0;
-        if (stop_reached(ctl))
-            return;
-    }
-    const int lane = threadIdx.x % kWave;
-    const int wave = threadIdx.x / kWave;
-    const int g = lane >> 4;
-    const int m = lane & 15;
-    const int64_t i = (int64_t)blockIdx.x * (4 * kRowsPerWave) +
-                      wave * kRowsPerWave + m;
-    const int64_t ic = (i < n) ? i : n - 1;
+// Column chunks: enough workgroups to fill the chip when rows are few.
+void chunking(int64_t n, int64_t *chunk_cols, int *nchunks)
+{
+    const int64_t groups = (n + kRowsPerGroup - 1) / kRowsPerGroup;
+    int64_t want = (4096 + groups - 1) / groups;     // >= 4 workgroups per CU
+    if (want < 1)
+        want = 1;
+    if (want > kMaxChunks)
+        want = kMaxChunks;
+    int64_t cols = (n + want - 1) / want;
+    cols = (cols + kTileCols - 1) / kTileCols * kTileCols;
+    *chunk_cols = cols;
+    *nchunks = (int)((n + cols - 1) / cols);
+}
 
-    // B operand: the row's coordinates g*KS .. g*KS+KS-1 (zero padded) and
-    // the row's squared norm (sequential float32 sum, same order as ns[]).
-    float bop[KS];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-        const int k = g * KS + s;
-        bop[s] = (k < d) ? X[ic * d + k] : 0.0f;
-    }
-    float ni = 0.0f;
-    for (int k = 0; k < d; ++k) {
-        const float x = X[ic * d + k];
-        ni = fmaf(x, x, ni);
-    }
+constexpr int kMaxKP = 4 * 33;               // largest augmented dimension
 
-    double acc = 0.0;
-    const int64_t ntiles = (n + kTileCols - 1) / kTileCols;
-    for (int64_t t = 0; t < ntiles; ++t) {
-        const int64_t jt = t * kTileCols;
-        __syncthreads();
-        // stage the column tile: 64 points x DP coordinates
-        for (int e = threadIdx.x; e < kTileCols * DP; e += kThreads) {
-            const int cj = e / DP, k = e % DP;
-            const int64_t j = (jt + cj < n) ? jt + cj : n - 1;
-            xs[cj * LS + k] = (k < d) ? X[j * d + k] : 0.0f;
-        }
-        if (MODE == kApply && threadIdx.x < kTileCols) {
-            const int64_t j = jt + threadIdx.x;
-            vs[threadIdx.x] = (j < n) ? v[j] : 0.0;
-        }
-        __syncthreads();
-        if (threadIdx.x < kTileCols) {
-            float s = 0.0f;
-            for (int k = 0; k < d; ++k) {
-                const float x = xs[threadIdx.x * LS + k];
-                s = fmaf(x, x, s);
-            }
-            ns[threadIdx.x] = s;
-        }
-        __syncthreads();
+int64_t padded_points(int64_t n) { return (n + kTileCols - 1) / kTileCols * kTileCols; }
 
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float *ap = xs + (q * 16 + m) * LS + g * KS;
-            floatx4 cacc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int s = 0; s < KS; ++s)
-                cacc = __builtin_amdgcn_mfma_f32_16x16x4f32(ap[s], bop[s], cacc,
-                                                            0, 0, 0);
-            const int cbase = q * 16 + 4 * g;           // column within tile
-            const float4 nj = *reinterpret_cast<const float4 *>(ns + cbase);
-            const float njr[4] = {nj.x, nj.y, nj.z, nj.w};
-            float a[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float d2 = ni + njr[r] - 2.0f * cacc[r];
-                d2 = fmaxf(d2, 0.0f);
-                const int64_t j = jt + cbase + r;
-                a[r] = (j == i || j >= n) ? 0.0f : exp2f(-c * d2);
-            }
-            const int64_t j0 = jt + cbase;
-            if (MODE == kStore) {
-                if (i < n) {
-                    float *dst = A + i * lda + j0;
-                    if (j0 + 3 < n) {
-                        *reinterpret_cast<float4 *>(dst) =
-                            make_float4(a[0], a[1], a[2], a[3]);
-                    } else {
-                        for (int r = 0; r < 4 && j0 + r < n; ++r)
-                            dst[r] = a[r];
-                    }
-                }
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    acc += (double)a[r];
-            } else if (MODE == kDegree) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    acc += (double)a[r];
-            } else {
-                const double2 v01 = *reinterpret_cast<const double2 *>(vs + cbase);
-                const double2 v23 = *reinterpret_cast<const double2 *>(vs + cbase + 2);
-                acc = fma((double)a[0], v01.x, acc);
-                acc = fma((double)a[1], v01.y, acc);
-                acc = fma((double)a[2], v23.x, acc);
-                acc = fma((double)a[3], v23.y, acc);
-            }
-        }
-    }
+int64_t al256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
-    // the four lanes sharing a row (g = 0..3) hold disjoint columns
-    acc += __shfl_xor(acc, 16, kWave);
-    acc += __shfl_xor(acc, 32, kWave);
-    double yabs = 0.0;
-    if (g == 0 && i < n) {
-        if (MODE == kApply) {
-            const double di = degree_in[i];
-            const double yi = (di == 0.0) ? 0.0 : acc / di;
-            out[i] = yi;
-            yabs = fabs(yi);
-        } else if (out != nullptr) {
-            out[i] = acc;
-        }
-    }
-    if (MODE == kApply && partial != nullptr) {
-        // rows of the block in ascending order: lanes 0..15 of each wave,
-        // then the waves in order
-        const double s = block_sum<kThreads>(yabs, red);
-        if (threadIdx.x == 0)
-            partial[blockIdx.x] = s;
-    }
+struct Ws {
+    float *xa;
+    float *xb;
+    double *part;
+};
+
+// [xa: np * kMaxKP floats][xb: same][per-chunk row sums: kMaxChunks * n]
+Ws carve(void *ws, int64_t n)
+{
+    char *b = static_cast<char *>(ws);
+    const int64_t ob = al256(padded_points(n) * kMaxKP * 4);
+    Ws w;
+    w.xa = reinterpret_cast<float *>(b);
+    w.xb = reinterpret_cast<float *>(b + ob);
+    w.part = reinterpret_cast<double *>(b + 2 * ob);
+    return w;
 }
 
 template <int MODE>
 hipError_t dispatch(const float *X, int64_t n, int d, float c, float *A,
                     int64_t lda, const double *v, const double *degree_in,
                     double *out, double *partial, StopCtl ctl, int use_ctl,
-                    hipStream_t s)
+                    void *ws, hipStream_t s)
 {
-    const dim3 block(kThreads);
-    if (d >= 16 && d <= 128) {
-        const dim3 grid((unsigned)((n + 63) / 64));
-        const int ks = (d + 3) / 4;
+    if (use_mfma(d)) {
+        const Ws w = carve(ws, n);
+        const int ks = ks_for(d);
+        const int64_t np = padded_points(n);
+        hipLaunchKernelGGL(augment_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
+                           dim3(kThreads), 0, s, X, n, np, d, 4 * ks, c, w.xa, w.xb);
+        int64_t chunk_cols;
+        int nchunks;
+        chunking(n, &chunk_cols, &nchunks);
+        const bool sums = (MODE != kStoreW) && (MODE != kStore || out != nullptr);
+        double *part = (sums && nchunks > 1) ? w.part : nullptr;
+        const dim3 grid((unsigned)((n + kRowsPerGroup - 1) / kRowsPerGroup),
+                        (unsigned)nchunks);
 #define GPIC_MFMA(KS)                                                          \
-    hipLaunchKernelGGL((affinity_mfma_kernel<KS, MODE>), grid, block, 0, s, X, \
-                       n, d, c, A, lda, v, degree_in, out, partial, ctl,      \
-                       use_ctl)
-        if (ks <= 4) GPIC_MFMA(4);
-        else if (ks <= 8) GPIC_MFMA(8);
-        else if (ks <= 16) GPIC_MFMA(16);
-        else GPIC_MFMA(32);
+    hipLaunchKernelGGL((affinity_mfma_kernel<KS, MODE>), grid, dim3(kThreads), 0, \
+                       s, w.xa, w.xb, n, chunk_cols, A, lda, v, degree_in, out,  \
+                       part, partial, ctl, use_ctl)
+        switch (ks) {
+        case 5: GPIC_MFMA(5); break;
+        case 6: GPIC_MFMA(6); break;
+        case 8: GPIC_MFMA(8); break;
+        case 10: GPIC_MFMA(10); break;
+        case 12: GPIC_MFMA(12); break;
+        case 14: GPIC_MFMA(14); break;
+        case 17: GPIC_MFMA(17); break;
+        case 20: GPIC_MFMA(20); break;
+        case 24: GPIC_MFMA(24); break;
+        case 28: GPIC_MFMA(28); break;
+        default: GPIC_MFMA(33); break;
+        }
 #undef GPIC_MFMA
+        if (part != nullptr) {
+            const dim3 rg((unsigned)((n + kThreads - 1) / kThreads));
+            if (MODE == kApply)
+                hipLaunchKernelGGL(chunk_reduce_kernel<kApply>, rg, dim3(kThreads), 0, s,
+                                   part, nchunks, n, degree_in, out, partial, ctl,
+                                   use_ctl);
+            else
+                hipLaunchKernelGGL(chunk_reduce_kernel<kDegree>, rg, dim3(kThreads), 0,
+                                   s, part, nchunks, n, degree_in, out, partial, ctl,
+                                   use_ctl);
+        }
         return hipGetLastError();
     }
+    const dim3 block(kThreads);
     constexpr int RB = 8;
     const dim3 grid((unsigned)((n + RB - 1) / RB));
 #define GPIC_VALU(D)                                                           \
@@ -362,36 +602,56 @@ hipError_t dispatch(const float *X, int64_t n, int d, float c, float *A,
 
 } // namespace
 
+size_t affinity_ws(int64_t n)
+{
+    return (size_t)(2 * al256(padded_points(n) * kMaxKP * 4) +
+                    al256((int64_t)kMaxChunks * n * 8));
+}
+
 int64_t fused_blocks(int64_t n, int d)
 {
-    if (d >= 16 && d <= 128)
-        return (n + 63) / 64;
-    return (n + 7) / 8;
+    if (!use_mfma(d))
+        return (n + 7) / 8;
+    int64_t chunk_cols;
+    int nchunks;
+    chunking(n, &chunk_cols, &nchunks);
+    if (nchunks > 1)
+        return (n + kThreads - 1) / kThreads;        // chunk_reduce workgroups
+    return (n + kRowsPerGroup - 1) / kRowsPerGroup;  // tile workgroups
 }
 
 hipError_t launch_affinity(const float *X, int64_t n, int d, float c, float *A,
-                           int64_t lda, double *degree, hipStream_t s)
+                           int64_t lda, double *degree, void *ws, hipStream_t s)
 {
     StopCtl none{};
     return dispatch<kStore>(X, n, d, c, A, lda, nullptr, nullptr, degree,
-                            nullptr, none, 0, s);
+                            nullptr, none, 0, ws, s);
+}
+
+hipError_t launch_affinity_w(const float *X, int64_t n, int d, float c,
+                             float *W, int64_t ldw, const double *degree,
+                             void *ws, hipStream_t s)
+{
+    StopCtl none{};
+    return dispatch<kStoreW>(X, n, d, c, W, ldw, nullptr, degree, nullptr,
+                             nullptr, none, 0, ws, s);
 }
 
 hipError_t launch_fused_degree(const float *X, int64_t n, int d, float c,
-                               double *degree, hipStream_t s)
+                               double *degree, void *ws, hipStream_t s)
 {
     StopCtl none{};
     return dispatch<kDegree>(X, n, d, c, nullptr, 0, nullptr, nullptr, degree,
-                             nullptr, none, 0, s);
+                             nullptr, none, 0, ws, s);
 }
 
 hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c,
                               const double *v, const double *degree, double *y,
                               double *partial, StopCtl ctl, bool use_ctl,
-                              hipStream_t s)
+                              void *ws, hipStream_t s)
 {
     return dispatch<kApply>(X, n, d, c, nullptr, 0, v, degree, y, partial, ctl,
-                            use_ctl ? 1 : 0, s);
+                            use_ctl ? 1 : 0, ws, s);
 }
 
 } // namespace gpic

@@ -78,6 +78,7 @@ gpic_status hip_fail(hipError_t e, const char *where)
     } while (0)
 
 size_t start_ws(int64_t n) { return al(start_vector_ws(n)); }
+size_t aff_ws(int64_t n) { return al(affinity_ws(n)); }
 
 size_t pi_ws(int64_t n, int64_t nb)
 {
@@ -85,6 +86,9 @@ size_t pi_ws(int64_t n, int64_t nb)
 }
 
 int64_t fused_nb_bound(int64_t n) { return (n + 7) / 8; }
+
+// the fused product's own scratch follows the power-iteration layout
+size_t pi_fused_ws(int64_t n) { return pi_ws(n, fused_nb_bound(n)) + aff_ws(n); }
 
 // exp(-x / (2 sigma^2)) = exp2(-c x) with c = log2(e) / (2 sigma^2)
 bool gauss_coefficient(float sigma, float *c)
@@ -208,11 +212,13 @@ struct FusedProduct : Product {
     int d;
     float c;
     const double *degree;
+    void *scratch;
     int64_t blocks() const override { return fused_blocks(n, d); }
     hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
                       hipStream_t s) const override
     {
-        return launch_fused_apply(X, n, d, c, v, degree, y, partial, ctl, true, s);
+        return launch_fused_apply(X, n, d, c, v, degree, y, partial, ctl, true,
+                                  scratch, s);
     }
 };
 
@@ -321,20 +327,23 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     if (n < 0 || nnz < 0 || k < 0)
         return 0;
     switch (op) {
-    case GPIC_OP_AFFINITY: return 0;
+    case GPIC_OP_AFFINITY: return aff_ws(n);
     case GPIC_OP_DEGREE_NORMALIZE: return start_ws(n);
     case GPIC_OP_DEGREE_NORMALIZE_CSR: return kCtlBytes + start_ws(n);
-    case GPIC_OP_DEGREE_FUSED: return start_ws(n);
+    case GPIC_OP_DEGREE_FUSED: return start_ws(n) + aff_ws(n);
     case GPIC_OP_PI_DENSE: return pi_ws(n, gemv_blocks(n));
-    case GPIC_OP_PI_FUSED: return pi_ws(n, fused_nb_bound(n));
+    case GPIC_OP_PI_FUSED: return pi_fused_ws(n);
     case GPIC_OP_PI_CSR: return pi_ws(n, spmv_blocks(n));
     case GPIC_OP_KMEANS1D: return kmeans_ws(n, k < 1 ? 1 : k);
+    case GPIC_OP_AFFINITY_NORMALIZED: return start_ws(n) + aff_ws(n);
+    case GPIC_OP_MATVEC_FUSED: return aff_ws(n);
     default: return 0;
     }
 }
 
 gpic_status gpic_affinity(const float *X, int64_t n, int32_t d, float sigma,
-                          float *A, int64_t lda, double *degree, void *stream)
+                          float *A, int64_t lda, double *degree, void *ws,
+                          size_t ws_bytes, void *stream)
 {
     gpic_status st = check_points(X, n, d, sigma);
     if (st != GPIC_OK)
@@ -345,10 +354,45 @@ gpic_status gpic_affinity(const float *X, int64_t n, int32_t d, float sigma,
               (long long)lda);
     if ((st = check_vec(degree, "degree", true)) != GPIC_OK)
         return st;
+    if ((st = check_ws(ws, ws_bytes, aff_ws(n))) != GPIC_OK)
+        return st;
     float c;
     gauss_coefficient(sigma, &c);
-    CHECK_HIP(launch_affinity(X, n, d, c, A, lda, degree, (hipStream_t)stream),
+    CHECK_HIP(launch_affinity(X, n, d, c, A, lda, degree, ws, (hipStream_t)stream),
               "affinity");
+    return GPIC_OK;
+}
+
+gpic_status gpic_affinity_normalized(const float *X, int64_t n, int32_t d,
+                                     float sigma, float *W, int64_t ldw,
+                                     double *degree, double *v0,
+                                     int64_t *n_zero_rows, void *ws,
+                                     size_t ws_bytes, void *stream)
+{
+    gpic_status st = check_points(X, n, d, sigma);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(W != nullptr, "W is null");
+    CHECK_ARG(aligned(W, 16), "W must be 16-byte aligned");
+    CHECK_ARG(ldw >= n && ldw % 4 == 0, "ldw = %lld must be >= n and a multiple of 4",
+              (long long)ldw);
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v0, "v0")) != GPIC_OK)
+        return st;
+    CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
+              "n_zero_rows misaligned");
+    if ((st = check_ws(ws, ws_bytes, start_ws(n) + aff_ws(n))) != GPIC_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    float c;
+    gauss_coefficient(sigma, &c);
+    void *aws = static_cast<char *>(ws) + start_ws(n);
+    CHECK_HIP(launch_fused_degree(X, n, d, c, degree, aws, s), "degree sweep");
+    int bad = 0;
+    CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
+    if (bad)
+        return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
+    CHECK_HIP(launch_affinity_w(X, n, d, c, W, ldw, degree, aws, s), "W sweep");
     return GPIC_OK;
 }
 
@@ -420,12 +464,14 @@ gpic_status gpic_degree_fused(const float *X, int64_t n, int32_t d, float sigma,
         return st;
     CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
               "n_zero_rows misaligned");
-    if ((st = check_ws(ws, ws_bytes, start_ws(n))) != GPIC_OK)
+    if ((st = check_ws(ws, ws_bytes, start_ws(n) + aff_ws(n))) != GPIC_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
     float c;
     gauss_coefficient(sigma, &c);
-    CHECK_HIP(launch_fused_degree(X, n, d, c, degree, s), "fused degree");
+    CHECK_HIP(launch_fused_degree(X, n, d, c, degree,
+                                  static_cast<char *>(ws) + start_ws(n), s),
+              "fused degree");
     int bad = 0;
     CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
     if (bad)
@@ -466,7 +512,7 @@ gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
 
 gpic_status gpic_matvec_fused(const float *X, int64_t n, int32_t d, float sigma,
                               const double *degree, const double *v, double *y,
-                              void *stream)
+                              void *ws, size_t ws_bytes, void *stream)
 {
     gpic_status st = check_points(X, n, d, sigma);
     if (st != GPIC_OK)
@@ -474,10 +520,12 @@ gpic_status gpic_matvec_fused(const float *X, int64_t n, int32_t d, float sigma,
     if ((st = check_vec(degree, "degree")) != GPIC_OK ||
         (st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
         return st;
+    if ((st = check_ws(ws, ws_bytes, aff_ws(n))) != GPIC_OK)
+        return st;
     float c;
     gauss_coefficient(sigma, &c);
     StopCtl none{};
-    CHECK_HIP(launch_fused_apply(X, n, d, c, v, degree, y, nullptr, none, false,
+    CHECK_HIP(launch_fused_apply(X, n, d, c, v, degree, y, nullptr, none, false, ws,
                                  (hipStream_t)stream),
               "fused product");
     return GPIC_OK;
@@ -529,7 +577,7 @@ gpic_status gpic_power_iterate_fused(const float *X, int64_t n, int32_t d,
         return st;
     if ((st = check_pi_common(n, params, v, delta, res)) != GPIC_OK)
         return st;
-    if ((st = check_ws(ws, ws_bytes, pi_ws(n, fused_nb_bound(n)))) != GPIC_OK)
+    if ((st = check_ws(ws, ws_bytes, pi_fused_ws(n))) != GPIC_OK)
         return st;
     FusedProduct op;
     op.X = X;
@@ -537,6 +585,7 @@ gpic_status gpic_power_iterate_fused(const float *X, int64_t n, int32_t d,
     op.d = d;
     gauss_coefficient(sigma, &op.c);
     op.degree = degree;
+    op.scratch = static_cast<char *>(ws) + pi_ws(n, fused_nb_bound(n));
     return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
 }
 

@@ -108,16 +108,22 @@ __device__ __forceinline__ bool stop_reached(const StopCtl &c)
 // Each returns hipSuccess or the launch error.
 const char *last_error_text();
 
-// affinity.hip
+// affinity.hip -- ws: affinity_ws(n) bytes (squared norms and per-chunk row
+// sums); needed for 16 <= d <= 128, ignored otherwise
+size_t affinity_ws(int64_t n);
 hipError_t launch_affinity(const float *X, int64_t n, int d, float c_log2,
-                           float *A, int64_t lda, double *degree,
+                           float *A, int64_t lda, double *degree, void *ws,
                            hipStream_t s);
+hipError_t launch_affinity_w(const float *X, int64_t n, int d, float c_log2,
+                             float *W, int64_t ldw, const double *degree,
+                             void *ws, hipStream_t s);
 hipError_t launch_fused_degree(const float *X, int64_t n, int d, float c_log2,
-                               double *degree, hipStream_t s);
+                               double *degree, void *ws, hipStream_t s);
 hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c_log2,
                               const double *v, const double *degree, double *y,
                               double *partial, StopCtl ctl, bool use_ctl,
-                              hipStream_t s);
+                              void *ws, hipStream_t s);
+// number of |y| partial sums the fused product writes
 int64_t fused_blocks(int64_t n, int d);
 
 // normalize.hip

@@ -36,33 +36,33 @@ __global__ __launch_bounds__(kThreads) void dense_degree_kernel(
         degree[i] = t;
 }
 
-// W_ij = A_ij / d_i in place (float64 reciprocal, one rounding to float32);
-// a zero-degree row is written as zeros.
+// W_ij = A_ij * r_i in place with r_i = float32(1 / d_i) (the float64
+// reciprocal rounded once); a zero-degree row is written as zeros.
 __global__ __launch_bounds__(kThreads) void dense_scale_kernel(
     float *__restrict__ A, int64_t n, int64_t lda, const double *__restrict__ degree)
 {
     const int64_t i = blockIdx.x;
     float *row = A + i * lda;
     const double di = degree[i];
-    const double r = (di == 0.0) ? 0.0 : 1.0 / di;
+    const float r = (di == 0.0) ? 0.0f : (float)(1.0 / di);
     const int64_t n4 = n >> 2;
     for (int64_t c = threadIdx.x; c < n4; c += kThreads) {
         float4 w = reinterpret_cast<float4 *>(row)[c];
-        w.x = (float)((double)w.x * r);
-        w.y = (float)((double)w.y * r);
-        w.z = (float)((double)w.z * r);
-        w.w = (float)((double)w.w * r);
+        w.x *= r;
+        w.y *= r;
+        w.z *= r;
+        w.w *= r;
         reinterpret_cast<float4 *>(row)[c] = w;
     }
     const int64_t tail = n - (n4 << 2);
     if (threadIdx.x < tail) {
         float *p = row + (n4 << 2) + threadIdx.x;
-        *p = (float)((double)*p * r);
+        *p *= r;
     }
 }
 
 // CSR: 16 lanes per row; lane-strided sums, a 16-lane butterfly, then the
-// row is scaled in place.
+// row is scaled in place by float32(1 / d_i).
 constexpr int kCsrLanes = 16;
 
 __global__ __launch_bounds__(kThreads) void csr_degree_scale_kernel(
@@ -82,9 +82,9 @@ __global__ __launch_bounds__(kThreads) void csr_degree_scale_kernel(
         return;
     if (sl == 0)
         degree[i] = s;
-    const double r = (s == 0.0) ? 0.0 : 1.0 / s;
+    const float r = (s == 0.0) ? 0.0f : (float)(1.0 / s);
     for (int64_t p = b + sl; p < e; p += kCsrLanes)
-        val[p] = (float)((double)val[p] * r);
+        val[p] *= r;
 }
 
 // ---- start vector: per-block partial sums and zero counts, a single-group

@@ -17,22 +17,27 @@ namespace gpic {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kGemvRows = 8;        // rows per workgroup of the dense product
+constexpr int kGemvRows = 4;        // rows per workgroup of the dense product
+constexpr int kGemvThreads = 512;   // threads per workgroup of the dense product
 constexpr int kSpmvLanes = 16;      // lanes per CSR row
 constexpr int kSpmvRows = 128;      // rows per workgroup of the CSR product
 
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
 // Dense product.  A workgroup owns kGemvRows consecutive rows; every thread
-// takes float4 column groups c, c + 256, ... and keeps one float64
+// takes 16-byte column groups c, c + NT, ... and keeps one float64
 // accumulator per row, so each 32-byte slice of v it loads is reused across
-// all rows of the block.  Rows past n are clamped for loading and never
-// written.
-template <int R>
-__global__ __launch_bounds__(kThreads) void gemv_kernel(
+// all rows of the block.  W is streamed exactly once per product, so its
+// loads are non-temporal (they do not displace v, which every workgroup
+// re-reads, from the caches).  Rows past n are clamped for loading and
+// never written.
+template <int R, int NT>
+__global__ __launch_bounds__(NT) void gemv_kernel(
     const float *__restrict__ W, int64_t n, int64_t ldw,
     const double *__restrict__ v, double *__restrict__ y,
     double *__restrict__ partial, StopCtl ctl, int use_ctl)
 {
-    __shared__ double red[R][kThreads / kWave];
+    __shared__ double red[R][NT / kWave];
     if (use_ctl) {
         if (blockIdx.x == 0 && threadIdx.x == 0)
             *ctl.cur_stat = 0.0;
@@ -40,11 +45,11 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(
             return;
     }
     const int64_t row0 = (int64_t)blockIdx.x * R;
-    const float4 *rp[R];
+    const floatx4 *rp[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int64_t i = (row0 + r < n) ? row0 + r : n - 1;
-        rp[r] = reinterpret_cast<const float4 *>(W + i * ldw);
+        rp[r] = reinterpret_cast<const floatx4 *>(W + i * ldw);
     }
     double acc[R];
 #pragma unroll
@@ -54,11 +59,11 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(
     const int64_t n4 = n >> 2;
     const double2 *v2 = reinterpret_cast<const double2 *>(v);
 #pragma unroll 2
-    for (int64_t c = threadIdx.x; c < n4; c += kThreads) {
-        float4 w[R];
+    for (int64_t c = threadIdx.x; c < n4; c += NT) {
+        floatx4 w[R];
 #pragma unroll
         for (int r = 0; r < R; ++r)
-            w[r] = rp[r][c];
+            w[r] = __builtin_nontemporal_load(rp[r] + c);
         const double2 va = v2[2 * c];
         const double2 vb = v2[2 * c + 1];
 #pragma unroll
@@ -93,7 +98,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(
         for (int r = 0; r < R; ++r) {
             double t = 0.0;
 #pragma unroll
-            for (int w = 0; w < kThreads / kWave; ++w)
+            for (int w = 0; w < NT / kWave; ++w)
                 t += red[r][w];
             if (row0 + r < n) {
                 y[row0 + r] = t;
@@ -223,9 +228,9 @@ hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
                        double *y, double *partial, StopCtl ctl, bool use_ctl,
                        hipStream_t s)
 {
-    hipLaunchKernelGGL(gemv_kernel<kGemvRows>, dim3((unsigned)gemv_blocks(n)),
-                       dim3(kThreads), 0, s, W, n, ldw, v, y, partial, ctl,
-                       use_ctl ? 1 : 0);
+    hipLaunchKernelGGL((gemv_kernel<kGemvRows, kGemvThreads>),
+                       dim3((unsigned)gemv_blocks(n)), dim3(kGemvThreads), 0, s, W,
+                       n, ldw, v, y, partial, ctl, use_ctl ? 1 : 0);
     return hipGetLastError();
 }
 

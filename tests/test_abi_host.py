@@ -38,8 +38,8 @@ def test_status_strings(L):
 
 def test_workspace_sizes(L):
     import paper_1604_02700_amd as g
-    assert g.workspace_bytes("affinity", 1000) == 0
-    for op in ("degree_normalize", "pi_dense", "pi_fused", "pi_csr", "kmeans1d"):
+    for op in ("affinity", "affinity_normalized", "degree_normalize", "degree_fused",
+               "pi_dense", "pi_fused", "pi_csr", "kmeans1d", "matvec_fused"):
         a = g.workspace_bytes(op, 1000, 5000, 3)
         b = g.workspace_bytes(op, 100000, 500000, 3)
         assert 0 < a < b
@@ -52,16 +52,21 @@ def test_argument_validation_before_launch(L):
     import paper_1604_02700_amd as g
     f = L.gpic_affinity
     dummy = C.c_void_p(4096)               # never dereferenced: checks fail first
-    assert f(None, 10, 2, 1.0, dummy, 12, None, None) == 1
-    assert f(dummy, 1, 2, 1.0, dummy, 12, None, None) == 1        # n < 2
-    assert f(dummy, 10, 0, 1.0, dummy, 12, None, None) == 1       # d < 1
-    assert f(dummy, 10, 2, 0.0, dummy, 12, None, None) == 1       # sigma <= 0
-    assert f(dummy, 10, 2, float("nan"), dummy, 12, None, None) == 1
-    assert f(dummy, 10, 2, 1e-30, dummy, 12, None, None) == 1     # overflowing 1/sigma^2
-    assert f(dummy, 10, 2, 1.0, dummy, 9, None, None) == 1        # lda < n
-    assert f(dummy, 10, 2, 1.0, dummy, 14, None, None) == 1       # lda % 4
-    assert f(dummy, 10, 2, 1.0, C.c_void_p(4100), 12, None, None) == 1  # A misaligned
+    W = (dummy, 1 << 20)                   # workspace pointer and size
+    assert f(None, 10, 2, 1.0, dummy, 12, None, *W, None) == 1
+    assert f(dummy, 1, 2, 1.0, dummy, 12, None, *W, None) == 1        # n < 2
+    assert f(dummy, 10, 0, 1.0, dummy, 12, None, *W, None) == 1       # d < 1
+    assert f(dummy, 10, 2, 0.0, dummy, 12, None, *W, None) == 1       # sigma <= 0
+    assert f(dummy, 10, 2, float("nan"), dummy, 12, None, *W, None) == 1
+    assert f(dummy, 10, 2, 1e-30, dummy, 12, None, *W, None) == 1     # 1/sigma^2 overflows
+    assert f(dummy, 10, 2, 1.0, dummy, 9, None, *W, None) == 1        # lda < n
+    assert f(dummy, 10, 2, 1.0, dummy, 14, None, *W, None) == 1       # lda % 4
+    assert f(dummy, 10, 2, 1.0, C.c_void_p(4100), 12, None, *W, None) == 1  # A misaligned
     assert b"lda" in L.gpic_last_error() or L.gpic_last_error()
+    assert f(dummy, 10, 2, 1.0, dummy, 12, None, dummy, 8, None) == 2  # workspace
+    fn = L.gpic_affinity_normalized
+    assert fn(dummy, 10, 2, 1.0, dummy, 12, dummy, dummy, None, dummy, 8, None) == 2
+    assert fn(dummy, 10, 2, 1.0, dummy, 12, None, dummy, None, *W, None) == 1
     p = g.PiParams()
     p.mode, p.max_iter, p.eps, p.check_every, p.reserved = 2, 10, 0.0, 0, 0
     r = g.PiResult()

@@ -38,7 +38,8 @@ def _t(a):
 # --------------------------------------------------------------- affinity
 @pytest.mark.parametrize("n,d", [(2, 2), (3, 1), (63, 2), (64, 3), (65, 15),
                                  (1000, 2), (1023, 5), (130, 16), (257, 17),
-                                 (200, 64), (129, 40), (77, 130)])
+                                 (200, 64), (129, 40), (77, 130), (150, 128),
+                                 (4100, 16), (70, 110)])
 def test_affinity_parity(g, orc, n, d):
     X = _pts(n, d, 1000 + n + d, scale=2.0)
     sigma = np.float32(1.5 * np.sqrt(d))
@@ -86,6 +87,21 @@ def test_degree_normalize_parity(g, orc, given):
     np.testing.assert_allclose(Wg, Ag / Ag.sum(1)[:, None], rtol=2 * EPS32, atol=1e-38)
     np.testing.assert_allclose(Wg.sum(1), 1.0, atol=n * EPS32)       # pin P1
     assert int(nz.item()) == nzr == 0
+
+
+@pytest.mark.parametrize("n,d", [(777, 3), (1025, 16), (300, 64), (99, 130)])
+def test_affinity_normalized_equals_two_calls(g, n, d):
+    """W written in one call is bitwise the two-call result (affinity with
+    row sums, then in-place scaling with the given degrees)."""
+    X = _pts(n, d, 60 + d, scale=1.3)
+    sigma = np.float32(np.sqrt(d))
+    W1, deg1, v01, nz1 = g.gpic_affinity_normalized(_t(X), sigma)
+    A, deg = g.gpic_affinity(_t(X), sigma)
+    W2, deg2, v02, nz2 = g.gpic_degree_normalize(A, n, deg, True)
+    torch.cuda.synchronize()
+    assert torch.equal(deg1, deg2) and torch.equal(v01, v02)
+    assert torch.equal(W1[:, :n], W2[:, :n])
+    assert int(nz1.item()) == int(nz2.item()) == 0
 
 
 def test_zero_degree_rows_and_numeric_error(g):
