@@ -91,7 +91,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-converge", action="store_true")
     ap.add_argument("--workload", default="blobs16d",
-                    choices=["blobs16d", "blobs64d", "knn8d", "rings2d", "blobs2d"],
+                    choices=["blobs16d", "blobs64d", "knn8d", "knn8d_rcm", "rings2d",
+                             "blobs2d"],
                     help="blobs16d is the headline line; the others measure the "
                          "fused, CSR and small dense paths")
     ap.add_argument("--copy-ref-gib", type=float, default=0.0,
@@ -254,6 +255,8 @@ def other_workload(args):
 
     dev = torch.device("cuda:0")
     cache = os.path.join(ROOT, ".cache")
+    log(f"bench: building workload {args.workload} (the kNN graph takes minutes "
+        f"on the host for knn8d)")
     w = workloads.make(args.workload, cache_dir=cache)
     log(f"bench: workload {w.name} n={w.n} d={w.d} path={w.path} mode={w.mode}")
     stream = torch.cuda.current_stream(dev)

@@ -238,8 +238,8 @@ gpic_status gpic_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
  * ascending centroid; centroids (float64 [k]) get the k_eff cluster means;
  * *cost (host, nullable) the total within-cluster sum of squares.  Split
  * ties go to the smallest sorted position.  Synchronises the stream.
- * Errors: INVALID_ARG for n < 1, k < 1, k > n, null pointers; values must
- * be finite.  ws: gpic_workspace_bytes(GPIC_OP_KMEANS1D, n, 0, k). */
+ * Errors: INVALID_ARG for n < 1, n > 2^30, k < 1, k > n, null pointers;
+ * values must be finite.  ws: gpic_workspace_bytes(GPIC_OP_KMEANS1D, n, 0, k). */
 gpic_status gpic_kmeans1d(const double *v, int64_t n, int32_t k,
                           int32_t *labels, double *centroids, int32_t *k_eff,
                           double *cost, void *ws, size_t ws_bytes,

@@ -42,30 +42,62 @@ def _L():
     if _lib is None:
         if not os.path.exists(_LIB_PATH):
             build(force=False)
-        lib = C.CDLL(_LIB_PATH)
-        p = C.c_void_p
-        i64, i32, f64 = C.c_int64, C.c_int32, C.c_double
-        lib.orc_num_threads.restype = i32
-        lib.orc_affinity_rows.argtypes = [p, i64, i32, f64, i64, i64, p]
-        lib.orc_degree_rows.argtypes = [p, i64, i32, f64, p, i64, p]
-        lib.orc_degree_normalize.argtypes = [p, i64, p, p]
-        lib.orc_degree_normalize.restype = i64
-        lib.orc_degree_normalize_csr.argtypes = [p, p, p, i64, p, p, p]
-        lib.orc_degree_normalize_csr.restype = i64
-        lib.orc_degree_onthefly.argtypes = [p, i64, i32, f64, p, p]
-        lib.orc_degree_onthefly.restype = i64
-        lib.orc_power_iterate_dense.argtypes = [p, i64, i32, i32, f64, p, p, p, p]
-        lib.orc_power_iterate_dense.restype = i32
-        lib.orc_power_iterate_csr.argtypes = [p, p, p, i64, i32, i32, f64, p, p, p, p]
-        lib.orc_power_iterate_csr.restype = i32
-        lib.orc_power_iterate_onthefly.argtypes = [p, i64, i32, f64, p, i32, i32,
-                                                   f64, p, p, p, p]
-        lib.orc_power_iterate_onthefly.restype = i32
-        lib.orc_matvec_onthefly_rows.argtypes = [p, i64, i32, f64, p, p, p, i64, p]
-        lib.orc_kmeans1d.argtypes = [p, i64, i32, i32, p, p, p, p]
-        lib.orc_kmeans1d.restype = i32
-        _lib = lib
+        _lib = _declare(C.CDLL(_LIB_PATH))
     return _lib
+
+
+class use_library:
+    """Temporarily route every oracle call through another build of the
+    oracle source (the mutation tests load deliberately broken copies)."""
+
+    def __init__(self, path):
+        self.path = path
+
+    def __enter__(self):
+        global _lib
+        self.saved = _L()
+        _lib = _declare(C.CDLL(self.path))
+        return self
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self.saved
+        return False
+
+
+def compile_source(src_path, out_path):
+    """Compile an oracle source file with the oracle's own flags."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off",
+           "-fno-fast-math", "-fPIC", "-shared", "-w", "-o", out_path,
+           src_path, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out_path
+
+
+def _declare(lib):
+    """Declare the argument and return types of every oracle function."""
+    p = C.c_void_p
+    i64, i32, f64 = C.c_int64, C.c_int32, C.c_double
+    lib.orc_num_threads.restype = i32
+    lib.orc_affinity_rows.argtypes = [p, i64, i32, f64, i64, i64, p]
+    lib.orc_degree_rows.argtypes = [p, i64, i32, f64, p, i64, p]
+    lib.orc_degree_normalize.argtypes = [p, i64, p, p]
+    lib.orc_degree_normalize.restype = i64
+    lib.orc_degree_normalize_csr.argtypes = [p, p, p, i64, p, p, p]
+    lib.orc_degree_normalize_csr.restype = i64
+    lib.orc_degree_onthefly.argtypes = [p, i64, i32, f64, p, p]
+    lib.orc_degree_onthefly.restype = i64
+    lib.orc_power_iterate_dense.argtypes = [p, i64, i32, i32, f64, p, p, p, p]
+    lib.orc_power_iterate_dense.restype = i32
+    lib.orc_power_iterate_csr.argtypes = [p, p, p, i64, i32, i32, f64, p, p, p, p]
+    lib.orc_power_iterate_csr.restype = i32
+    lib.orc_power_iterate_onthefly.argtypes = [p, i64, i32, f64, p, i32, i32,
+                                               f64, p, p, p, p]
+    lib.orc_power_iterate_onthefly.restype = i32
+    lib.orc_matvec_onthefly_rows.argtypes = [p, i64, i32, f64, p, p, p, i64, p]
+    lib.orc_kmeans1d.argtypes = [p, i64, i32, i32, p, p, p, p]
+    lib.orc_kmeans1d.restype = i32
+    return lib
 
 
 def _ptr(a: np.ndarray):

@@ -38,6 +38,7 @@ using namespace gpic;
 namespace {
 
 constexpr int64_t kMaxN = 2147483647LL;     // indices are int32 in places
+constexpr int64_t kMaxKmeansN = 1LL << 30;  // keeps the split-point recursion within 5 levels
 constexpr int64_t kRing = 1024;             // statistic slots on the device
 constexpr size_t kCtlBytes = 256;           // err @0, tau @8, csr flag @16
 
@@ -617,7 +618,7 @@ gpic_status gpic_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels
                           double *centroids, int32_t *k_eff, double *cost, void *ws,
                           size_t ws_bytes, void *stream)
 {
-    CHECK_ARG(n >= 1 && n <= kMaxN, "n = %lld out of range [1, 2^31-1]", (long long)n);
+    CHECK_ARG(n >= 1 && n <= kMaxKmeansN, "n = %lld out of range [1, 2^30]", (long long)n);
     CHECK_ARG(k >= 1 && (int64_t)k <= n, "k = %d must be in [1, n]", k);
     gpic_status st;
     if ((st = check_vec(v, "v")) != GPIC_OK ||

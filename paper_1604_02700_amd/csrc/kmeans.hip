@@ -14,7 +14,7 @@
 //        cost(j, i) = max(0, (S2[i+1]-S2[j]) - (S1[i+1]-S1[j])^2 / (i-j+1)),
 //      with the leftmost argmin; split points are monotone in i (quadrangle
 //      inequality of the 1-D within-cluster sum of squares), so each layer
-//      is solved by divide and conquer, one launch per recursion level;
+//      is solved by F-ary divide and conquer (a few dependent levels);
 //   4. backtrack, per-cluster means and sums of squares, labels by
 //      ascending centroid.
 #include "common.h"
@@ -333,22 +333,52 @@ __global__ __launch_bounds__(kThreads) void first_layer_kernel(
         D[i] = seg_cost(S1, S2, 0, i);
 }
 
-// Node q of recursion level L over rows [0, n-1]: returns false if empty.
-__device__ __forceinline__ bool dc_node(int64_t n, int L, int64_t q, int64_t &lo,
-                                        int64_t &hi)
+// ---------------------------------------------------------------- layers
+//
+// Each layer is solved by F-ary divide and conquer: an interval of rows
+// [lo, hi] whose neighbours' optimal split points are known takes F evenly
+// spaced sample rows (all its rows if it has at most F) and computes their
+// leftmost argmins in parallel, each over the interval's bounds
+// [opt(lo-1), opt(hi+1)]; the F+1 gaps between samples are the next
+// level's intervals.  ceil(log_{F+1} n) levels replace the log2 n of a
+// binary split, which matters because every level is a dependent step.
+constexpr int kF = 64;
+constexpr int kShortScan = 32;        // longer ranges go to the work queue
+
+// Sample f of interval [lo, hi] (m = hi - lo + 1 rows): every row if m <= F,
+// else lo + (f + 1)(m + 1) / (F + 1) - 1; returns -1 if there is none.
+__device__ __forceinline__ int64_t sample_row(int64_t lo, int64_t hi, int f)
 {
+    const int64_t m = hi - lo + 1;
+    if (m <= kF)
+        return (f < m) ? lo + f : -1;
+    return lo + ((int64_t)(f + 1) * (m + 1)) / (kF + 1) - 1;
+}
+
+// Interval of node q at level L (digits of q in base F + 1, most significant
+// first, choose the gap between samples); false if the node does not exist.
+__device__ __forceinline__ bool fary_node(int64_t n, int L, int64_t q, int64_t &lo,
+                                          int64_t &hi)
+{
+    int dig[8];
+    for (int l = 0; l < L; ++l) {
+        dig[l] = (int)(q % (kF + 1));
+        q /= (kF + 1);
+    }
     lo = 0;
     hi = n - 1;
-    for (int b = L - 1; b >= 0; --b) {
+    for (int l = L - 1; l >= 0; --l) {
+        if (hi - lo + 1 <= kF)
+            return false;                     // a leaf interval has no gaps
+        const int c = dig[l];
+        const int64_t nlo = (c == 0) ? lo : sample_row(lo, hi, c - 1) + 1;
+        const int64_t nhi = (c == kF) ? hi : sample_row(lo, hi, c) - 1;
+        lo = nlo;
+        hi = nhi;
         if (lo > hi)
             return false;
-        const int64_t mid = lo + (hi - lo) / 2;
-        if ((q >> b) & 1)
-            lo = mid + 1;
-        else
-            hi = mid - 1;
     }
-    return lo <= hi;
+    return true;
 }
 
 // Leftmost-argmin merge of (value, index) pairs.
@@ -361,64 +391,192 @@ __device__ __forceinline__ void amin_merge(double &b, int64_t &a, double ob,
     }
 }
 
-// One recursion level of one layer.  G threads per node (G = 256: one
-// workgroup per node; G = 64: one wave per node).
-template <int G>
-__global__ __launch_bounds__(kThreads) void dc_level_kernel(
+// Scan split points j = from, from + stride, ... <= ahi for row r, keeping
+// the leftmost minimum of Dprev[j-1] + cost(j, r) over run starts.  Every
+// candidate is evaluated without branching so successive loads overlap.
+__device__ __forceinline__ void scan_range(const double *__restrict__ S1,
+                                           const double *__restrict__ S2,
+                                           const int32_t *__restrict__ run,
+                                           const double *__restrict__ Dprev,
+                                           int64_t r, int64_t from, int64_t ahi,
+                                           int64_t stride, double &best,
+                                           int64_t &arg)
+{
+#pragma unroll 4
+    for (int64_t j = from; j <= ahi; j += stride) {
+        const double cst = Dprev[j - 1] + seg_cost(S1, S2, j, r);
+        const double c = run[j] ? cst : INFINITY;
+        if (c < best) {
+            best = c;
+            arg = j;
+        }
+    }
+}
+
+__device__ __forceinline__ void wave_argmin(double &best, int64_t &arg)
+{
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const double ob = __shfl_xor(best, o, kWave);
+        const long long oa = __shfl_xor((long long)arg, o, kWave);
+        amin_merge(best, arg, ob, (int64_t)oa);
+    }
+}
+
+// Workgroup argmin; the result is valid in thread 0.
+__device__ __forceinline__ void block_argmin(double &best, int64_t &arg, double *rb,
+                                             int64_t *ra)
+{
+    wave_argmin(best, arg);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x % kWave) == 0) {
+        rb[w] = best;
+        ra[w] = arg;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0)
+        for (int i = 1; i < kThreads / kWave; ++i)
+            amin_merge(best, arg, rb[i], ra[i]);
+    __syncthreads();
+}
+
+// Row r of interval [lo, hi]: candidate split points [alo, ahi].
+__device__ __forceinline__ void row_bounds(const int32_t *__restrict__ opt, int64_t n,
+                                           int64_t lo, int64_t hi, int64_t r,
+                                           int64_t &alo, int64_t &ahi)
+{
+    const int64_t olo = (lo > 0) ? (int64_t)opt[lo - 1] : 1;
+    const int64_t ohi = (hi < n - 1) ? (int64_t)opt[hi + 1] : n - 1;
+    alo = olo < 1 ? 1 : olo;
+    ahi = ohi < r ? ohi : r;
+}
+
+__device__ __forceinline__ void store_result(double *__restrict__ Dcur,
+                                             int32_t *__restrict__ opt, int64_t r,
+                                             double best, int64_t arg, int64_t alo)
+{
+    Dcur[r] = best;
+    opt[r] = (int32_t)((arg == INT64_MAX) ? alo : arg);
+}
+
+// Wide levels (few items, long ranges): workgroup (item, b) scans part b of
+// item = (node, sample)'s range with stride B * 256; B == 1 writes the
+// result, otherwise a partial for fary_merge_kernel.
+__global__ __launch_bounds__(kThreads) void fary_wide_kernel(
     const double *__restrict__ S1, const double *__restrict__ S2,
     const int32_t *__restrict__ run, const double *__restrict__ Dprev,
     double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
-    int64_t nodes)
+    int B, double *__restrict__ pbest, int64_t *__restrict__ parg)
 {
-    constexpr int per_block = kThreads / G;
     __shared__ double rb[kThreads / kWave];
     __shared__ int64_t ra[kThreads / kWave];
-    const int64_t q = (int64_t)blockIdx.x * per_block + threadIdx.x / G;
-    const int t = threadIdx.x % G;
-    int64_t lo = 0, hi = -1;
-    const bool live = q < nodes && dc_node(n, L, q, lo, hi);
+    const int64_t item = blockIdx.x;
+    const int b = blockIdx.y;
+    int64_t lo, hi;
+    if (!fary_node(n, L, item / kF, lo, hi))
+        return;                                   // uniform per workgroup
+    const int64_t r = sample_row(lo, hi, (int)(item % kF));
+    if (r < 0)
+        return;
+    int64_t alo, ahi;
+    row_bounds(opt, n, lo, hi, r, alo, ahi);
     double best = INFINITY;
     int64_t arg = INT64_MAX;
-    int64_t mid = 0, alo = 1;
-    if (live) {
-        mid = lo + (hi - lo) / 2;
-        const int64_t olo = (lo > 0) ? (int64_t)opt[lo - 1] : 1;
-        const int64_t ohi = (hi < n - 1) ? (int64_t)opt[hi + 1] : n - 1;
-        alo = olo < 1 ? 1 : olo;
-        const int64_t ahi = ohi < mid ? ohi : mid;
-        for (int64_t j = alo + t; j <= ahi; j += G) {
-            if (!run[j])
-                continue;
-            const double c = Dprev[j - 1] + seg_cost(S1, S2, j, mid);
-            if (c < best) {
-                best = c;
-                arg = j;
-            }
+    scan_range(S1, S2, run, Dprev, r, alo + (int64_t)b * kThreads + threadIdx.x, ahi,
+               (int64_t)B * kThreads, best, arg);
+    block_argmin(best, arg, rb, ra);
+    if (threadIdx.x == 0) {
+        if (B == 1) {
+            store_result(Dcur, opt, r, best, arg, alo);
+        } else {
+            pbest[item * B + b] = best;
+            parg[item * B + b] = arg;
         }
     }
-    // reduce within the node's group of G lanes
-#pragma unroll
-    for (int o = (G < kWave ? G : kWave) / 2; o > 0; o >>= 1) {
-        const double ob = __shfl_xor(best, o, kWave);
-        const int64_t oa = __shfl_xor(arg, o, kWave);
-        amin_merge(best, arg, ob, oa);
+}
+
+__global__ __launch_bounds__(kThreads) void fary_merge_kernel(
+    const double *__restrict__ pbest, const int64_t *__restrict__ parg,
+    double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
+    int64_t items, int B)
+{
+    const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    int64_t lo, hi;
+    if (item >= items || !fary_node(n, L, item / kF, lo, hi))
+        return;
+    const int64_t r = sample_row(lo, hi, (int)(item % kF));
+    if (r < 0)
+        return;
+    int64_t alo, ahi;
+    row_bounds(opt, n, lo, hi, r, alo, ahi);
+    double best = INFINITY;
+    int64_t arg = INT64_MAX;
+    for (int b = 0; b < B; ++b)
+        amin_merge(best, arg, pbest[item * B + b], parg[item * B + b]);
+    store_result(Dcur, opt, r, best, arg, alo);
+}
+
+// Narrow levels (many items, mostly short ranges): a thread per item scans
+// a short range itself; a long one (a node straddling a jump of the
+// optimal split point) is appended to a work queue (order of entries does
+// not matter: each is finished independently and deterministically).
+struct QueueEntry {
+    int64_t r, alo, ahi;
+};
+
+__global__ __launch_bounds__(kThreads) void fary_narrow_kernel(
+    const double *__restrict__ S1, const double *__restrict__ S2,
+    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
+    double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
+    int64_t items, QueueEntry *__restrict__ queue, unsigned int *__restrict__ qlen)
+{
+    const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    int64_t lo, hi;
+    if (item >= items || !fary_node(n, L, item / kF, lo, hi))
+        return;
+    const int64_t r = sample_row(lo, hi, (int)(item % kF));
+    if (r < 0)
+        return;
+    int64_t alo, ahi;
+    row_bounds(opt, n, lo, hi, r, alo, ahi);
+    if (ahi - alo < kShortScan) {
+        double best = INFINITY;
+        int64_t arg = INT64_MAX;
+        scan_range(S1, S2, run, Dprev, r, alo, ahi, 1, best, arg);
+        store_result(Dcur, opt, r, best, arg, alo);
+    } else {
+        const unsigned int e = atomicAdd(qlen, 1u);
+        queue[e] = QueueEntry{r, alo, ahi};
     }
-    if (G > kWave) {
-        const int w = threadIdx.x / kWave;
-        if ((threadIdx.x % kWave) == 0) {
-            rb[w] = best;
-            ra[w] = arg;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            for (int i = 1; i < kThreads / kWave; ++i)
-                amin_merge(best, arg, rb[i], ra[i]);
-        }
+}
+
+// Work queue of long ranges: wave w of the grid takes entries w, w + waves,
+// ... and scans each with its 64 lanes (no workgroup barriers).
+__global__ __launch_bounds__(kThreads) void fary_queue_kernel(
+    const double *__restrict__ S1, const double *__restrict__ S2,
+    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
+    double *__restrict__ Dcur, int32_t *__restrict__ opt,
+    const QueueEntry *__restrict__ queue, const unsigned int *__restrict__ qlen)
+{
+    const unsigned int len = *qlen;
+    const unsigned int waves = gridDim.x * (kThreads / kWave);
+    const int lane = threadIdx.x % kWave;
+    for (unsigned int e = blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave; e < len;
+         e += waves) {
+        const QueueEntry q = queue[e];
+        double best = INFINITY;
+        int64_t arg = INT64_MAX;
+        scan_range(S1, S2, run, Dprev, q.r, q.alo + lane, q.ahi, kWave, best, arg);
+        wave_argmin(best, arg);
+        if (lane == 0)
+            store_result(Dcur, opt, q.r, best, arg, q.alo);
     }
-    if (live && t == 0) {
-        Dcur[mid] = best;
-        opt[mid] = (int32_t)((arg == INT64_MAX) ? alo : arg);
-    }
+}
+
+__global__ void clear_counters_kernel(unsigned int *c, int m)
+{
+    if (threadIdx.x < m)
+        c[threadIdx.x] = 0u;
 }
 
 __global__ void backtrack_kernel(const int32_t *__restrict__ opt, int64_t n,
@@ -481,7 +639,7 @@ inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct KmLayout {
     size_t keyA, keyB, idxA, idxB, hist, sv, run, t1, t2, S1, S2, Da, Db, opt,
-        sc, first, costs, total;
+        pbest, parg, queue, qlen, sc, first, costs, total;
 };
 
 KmLayout layout(int64_t n, int32_t k)
@@ -508,6 +666,10 @@ KmLayout layout(int64_t n, int32_t k)
     L.Da = take(n * 8);
     L.Db = take(n * 8);
     L.opt = take((size_t)k * n * 4);
+    L.pbest = take((size_t)(n + 1) * 8);
+    L.parg = take((size_t)(n + 1) * 8);
+    L.queue = take((size_t)(n + 1) * sizeof(QueueEntry));
+    L.qlen = take(64 * 4);
     L.sc = take(sizeof(KmScalars));
     L.first = take((size_t)(k + 1) * 8);
     L.costs = take((size_t)k * 8);
@@ -543,6 +705,10 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     double *S1 = (double *)(w + L.S1), *S2 = (double *)(w + L.S2);
     double *Da = (double *)(w + L.Da), *Db = (double *)(w + L.Db);
     int32_t *opt = (int32_t *)(w + L.opt);
+    double *pbest = (double *)(w + L.pbest);
+    int64_t *parg = (int64_t *)(w + L.parg);
+    QueueEntry *queue = (QueueEntry *)(w + L.queue);
+    unsigned int *qlen = (unsigned int *)(w + L.qlen);
     KmScalars *sc = (KmScalars *)(w + L.sc);
     int64_t *first = (int64_t *)(w + L.first);
     double *costs = (double *)(w + L.costs);
@@ -583,24 +749,39 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     // 3. layers
     hipLaunchKernelGGL(first_layer_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
                        S1, S2, n, Da);
-    int levels = 0;
-    while (levels < 63 && ((int64_t)1 << levels) <= n)
+    // levels of the F-ary recursion: until every interval has <= F rows
+    int levels = 1;
+    for (int64_t m = n; m > kF; m /= (kF + 1))     // gaps hold <= m / (F+1) rows
         ++levels;
     double *Dprev = Da, *Dcur = Db;
     for (int c = 1; c < ke; ++c) {
         int32_t *oc = opt + (int64_t)c * n;
-        for (int Lv = 0; Lv < levels; ++Lv) {
-            const int64_t nodes = (int64_t)1 << Lv;
-            if (nodes <= 2048) {
-                hipLaunchKernelGGL(dc_level_kernel<kThreads>, dim3((unsigned)nodes),
-                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur,
-                                   oc, n, Lv, nodes);
+        hipLaunchKernelGGL(clear_counters_kernel, dim3(1), dim3(64), 0, s, qlen, levels);
+        int64_t nodes = 1;
+        for (int Lv = 0; Lv < levels; ++Lv, nodes *= (kF + 1)) {
+            const int64_t items = nodes * kF;
+            const int64_t span = n / nodes;             // typical range of a node
+            if (span >= 2048) {
+                int64_t B = span / 2048;
+                if (B < 1)
+                    B = 1;
+                if (B > 256)
+                    B = 256;
+                hipLaunchKernelGGL(fary_wide_kernel, dim3((unsigned)items, (unsigned)B),
+                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur, oc,
+                                   n, Lv, (int)B, pbest, parg);
+                if (B > 1)
+                    hipLaunchKernelGGL(fary_merge_kernel,
+                                       dim3((unsigned)((items + kThreads - 1) / kThreads)),
+                                       dim3(kThreads), 0, s, pbest, parg, Dcur, oc, n,
+                                       Lv, items, (int)B);
             } else {
-                const int64_t per = kThreads / kWave;
-                hipLaunchKernelGGL(dc_level_kernel<kWave>,
-                                   dim3((unsigned)((nodes + per - 1) / per)),
-                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur,
-                                   oc, n, Lv, nodes);
+                hipLaunchKernelGGL(fary_narrow_kernel,
+                                   dim3((unsigned)((items + kThreads - 1) / kThreads)),
+                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur, oc,
+                                   n, Lv, items, queue, qlen + Lv);
+                hipLaunchKernelGGL(fary_queue_kernel, dim3(2048), dim3(kThreads), 0, s,
+                                   S1, S2, run, Dprev, Dcur, oc, queue, qlen + Lv);
             }
         }
         double *tmp = Dprev; Dprev = Dcur; Dcur = tmp;

@@ -9,6 +9,7 @@ benchmark times.
   and one product from the GPU's own iterate), plus invariants of the whole
   vector; a reduced n runs end to end.
 * kNN graph (CSR) at a reduced n, end to end.
+* 1-D k-means at the kNN workload's full size (n = 2,000,000, k = 50).
 """
 import numpy as np
 import pytest
@@ -136,6 +137,26 @@ def test_blobs64d_reduced_end_to_end(g, orc):
         assert matched_agreement(out.km.labels.cpu().numpy(), km.labels) >= 0.999
 
 
+def test_knn_csr_relabelled_matches_original(g):
+    """Renumbering the graph's nodes permutes v (up to summation order)."""
+    import workloads
+    w = workloads.make("knn8d", n=50000)
+    r = workloads.relabel_rcm(w)
+    outs = []
+    for x in (w, r):
+        outs.append(g.pic_csr(_t(x.row_ptr), _t(x.col), _t(x.val.copy()), x.k, "fixed",
+                              20))
+    perm = np.empty(w.n, dtype=np.int64)
+    # r.X[i] == w.X[perm_i]: recover perm from the points
+    order_w = np.lexsort(w.X.T[::-1])
+    order_r = np.lexsort(r.X.T[::-1])
+    perm[order_r] = order_w
+    assert np.array_equal(r.X, w.X[perm])
+    v0 = outs[0].pi.v.cpu().numpy()
+    v1 = outs[1].pi.v.cpu().numpy()
+    np.testing.assert_allclose(v1, v0[perm], rtol=1e-10)
+
+
 def test_knn_csr_reduced_end_to_end(g, orc):
     """kNN graph path at n = 100,000 (same generator), to convergence."""
     import workloads
@@ -152,3 +173,15 @@ def test_knn_csr_reduced_end_to_end(g, orc):
     assert ref.converged == out.pi.converged
     assert out.pi.iterations == ref.iterations
     assert rel_l1(out.pi.v.cpu().numpy(), ref.v) <= 1e-4
+
+
+def test_kmeans1d_full_size(g, orc):
+    """n = 2,000,000 scalars into k = 50 clusters: the exact optimum."""
+    from test_gpu_parity import _check_kmeans
+    rng = np.random.default_rng(2_000_050)
+    n, k = 2_000_000, 50
+    centres = np.sort(rng.uniform(0, 100, size=k))
+    v = centres[rng.integers(0, k, size=n)] + rng.standard_normal(n) * 0.5
+    print(f"gpu: kmeans1d n={n} k={k}", flush=True)
+    out = g.gpic_kmeans1d(_t(v), k)
+    _check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))

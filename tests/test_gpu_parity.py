@@ -269,10 +269,15 @@ def _check_kmeans(v, out, ref):
 
 
 @pytest.mark.parametrize("n,k,dup", [(1, 1, False), (2, 2, False), (5, 3, False),
+                                     (64, 8, False), (65, 8, False), (66, 8, True),
                                      (1000, 4, False), (4097, 10, False),
-                                     (4097, 10, True), (50000, 10, False),
-                                     (20000, 50, True)])
+                                     (4097, 10, True), (4225, 20, True),
+                                     (4291, 7, False), (50000, 10, False),
+                                     (20000, 50, True), (274626, 30, False),
+                                     (500000, 50, False)])
 def test_kmeans1d_parity(g, orc, n, k, dup):
+    """Sizes straddle the recursion's level counts (64 rows per interval and
+    65 children: n = 64 / 65, 4225 / 4291, 274625 / 274626)."""
     rng = np.random.default_rng(n + k)
     m = max(1, min(k, n))
     centres = np.sort(rng.uniform(0, 100, size=m))
@@ -282,6 +287,14 @@ def test_kmeans1d_parity(g, orc, n, k, dup):
     out = g.gpic_kmeans1d(_t(v), k)
     ref = orc.kmeans1d(v, k, "dc" if n > 2000 else "plain")
     _check_kmeans(v, out, ref)
+
+
+@pytest.mark.parametrize("n,k", [(30000, 50), (100000, 17)])
+def test_kmeans1d_unclustered(g, orc, n, k):
+    """Uniform values (no cluster structure): split points move smoothly."""
+    v = np.random.default_rng(n).uniform(-1.0, 1.0, size=n)
+    out = g.gpic_kmeans1d(_t(v), k)
+    _check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))
 
 
 def test_kmeans1d_special_values(g, orc):

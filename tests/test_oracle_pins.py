@@ -133,6 +133,16 @@ def test_uniform_vector_is_fixed_point(orc):
     assert r.stats[0] == pytest.approx(1.0 / n, rel=1e-12)
     assert r.stats[1] < 1e-15
 
+def test_stop_test_is_less_or_equal(orc):
+    """The stop test is "<=" (Algorithms 1 and 2).  Two points with
+    v0 = (1/2, 1/2) are exact in floating point: the statistic is 1/2, then
+    exactly 0, so even eps = 0 stops the run after 2 products."""
+    X = np.array([[0, 0], [1, 0]], dtype=np.float32)
+    W, _, v0, _ = orc.degree_normalize(orc.affinity(X, 1.0))
+    r = orc.power_iterate_dense(W, v0, "converge", 50, 0.0)
+    assert r.converged and r.iterations == 2
+    assert list(r.stats) == [0.5, 0.0]
+
 
 def _block_diag_constant(sizes, consts):
     n = sum(sizes)

@@ -263,6 +263,26 @@ def _c5(seed, n, cache_dir=None):
                     "converge", 1000, "csr", seed, rp, col, val)
 
 
+def relabel_rcm(w: Workload) -> Workload:
+    """The same graph and points with nodes renumbered by reverse
+    Cuthill-McKee (scipy), so that neighbours get nearby numbers.  Point i of
+    the result is point perm[i] of the input; rows stay sorted by column."""
+    import scipy.sparse as sp
+    from scipy.sparse.csgraph import reverse_cuthill_mckee
+    S = sp.csr_matrix((w.val, w.col, w.row_ptr), shape=(w.n, w.n))
+    perm = reverse_cuthill_mckee(S, symmetric_mode=True)
+    P = S[perm][:, perm].tocsr()
+    P.sort_indices()
+    return Workload(w.name + "_rcm", np.ascontiguousarray(w.X[perm]),
+                    np.ascontiguousarray(w.y_true[perm]), w.sigma, w.eps, w.k,
+                    w.mode, w.max_iter, w.path, w.seed, P.indptr.astype(np.int64),
+                    P.indices.astype(np.int32), P.data.astype(np.float32))
+
+
+def _c5_rcm(seed, n, cache_dir=None):
+    return relabel_rcm(_c5(seed, n, cache_dir))
+
+
 WORKLOADS = {
     # n=1,000, d=2, 3 blobs (centres U[-10,10]^2), sigma 1, to convergence
     "blobs2d": (_c1, 1),
@@ -275,6 +295,8 @@ WORKLOADS = {
     "blobs64d": (_c4, 4),
     # n=2,000,000, d=8, 50 blobs, 32-NN union graph, CSR, to convergence
     "knn8d": (_c5, 5),
+    # the same graph with nodes renumbered by reverse Cuthill-McKee
+    "knn8d_rcm": (_c5_rcm, 5),
 }
 
 
@@ -283,6 +305,6 @@ def make(name: str, seed: Optional[int] = None, n: Optional[int] = None,
     """Build a named workload; `n` shrinks it for quick parity cases."""
     fn, default_seed = WORKLOADS[name]
     s = default_seed if seed is None else seed
-    if name == "knn8d":
+    if name in ("knn8d", "knn8d_rcm"):
         return fn(s, n, cache_dir)
     return fn(s, n)
