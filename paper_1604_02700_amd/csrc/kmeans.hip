@@ -326,11 +326,13 @@ __device__ __forceinline__ double seg_cost(const double *__restrict__ S1,
 
 __global__ __launch_bounds__(kThreads) void first_layer_kernel(
     const double *__restrict__ S1, const double *__restrict__ S2, int64_t n,
-    double *__restrict__ D)
+    double *__restrict__ D, unsigned long long *__restrict__ qlen)
 {
     const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (i < n)
         D[i] = seg_cost(S1, S2, 0, i);
+    if (i < 4)
+        qlen[i] = 0ull;                 // the recursion's part and row counters
 }
 
 // ---------------------------------------------------------------- layers
@@ -344,6 +346,7 @@ __global__ __launch_bounds__(kThreads) void first_layer_kernel(
 // binary split, which matters because every level is a dependent step.
 constexpr int kF = 64;
 constexpr int kShortScan = 32;        // longer ranges go to the work queue
+constexpr int kChunk = 1024;          // candidates per queued part (16 per lane)
 
 // Sample f of interval [lo, hi] (m = hi - lo + 1 rows): every row if m <= F,
 // else lo + (f + 1)(m + 1) / (F + 1) - 1; returns -1 if there is none.
@@ -423,23 +426,6 @@ __device__ __forceinline__ void wave_argmin(double &best, int64_t &arg)
     }
 }
 
-// Workgroup argmin; the result is valid in thread 0.
-__device__ __forceinline__ void block_argmin(double &best, int64_t &arg, double *rb,
-                                             int64_t *ra)
-{
-    wave_argmin(best, arg);
-    const int w = threadIdx.x / kWave;
-    if ((threadIdx.x % kWave) == 0) {
-        rb[w] = best;
-        ra[w] = arg;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0)
-        for (int i = 1; i < kThreads / kWave; ++i)
-            amin_merge(best, arg, rb[i], ra[i]);
-    __syncthreads();
-}
-
 // Row r of interval [lo, hi]: candidate split points [alo, ahi].
 __device__ __forceinline__ void row_bounds(const int32_t *__restrict__ opt, int64_t n,
                                            int64_t lo, int64_t hi, int64_t r,
@@ -459,124 +445,132 @@ __device__ __forceinline__ void store_result(double *__restrict__ Dcur,
     opt[r] = (int32_t)((arg == INT64_MAX) ? alo : arg);
 }
 
-// Wide levels (few items, long ranges): workgroup (item, b) scans part b of
-// item = (node, sample)'s range with stride B * 256; B == 1 writes the
-// result, otherwise a partial for fary_merge_kernel.
-__global__ __launch_bounds__(kThreads) void fary_wide_kernel(
+// A queued part: candidates [alo, ahi] of row r; head is the slot of the
+// row's first part (its part count lives there).  r < 0
+// marks a slot that holds no work.
+struct QueuePart {
+    int32_t r, alo, ahi, head;
+};
+
+struct LevelQueue {
+    QueuePart *part;
+    int32_t *nparts;                     // indexed by head
+    int32_t *heads;                      // heads of rows with more than one part
+    double *pbest;                       // per part
+    int32_t *parg;
+    unsigned long long *qlen;            // parts: [g & 1]; rows: [2 + (g & 1)]
+    int64_t cap;
+};
+
+// One recursion level: a thread per (node, sample).  A short range is
+// scanned by the thread itself; a long one is cut into parts of kChunk
+// candidates appended to the queue (the order of appends does not matter:
+// every row's parts are merged by an order-independent minimum).  Item 0
+// clears the other pair of counters, whose level has finished.
+__global__ __launch_bounds__(kThreads) void fary_level_kernel(
     const double *__restrict__ S1, const double *__restrict__ S2,
     const int32_t *__restrict__ run, const double *__restrict__ Dprev,
     double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
-    int B, double *__restrict__ pbest, int64_t *__restrict__ parg)
+    int64_t items, LevelQueue Q, int g)
 {
-    __shared__ double rb[kThreads / kWave];
-    __shared__ int64_t ra[kThreads / kWave];
-    const int64_t item = blockIdx.x;
-    const int b = blockIdx.y;
+    const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (item == 0) {
+        Q.qlen[(g + 1) & 1] = 0ull;
+        Q.qlen[2 + ((g + 1) & 1)] = 0ull;
+    }
     int64_t lo, hi;
-    if (!fary_node(n, L, item / kF, lo, hi))
-        return;                                   // uniform per workgroup
+    if (item >= items || !fary_node(n, L, item / kF, lo, hi))
+        return;
     const int64_t r = sample_row(lo, hi, (int)(item % kF));
     if (r < 0)
         return;
     int64_t alo, ahi;
     row_bounds(opt, n, lo, hi, r, alo, ahi);
+    const int64_t len = ahi - alo + 1;
+    if (len > kShortScan) {
+        const int64_t C = (len + kChunk - 1) / kChunk;
+        const int64_t e0 = (int64_t)atomicAdd(&Q.qlen[g & 1], (unsigned long long)C);
+        if (e0 + C <= Q.cap) {
+            Q.nparts[e0] = (int32_t)C;
+            if (C > 1) {
+                const unsigned long long h = atomicAdd(&Q.qlen[2 + (g & 1)], 1ull);
+                Q.heads[h] = (int32_t)e0;             // h < e0 + 1 <= cap
+            }
+            for (int64_t p = 0; p < C; ++p) {
+                const int64_t plo = alo + p * kChunk;
+                const int64_t phi = plo + kChunk - 1 < ahi ? plo + kChunk - 1 : ahi;
+                Q.part[e0 + p] = QueuePart{(int32_t)r, (int32_t)plo, (int32_t)phi,
+                                           (int32_t)e0};
+            }
+            return;
+        }
+        // no room left (only if split points were far from monotone):
+        // void the reserved slots below the capacity and scan here
+        for (int64_t e = e0; e < e0 + C && e < Q.cap; ++e)
+            Q.part[e] = QueuePart{-1, 0, -1, 0};
+    }
     double best = INFINITY;
     int64_t arg = INT64_MAX;
-    scan_range(S1, S2, run, Dprev, r, alo + (int64_t)b * kThreads + threadIdx.x, ahi,
-               (int64_t)B * kThreads, best, arg);
-    block_argmin(best, arg, rb, ra);
-    if (threadIdx.x == 0) {
-        if (B == 1) {
-            store_result(Dcur, opt, r, best, arg, alo);
-        } else {
-            pbest[item * B + b] = best;
-            parg[item * B + b] = arg;
+    scan_range(S1, S2, run, Dprev, r, alo, ahi, 1, best, arg);
+    store_result(Dcur, opt, r, best, arg, alo);
+}
+
+// The level's queued parts: wave w of the grid takes parts w, w + waves, ...
+// and scans each with its 64 lanes.  A row with one part is finished here;
+// otherwise the part leaves its minimum for fary_merge_kernel.
+__global__ __launch_bounds__(kThreads) void fary_queue_kernel(
+    const double *__restrict__ S1, const double *__restrict__ S2,
+    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
+    double *__restrict__ Dcur, int32_t *__restrict__ opt, LevelQueue Q, int g)
+{
+    const int64_t total = (int64_t)Q.qlen[g & 1];
+    const int64_t len = total < Q.cap ? total : Q.cap;
+    const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
+    const int lane = threadIdx.x % kWave;
+    for (int64_t e = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
+         e < len; e += waves) {
+        const QueuePart q = Q.part[e];
+        if (q.r < 0)
+            continue;                                   // uniform per wave
+        double best = INFINITY;
+        int64_t arg = INT64_MAX;
+        scan_range(S1, S2, run, Dprev, q.r, (int64_t)q.alo + lane, q.ahi, kWave, best,
+                   arg);
+        wave_argmin(best, arg);
+        if (lane == 0) {
+            if (Q.nparts[q.head] == 1) {
+                store_result(Dcur, opt, q.r, best, arg, q.alo);
+            } else {
+                Q.pbest[e] = best;
+                Q.parg[e] = (arg == INT64_MAX) ? INT32_MAX : (int32_t)arg;
+            }
         }
     }
 }
 
+// Rows with several parts: a wave per row merges its parts' minima.
 __global__ __launch_bounds__(kThreads) void fary_merge_kernel(
-    const double *__restrict__ pbest, const int64_t *__restrict__ parg,
-    double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
-    int64_t items, int B)
+    double *__restrict__ Dcur, int32_t *__restrict__ opt, LevelQueue Q, int g)
 {
-    const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    int64_t lo, hi;
-    if (item >= items || !fary_node(n, L, item / kF, lo, hi))
-        return;
-    const int64_t r = sample_row(lo, hi, (int)(item % kF));
-    if (r < 0)
-        return;
-    int64_t alo, ahi;
-    row_bounds(opt, n, lo, hi, r, alo, ahi);
-    double best = INFINITY;
-    int64_t arg = INT64_MAX;
-    for (int b = 0; b < B; ++b)
-        amin_merge(best, arg, pbest[item * B + b], parg[item * B + b]);
-    store_result(Dcur, opt, r, best, arg, alo);
-}
-
-// Narrow levels (many items, mostly short ranges): a thread per item scans
-// a short range itself; a long one (a node straddling a jump of the
-// optimal split point) is appended to a work queue (order of entries does
-// not matter: each is finished independently and deterministically).
-struct QueueEntry {
-    int64_t r, alo, ahi;
-};
-
-__global__ __launch_bounds__(kThreads) void fary_narrow_kernel(
-    const double *__restrict__ S1, const double *__restrict__ S2,
-    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
-    double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
-    int64_t items, QueueEntry *__restrict__ queue, unsigned int *__restrict__ qlen)
-{
-    const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    int64_t lo, hi;
-    if (item >= items || !fary_node(n, L, item / kF, lo, hi))
-        return;
-    const int64_t r = sample_row(lo, hi, (int)(item % kF));
-    if (r < 0)
-        return;
-    int64_t alo, ahi;
-    row_bounds(opt, n, lo, hi, r, alo, ahi);
-    if (ahi - alo < kShortScan) {
-        double best = INFINITY;
-        int64_t arg = INT64_MAX;
-        scan_range(S1, S2, run, Dprev, r, alo, ahi, 1, best, arg);
-        store_result(Dcur, opt, r, best, arg, alo);
-    } else {
-        const unsigned int e = atomicAdd(qlen, 1u);
-        queue[e] = QueueEntry{r, alo, ahi};
-    }
-}
-
-// Work queue of long ranges: wave w of the grid takes entries w, w + waves,
-// ... and scans each with its 64 lanes (no workgroup barriers).
-__global__ __launch_bounds__(kThreads) void fary_queue_kernel(
-    const double *__restrict__ S1, const double *__restrict__ S2,
-    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
-    double *__restrict__ Dcur, int32_t *__restrict__ opt,
-    const QueueEntry *__restrict__ queue, const unsigned int *__restrict__ qlen)
-{
-    const unsigned int len = *qlen;
-    const unsigned int waves = gridDim.x * (kThreads / kWave);
+    const int64_t nh = (int64_t)Q.qlen[2 + (g & 1)];
+    const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
     const int lane = threadIdx.x % kWave;
-    for (unsigned int e = blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave; e < len;
-         e += waves) {
-        const QueueEntry q = queue[e];
+    for (int64_t h = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
+         h < nh; h += waves) {
+        const int64_t head = Q.heads[h];
+        const QueuePart q = Q.part[head];
+        const int C = Q.nparts[head];
         double best = INFINITY;
         int64_t arg = INT64_MAX;
-        scan_range(S1, S2, run, Dprev, q.r, q.alo + lane, q.ahi, kWave, best, arg);
+        for (int p = lane; p < C; p += kWave) {
+            const int32_t a = Q.parg[head + p];
+            amin_merge(best, arg, Q.pbest[head + p],
+                       a == INT32_MAX ? INT64_MAX : (int64_t)a);
+        }
         wave_argmin(best, arg);
         if (lane == 0)
             store_result(Dcur, opt, q.r, best, arg, q.alo);
     }
-}
-
-__global__ void clear_counters_kernel(unsigned int *c, int m)
-{
-    if (threadIdx.x < m)
-        c[threadIdx.x] = 0u;
 }
 
 __global__ void backtrack_kernel(const int32_t *__restrict__ opt, int64_t n,
@@ -639,8 +633,14 @@ inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct KmLayout {
     size_t keyA, keyB, idxA, idxB, hist, sv, run, t1, t2, S1, S2, Da, Db, opt,
-        pbest, parg, queue, qlen, sc, first, costs, total;
+        qpart, qnparts, qheads, qbest, qarg, qlen, sc, first, costs, total;
 };
+
+// Queue slots per level.  With monotone split points the ranges of one
+// level overlap only at their ends, so they hold at most 2 F n candidates
+// and at most n + 2 F n / kChunk parts; a level that would need more
+// scans the excess in place.
+int64_t queue_cap(int64_t n) { return n + (2 * kF * n) / kChunk + 1024; }
 
 KmLayout layout(int64_t n, int32_t k)
 {
@@ -666,10 +666,13 @@ KmLayout layout(int64_t n, int32_t k)
     L.Da = take(n * 8);
     L.Db = take(n * 8);
     L.opt = take((size_t)k * n * 4);
-    L.pbest = take((size_t)(n + 1) * 8);
-    L.parg = take((size_t)(n + 1) * 8);
-    L.queue = take((size_t)(n + 1) * sizeof(QueueEntry));
-    L.qlen = take(64 * 4);
+    const size_t cap = (size_t)queue_cap(n);
+    L.qpart = take(cap * sizeof(QueuePart));
+    L.qnparts = take(cap * 4);
+    L.qheads = take(cap * 4);
+    L.qbest = take(cap * 8);
+    L.qarg = take(cap * 4);
+    L.qlen = take(4 * 8);
     L.sc = take(sizeof(KmScalars));
     L.first = take((size_t)(k + 1) * 8);
     L.costs = take((size_t)k * 8);
@@ -705,10 +708,14 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     double *S1 = (double *)(w + L.S1), *S2 = (double *)(w + L.S2);
     double *Da = (double *)(w + L.Da), *Db = (double *)(w + L.Db);
     int32_t *opt = (int32_t *)(w + L.opt);
-    double *pbest = (double *)(w + L.pbest);
-    int64_t *parg = (int64_t *)(w + L.parg);
-    QueueEntry *queue = (QueueEntry *)(w + L.queue);
-    unsigned int *qlen = (unsigned int *)(w + L.qlen);
+    LevelQueue Q;
+    Q.part = (QueuePart *)(w + L.qpart);
+    Q.nparts = (int32_t *)(w + L.qnparts);
+    Q.heads = (int32_t *)(w + L.qheads);
+    Q.pbest = (double *)(w + L.qbest);
+    Q.parg = (int32_t *)(w + L.qarg);
+    Q.qlen = (unsigned long long *)(w + L.qlen);
+    Q.cap = queue_cap(n);
     KmScalars *sc = (KmScalars *)(w + L.sc);
     int64_t *first = (int64_t *)(w + L.first);
     double *costs = (double *)(w + L.costs);
@@ -748,41 +755,26 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
 
     // 3. layers
     hipLaunchKernelGGL(first_layer_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
-                       S1, S2, n, Da);
+                       S1, S2, n, Da, Q.qlen);
     // levels of the F-ary recursion: until every interval has <= F rows
     int levels = 1;
     for (int64_t m = n; m > kF; m /= (kF + 1))     // gaps hold <= m / (F+1) rows
         ++levels;
     double *Dprev = Da, *Dcur = Db;
+    int g = 0;                                     // levels run so far
     for (int c = 1; c < ke; ++c) {
         int32_t *oc = opt + (int64_t)c * n;
-        hipLaunchKernelGGL(clear_counters_kernel, dim3(1), dim3(64), 0, s, qlen, levels);
         int64_t nodes = 1;
-        for (int Lv = 0; Lv < levels; ++Lv, nodes *= (kF + 1)) {
+        for (int Lv = 0; Lv < levels; ++Lv, nodes *= (kF + 1), ++g) {
             const int64_t items = nodes * kF;
-            const int64_t span = n / nodes;             // typical range of a node
-            if (span >= 2048) {
-                int64_t B = span / 2048;
-                if (B < 1)
-                    B = 1;
-                if (B > 256)
-                    B = 256;
-                hipLaunchKernelGGL(fary_wide_kernel, dim3((unsigned)items, (unsigned)B),
-                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur, oc,
-                                   n, Lv, (int)B, pbest, parg);
-                if (B > 1)
-                    hipLaunchKernelGGL(fary_merge_kernel,
-                                       dim3((unsigned)((items + kThreads - 1) / kThreads)),
-                                       dim3(kThreads), 0, s, pbest, parg, Dcur, oc, n,
-                                       Lv, items, (int)B);
-            } else {
-                hipLaunchKernelGGL(fary_narrow_kernel,
-                                   dim3((unsigned)((items + kThreads - 1) / kThreads)),
-                                   dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur, oc,
-                                   n, Lv, items, queue, qlen + Lv);
-                hipLaunchKernelGGL(fary_queue_kernel, dim3(2048), dim3(kThreads), 0, s,
-                                   S1, S2, run, Dprev, Dcur, oc, queue, qlen + Lv);
-            }
+            hipLaunchKernelGGL(fary_level_kernel,
+                               dim3((unsigned)((items + kThreads - 1) / kThreads)),
+                               dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur, oc, n, Lv,
+                               items, Q, g);
+            hipLaunchKernelGGL(fary_queue_kernel, dim3(2048), dim3(kThreads), 0, s, S1,
+                               S2, run, Dprev, Dcur, oc, Q, g);
+            hipLaunchKernelGGL(fary_merge_kernel, dim3(512), dim3(kThreads), 0, s, Dcur,
+                               oc, Q, g);
         }
         double *tmp = Dprev; Dprev = Dcur; Dcur = tmp;
     }
