@@ -1,4 +1,5 @@
-// Power-iteration kernels for gfx950: the product y = W v (dense, CSR),
+// Power-iteration kernels for gfx950: the CSR product y = W v (the dense
+// product is in gemv.hip),
 // the L1 norm tau = sum_i |y_i|, and the update
 //   v_{t+1} = y / tau,  delta_{t+1} = |v_{t+1} - v_t|,
 //   s_t = max_i |delta_{t+1,i} - delta_{t,i}|
@@ -17,102 +18,15 @@ namespace gpic {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kGemvRows = 4;        // rows per workgroup of the dense product
-constexpr int kGemvThreads = 512;   // threads per workgroup of the dense product
 constexpr int kSpmvLanes = 16;      // lanes per CSR row
-constexpr int kSpmvRows = 128;      // rows per workgroup of the CSR product
+constexpr int kSpmvRows = 32;       // rows per workgroup of the CSR product
+constexpr int kSpmvUnroll = 4;      // independent gathers in flight per lane
 
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-
-// Dense product.  A workgroup owns kGemvRows consecutive rows; every thread
-// takes 16-byte column groups c, c + NT, ... and keeps one float64
-// accumulator per row, so each 32-byte slice of v it loads is reused across
-// all rows of the block.  W is streamed exactly once per product, so its
-// loads are non-temporal (they do not displace v, which every workgroup
-// re-reads, from the caches).  Rows past n are clamped for loading and
-// never written.
-template <int R, int NT>
-__global__ __launch_bounds__(NT) void gemv_kernel(
-    const float *__restrict__ W, int64_t n, int64_t ldw,
-    const double *__restrict__ v, double *__restrict__ y,
-    double *__restrict__ partial, StopCtl ctl, int use_ctl)
-{
-    __shared__ double red[R][NT / kWave];
-    if (use_ctl) {
-        if (blockIdx.x == 0 && threadIdx.x == 0)
-            *ctl.cur_stat = 0.0;
-        if (stop_reached(ctl))
-            return;
-    }
-    const int64_t row0 = (int64_t)blockIdx.x * R;
-    const floatx4 *rp[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int64_t i = (row0 + r < n) ? row0 + r : n - 1;
-        rp[r] = reinterpret_cast<const floatx4 *>(W + i * ldw);
-    }
-    double acc[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-        acc[r] = 0.0;
-
-    const int64_t n4 = n >> 2;
-    const double2 *v2 = reinterpret_cast<const double2 *>(v);
-#pragma unroll 2
-    for (int64_t c = threadIdx.x; c < n4; c += NT) {
-        floatx4 w[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-            w[r] = __builtin_nontemporal_load(rp[r] + c);
-        const double2 va = v2[2 * c];
-        const double2 vb = v2[2 * c + 1];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            acc[r] = fma((double)w[r].x, va.x, acc[r]);
-            acc[r] = fma((double)w[r].y, va.y, acc[r]);
-            acc[r] = fma((double)w[r].z, vb.x, acc[r]);
-            acc[r] = fma((double)w[r].w, vb.y, acc[r]);
-        }
-    }
-    const int64_t tail = n - (n4 << 2);
-    if (threadIdx.x < tail) {
-        const int64_t j = (n4 << 2) + threadIdx.x;
-        const double vj = v[j];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const float *row = reinterpret_cast<const float *>(rp[r]);
-            acc[r] = fma((double)row[j], vj, acc[r]);
-        }
-    }
-    const int wave = threadIdx.x / kWave;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const double t = wave_sum(acc[r]);
-        if ((threadIdx.x % kWave) == 0)
-            red[r][wave] = t;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        double part = 0.0;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            double t = 0.0;
-#pragma unroll
-            for (int w = 0; w < NT / kWave; ++w)
-                t += red[r][w];
-            if (row0 + r < n) {
-                y[row0 + r] = t;
-                part += fabs(t);
-            }
-        }
-        if (partial != nullptr)
-            partial[blockIdx.x] = part;
-    }
-}
-
-// CSR product: 16 lanes per row, lane-strided over the row's entries, a
-// 16-lane butterfly per row; a workgroup walks kSpmvRows rows in passes of
-// 16.
+// CSR product: 16 lanes per row, lane l summing entries l, l + 16, ... of
+// its row in that order, then a 16-lane butterfly.  The workgroup's row
+// pointers are staged in LDS first, and each lane issues kSpmvUnroll column
+// loads and then kSpmvUnroll gathers of v before using any of them, so
+// several gathers are in flight per lane (the order of the sum is unchanged).
 __global__ __launch_bounds__(kThreads) void spmv_kernel(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
     const float *__restrict__ val, int64_t n, const double *__restrict__ v,
@@ -120,23 +34,45 @@ __global__ __launch_bounds__(kThreads) void spmv_kernel(
     int use_ctl)
 {
     __shared__ double red[kThreads / kWave];
+    __shared__ int64_t rp[kSpmvRows + 1];
     if (use_ctl) {
         if (blockIdx.x == 0 && threadIdx.x == 0)
             *ctl.cur_stat = 0.0;
         if (stop_reached(ctl))
             return;
     }
+    const int64_t base = (int64_t)blockIdx.x * kSpmvRows;
+    for (int t = threadIdx.x; t <= kSpmvRows; t += kThreads)
+        rp[t] = row_ptr[base + t < n ? base + t : n];
+    __syncthreads();
     const int sl = threadIdx.x % kSpmvLanes;
     const int grp = threadIdx.x / kSpmvLanes;
     constexpr int groups = kThreads / kSpmvLanes;
     double part = 0.0;
     for (int pass = 0; pass < kSpmvRows / groups; ++pass) {
-        const int64_t i = (int64_t)blockIdx.x * kSpmvRows + pass * groups + grp;
+        const int li = pass * groups + grp;
+        const int64_t i = base + li;
         double s = 0.0;
         if (i < n) {
-            const int64_t b = row_ptr[i], e = row_ptr[i + 1];
-            for (int64_t p = b + sl; p < e; p += kSpmvLanes)
-                s = fma((double)val[p], v[col[p]], s);
+            const int64_t b = rp[li], e = rp[li + 1];
+            for (int64_t p0 = b + sl; p0 < e; p0 += kSpmvLanes * kSpmvUnroll) {
+                int32_t c[kSpmvUnroll];
+                float w[kSpmvUnroll];
+                double x[kSpmvUnroll];
+#pragma unroll
+                for (int u = 0; u < kSpmvUnroll; ++u) {
+                    const int64_t p = p0 + (int64_t)u * kSpmvLanes;
+                    c[u] = p < e ? col[p] : -1;
+                    w[u] = p < e ? val[p] : 0.0f;
+                }
+#pragma unroll
+                for (int u = 0; u < kSpmvUnroll; ++u)
+                    x[u] = c[u] >= 0 ? v[c[u]] : 0.0;
+#pragma unroll
+                for (int u = 0; u < kSpmvUnroll; ++u)
+                    if (c[u] >= 0)
+                        s = fma((double)w[u], x[u], s);
+            }
         }
         s = group_sum<kSpmvLanes>(s);
         if (i < n && sl == 0) {
@@ -221,18 +157,7 @@ unsigned grid_for(int64_t n, int64_t cap)
 
 } // namespace
 
-int64_t gemv_blocks(int64_t n) { return (n + kGemvRows - 1) / kGemvRows; }
 int64_t spmv_blocks(int64_t n) { return (n + kSpmvRows - 1) / kSpmvRows; }
-
-hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
-                       double *y, double *partial, StopCtl ctl, bool use_ctl,
-                       hipStream_t s)
-{
-    hipLaunchKernelGGL((gemv_kernel<kGemvRows, kGemvThreads>),
-                       dim3((unsigned)gemv_blocks(n)), dim3(kGemvThreads), 0, s, W,
-                       n, ldw, v, y, partial, ctl, use_ctl ? 1 : 0);
-    return hipGetLastError();
-}
 
 hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
                        const float *val, int64_t n, const double *v, double *y,
