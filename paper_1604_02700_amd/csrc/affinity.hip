@@ -12,9 +12,11 @@
 //     operands [-2c x_i, c, c |x_i|^2], so one fp32 Gram product gives
 //     c (|x_i|^2 + |x_j|^2 - 2 x_i.x_j); it is clamped at 0 before exp2.
 //     A prologue kernel writes both augmented operand arrays once per call
-//     (squared norms as float64 sums rounded to float32, rows padded with
-//     zeros to a multiple of 64), so staging a column tile is a contiguous
-//     16-byte copy.
+//     (squared norms as float64 sums rounded to float32, points padded with
+//     zeros to a multiple of 64); the column operand is stored coordinate-
+//     major, so a column tile is staged into LDS by contiguous 16-byte
+//     copies and every wave reads its matrix-core operands for four column
+//     blocks with one conflict-free 16-byte LDS read.
 //   * VALU, other d: squared distances from coordinate differences.
 // A workgroup owns a block of rows and a range of columns (a chunk); when
 // the rows alone would not fill the chip the columns are split in chunks,
@@ -58,8 +60,8 @@ __device__ __forceinline__ void store4(float *dst, float a, float b, float c, fl
 // ------------------------------------------------------------ prologue
 
 // Augmented operands, KP floats per point (KP = 4 KS >= d + 2):
-//   xa[p] = [x_p, |x_p|^2, 1, 0...]          (column operand)
-//   xb[p] = [-2c x_p, c, c |x_p|^2, 0...]    (row operand)
+//   column operand, coordinate-major: xa[k * np + p] = [x_p, |x_p|^2, 1, 0...]_k
+//   row operand, point-major:         xb[p * KP + k] = [-2c x_p, c, c |x_p|^2, 0...]_k
 // |x_p|^2 is a float64 sum rounded once to float32.  Points n .. np-1
 // (padding up to a multiple of the column tile) are all zeros.
 __global__ __launch_bounds__(kThreads) void augment_kernel(
@@ -69,11 +71,11 @@ __global__ __launch_bounds__(kThreads) void augment_kernel(
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (p >= np)
         return;
-    float *a = xa + p * KP;
+    float *a = xa + p;                            // stride np
     float *b = xb + p * KP;
     if (p >= n) {
         for (int k = 0; k < KP; ++k) {
-            a[k] = 0.0f;
+            a[k * np] = 0.0f;
             b[k] = 0.0f;
         }
         return;
@@ -87,16 +89,16 @@ __global__ __launch_bounds__(kThreads) void augment_kernel(
     for (int k = 0; k < KP; ++k) {
         if (k < d) {
             const float x = X[p * d + k];
-            a[k] = x;
+            a[k * np] = x;
             b[k] = -2.0f * c * x;
         } else if (k == d) {
-            a[k] = nrm;
+            a[k * np] = nrm;
             b[k] = c;
         } else if (k == d + 1) {
-            a[k] = 1.0f;
+            a[k * np] = 1.0f;
             b[k] = c * nrm;
         } else {
-            a[k] = 0.0f;
+            a[k * np] = 0.0f;
             b[k] = 0.0f;
         }
     }
@@ -139,34 +141,40 @@ __global__ __launch_bounds__(kThreads) void chunk_reduce_kernel(
 
 // ------------------------------------------------------------------ MFMA
 
-// Workgroup: 4 waves x 16 rows = 64 rows; columns [c0, c1) of its chunk in
-// tiles of 64 staged through double-buffered LDS.
+// Workgroup: kMfmaWaves waves x 16 rows; columns [c0, c1) of its chunk in
+// tiles of 64 staged through double-buffered LDS, coordinate-major: tile
+// column c of coordinate k sits at xs[k][c ^ (16 (k % 4))].  The XOR
+// swizzle spreads the four coordinates a wave reads at once over all 64
+// banks (conflict-free 4-byte reads) and keeps 4-column groups contiguous
+// for 16-byte staging writes.
 //
 // v_mfma_f32_16x16x4f32 operand layout (lane l, g = l / 16, m = l % 16):
 //   A operand : element (row m,  k = g)
 //   B operand : element (k = g,  column m)
 //   result    : elements (row 4g + r, column m), r = 0..3
-// The A operand carries 16 affinity columns j and the B operand the wave's
-// 16 rows i, so every lane ends with one row i and four consecutive
-// columns: one 16-byte store per lane.  K-step s, slot g holds augmented
-// coordinate 4 s + g.
+// The A operand of block q (q = 0..3) carries tile columns 16 q + a and
+// the B operand the wave's 16 rows i.  Lane (m, g) ends with row i and
+// columns 16 q + 4 g + r: per block one 16-byte store, and the four lanes
+// of a row write 64 contiguous bytes.
+constexpr int kMfmaWaves = 4;                 // waves (16 rows each) per workgroup
+constexpr int kMfmaThreads = kMfmaWaves * 64;
 constexpr int kRowsPerWave = 16;
-constexpr int kRowsPerGroup = 4 * kRowsPerWave;
+constexpr int kRowsPerGroup = kMfmaWaves * kRowsPerWave;
 constexpr int kTileCols = 64;
 
 template <int KS, int MODE>
-__global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
-    const float *__restrict__ xa, const float *__restrict__ xb, int64_t n,
+__global__ __launch_bounds__(kMfmaThreads) void affinity_mfma_kernel(
+    const float *__restrict__ xa, int64_t np, const float *__restrict__ xb, int64_t n,
     int64_t chunk_cols, float *__restrict__ A, int64_t lda,
     const double *__restrict__ v, const double *__restrict__ degree_in,
     double *__restrict__ out, double *__restrict__ part,
     double *__restrict__ partial, StopCtl ctl, int use_ctl)
 {
-    constexpr int KP = 4 * KS;   // augmented, padded dimension
-    constexpr int LS = KP + 1;   // LDS row stride (odd: no bank conflicts)
-    __shared__ float xs[2][kTileCols * LS];
+    constexpr int KP = 4 * KS;               // augmented, padded dimension
+    constexpr int kRow4 = kTileCols / 4;     // 16-byte pieces per coordinate
+    __shared__ floatx4 xs[2][KP * kRow4];
     __shared__ double vs[2][kTileCols];
-    __shared__ double red[kThreads / kWave];
+    __shared__ double red[kMfmaThreads / kWave];
 
     if (MODE == kApply && use_ctl) {
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
@@ -196,20 +204,19 @@ __global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
         rs = (di == 0.0) ? 0.0f : (float)(1.0 / di);
     }
 
-    // staging: the tile is 64 * KP contiguous floats of xa (rows padded to
-    // a multiple of 64), copied as 16-byte pieces: piece f holds column
-    // f / KS, coordinates 4 (f % KS) .. + 3
-    constexpr int kPieces = kTileCols * KS;
-    constexpr int kPer = (kPieces + kThreads - 1) / kThreads;
+    // staging: piece f = k * 16 + cg holds columns 4 cg .. 4 cg + 3 of
+    // coordinate k (tiles start at multiples of 64 <= np - 64)
+    constexpr int kPieces = KP * kRow4;
+    constexpr int kPer = (kPieces + kMfmaThreads - 1) / kMfmaThreads;
     floatx4 stage[kPer];
     double vstage = 0.0;
     auto fetch = [&](int64_t jt) {
-        const floatx4 *src = reinterpret_cast<const floatx4 *>(xa + jt * KP);
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
-            const int f = threadIdx.x + u * kThreads;
-            if (kPieces % kThreads == 0 || f < kPieces)
-                stage[u] = src[f];
+            const int f = threadIdx.x + u * kMfmaThreads;
+            if (kPieces % kMfmaThreads == 0 || f < kPieces)
+                stage[u] = *reinterpret_cast<const floatx4 *>(
+                    xa + (int64_t)(f / kRow4) * np + jt + 4 * (f % kRow4));
         }
         if (MODE == kApply && threadIdx.x < kTileCols) {
             const int64_t j = jt + threadIdx.x;
@@ -219,13 +226,10 @@ __global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
     auto commit = [&](int buf) {
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
-            const int f = threadIdx.x + u * kThreads;
-            if (kPieces % kThreads == 0 || f < kPieces) {
-                float *dst = xs[buf] + (f / KS) * LS + 4 * (f % KS);
-                dst[0] = stage[u][0];
-                dst[1] = stage[u][1];
-                dst[2] = stage[u][2];
-                dst[3] = stage[u][3];
+            const int f = threadIdx.x + u * kMfmaThreads;
+            if (kPieces % kMfmaThreads == 0 || f < kPieces) {
+                const int k = f / kRow4;
+                xs[buf][k * kRow4 + ((f % kRow4) ^ (4 * (k & 3)))] = stage[u];
             }
         }
         if (MODE == kApply && threadIdx.x < kTileCols)
@@ -244,15 +248,16 @@ __global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
             fetch(jt + kTileCols);                  // in flight during compute
         const bool diag = (wrow0 >= jt) && (wrow0 < jt + kTileCols);
         const bool tail = jt + kTileCols > c1;
-        const float *xb = xs[buf];
+        // coordinate 4 s + g, tile column 16 q + m, swizzled by 16 g
+        const float *tile = reinterpret_cast<const float *>(xs[buf]) + g * kTileCols;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             floatx4 cacc = {0.0f, 0.0f, 0.0f, 0.0f};
-            const float *ap = xb + (q * 16 + m) * LS + g;
+            const float *ap = tile + ((16 * q + m) ^ (16 * g));
 #pragma unroll
             for (int s = 0; s < KS; ++s)
-                cacc = __builtin_amdgcn_mfma_f32_16x16x4f32(ap[4 * s], bop[s], cacc,
-                                                            0, 0, 0);
+                cacc = __builtin_amdgcn_mfma_f32_16x16x4f32(ap[4 * s * kTileCols], bop[s],
+                                                            cacc, 0, 0, 0);
             float a[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r)
@@ -284,7 +289,7 @@ __global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
                 for (int r = 0; r < 4; ++r)
                     acc += (double)a[r];
             } else if (MODE == kApply) {
-                const double *vp = vs[buf] + q * 16 + 4 * g;
+                const double *vp = vs[buf] + 16 * q + 4 * g;
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                     acc = fma((double)a[r], vp[r], acc);
@@ -322,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void affinity_mfma_kernel(
         }
     }
     if (MODE == kApply && partial != nullptr) {
-        const double sum = block_sum<kThreads>(yabs, red);
+        const double sum = block_sum<kMfmaThreads>(yabs, red);
         if (threadIdx.x == 0)
             partial[blockIdx.x] = sum;
     }
@@ -548,9 +553,9 @@ hipError_t dispatch(const float *X, int64_t n, int d, float c, float *A,
         const dim3 grid((unsigned)((n + kRowsPerGroup - 1) / kRowsPerGroup),
                         (unsigned)nchunks);
 #define GPIC_MFMA(KS)                                                          \
-    hipLaunchKernelGGL((affinity_mfma_kernel<KS, MODE>), grid, dim3(kThreads), 0, \
-                       s, w.xa, w.xb, n, chunk_cols, A, lda, v, degree_in, out,  \
-                       part, partial, ctl, use_ctl)
+    hipLaunchKernelGGL((affinity_mfma_kernel<KS, MODE>), grid, dim3(kMfmaThreads), 0, \
+                       s, w.xa, np, w.xb, n, chunk_cols, A, lda, v, degree_in,   \
+                       out, part, partial, ctl, use_ctl)
         switch (ks) {
         case 5: GPIC_MFMA(5); break;
         case 6: GPIC_MFMA(6); break;
