@@ -88,6 +88,12 @@ size_t pi_ws(int64_t n, int64_t nb)
 
 int64_t fused_nb_bound(int64_t n) { return (n + 7) / 8; }
 
+// the column-blocked copy of a CSR W follows the power-iteration layout
+size_t pi_csr_ws(int64_t n, int64_t nnz)
+{
+    return pi_ws(n, spmv_blocks(n)) + al(csr_blocked_ws(n, nnz));
+}
+
 // the fused product's own scratch follows the power-iteration layout
 size_t pi_fused_ws(int64_t n) { return pi_ws(n, fused_nb_bound(n)) + aff_ws(n); }
 
@@ -204,6 +210,16 @@ struct CsrProduct : Product {
                       hipStream_t s) const override
     {
         return launch_spmv(row_ptr, col, val, n, v, y, partial, ctl, true, s);
+    }
+};
+
+struct BlockedCsrProduct : Product {
+    CsrBlocked B;
+    int64_t blocks() const override { return csr_blocked_partials(B.n); }
+    hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
+                      hipStream_t s) const override
+    {
+        return launch_spmv_blocked(B, v, y, partial, ctl, s);
     }
 };
 
@@ -334,7 +350,7 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     case GPIC_OP_DEGREE_FUSED: return start_ws(n) + aff_ws(n);
     case GPIC_OP_PI_DENSE: return pi_ws(n, gemv_blocks(n));
     case GPIC_OP_PI_FUSED: return pi_fused_ws(n);
-    case GPIC_OP_PI_CSR: return pi_ws(n, spmv_blocks(n));
+    case GPIC_OP_PI_CSR: return pi_csr_ws(n, nnz);
     case GPIC_OP_KMEANS1D: return kmeans_ws(n, k < 1 ? 1 : k);
     case GPIC_OP_AFFINITY_NORMALIZED: return start_ws(n) + aff_ws(n);
     case GPIC_OP_MATVEC_FUSED: return aff_ws(n);
@@ -601,11 +617,21 @@ gpic_status gpic_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
         return st;
     if ((st = check_pi_common(n, params, v, delta, res)) != GPIC_OK)
         return st;
-    if ((st = check_ws(ws, ws_bytes, pi_ws(n, spmv_blocks(n)))) != GPIC_OK)
+    if ((st = check_ws(ws, ws_bytes, pi_csr_ws(n, nnz))) != GPIC_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
     if ((st = verify_csr(row_ptr, col, n, nnz, ws, s)) != GPIC_OK)
         return st;
+    if (csr_blocked_applies(n) && nnz > 0) {
+        BlockedCsrProduct bop;
+        int usable = 0;
+        CHECK_HIP(build_csr_blocked(row_ptr, col, val, n, nnz,
+                                    static_cast<char *>(ws) + pi_ws(n, spmv_blocks(n)),
+                                    &bop.B, s, &usable),
+                  "blocked CSR copy");
+        if (usable)
+            return run_power_iteration(bop, n, params, v, delta, ws, res, s);
+    }
     CsrProduct op;
     op.row_ptr = row_ptr;
     op.col = col;

@@ -162,6 +162,33 @@ hipError_t launch_init_state(double *ring, int64_t ring_len, int *err,
                              const double *v, double *delta, int64_t n,
                              bool copy_delta, hipStream_t s);
 
+// spmv_blocked.hip -- column-blocked copy of a CSR W for the product
+struct CsrBlocked {
+    int64_t n, nb;     // rows, column blocks
+    int lanes;         // lanes per row in the product (1, 2, 4, 8 or 16)
+    int64_t *base;     // [nb + 1] first entry of each block in colb / valb
+    int32_t *rpb;      // [nb][n + 1] row offsets relative to base[b]
+    int32_t *colb;     // [nnz]
+    float *valb;       // [nnz]
+    double *ypart;     // [nb][n] per-block row sums
+};
+// true when n spans 2 .. 32 column blocks of 2^18 columns
+bool csr_blocked_applies(int64_t n);
+// workspace bytes for the copy (0 when it does not apply)
+size_t csr_blocked_ws(int64_t n, int64_t nnz);
+// number of |y| partial sums the blocked product writes
+int64_t csr_blocked_partials(int64_t n);
+// Builds the copy in ws; synchronises.  *usable_host = 0 (nothing built)
+// when a row's columns are not ascending, fewer than a quarter of the
+// entries lie more than 2^17 columns from the diagonal, or a block holds
+// >= 2^31 entries.
+hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
+                             const float *val, int64_t n, int64_t nnz, void *ws,
+                             CsrBlocked *out, hipStream_t s, int *usable_host);
+// Product (two launches): per-block row sums, then y and |y| partials.
+hipError_t launch_spmv_blocked(const CsrBlocked &B, const double *v, double *y,
+                               double *partial, StopCtl ctl, hipStream_t s);
+
 // kmeans.hip
 size_t kmeans_ws(int64_t n, int32_t k);
 // Runs the whole exact 1-D k-means; synchronises the stream.

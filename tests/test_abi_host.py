@@ -44,6 +44,13 @@ def test_workspace_sizes(L):
         b = g.workspace_bytes(op, 100000, 500000, 3)
         assert 0 < a < b
     assert g.workspace_bytes("kmeans1d", 10**6, 0, 50) > 50 * 4 * 10**6
+    # above 2^18 rows the CSR power iteration also holds a column-blocked
+    # copy of W (8 bytes per stored entry) and per-block row sums
+    small = g.workspace_bytes("pi_csr", 1 << 18, 10**7, 0)
+    assert small == g.workspace_bytes("pi_csr", 1 << 18, 0, 0)
+    big, big0 = (g.workspace_bytes("pi_csr", 600_000, 10**7, 0),
+                 g.workspace_bytes("pi_csr", 600_000, 0, 0))
+    assert big - big0 >= 8 * 10**7 and big0 > 3 * 600_000 * 8
     assert L.gpic_workspace_bytes(99, 10, 0, 0) == 0
     assert L.gpic_workspace_bytes(4, -1, 0, 0) == 0
 

@@ -8,7 +8,8 @@ benchmark times.
   sweeps of 4e10 pairs, so sampled rows are recomputed one by one (degrees
   and one product from the GPU's own iterate), plus invariants of the whole
   vector; a reduced n runs end to end.
-* kNN graph (CSR) at a reduced n, end to end.
+* kNN graph (CSR) at a reduced n, end to end, and at its full size
+  (n = 2,000,000, the column-blocked product) to convergence.
 * 1-D k-means at the kNN workload's full size (n = 2,000,000, k = 50).
 """
 import numpy as np
@@ -185,3 +186,22 @@ def test_kmeans1d_full_size(g, orc):
     print(f"gpu: kmeans1d n={n} k={k}", flush=True)
     out = g.gpic_kmeans1d(_t(v), k)
     _check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))
+
+
+def test_knn_csr_full_size_converge(g, orc):
+    """knn8d at n = 2,000,000 (90M stored entries, random node order): the
+    column-blocked product to convergence against the oracle."""
+    import workloads
+    w = workloads.make("knn8d")
+    print(f"gpu: knn8d n={w.n} nnz={w.val.shape[0]}", flush=True)
+    out = g.pic_csr(_t(w.row_ptr), _t(w.col), _t(w.val.copy()), w.k, "converge",
+                    1000, w.eps)
+    wr, dr, v0r, _ = orc.degree_normalize_csr(w.row_ptr, w.col, w.val)
+    ref = orc.power_iterate_csr(w.row_ptr, w.col, wr, v0r, "converge", 1000, w.eps)
+    mu = stop_margin(ref.stats, w.eps, ref.iterations)
+    print(f"  iterations gpu={out.pi.iterations} oracle={ref.iterations} "
+          f"margin={mu:.3g}", flush=True)
+    np.testing.assert_allclose(out.degree.cpu().numpy(), dr, rtol=1e-12)
+    assert ref.converged and out.pi.converged
+    assert out.pi.iterations == ref.iterations
+    assert rel_l1(out.pi.v.cpu().numpy(), ref.v) <= 1e-4

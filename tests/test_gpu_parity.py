@@ -342,6 +342,61 @@ def test_csr_parity_knn(g, orc):
     assert rel_l1(v, ref.v) <= 1e-4
 
 
+def _random_graph(n, per_row, seed, sort_rows=True, band=None):
+    """Symmetric random graph, float32 weights in [0.1, 1): neighbours
+    anywhere (no locality in the numbering) or within +-band of the row;
+    rows sorted by column unless asked otherwise."""
+    import scipy.sparse as sp
+    rng = np.random.default_rng(seed)
+    i = np.repeat(np.arange(n), per_row)
+    if band is None:
+        j = rng.integers(0, n, size=n * per_row)
+    else:
+        j = np.clip(i + rng.integers(-band, band + 1, size=n * per_row), 0, n - 1)
+    keep = i != j
+    w = rng.uniform(0.1, 1.0, size=keep.sum())
+    S = sp.coo_matrix((w, (i[keep], j[keep])), shape=(n, n)).tocsr()
+    S = S.maximum(S.T).tocsr()
+    S.sort_indices()
+    rp, col, val = (S.indptr.astype(np.int64), S.indices.astype(np.int32),
+                    S.data.astype(np.float32))
+    if not sort_rows:
+        col, val = col.copy(), val.copy()
+        for r in range(0, n, max(1, n // 500)):       # reverse some rows
+            a, b = rp[r], rp[r + 1]
+            col[a:b], val[a:b] = col[a:b][::-1].copy(), val[a:b][::-1].copy()
+    return rp, col, val
+
+
+@pytest.mark.parametrize("sort_rows,band", [(True, None), (False, None), (True, 5000)])
+def test_csr_column_blocked_parity(g, orc, sort_rows, band):
+    """n = 600,000 spans three column blocks of 2^18: sorted rows with far
+    neighbours take the column-blocked product; unsorted rows, or
+    neighbours near the diagonal, the row-wise one.  Stage isolation: the
+    oracle iterates on the GPU's float32 W, so v must agree to rounding
+    after T = 20, and both must stop at the same update."""
+    n = 600_000
+    rp, col, val = _random_graph(n, 8, 77, sort_rows, band)
+    print(f"gpu: random graph n={n} nnz={col.size} sorted={sort_rows} band={band}",
+          flush=True)
+    _, dr, v0r, _ = orc.degree_normalize_csr(rp, col, val)
+    valg = _t(val.copy())
+    _, deg, v0, _ = g.gpic_degree_normalize_csr(_t(rp), _t(col), valg)
+    np.testing.assert_allclose(deg.cpu().numpy(), dr, rtol=1e-12)
+    wg = valg.cpu().numpy().astype(np.float64)               # the GPU's W
+    ref = orc.power_iterate_csr(rp, col, wg, v0r, "fixed", 20)
+    v = v0.clone()
+    out = g.gpic_power_iterate_csr(_t(rp), _t(col), valg, v, None, "fixed", 20)
+    np.testing.assert_allclose(v.cpu().numpy(), ref.v, rtol=1e-9)
+    np.testing.assert_allclose(out.stats, ref.stats, rtol=1e-6, atol=1e-18)
+    eps = 0.5 * (ref.stats[5] + ref.stats[6])             # a stop between updates 6 and 7
+    refc = orc.power_iterate_csr(rp, col, wg, v0r, "converge", 100, eps)
+    v = v0.clone()
+    outc = g.gpic_power_iterate_csr(_t(rp), _t(col), valg, v, None, "converge", 100, eps)
+    assert outc.iterations == refc.iterations == 7
+    np.testing.assert_allclose(v.cpu().numpy(), refc.v, rtol=1e-9)
+
+
 def test_csr_full_pattern_equals_dense(g):
     n = 300
     X = _pts(n, 2, 50)
