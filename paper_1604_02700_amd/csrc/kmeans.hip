@@ -343,39 +343,46 @@ __global__ __launch_bounds__(kThreads) void first_layer_kernel(
 // leftmost argmins in parallel, each over the interval's bounds
 // [opt(lo-1), opt(hi+1)]; the F+1 gaps between samples are the next
 // level's intervals.  ceil(log_{F+1} n) levels replace the log2 n of a
-// binary split, which matters because every level is a dependent step.
-constexpr int kF = 64;
+// binary split, which matters because every level is a dependent step; in
+// exchange every candidate of a level is scanned by F samples.  F = 64 up
+// to 2^18 rows (few dependent steps), F = 8 above (less redundant work).
+constexpr int kFSmall = 64;
+constexpr int kFLarge = 8;
+constexpr int64_t kFLargeFrom = (int64_t)1 << 18;
+constexpr int kMaxLevels = 16;
 constexpr int kShortScan = 32;        // longer ranges go to the work queue
 constexpr int kChunk = 1024;          // candidates per queued part (16 per lane)
 
 // Sample f of interval [lo, hi] (m = hi - lo + 1 rows): every row if m <= F,
 // else lo + (f + 1)(m + 1) / (F + 1) - 1; returns -1 if there is none.
+template <int F>
 __device__ __forceinline__ int64_t sample_row(int64_t lo, int64_t hi, int f)
 {
     const int64_t m = hi - lo + 1;
-    if (m <= kF)
+    if (m <= F)
         return (f < m) ? lo + f : -1;
-    return lo + ((int64_t)(f + 1) * (m + 1)) / (kF + 1) - 1;
+    return lo + ((int64_t)(f + 1) * (m + 1)) / (F + 1) - 1;
 }
 
 // Interval of node q at level L (digits of q in base F + 1, most significant
 // first, choose the gap between samples); false if the node does not exist.
+template <int F>
 __device__ __forceinline__ bool fary_node(int64_t n, int L, int64_t q, int64_t &lo,
                                           int64_t &hi)
 {
-    int dig[8];
+    int dig[kMaxLevels];
     for (int l = 0; l < L; ++l) {
-        dig[l] = (int)(q % (kF + 1));
-        q /= (kF + 1);
+        dig[l] = (int)(q % (F + 1));
+        q /= (F + 1);
     }
     lo = 0;
     hi = n - 1;
     for (int l = L - 1; l >= 0; --l) {
-        if (hi - lo + 1 <= kF)
+        if (hi - lo + 1 <= F)
             return false;                     // a leaf interval has no gaps
         const int c = dig[l];
-        const int64_t nlo = (c == 0) ? lo : sample_row(lo, hi, c - 1) + 1;
-        const int64_t nhi = (c == kF) ? hi : sample_row(lo, hi, c) - 1;
+        const int64_t nlo = (c == 0) ? lo : sample_row<F>(lo, hi, c - 1) + 1;
+        const int64_t nhi = (c == F) ? hi : sample_row<F>(lo, hi, c) - 1;
         lo = nlo;
         hi = nhi;
         if (lo > hi)
@@ -467,6 +474,7 @@ struct LevelQueue {
 // candidates appended to the queue (the order of appends does not matter:
 // every row's parts are merged by an order-independent minimum).  Item 0
 // clears the other pair of counters, whose level has finished.
+template <int F>
 __global__ __launch_bounds__(kThreads) void fary_level_kernel(
     const double *__restrict__ S1, const double *__restrict__ S2,
     const int32_t *__restrict__ run, const double *__restrict__ Dprev,
@@ -479,9 +487,9 @@ __global__ __launch_bounds__(kThreads) void fary_level_kernel(
         Q.qlen[2 + ((g + 1) & 1)] = 0ull;
     }
     int64_t lo, hi;
-    if (item >= items || !fary_node(n, L, item / kF, lo, hi))
+    if (item >= items || !fary_node<F>(n, L, item / F, lo, hi))
         return;
-    const int64_t r = sample_row(lo, hi, (int)(item % kF));
+    const int64_t r = sample_row<F>(lo, hi, (int)(item % F));
     if (r < 0)
         return;
     int64_t alo, ahi;
@@ -640,7 +648,7 @@ struct KmLayout {
 // level overlap only at their ends, so they hold at most 2 F n candidates
 // and at most n + 2 F n / kChunk parts; a level that would need more
 // scans the excess in place.
-int64_t queue_cap(int64_t n) { return n + (2 * kF * n) / kChunk + 1024; }
+int64_t queue_cap(int64_t n) { return n + (2 * kFSmall * n) / kChunk + 1024; }
 
 KmLayout layout(int64_t n, int32_t k)
 {
@@ -756,21 +764,27 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     // 3. layers
     hipLaunchKernelGGL(first_layer_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
                        S1, S2, n, Da, Q.qlen);
+    const int F = (n >= kFLargeFrom) ? kFLarge : kFSmall;
     // levels of the F-ary recursion: until every interval has <= F rows
     int levels = 1;
-    for (int64_t m = n; m > kF; m /= (kF + 1))     // gaps hold <= m / (F+1) rows
+    for (int64_t m = n; m > F; m /= (F + 1))       // gaps hold <= m / (F+1) rows
         ++levels;
+    if (levels > kMaxLevels)
+        return hipErrorInvalidValue;               // not reachable for n <= 2^30
     double *Dprev = Da, *Dcur = Db;
     int g = 0;                                     // levels run so far
     for (int c = 1; c < ke; ++c) {
         int32_t *oc = opt + (int64_t)c * n;
         int64_t nodes = 1;
-        for (int Lv = 0; Lv < levels; ++Lv, nodes *= (kF + 1), ++g) {
-            const int64_t items = nodes * kF;
-            hipLaunchKernelGGL(fary_level_kernel,
-                               dim3((unsigned)((items + kThreads - 1) / kThreads)),
-                               dim3(kThreads), 0, s, S1, S2, run, Dprev, Dcur, oc, n, Lv,
-                               items, Q, g);
+        for (int Lv = 0; Lv < levels; ++Lv, nodes *= (F + 1), ++g) {
+            const int64_t items = nodes * F;
+            const dim3 grid((unsigned)((items + kThreads - 1) / kThreads));
+            if (F == kFSmall)
+                hipLaunchKernelGGL(fary_level_kernel<kFSmall>, grid, dim3(kThreads), 0, s,
+                                   S1, S2, run, Dprev, Dcur, oc, n, Lv, items, Q, g);
+            else
+                hipLaunchKernelGGL(fary_level_kernel<kFLarge>, grid, dim3(kThreads), 0, s,
+                                   S1, S2, run, Dprev, Dcur, oc, n, Lv, items, Q, g);
             hipLaunchKernelGGL(fary_queue_kernel, dim3(2048), dim3(kThreads), 0, s, S1,
                                S2, run, Dprev, Dcur, oc, Q, g);
             hipLaunchKernelGGL(fary_merge_kernel, dim3(512), dim3(kThreads), 0, s, Dcur,
