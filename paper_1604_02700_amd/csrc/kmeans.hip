@@ -72,9 +72,37 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(
     hist[(int64_t)threadIdx.x * gridDim.x + blockIdx.x] = h[threadIdx.x];
 }
 
-// Exclusive scan of m uint32 counts, in place, by one workgroup of 1024.
-__global__ __launch_bounds__(1024) void scan_counts_kernel(uint32_t *__restrict__ a,
-                                                           int64_t m)
+// Exclusive scan of m uint32 counts, in place, in three launches: each
+// workgroup sums kTile counts, one workgroup scans those sums, and each
+// workgroup rescans its counts from its offset.
+__global__ __launch_bounds__(kThreads) void scan_sums_kernel(const uint32_t *__restrict__ a,
+                                                             int64_t m,
+                                                             uint32_t *__restrict__ bsum)
+{
+    __shared__ uint32_t red[kThreads / kWave];
+    const int64_t b0 = (int64_t)blockIdx.x * kTile;
+    uint32_t t = 0;
+    for (int k = threadIdx.x; k < kTile; k += kThreads)
+        if (b0 + k < m)
+            t += a[b0 + k];
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1)
+        t += __shfl_xor(t, o, kWave);
+    if ((threadIdx.x % kWave) == 0)
+        red[threadIdx.x / kWave] = t;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t u = 0;
+        for (int w = 0; w < kThreads / kWave; ++w)
+            u += red[w];
+        bsum[blockIdx.x] = u;
+    }
+}
+
+// One workgroup of 1024: exclusive scan of m counts (the block sums, or a
+// short count array directly), in place.
+__global__ __launch_bounds__(1024) void scan_bsums_kernel(uint32_t *__restrict__ a,
+                                                          int64_t m)
 {
     __shared__ uint32_t s[1024];
     const int64_t per = (m + 1023) / 1024;
@@ -97,6 +125,34 @@ __global__ __launch_bounds__(1024) void scan_counts_kernel(uint32_t *__restrict_
         a[i] = run;
         run += x;
     }
+}
+
+// Each thread owns kItems consecutive counts of its workgroup's tile.
+__global__ __launch_bounds__(kThreads) void scan_apply_kernel(uint32_t *__restrict__ a,
+                                                              int64_t m,
+                                                              const uint32_t *__restrict__ boff)
+{
+    __shared__ uint32_t part[kThreads];
+    const int64_t x0 = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+    uint32_t t = 0;
+    for (int k = 0; k < kItems; ++k)
+        if (x0 + k < m)
+            t += a[x0 + k];
+    part[threadIdx.x] = t;
+    __syncthreads();
+    for (int o = 1; o < kThreads; o <<= 1) {
+        const uint32_t x = (threadIdx.x >= (unsigned)o) ? part[threadIdx.x - o] : 0u;
+        __syncthreads();
+        part[threadIdx.x] += x;
+        __syncthreads();
+    }
+    uint32_t run = boff[blockIdx.x] + part[threadIdx.x] - t;
+    for (int k = 0; k < kItems; ++k)
+        if (x0 + k < m) {
+            const uint32_t x = a[x0 + k];
+            a[x0 + k] = run;
+            run += x;
+        }
 }
 
 // Stable scatter of one tile.  Element order inside a tile is
@@ -486,37 +542,61 @@ __global__ __launch_bounds__(kThreads) void fary_level_kernel(
         Q.qlen[(g + 1) & 1] = 0ull;
         Q.qlen[2 + ((g + 1) & 1)] = 0ull;
     }
-    int64_t lo, hi;
-    if (item >= items || !fary_node<F>(n, L, item / F, lo, hi))
-        return;
-    const int64_t r = sample_row<F>(lo, hi, (int)(item % F));
-    if (r < 0)
-        return;
-    int64_t alo, ahi;
-    row_bounds(opt, n, lo, hi, r, alo, ahi);
+    int64_t lo = 0, hi = -1, r = -1, alo = 1, ahi = 0;
+    if (item < items && fary_node<F>(n, L, item / F, lo, hi)) {
+        r = sample_row<F>(lo, hi, (int)(item % F));
+        if (r >= 0)
+            row_bounds(opt, n, lo, hi, r, alo, ahi);
+    }
     const int64_t len = ahi - alo + 1;
-    if (len > kShortScan) {
-        const int64_t C = (len + kChunk - 1) / kChunk;
-        const int64_t e0 = (int64_t)atomicAdd(&Q.qlen[g & 1], (unsigned long long)C);
-        if (e0 + C <= Q.cap) {
+    // long ranges: reserve parts; up to 64 parts are written by their own
+    // thread, more by the whole wave, one such lane after the other
+    bool queued = false;
+    int64_t e0 = 0, C = 0;
+    if (r >= 0 && len > kShortScan) {
+        C = (len + kChunk - 1) / kChunk;
+        e0 = (int64_t)atomicAdd(&Q.qlen[g & 1], (unsigned long long)C);
+        queued = e0 + C <= Q.cap;
+        if (queued) {
             Q.nparts[e0] = (int32_t)C;
             if (C > 1) {
                 const unsigned long long h = atomicAdd(&Q.qlen[2 + (g & 1)], 1ull);
                 Q.heads[h] = (int32_t)e0;             // h < e0 + 1 <= cap
             }
-            for (int64_t p = 0; p < C; ++p) {
-                const int64_t plo = alo + p * kChunk;
-                const int64_t phi = plo + kChunk - 1 < ahi ? plo + kChunk - 1 : ahi;
-                Q.part[e0 + p] = QueuePart{(int32_t)r, (int32_t)plo, (int32_t)phi,
-                                           (int32_t)e0};
-            }
-            return;
+        } else {
+            // no room left (only if split points were far from monotone):
+            // void the reserved slots below the capacity and scan here
+            for (int64_t e = e0; e < e0 + C && e < Q.cap; ++e)
+                Q.part[e] = QueuePart{-1, 0, -1, 0};
         }
-        // no room left (only if split points were far from monotone):
-        // void the reserved slots below the capacity and scan here
-        for (int64_t e = e0; e < e0 + C && e < Q.cap; ++e)
-            Q.part[e] = QueuePart{-1, 0, -1, 0};
     }
+    if (queued && C <= kWave) {
+        for (int64_t p = 0; p < C; ++p) {
+            const int64_t plo = alo + p * kChunk;
+            const int64_t phi = plo + kChunk - 1 < ahi ? plo + kChunk - 1 : ahi;
+            Q.part[e0 + p] = QueuePart{(int32_t)r, (int32_t)plo, (int32_t)phi,
+                                       (int32_t)e0};
+        }
+    }
+    const int lane = threadIdx.x % kWave;
+    unsigned long long mask = __ballot(queued && C > kWave);
+    while (mask) {
+        const int src = __ffsll((long long)mask) - 1;
+        mask &= mask - 1;
+        const long long qe0 = __shfl((long long)e0, src, kWave);
+        const long long qC = __shfl((long long)C, src, kWave);
+        const long long qr = __shfl((long long)r, src, kWave);
+        const long long qalo = __shfl((long long)alo, src, kWave);
+        const long long qahi = __shfl((long long)ahi, src, kWave);
+        for (long long p = lane; p < qC; p += kWave) {
+            const long long plo = qalo + p * kChunk;
+            const long long phi = plo + kChunk - 1 < qahi ? plo + kChunk - 1 : qahi;
+            Q.part[qe0 + p] = QueuePart{(int32_t)qr, (int32_t)plo, (int32_t)phi,
+                                        (int32_t)qe0};
+        }
+    }
+    if (r < 0 || queued)
+        return;
     double best = INFINITY;
     int64_t arg = INT64_MAX;
     scan_range(S1, S2, run, Dprev, r, alo, ahi, 1, best, arg);
@@ -640,7 +720,7 @@ __global__ __launch_bounds__(kThreads) void labels_kernel(
 inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct KmLayout {
-    size_t keyA, keyB, idxA, idxB, hist, sv, run, t1, t2, S1, S2, Da, Db, opt,
+    size_t keyA, keyB, idxA, idxB, hist, hsum, sv, run, t1, t2, S1, S2, Da, Db, opt,
         qpart, qnparts, qheads, qbest, qarg, qlen, sc, first, costs, total;
 };
 
@@ -665,6 +745,7 @@ KmLayout layout(int64_t n, int32_t k)
     L.idxA = take(n * 4);
     L.idxB = take(n * 4);
     L.hist = take((size_t)kRadix * nt * 4);
+    L.hsum = take((size_t)tiles(kRadix * nt) * 4);
     L.sv = take(n * 8);
     L.run = take(n * 4);
     L.t1 = take(nt * 8);
@@ -710,6 +791,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     uint64_t *keyA = (uint64_t *)(w + L.keyA), *keyB = (uint64_t *)(w + L.keyB);
     int32_t *idxA = (int32_t *)(w + L.idxA), *idxB = (int32_t *)(w + L.idxB);
     uint32_t *hist = (uint32_t *)(w + L.hist);
+    uint32_t *hsum = (uint32_t *)(w + L.hsum);
     double *sv = (double *)(w + L.sv);
     int32_t *run = (int32_t *)(w + L.run);
     double *t1 = (double *)(w + L.t1), *t2 = (double *)(w + L.t2);
@@ -736,8 +818,18 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
         const int shift = 8 * pass;
         hipLaunchKernelGGL(radix_hist_kernel, dim3((unsigned)nt), dim3(kThreads), 0,
                            s, keyA, n, shift, hist);
-        hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(1024), 0, s, hist,
-                           (int64_t)kRadix * nt);
+        const int64_t hm = (int64_t)kRadix * nt;
+        if (hm <= 16 * kTile) {             // one workgroup is quickest
+            hipLaunchKernelGGL(scan_bsums_kernel, dim3(1), dim3(1024), 0, s, hist, hm);
+        } else {
+            const unsigned hb = (unsigned)tiles(hm);
+            hipLaunchKernelGGL(scan_sums_kernel, dim3(hb), dim3(kThreads), 0, s, hist, hm,
+                               hsum);
+            hipLaunchKernelGGL(scan_bsums_kernel, dim3(1), dim3(1024), 0, s, hsum,
+                               (int64_t)hb);
+            hipLaunchKernelGGL(scan_apply_kernel, dim3(hb), dim3(kThreads), 0, s, hist, hm,
+                               hsum);
+        }
         hipLaunchKernelGGL(radix_scatter_kernel, dim3((unsigned)nt), dim3(kThreads),
                            0, s, keyA, idxA, keyB, idxB, n, shift, hist);
         uint64_t *tk = keyA; keyA = keyB; keyB = tk;
