@@ -158,6 +158,12 @@ hipError_t launch_reduce_tau(const double *partial, int64_t nb, double *tau,
                              StopCtl ctl, hipStream_t s);
 hipError_t launch_update(const double *y, const double *tau, double *v,
                          double *delta, int64_t n, StopCtl ctl, hipStream_t s);
+// tau and the update in one launch (bitwise the same results); used for
+// n up to tau_update_fused's bound, where launches dominate
+bool tau_update_fused(int64_t n);
+hipError_t launch_tau_update(const double *partial, int64_t nb, double *tau,
+                             const double *y, double *v, double *delta, int64_t n,
+                             StopCtl ctl, hipStream_t s);
 hipError_t launch_init_state(double *ring, int64_t ring_len, int *err,
                              const double *v, double *delta, int64_t n,
                              bool copy_delta, hipStream_t s);

@@ -12,6 +12,8 @@
 // ascending block order), update (grid-wide; block maxima of the statistic
 // are combined with an integer atomic max on the bit pattern of the
 // non-negative float64, which is order-free and therefore deterministic).
+// Up to 16,384 rows, tau and the update share one launch, in which every
+// workgroup forms tau itself in the same order (so the same bits).
 #include "common.h"
 
 namespace gpic {
@@ -21,6 +23,7 @@ constexpr int kThreads = 256;
 constexpr int kSpmvLanes = 16;      // lanes per CSR row
 constexpr int kSpmvRows = 32;       // rows per workgroup of the CSR product
 constexpr int kSpmvUnroll = 4;      // independent gathers in flight per lane
+constexpr int64_t kTauUpdateMaxN = 16384;   // one launch for tau and the update
 
 // CSR product: 16 lanes per row, lane l summing entries l, l + 16, ... of
 // its row in that order, then a 16-lane butterfly.  The workgroup's row
@@ -129,6 +132,44 @@ __global__ __launch_bounds__(kThreads) void update_kernel(
                   (unsigned long long)__double_as_longlong(m));
 }
 
+// Both steps in one launch for small n: every workgroup forms tau from the
+// partials exactly as reduce_tau_kernel does (same order, so the same
+// bits), then updates its rows.
+__global__ __launch_bounds__(1024) void tau_update_kernel(
+    const double *__restrict__ partial, int64_t nb, double *__restrict__ tau,
+    const double *__restrict__ y, double *__restrict__ v, double *__restrict__ delta,
+    int64_t n, StopCtl ctl)
+{
+    __shared__ double red[1024 / kWave];
+    if (stop_reached(ctl))
+        return;
+    double s = 0.0;
+    for (int64_t b = threadIdx.x; b < nb; b += 1024)
+        s += partial[b];
+    const double t = block_sum<1024>(s, red);
+    const bool bad = !(t > 0.0) || !isfinite(t);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        *tau = t;
+        if (bad)
+            *ctl.err = 1;
+    }
+    if (bad)
+        return;                                     // uniform: t is the same everywhere
+    double m = 0.0;
+    const int64_t stride = (int64_t)gridDim.x * 1024;
+    for (int64_t i = (int64_t)blockIdx.x * 1024 + threadIdx.x; i < n; i += stride) {
+        const double vn = y[i] / t;
+        const double dn = fabs(vn - v[i]);
+        m = fmax(m, fabs(dn - delta[i]));
+        v[i] = vn;
+        delta[i] = dn;
+    }
+    m = block_max<1024>(m, red);
+    if (threadIdx.x == 0)
+        atomicMax(reinterpret_cast<unsigned long long *>(ctl.cur_stat),
+                  (unsigned long long)__double_as_longlong(m));
+}
+
 __global__ __launch_bounds__(kThreads) void init_state_kernel(
     double *__restrict__ ring, int64_t ring_len, int *__restrict__ err,
     const double *__restrict__ v, double *__restrict__ delta, int64_t n,
@@ -174,6 +215,17 @@ hipError_t launch_reduce_tau(const double *partial, int64_t nb, double *tau,
 {
     hipLaunchKernelGGL(reduce_tau_kernel, dim3(1), dim3(1024), 0, s, partial, nb,
                        tau, ctl);
+    return hipGetLastError();
+}
+
+bool tau_update_fused(int64_t n) { return n <= kTauUpdateMaxN; }
+
+hipError_t launch_tau_update(const double *partial, int64_t nb, double *tau,
+                             const double *y, double *v, double *delta, int64_t n,
+                             StopCtl ctl, hipStream_t s)
+{
+    hipLaunchKernelGGL(tau_update_kernel, dim3((unsigned)((n + 1023) / 1024)), dim3(1024),
+                       0, s, partial, nb, tau, y, v, delta, n, ctl);
     return hipGetLastError();
 }
 
