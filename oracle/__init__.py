@@ -80,6 +80,7 @@ def _declare(lib):
     i64, i32, f64 = C.c_int64, C.c_int32, C.c_double
     lib.orc_num_threads.restype = i32
     lib.orc_affinity_rows.argtypes = [p, i64, i32, f64, i64, i64, p]
+    lib.orc_affinity_cosine_rows.argtypes = [p, i64, i32, i64, i64, p]
     lib.orc_degree_rows.argtypes = [p, i64, i32, f64, p, i64, p]
     lib.orc_degree_normalize.argtypes = [p, i64, p, p]
     lib.orc_degree_normalize.restype = i64
@@ -124,6 +125,26 @@ def affinity(X, sigma) -> np.ndarray:
     A = np.empty((n, n), dtype=np.float64)
     _L().orc_affinity_rows(_ptr(X), n, d, float(np.float32(sigma)), 0, n, _ptr(A))
     return A
+
+
+def affinity_cosine(X) -> np.ndarray:
+    """Full n x n cosine affinity (1 + cos) / 2 with a zero diagonal, float64."""
+    X = _f32(X)
+    n, d = X.shape
+    A = np.empty((n, n), dtype=np.float64)
+    _L().orc_affinity_cosine_rows(_ptr(X), n, d, 0, n, _ptr(A))
+    return A
+
+
+def affinity_cosine_rows(X, rows) -> np.ndarray:
+    """Rows `rows` of the cosine A (recomputed), float64 [len(rows), n]."""
+    X = _f32(X)
+    n, d = X.shape
+    out = np.empty((len(rows), n), dtype=np.float64)
+    for r, i in enumerate(rows):
+        _L().orc_affinity_cosine_rows(_ptr(X), n, d, int(i), 1,
+                                      C.c_void_p(out.ctypes.data + r * n * 8))
+    return out
 
 
 def affinity_rows(X, sigma, rows) -> np.ndarray:

@@ -18,8 +18,10 @@
  *   orc_affinity_rows      affinity matrix A of the graph G (section
  *                          "Spectral Cluster"); Gaussian kernel with a zero
  *                          diagonal, the reading taken because the paper
- *                          never writes its kernel down (its Experiment I
- *                          used cosine similarity, Table 2 caption).
+ *                          never writes its kernel down.
+ *   orc_affinity_cosine_rows  the cosine similarity of Experiment I (Table 2
+ *                          caption), shifted to (1 + cos) / 2 so that A stays
+ *                          non-negative, zero diagonal.
  *   orc_degree_normalize   d_ii = sum_j a_ij and W = D^-1 A ("Spectral
  *                          Cluster"); v0 = D / sum(D) (Algorithm 2, the
  *                          Reduction and Norm steps before the loop).
@@ -77,6 +79,38 @@ static double gauss_affinity(const float *X, int32_t d, int64_t i, int64_t j,
         dist2 += diff * diff;
     }
     return exp(-dist2 / two_sigma2);
+}
+
+/* Cosine similarity, read as a_ij = (1 + cos(x_i, x_j)) / 2 for i != j and
+ * a_ii = 0, cos = x_i . x_j / (||x_i|| ||x_j||), taken as 0 when either
+ * point is the origin.  The shift keeps A >= 0 (cosine alone is negative
+ * for points more than a right angle apart, and W = D^-1 A needs A >= 0). */
+static double cosine_affinity(const float *X, int32_t d, int64_t i, int64_t j)
+{
+    if (i == j)
+        return 0.0;
+    const float *xi = X + i * (int64_t)d;
+    const float *xj = X + j * (int64_t)d;
+    double dot = 0.0, ni = 0.0, nj = 0.0;
+    for (int32_t c = 0; c < d; ++c) {
+        const double a = (double)xi[c], b = (double)xj[c];
+        dot += a * b;
+        ni += a * a;
+        nj += b * b;
+    }
+    if (ni == 0.0 || nj == 0.0)
+        return 0.5;
+    return 0.5 * (1.0 + dot / (sqrt(ni) * sqrt(nj)));
+}
+
+/* Rows row0 .. row0+nrows-1 of the cosine A, written to out[r * n + j]. */
+void orc_affinity_cosine_rows(const float *X, int64_t n, int32_t d, int64_t row0,
+                              int64_t nrows, double *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < nrows; ++r)
+        for (int64_t j = 0; j < n; ++j)
+            out[r * n + j] = cosine_affinity(X, d, row0 + r, j);
 }
 
 /* Rows row0 .. row0+nrows-1 of A, written to out[r * n + j]. */

@@ -33,6 +33,10 @@ MUTATIONS = {
     "strict_stop_test": ("if (mode == 1 && s <= eps)", "if (mode == 1 && s < eps)"),
     "iterations_off_by_one": ("done = t + 1;", "done = t;"),
     "segment_size_off_by_one": ("double m = (double)(i - j + 1);", "double m = (double)(i - j + 2);"),
+    "cosine_without_shift": ("return 0.5 * (1.0 + dot / (sqrt(ni) * sqrt(nj)));",
+                             "return dot / (sqrt(ni) * sqrt(nj));"),
+    "cosine_norm_not_square_rooted": ("return 0.5 * (1.0 + dot / (sqrt(ni) * sqrt(nj)));",
+                                      "return 0.5 * (1.0 + dot / (ni * nj));"),
     "dc_left_bound_too_tight": ("dc_layer(P, run_start, prev, cur, opt, lo, mid - 1, olo, opt[mid]);",
                                 "dc_layer(P, run_start, prev, cur, opt, lo, mid - 1, olo, opt[mid] - 1);"),
 }
@@ -45,6 +49,8 @@ def _pin_suite(orc):
         ("affinity_scipy", lambda: pins.test_affinity_matches_scipy_distance(orc)),
         ("affinity_closed", lambda: pins.test_affinity_closed_form_two_points(orc)),
         ("affinity_invariant", lambda: pins.test_affinity_symmetric_and_invariant(orc)),
+        ("cosine_scipy", lambda: pins.test_cosine_affinity_matches_scipy_distance(orc)),
+        ("cosine_closed", lambda: pins.test_cosine_affinity_closed_form_and_invariance(orc)),
         ("row_sums_v0", lambda: pins.test_rows_of_W_sum_to_one_and_v0(orc)),
         ("zero_degree", lambda: pins.test_zero_degree_row_is_counted(orc)),
         ("two_points", lambda: pins.test_two_points_give_swap_matrix(orc)),

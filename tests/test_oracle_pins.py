@@ -63,6 +63,39 @@ def test_affinity_rows_and_degree_rows_agree(orc):
                                rtol=1e-14)
 
 
+def test_cosine_affinity_matches_scipy_distance(orc):
+    """Cosine affinity (1 + cos) / 2 equals 1 - cdist_cosine / 2 off the
+    diagonal (scipy's cosine distance is 1 - cos)."""
+    X = _pts(61, 5, 11)
+    A = orc.affinity_cosine(X)
+    ref = 1.0 - 0.5 * cdist(X.astype(np.float64), X.astype(np.float64), "cosine")
+    np.fill_diagonal(ref, 0.0)
+    np.testing.assert_allclose(A, ref, rtol=1e-12, atol=1e-15)
+    assert np.all(np.diag(A) == 0.0) and A.min() >= 0.0
+
+
+def test_cosine_affinity_closed_form_and_invariance(orc):
+    """Points on rays at angles t: a = (1 + cos(t_i - t_j)) / 2; scaling
+    points by powers of two and a quarter turn (exact in float32) leave A
+    unchanged; the origin gets 1/2 against every point."""
+    t = np.array([0.0, 0.5, 1.9, 3.0, 4.4])
+    r = np.array([1.0, 2.0, 0.25, 8.0, 3.0])
+    X = np.stack([r * np.cos(t), r * np.sin(t)], axis=1).astype(np.float32)
+    A = orc.affinity_cosine(X)
+    tt = np.arctan2(X[:, 1].astype(np.float64), X[:, 0].astype(np.float64))
+    ref = 0.5 * (1.0 + np.cos(tt[:, None] - tt[None, :]))
+    np.fill_diagonal(ref, 0.0)
+    np.testing.assert_allclose(A, ref, rtol=1e-13, atol=1e-15)
+    scale = np.array([1, 4, 0.5, 2, 0.125], dtype=np.float32)[:, None]
+    np.testing.assert_array_equal(orc.affinity_cosine(X * scale), A)
+    Xr = np.stack([-X[:, 1], X[:, 0]], axis=1)
+    np.testing.assert_allclose(orc.affinity_cosine(Xr), A, rtol=1e-15, atol=1e-16)
+    Z = np.vstack([X, np.zeros((1, 2), np.float32)])
+    Az = orc.affinity_cosine(Z)
+    assert np.all(Az[-1, :-1] == 0.5) and np.all(Az[:-1, -1] == 0.5) and Az[-1, -1] == 0.0
+    assert np.array_equal(orc.affinity_cosine_rows(X, [1, 3]), A[[1, 3]])
+
+
 # ------------------------------------------------------ degree / normalise
 def test_rows_of_W_sum_to_one_and_v0(orc):
     """P1, P2: W = D^-1 A has unit row sums; v0 = d / sum d has L1 norm 1."""
