@@ -92,9 +92,12 @@ def main():
     ap.add_argument("--no-converge", action="store_true")
     ap.add_argument("--workload", default="blobs16d",
                     choices=["blobs16d", "blobs64d", "knn8d", "knn8d_rcm", "rings2d",
-                             "blobs2d"],
+                             "blobs2d", "moons", "circles3"],
                     help="blobs16d is the headline line; the others measure the "
-                         "fused, CSR and small dense paths")
+                         "fused, CSR, small dense and cosine (the paper's "
+                         "Experiment I shapes) paths")
+    ap.add_argument("--wn", type=int, default=None,
+                    help="points of a non-headline workload (its default if unset)")
     ap.add_argument("--copy-ref-gib", type=float, default=0.0,
                     help="also time a plain torch copy of this many GiB (the "
                          "reference kernel for counter scaling)")
@@ -247,6 +250,13 @@ def main():
     print(json.dumps(line), flush=True)
 
 
+# GPIC seconds the paper reports for its Experiment I shapes (Table 2:
+# cosine similarity, at most 3 updates, eps = 1e-5/n, Tesla K40m)
+PAPER_GPIC_S = {("moons", 15000): 3.99, ("circles3", 15000): 4.03,
+                ("moons", 30000): 18.00, ("circles3", 30000): 18.03,
+                ("moons", 45000): 45.07, ("circles3", 45000): 45.90}
+
+
 def other_workload(args):
     """Fused (blobs64d), CSR (knn8d) and small dense workloads: one JSON line
     with the path's own rate; not the headline line."""
@@ -258,11 +268,12 @@ def other_workload(args):
     cache = os.path.join(ROOT, ".cache")
     log(f"bench: building workload {args.workload} (the kNN graph takes minutes "
         f"on the host for knn8d)")
-    w = workloads.make(args.workload, cache_dir=cache)
+    w = workloads.make(args.workload, n=args.wn, cache_dir=cache)
     log(f"bench: workload {w.name} n={w.n} d={w.d} path={w.path} mode={w.mode}")
     stream = torch.cuda.current_stream(dev)
     X = torch.from_numpy(w.X).to(dev)
-    T = w.max_iter if w.mode == "fixed" else 1000
+    # the cosine workloads keep the paper's cap of 3 updates
+    T = w.max_iter if (w.mode == "fixed" or w.path == "cosine") else 1000
     extra = {}
     if w.path == "csr":
         rp = torch.from_numpy(w.row_ptr).to(dev)
@@ -277,6 +288,11 @@ def other_workload(args):
     elif w.path == "fused":
         def step():
             return g.pic_fused(X, w.sigma, w.k, w.mode, T, w.eps)
+    elif w.path == "cosine":
+        A = torch.empty((w.n, g.padded_ld(w.n)), dtype=torch.float32, device=dev)
+
+        def step():
+            return g.pic_cosine(X, w.k, w.mode, T, w.eps, W=A)
     else:
         A = torch.empty((w.n, g.padded_ld(w.n)), dtype=torch.float32, device=dev)
 
@@ -340,6 +356,11 @@ def other_workload(args):
             "iterations": it, "converged": out.pi.converged,
             "pi_ms": round(pi_ms, 4), "ms_per_update": round(pi_ms / max(it, 1), 5),
             "rate": rate}
+    paper = PAPER_GPIC_S.get((w.name, w.n))
+    if paper is not None:
+        # the paper's own GPIC time for this shape (another machine: context)
+        line["paper_context"] = {"gpic_s": paper, "hardware": "Tesla K40m",
+                                 "source": "Table 2", "e2e_s_here": round(ms / 1e3, 5)}
     print(json.dumps(line), flush=True)
 
 

@@ -70,7 +70,9 @@ enum {
     GPIC_OP_PI_CSR = 6,
     GPIC_OP_KMEANS1D = 7,
     GPIC_OP_AFFINITY_NORMALIZED = 8,
-    GPIC_OP_MATVEC_FUSED = 9
+    GPIC_OP_MATVEC_FUSED = 9,
+    GPIC_OP_AFFINITY_COSINE = 10,
+    GPIC_OP_AFFINITY_COSINE_NORMALIZED = 11
 };
 
 /* Power-iteration modes. */
@@ -143,6 +145,29 @@ gpic_status gpic_affinity_normalized(const float *X, int64_t n, int32_t d,
                                      double *degree, double *v0,
                                      int64_t *n_zero_rows, void *ws,
                                      size_t ws_bytes, void *stream);
+
+/* Dense cosine affinity, the similarity of the paper's Experiment I (Table
+ * 2 caption), shifted so that A stays non-negative (W = D^-1 A needs it):
+ *   A_ij = max(0, (1 + cos(x_i, x_j)) / 2) for i != j,  A_ii = 0,
+ *   cos(x_i, x_j) = x_i . x_j / (||x_i|| ||x_j||), taken as 0 when either
+ *   point is the origin (so the origin has A = 1/2 against every point).
+ * The dot product is a float32 sum over the raw coordinates, scaled by the
+ * reciprocal norms (float64, rounded once).  X, A, lda, degree as in
+ * gpic_affinity.  ws: gpic_workspace_bytes(GPIC_OP_AFFINITY_COSINE, n, 0, 0)
+ * bytes (reciprocal norms).  Errors: INVALID_ARG for null X/A, n < 2,
+ * d < 1, lda < n, lda % 4 != 0, misaligned pointers.  Asynchronous. */
+gpic_status gpic_affinity_cosine(const float *X, int64_t n, int32_t d, float *A,
+                                 int64_t lda, double *degree, void *ws,
+                                 size_t ws_bytes, void *stream);
+
+/* gpic_affinity_normalized for the cosine affinity: a degree sweep, v0 and
+ * the zero-degree count, then W_ij = A_ij * float32(1 / d_i) written
+ * directly.  Synchronises the stream (sum(D) check).
+ * ws: gpic_workspace_bytes(GPIC_OP_AFFINITY_COSINE_NORMALIZED, n, 0, 0). */
+gpic_status gpic_affinity_cosine_normalized(const float *X, int64_t n, int32_t d,
+                                            float *W, int64_t ldw, double *degree,
+                                            double *v0, int64_t *n_zero_rows,
+                                            void *ws, size_t ws_bytes, void *stream);
 
 /* --------------------------------- 2. degrees, W = D^-1 A, v0 = D / sum D */
 

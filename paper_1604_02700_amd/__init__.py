@@ -28,7 +28,8 @@ STATUS = {0: "GPIC_OK", 1: "GPIC_ERR_INVALID_ARG", 2: "GPIC_ERR_WORKSPACE",
           3: "GPIC_ERR_HIP", 4: "GPIC_ERR_NUMERIC", 5: "GPIC_ERR_UNSUPPORTED"}
 OP = {"affinity": 0, "degree_normalize": 1, "degree_normalize_csr": 2,
       "degree_fused": 3, "pi_dense": 4, "pi_fused": 5, "pi_csr": 6,
-      "kmeans1d": 7, "affinity_normalized": 8, "matvec_fused": 9}
+      "kmeans1d": 7, "affinity_normalized": 8, "matvec_fused": 9,
+      "affinity_cosine": 10, "affinity_cosine_normalized": 11}
 MODES = {"fixed": 0, "converge": 1}
 
 # C entry points declared in include/gpic.h (checked by the tests)
@@ -39,6 +40,7 @@ EXPORTS = (
     "gpic_degree_normalize_csr", "gpic_degree_fused", "gpic_matvec_dense",
     "gpic_matvec_csr", "gpic_matvec_fused", "gpic_power_iterate_dense",
     "gpic_power_iterate_fused", "gpic_power_iterate_csr", "gpic_kmeans1d",
+    "gpic_affinity_cosine", "gpic_affinity_cosine_normalized",
 )
 
 
@@ -81,6 +83,8 @@ def lib() -> C.CDLL:
         sigs = {
             "gpic_affinity": [p, i64, i32, f32, p, i64, p, p, sz, p],
             "gpic_affinity_normalized": [p, i64, i32, f32, p, i64, p, p, p, p, sz, p],
+            "gpic_affinity_cosine": [p, i64, i32, p, i64, p, p, sz, p],
+            "gpic_affinity_cosine_normalized": [p, i64, i32, p, i64, p, p, p, p, sz, p],
             "gpic_degree_normalize": [p, i64, i64, p, i32, p, p, p, sz, p],
             "gpic_degree_normalize_csr": [p, p, p, i64, i64, p, p, p, p, sz, p],
             "gpic_degree_fused": [p, i64, i32, f32, p, p, p, p, sz, p],
@@ -191,6 +195,47 @@ def gpic_affinity_normalized(X: torch.Tensor, sigma: float,
     _check(lib().gpic_affinity_normalized(_ptr(X), n, d, float(sigma), _ptr(W),
                                           W.stride(0), _ptr(degree), _ptr(v0),
                                           _ptr(nz), _ptr(ws), nb, _stream(dev)))
+    return W, degree, v0, nz
+
+
+def _square(M, n, name, dev):
+    if M is None:
+        M = torch.empty((n, padded_ld(n)), dtype=torch.float32, device=dev)
+    _dev(M, torch.float32, name)
+    if M.dim() != 2 or M.shape[0] != n or M.stride(1) != 1 or M.shape[1] < n:
+        raise ValueError(f"{name} must be [n, >= n] with unit column stride")
+    return M
+
+
+def gpic_affinity_cosine(X: torch.Tensor, A: Optional[torch.Tensor] = None,
+                         want_degree: bool = True):
+    """Cosine affinity (1 + cos) / 2 (float32 [n, lda]) and optional degrees."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    A = _square(A, n, "A", X.device)
+    deg = torch.empty(n, dtype=torch.float64, device=X.device) if want_degree else None
+    ws, nb = workspace("affinity_cosine", n, device=X.device)
+    _check(lib().gpic_affinity_cosine(_ptr(X), n, d, _ptr(A), A.stride(0), _ptr(deg),
+                                      _ptr(ws), nb, _stream(X.device)))
+    return A, deg
+
+
+def gpic_affinity_cosine_normalized(X: torch.Tensor, W: Optional[torch.Tensor] = None):
+    """W = D^-1 A for the cosine affinity, written directly; returns
+    (W, degree, v0, n_zero_rows tensor)."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    dev = X.device
+    W = _square(W, n, "W", dev)
+    degree = torch.empty(n, dtype=torch.float64, device=dev)
+    v0 = torch.empty(n, dtype=torch.float64, device=dev)
+    nz = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws, nb = workspace("affinity_cosine_normalized", n, device=dev)
+    _check(lib().gpic_affinity_cosine_normalized(_ptr(X), n, d, _ptr(W), W.stride(0),
+                                                 _ptr(degree), _ptr(v0), _ptr(nz),
+                                                 _ptr(ws), nb, _stream(dev)))
     return W, degree, v0, nz
 
 
@@ -398,6 +443,18 @@ def pic_dense(X, sigma, k, mode="converge", max_iter=1000, eps=0.0, check_every=
     else:
         A, deg = gpic_affinity(X, sigma, A)
         W, deg, v0, nz = gpic_degree_normalize(A, n, deg, degree_given=True)
+    v = v0.clone()
+    pi = gpic_power_iterate_dense(W, v, None, mode, max_iter, eps, check_every, n=n)
+    km = gpic_kmeans1d(pi.v, k)
+    return PICOut(deg, v0, pi, km, int(nz.item()))
+
+
+def pic_cosine(X, k, mode="converge", max_iter=3, eps=0.0, check_every=0,
+               W: Optional[torch.Tensor] = None) -> PICOut:
+    """The dense path with the cosine affinity of the paper's Experiment I
+    (its runs stop after at most 3 updates)."""
+    n = X.shape[0]
+    W, deg, v0, nz = gpic_affinity_cosine_normalized(X, W)
     v = v0.clone()
     pi = gpic_power_iterate_dense(W, v, None, mode, max_iter, eps, check_every, n=n)
     km = gpic_kmeans1d(pi.v, k)

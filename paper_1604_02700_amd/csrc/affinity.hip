@@ -1,4 +1,5 @@
-// Gaussian affinity tiles for gfx950, and the fused operator built on them.
+// Gaussian affinity tiles for gfx950, the fused operator built on them, and
+// the cosine affinity of the paper's Experiment I.
 //
 // A_ij = exp(-||x_i - x_j||^2 / (2 sigma^2)) for i != j, A_ii = 0: the
 // affinity matrix of section "Spectral Cluster" (AffinityMatrix step of
@@ -38,6 +39,7 @@ namespace gpic {
 namespace {
 
 enum { kStore = 0, kApply = 1, kDegree = 2, kStoreW = 3 };
+enum { kGauss = 0, kCosine = 1 };             // affinity kind (VALU engine)
 
 constexpr int kThreads = 256;
 constexpr int kMaxChunks = 16;
@@ -102,6 +104,24 @@ __global__ __launch_bounds__(kThreads) void augment_kernel(
             b[k] = 0.0f;
         }
     }
+}
+
+// rinv[p] = 1 / ||x_p|| (float64, rounded once), 0 for the origin: the
+// cosine affinity (1 + x_i.x_j rinv_i rinv_j) / 2 then gives the origin
+// 1/2 against every point.
+__global__ __launch_bounds__(kThreads) void inv_norm_kernel(const float *__restrict__ X,
+                                                            int64_t n, int d,
+                                                            float *__restrict__ rinv)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= n)
+        return;
+    double s = 0.0;
+    for (int k = 0; k < d; ++k) {
+        const double x = (double)X[p * d + k];
+        s = fma(x, x, s);
+    }
+    rinv[p] = (s > 0.0) ? (float)(1.0 / sqrt(s)) : 0.0f;
 }
 
 // ---------------------------------------------------- chunk row-sum reduce
@@ -337,12 +357,16 @@ __global__ __launch_bounds__(kMfmaThreads) void affinity_mfma_kernel(
 
 // Block: 256 threads, RB rows; each thread takes groups of 4 consecutive
 // columns (one 16-byte store per row), stepping by 1024 columns.
-template <int D, int RB, int MODE>
+// KIND kGauss: exp2(-c dist^2) from coordinate differences; kCosine:
+// max(0, (1 + (x_i.x_j) rinv_i rinv_j) / 2), the float32 dot product of the
+// raw coordinates scaled by the reciprocal norms.
+template <int D, int RB, int MODE, int KIND = kGauss>
 __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
     const float *__restrict__ X, int64_t n, int dyn_d, float c,
     float *__restrict__ A, int64_t lda, const double *__restrict__ v,
     const double *__restrict__ degree_in, double *__restrict__ out,
-    double *__restrict__ partial, StopCtl ctl, int use_ctl)
+    double *__restrict__ partial, StopCtl ctl, int use_ctl,
+    const float *__restrict__ rinv = nullptr)
 {
     __shared__ double red[kThreads / kWave];
     if (MODE == kApply && use_ctl) {
@@ -366,10 +390,12 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
     }
     double acc[RB];
     float rs[RB];
+    float ri[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
         acc[r] = 0.0;
         rs[r] = 0.0f;
+        ri[r] = (KIND == kCosine) ? rinv[(row0 + r < n) ? row0 + r : n - 1] : 0.0f;
         if (MODE == kStoreW) {
             const int64_t i = (row0 + r < n) ? row0 + r : n - 1;
             const double di = degree_in[i];
@@ -390,17 +416,30 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
                 for (int k = 0; k < DR; ++k)
                     xj[q][k] = X[j * d + k];
             }
+            float rj[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (KIND == kCosine) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    rj[q] = rinv[(j0 + q < n) ? j0 + q : n - 1];
+            }
 #pragma unroll
             for (int r = 0; r < RB; ++r)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     float s = 0.0f;
+                    if (KIND == kCosine) {
 #pragma unroll
-                    for (int k = 0; k < DR; ++k) {
-                        const float df = xi[r][k] - xj[q][k];
-                        s = fmaf(df, df, s);
+                        for (int k = 0; k < DR; ++k)
+                            s = fmaf(xi[r][k], xj[q][k], s);
+                        a[r][q] = fmaxf(fmaf(0.5f, s * (ri[r] * rj[q]), 0.5f), 0.0f);
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < DR; ++k) {
+                            const float df = xi[r][k] - xj[q][k];
+                            s = fmaf(df, df, s);
+                        }
+                        a[r][q] = exp2_fast(-c * s);
                     }
-                    a[r][q] = exp2_fast(-c * s);
                 }
         } else {
             // any d (used above the matrix-core range): coordinates re-read
@@ -411,11 +450,17 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
                 for (int q = 0; q < 4; ++q) {
                     const int64_t j = (j0 + q < n) ? j0 + q : n - 1;
                     float s = 0.0f;
-                    for (int k = 0; k < d; ++k) {
-                        const float df = X[i * d + k] - X[j * d + k];
-                        s = fmaf(df, df, s);
+                    if (KIND == kCosine) {
+                        for (int k = 0; k < d; ++k)
+                            s = fmaf(X[i * d + k], X[j * d + k], s);
+                        a[r][q] = fmaxf(fmaf(0.5f, s * (ri[r] * rinv[j]), 0.5f), 0.0f);
+                    } else {
+                        for (int k = 0; k < d; ++k) {
+                            const float df = X[i * d + k] - X[j * d + k];
+                            s = fmaf(df, df, s);
+                        }
+                        a[r][q] = exp2_fast(-c * s);
                     }
-                    a[r][q] = exp2_fast(-c * s);
                 }
             }
         }
@@ -605,7 +650,61 @@ hipError_t dispatch(const float *X, int64_t n, int d, float c, float *A,
     return hipGetLastError();
 }
 
+template <int MODE>
+hipError_t dispatch_cosine(const float *X, int64_t n, int d, float *A, int64_t lda,
+                           const double *degree_in, double *out, float *rinv,
+                           hipStream_t s)
+{
+    hipLaunchKernelGGL(inv_norm_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, X, n, d, rinv);
+    const dim3 block(kThreads);
+    constexpr int RB = 8;
+    const dim3 grid((unsigned)((n + RB - 1) / RB));
+    StopCtl none{};
+#define GPIC_COS(D)                                                             \
+    case D:                                                                    \
+        hipLaunchKernelGGL((affinity_valu_kernel<D, RB, MODE, kCosine>), grid, block, \
+                           0, s, X, n, d, 0.0f, A, lda, nullptr, degree_in, out, \
+                           nullptr, none, 0, rinv);                            \
+        break;
+    switch (d) {
+        GPIC_COS(1) GPIC_COS(2) GPIC_COS(3) GPIC_COS(4) GPIC_COS(5)
+        GPIC_COS(6) GPIC_COS(7) GPIC_COS(8) GPIC_COS(9) GPIC_COS(10)
+        GPIC_COS(11) GPIC_COS(12) GPIC_COS(13) GPIC_COS(14) GPIC_COS(15)
+        GPIC_COS(16)
+    default:
+        hipLaunchKernelGGL((affinity_valu_kernel<0, RB, MODE, kCosine>), grid, block, 0,
+                           s, X, n, d, 0.0f, A, lda, nullptr, degree_in, out, nullptr,
+                           none, 0, rinv);
+    }
+#undef GPIC_COS
+    return hipGetLastError();
+}
+
 } // namespace
+
+size_t cosine_ws(int64_t n) { return (size_t)al256(n * 4); }
+
+hipError_t launch_affinity_cosine(const float *X, int64_t n, int d, float *A,
+                                  int64_t lda, double *degree, void *ws, hipStream_t s)
+{
+    return dispatch_cosine<kStore>(X, n, d, A, lda, nullptr, degree,
+                                   static_cast<float *>(ws), s);
+}
+
+hipError_t launch_cosine_degree(const float *X, int64_t n, int d, double *degree,
+                                void *ws, hipStream_t s)
+{
+    return dispatch_cosine<kDegree>(X, n, d, nullptr, 0, nullptr, degree,
+                                    static_cast<float *>(ws), s);
+}
+
+hipError_t launch_cosine_w(const float *X, int64_t n, int d, float *W, int64_t ldw,
+                           const double *degree, void *ws, hipStream_t s)
+{
+    return dispatch_cosine<kStoreW>(X, n, d, W, ldw, degree, nullptr,
+                                    static_cast<float *>(ws), s);
+}
 
 size_t affinity_ws(int64_t n)
 {

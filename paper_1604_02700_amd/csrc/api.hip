@@ -106,12 +106,20 @@ bool gauss_coefficient(float sigma, float *c)
     return isfinite(*c) && *c > 0.0f;
 }
 
-gpic_status check_points(const float *X, int64_t n, int32_t d, float sigma)
+gpic_status check_coords(const float *X, int64_t n, int32_t d)
 {
     CHECK_ARG(X != nullptr, "X is null");
     CHECK_ARG(aligned(X, 4), "X must be 4-byte aligned");
     CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range [2, 2^31-1]", (long long)n);
     CHECK_ARG(d >= 1, "d = %d must be >= 1", d);
+    return GPIC_OK;
+}
+
+gpic_status check_points(const float *X, int64_t n, int32_t d, float sigma)
+{
+    gpic_status st = check_coords(X, n, d);
+    if (st != GPIC_OK)
+        return st;
     CHECK_ARG(isfinite(sigma) && sigma > 0.0f, "sigma must be finite and > 0");
     float c;
     CHECK_ARG(gauss_coefficient(sigma, &c), "sigma too small (1/(2 sigma^2) overflows)");
@@ -360,6 +368,8 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     case GPIC_OP_KMEANS1D: return kmeans_ws(n, k < 1 ? 1 : k);
     case GPIC_OP_AFFINITY_NORMALIZED: return start_ws(n) + aff_ws(n);
     case GPIC_OP_MATVEC_FUSED: return aff_ws(n);
+    case GPIC_OP_AFFINITY_COSINE: return al(cosine_ws(n));
+    case GPIC_OP_AFFINITY_COSINE_NORMALIZED: return start_ws(n) + al(cosine_ws(n));
     default: return 0;
     }
 }
@@ -416,6 +426,56 @@ gpic_status gpic_affinity_normalized(const float *X, int64_t n, int32_t d,
     if (bad)
         return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
     CHECK_HIP(launch_affinity_w(X, n, d, c, W, ldw, degree, aws, s), "W sweep");
+    return GPIC_OK;
+}
+
+gpic_status gpic_affinity_cosine(const float *X, int64_t n, int32_t d, float *A,
+                                 int64_t lda, double *degree, void *ws, size_t ws_bytes,
+                                 void *stream)
+{
+    gpic_status st = check_coords(X, n, d);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(A != nullptr, "A is null");
+    CHECK_ARG(aligned(A, 16), "A must be 16-byte aligned");
+    CHECK_ARG(lda >= n && lda % 4 == 0, "lda = %lld must be >= n and a multiple of 4",
+              (long long)lda);
+    if ((st = check_vec(degree, "degree", true)) != GPIC_OK)
+        return st;
+    if ((st = check_ws(ws, ws_bytes, al(cosine_ws(n)))) != GPIC_OK)
+        return st;
+    CHECK_HIP(launch_affinity_cosine(X, n, d, A, lda, degree, ws, (hipStream_t)stream),
+              "cosine affinity");
+    return GPIC_OK;
+}
+
+gpic_status gpic_affinity_cosine_normalized(const float *X, int64_t n, int32_t d,
+                                            float *W, int64_t ldw, double *degree,
+                                            double *v0, int64_t *n_zero_rows, void *ws,
+                                            size_t ws_bytes, void *stream)
+{
+    gpic_status st = check_coords(X, n, d);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(W != nullptr, "W is null");
+    CHECK_ARG(aligned(W, 16), "W must be 16-byte aligned");
+    CHECK_ARG(ldw >= n && ldw % 4 == 0, "ldw = %lld must be >= n and a multiple of 4",
+              (long long)ldw);
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v0, "v0")) != GPIC_OK)
+        return st;
+    CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
+              "n_zero_rows misaligned");
+    if ((st = check_ws(ws, ws_bytes, start_ws(n) + al(cosine_ws(n)))) != GPIC_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    void *cws = static_cast<char *>(ws) + start_ws(n);
+    CHECK_HIP(launch_cosine_degree(X, n, d, degree, cws, s), "degree sweep");
+    int bad = 0;
+    CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
+    if (bad)
+        return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
+    CHECK_HIP(launch_cosine_w(X, n, d, W, ldw, degree, cws, s), "W sweep");
     return GPIC_OK;
 }
 

@@ -125,6 +125,15 @@ hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c_log2,
                               void *ws, hipStream_t s);
 // number of |y| partial sums the fused product writes
 int64_t fused_blocks(int64_t n, int d);
+// cosine affinity (1 + cos) / 2, zero diagonal -- ws: cosine_ws(n) bytes
+// (reciprocal norms)
+size_t cosine_ws(int64_t n);
+hipError_t launch_affinity_cosine(const float *X, int64_t n, int d, float *A,
+                                  int64_t lda, double *degree, void *ws, hipStream_t s);
+hipError_t launch_cosine_degree(const float *X, int64_t n, int d, double *degree,
+                                void *ws, hipStream_t s);
+hipError_t launch_cosine_w(const float *X, int64_t n, int d, float *W, int64_t ldw,
+                           const double *degree, void *ws, hipStream_t s);
 
 // normalize.hip
 hipError_t launch_dense_degree(const float *A, int64_t n, int64_t lda,

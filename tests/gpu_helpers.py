@@ -65,3 +65,13 @@ def affinity_tolerance(X, sigma, A_ref, gram: bool):
     e = e + 4 * EPS32 * dist2
     # float32 underflow: values below the smallest normal may flush to 0
     return A_ref * e / s2 + 8 * EPS32 * A_ref + 2.4e-38
+
+
+def cosine_tolerance(d):
+    """Absolute bound on |A_gpu - A_ref| for the cosine affinity
+    max(0, (1 + x_i.x_j rinv_i rinv_j) / 2): the float32 dot product of d
+    terms is off by at most d eps32 |x_i| |x_j| (Cauchy-Schwarz), the
+    reciprocal norms and the two products add 4 eps32 relative, halving
+    keeps that, and the final fused multiply-add rounds once at magnitude
+    <= 1; (d + 8) eps32 covers the sum with margin."""
+    return (d + 8) * EPS32

@@ -39,7 +39,8 @@ def test_status_strings(L):
 def test_workspace_sizes(L):
     import paper_1604_02700_amd as g
     for op in ("affinity", "affinity_normalized", "degree_normalize", "degree_fused",
-               "pi_dense", "pi_fused", "pi_csr", "kmeans1d", "matvec_fused"):
+               "pi_dense", "pi_fused", "pi_csr", "kmeans1d", "matvec_fused",
+               "affinity_cosine", "affinity_cosine_normalized"):
         a = g.workspace_bytes(op, 1000, 5000, 3)
         b = g.workspace_bytes(op, 100000, 500000, 3)
         assert 0 < a < b
@@ -74,6 +75,15 @@ def test_argument_validation_before_launch(L):
     fn = L.gpic_affinity_normalized
     assert fn(dummy, 10, 2, 1.0, dummy, 12, dummy, dummy, None, dummy, 8, None) == 2
     assert fn(dummy, 10, 2, 1.0, dummy, 12, None, dummy, None, *W, None) == 1
+    fc = L.gpic_affinity_cosine
+    assert fc(None, 10, 2, dummy, 12, None, *W, None) == 1
+    assert fc(dummy, 1, 2, dummy, 12, None, *W, None) == 1               # n < 2
+    assert fc(dummy, 10, 0, dummy, 12, None, *W, None) == 1              # d < 1
+    assert fc(dummy, 10, 2, dummy, 9, None, *W, None) == 1               # lda < n
+    assert fc(dummy, 10, 2, dummy, 12, None, dummy, 8, None) == 2        # workspace
+    fcn = L.gpic_affinity_cosine_normalized
+    assert fcn(dummy, 10, 2, dummy, 12, None, dummy, None, *W, None) == 1   # degree null
+    assert fcn(dummy, 10, 2, dummy, 12, dummy, dummy, None, dummy, 8, None) == 2
     p = g.PiParams()
     p.mode, p.max_iter, p.eps, p.check_every, p.reserved = 2, 10, 0.0, 0, 0
     r = g.PiResult()

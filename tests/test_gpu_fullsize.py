@@ -11,6 +11,8 @@ benchmark times.
 * kNN graph (CSR) at a reduced n, end to end, and at its full size
   (n = 2,000,000, the column-blocked product) to convergence.
 * 1-D k-means at the kNN workload's full size (n = 2,000,000, k = 50).
+* The paper's Experiment I shape at its largest size: two moons, n = 45,000,
+  cosine affinity, at most 3 updates, end to end.
 """
 import numpy as np
 import pytest
@@ -205,3 +207,25 @@ def test_knn_csr_full_size_converge(g, orc):
     assert ref.converged and out.pi.converged
     assert out.pi.iterations == ref.iterations
     assert rel_l1(out.pi.v.cpu().numpy(), ref.v) <= 1e-4
+
+
+def test_moons_full_size_cosine(g, orc):
+    """Two moons, n = 45,000, cosine affinity (dense W of 8.1 GB), at most 3
+    updates with eps = 1e-5 / n: degrees, stop and v against the oracle."""
+    import workloads
+    w = workloads.make("moons")
+    print(f"gpu: moons n={w.n} cosine, <= {w.max_iter} updates", flush=True)
+    out = g.pic_cosine(_t(w.X), w.k, "converge", w.max_iter, w.eps)
+    vg = out.pi.v.cpu().numpy()
+    dg = out.degree.cpu().numpy()
+    it, conv = out.pi.iterations, out.pi.converged
+    del out
+    torch.cuda.empty_cache()
+    print("oracle: moons n=45000 (cosine affinity, normalise, <= 3 updates)", flush=True)
+    A = orc.affinity_cosine(w.X)
+    W, deg, v0, _ = orc.degree_normalize(A, copy=False)
+    ref = orc.power_iterate_dense(W, v0, "converge", w.max_iter, w.eps)
+    del A, W
+    np.testing.assert_allclose(dg, deg, rtol=1e-5)
+    assert it == ref.iterations and conv == ref.converged
+    assert rel_l1(vg, ref.v) <= 1e-4

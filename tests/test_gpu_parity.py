@@ -7,7 +7,7 @@ state in float64; the oracle is float64 throughout.
 import numpy as np
 import pytest
 
-from gpu_helpers import (EPS32, affinity_tolerance, matched_agreement, rel_l1,
+from gpu_helpers import (cosine_tolerance, EPS32, affinity_tolerance, matched_agreement, rel_l1,
                          separation_ok, stop_margin)
 
 pytestmark = pytest.mark.gpu
@@ -55,6 +55,38 @@ def test_affinity_parity(g, orc, n, d):
     assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
     # degrees are the float64 sums of the stored float32 values
     np.testing.assert_allclose(deg.cpu().numpy(), Ag.sum(1), rtol=1e-13)
+
+
+@pytest.mark.parametrize("n,d", [(2, 2), (3, 1), (64, 2), (1000, 2), (1023, 5),
+                                 (300, 16), (257, 17), (99, 40)])
+def test_cosine_affinity_parity(g, orc, n, d):
+    """Cosine affinity (1 + cos) / 2 against the oracle, with the origin and
+    an antipodal pair among the points."""
+    X = _pts(n, d, 2000 + n + d, scale=2.0)
+    X[0] = 0.0
+    if n > 2:
+        X[2] = -X[1] * np.float32(3.0)            # cos = -1 with row 1
+    print(f"cosine affinity n={n} d={d}", flush=True)
+    A, deg = g.gpic_affinity_cosine(_t(X))
+    torch.cuda.synchronize()
+    Ag = A[:, :n].cpu().numpy().astype(np.float64)
+    Ar = orc.affinity_cosine(X)
+    assert np.all(np.diag(Ag) == 0.0) and Ag.min() >= 0.0
+    err = np.abs(Ag - Ar)
+    assert err.max() <= cosine_tolerance(d), f"max err {err.max():.3g}"
+    assert np.all(Ag[0, 1:] == 0.5) and np.all(Ag[1:, 0] == 0.5)
+    np.testing.assert_allclose(deg.cpu().numpy(), Ag.sum(1), rtol=1e-13)
+
+
+@pytest.mark.parametrize("n,d", [(777, 2), (1025, 16)])
+def test_cosine_normalized_equals_two_calls(g, n, d):
+    X = _pts(n, d, 3000 + n, scale=1.5)
+    A, deg = g.gpic_affinity_cosine(_t(X))
+    W2, deg2, v02, _ = g.gpic_degree_normalize(A, n, deg, True)
+    W, degree, v0, nz = g.gpic_affinity_cosine_normalized(_t(X))
+    torch.cuda.synchronize()
+    assert torch.equal(W[:, :n], W2[:, :n]) and torch.equal(degree, deg2)
+    assert torch.equal(v0, v02) and int(nz.item()) == 0
 
 
 def test_affinity_padding_untouched(g):
@@ -237,6 +269,25 @@ def test_pic_dense_fixed_T_parity_16d(g, orc, n):
     # the statistic only matters against eps = 1e-5/n: agree to 1e-3 relative
     # or 1e-3 eps absolute (below that it is rounding noise of v)
     np.testing.assert_allclose(out.pi.stats, ref.pi.stats, rtol=1e-3, atol=1e-3 * w.eps)
+
+
+@pytest.mark.parametrize("name", ["moons", "circles3"])
+def test_pic_cosine_parity(g, orc, name):
+    """The paper's Experiment I path at n = 3,000: cosine affinity, W, at
+    most 3 updates with eps = 1e-5 / n, then k-means, against the oracle."""
+    import workloads
+    w = workloads.make(name, n=3000)
+    out = g.pic_cosine(_t(w.X), w.k, "converge", w.max_iter, w.eps)
+    A = orc.affinity_cosine(w.X)
+    W, deg, v0, _ = orc.degree_normalize(A, copy=False)
+    ref = orc.power_iterate_dense(W, v0, "converge", w.max_iter, w.eps)
+    np.testing.assert_allclose(out.degree.cpu().numpy(), deg, rtol=1e-5)
+    assert out.pi.iterations == ref.iterations and out.pi.converged == ref.converged
+    vg = out.pi.v.cpu().numpy()
+    assert rel_l1(vg, ref.v) <= 1e-4
+    km = orc.kmeans1d(ref.v, w.k)
+    if separation_ok(ref.v, vg, km.labels):
+        assert matched_agreement(out.km.labels.cpu().numpy(), km.labels) >= 0.999
 
 
 # ------------------------------------------------------------------ k-means

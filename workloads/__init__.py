@@ -25,7 +25,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = [
-    "Workload", "WORKLOADS", "make", "blobs_uniform_centres", "rings",
+    "Workload", "WORKLOADS", "make", "blobs_uniform_centres", "rings", "two_moons",
     "blobs_dirichlet", "blobs_equal", "knn_graph", "sha256_of",
     "split_equal", "split_dirichlet", "median_pair_distance_sigma",
 ]
@@ -41,7 +41,7 @@ class Workload:
     k: int                        # clusters for the final 1-D k-means
     mode: str                     # "converge" or "fixed"
     max_iter: int                 # T in fixed mode, the cap otherwise
-    path: str                     # "dense", "fused" or "csr"
+    path: str                     # "dense", "fused", "csr" or "cosine" (dense W)
     seed: int
     # sparse workload only: fp32 CSR affinity graph, rows sorted by column
     row_ptr: Optional[np.ndarray] = None   # int64 [n + 1]
@@ -135,6 +135,24 @@ def rings(n=10000, radii=(1.0, 3.0, 5.0), noise=0.1, seed=2):
         th = rng.uniform(0.0, 2.0 * np.pi, size=int(m))
         rr = r + noise * rng.standard_normal(int(m))
         pts.append(np.stack([rr * np.cos(th), rr * np.sin(th)], axis=1))
+        lab.append(np.full(int(m), c, dtype=np.int32))
+    return _finish(rng, np.concatenate(pts), np.concatenate(lab))
+
+
+def two_moons(n=45000, noise=0.05, seed=6):
+    """Two interleaved half circles in 2-D (the classic two-moons shape):
+    upper (cos t, sin t), lower (1 - cos t, 1/2 - sin t), t ~ U[0, pi],
+    plus N(0, noise^2) on each coordinate."""
+    rng = np.random.default_rng(seed)
+    sizes = split_equal(n, 2)
+    pts, lab = [], []
+    for c, m in enumerate(sizes):
+        t = rng.uniform(0.0, np.pi, size=int(m))
+        if c == 0:
+            p = np.stack([np.cos(t), np.sin(t)], axis=1)
+        else:
+            p = np.stack([1.0 - np.cos(t), 0.5 - np.sin(t)], axis=1)
+        pts.append(p + noise * rng.standard_normal(p.shape))
         lab.append(np.full(int(m), c, dtype=np.int32))
     return _finish(rng, np.concatenate(pts), np.concatenate(lab))
 
@@ -241,6 +259,20 @@ def _c4(seed, n):
                     "fixed", 30, "fused", seed)
 
 
+def _moons(seed, n):
+    n = n or 45000
+    X, y = two_moons(n=n, seed=seed)
+    return Workload("moons", X, y, np.float32(1.0), 1e-5 / n, 2,
+                    "converge", 3, "cosine", seed)
+
+
+def _circles3(seed, n):
+    n = n or 45000
+    X, y = rings(n=n, radii=(1.0, 2.0, 3.0), noise=0.05, seed=seed)
+    return Workload("circles3", X, y, np.float32(1.0), 1e-5 / n, 3,
+                    "converge", 3, "cosine", seed)
+
+
 def _c5(seed, n, cache_dir=None):
     n = n or 2000000
     k = 50
@@ -297,6 +329,10 @@ WORKLOADS = {
     "knn8d": (_c5, 5),
     # the same graph with nodes renumbered by reverse Cuthill-McKee
     "knn8d_rcm": (_c5_rcm, 5),
+    # the paper's Experiment I shapes: n=45,000 (15k, 30k via n=), d=2,
+    # cosine affinity, at most 3 updates, eps = 1e-5/n, dense W
+    "moons": (_moons, 6),
+    "circles3": (_circles3, 7),
 }
 
 
