@@ -51,6 +51,8 @@ def _pin_suite(orc):
         ("affinity_invariant", lambda: pins.test_affinity_symmetric_and_invariant(orc)),
         ("cosine_scipy", lambda: pins.test_cosine_affinity_matches_scipy_distance(orc)),
         ("cosine_closed", lambda: pins.test_cosine_affinity_closed_form_and_invariance(orc)),
+        ("brute_gauss", lambda: pins.test_brute_force_fifty_digits(orc, 8, 2, "gauss")),
+        ("brute_cosine", lambda: pins.test_brute_force_fifty_digits(orc, 7, 3, "cosine")),
         ("row_sums_v0", lambda: pins.test_rows_of_W_sum_to_one_and_v0(orc)),
         ("zero_degree", lambda: pins.test_zero_degree_row_is_counted(orc)),
         ("two_points", lambda: pins.test_two_points_give_swap_matrix(orc)),

@@ -408,3 +408,78 @@ def test_pic_recovers_separated_blobs(orc):
     assert r.pi.converged
     from sklearn.metrics import adjusted_rand_score
     assert adjusted_rand_score(w.y_true, r.km.labels) > 0.99
+
+
+# ------------------------------------------------ P7: 50-digit brute force
+def _mp_pic(X, sigma, T, kind="gauss"):
+    """Algorithm 1 at 50 significant digits (mpmath), from the float32
+    points promoted exactly: A, D, W = D^-1 A, v0 = d / sum d, delta_0 = v0,
+    then T updates v <- W v / ||W v||_1 with the velocity statistic."""
+    import mpmath as mp
+    mp.mp.dps = 50
+    n, d = X.shape
+    P = [[mp.mpf(float(X[i, c])) for c in range(d)] for i in range(n)]
+    s2 = 2 * mp.mpf(float(np.float32(sigma))) ** 2
+    A = [[mp.mpf(0)] * n for _ in range(n)]
+    for i in range(n):
+        for j in range(n):
+            if i == j:
+                continue
+            if kind == "gauss":
+                A[i][j] = mp.e ** (-sum((P[i][c] - P[j][c]) ** 2 for c in range(d)) / s2)
+            else:
+                dot = sum(P[i][c] * P[j][c] for c in range(d))
+                ni = mp.sqrt(sum(x * x for x in P[i]))
+                nj = mp.sqrt(sum(x * x for x in P[j]))
+                A[i][j] = (1 + dot / (ni * nj)) / 2
+    deg = [sum(A[i]) for i in range(n)]
+    W = [[A[i][j] / deg[i] for j in range(n)] for i in range(n)]
+    tot = sum(deg)
+    v = [x / tot for x in deg]
+    delta = list(v)
+    stats = []
+    for _ in range(T):
+        y = [sum(W[i][j] * v[j] for j in range(n)) for i in range(n)]
+        tau = sum(abs(x) for x in y)
+        vn = [x / tau for x in y]
+        dn = [abs(a - b) for a, b in zip(vn, v)]
+        stats.append(max(abs(a - b) for a, b in zip(dn, delta)))
+        v, delta = vn, dn
+    return ([float(x) for x in deg], np.array([float(x) for x in v]),
+            np.array([float(x) for x in stats]), [[float(x) for x in r] for r in W])
+
+
+@pytest.mark.parametrize("n,seed,kind", [(5, 1, "gauss"), (8, 2, "gauss"), (7, 3, "cosine")])
+def test_brute_force_fifty_digits(orc, n, seed, kind):
+    """P7: the whole method on n <= 8 points at 50 digits agrees with the
+    float64 oracle to rounding: degrees, W, v and every statistic after
+    T = 6 updates; a stop threshold placed between two statistics stops
+    both at the same update; k-means against all contiguous partitions."""
+    X = _pts(n, 2, 900 + seed, scale=1.2)
+    sigma = np.float32(0.9)
+    T = 6
+    deg_m, v_m, st_m, W_m = _mp_pic(X, sigma, T, kind)
+    A = orc.affinity(X, sigma) if kind == "gauss" else orc.affinity_cosine(X)
+    W, deg, v0, _ = orc.degree_normalize(A)
+    np.testing.assert_allclose(deg, deg_m, rtol=1e-14)
+    # absolute floor: (1 + cos) / 2 for nearly opposite points cancels in
+    # float64 (an error of 1e-16 in cos on an entry near 0)
+    np.testing.assert_allclose(W, np.array(W_m), rtol=1e-14, atol=4e-16)
+    r = orc.power_iterate_dense(W, v0, "fixed", T)
+    np.testing.assert_allclose(r.v, v_m, rtol=1e-13)
+    np.testing.assert_allclose(r.stats, st_m, rtol=1e-9, atol=1e-17)
+    # stop between updates 3 and 4 (statistics decreasing there)
+    if st_m[2] > st_m[3]:
+        eps = float(np.sqrt(st_m[2] * st_m[3]))
+        rc = orc.power_iterate_dense(W, v0, "converge", 100, eps)
+        stop = next(t for t in range(T) if st_m[t] <= eps) + 1
+        assert rc.iterations == stop and rc.converged
+    # k-means of the 50-digit v by enumerating contiguous partitions
+    order = np.argsort(v_m, kind="stable")
+    vs = v_m[order]
+    for k in (2, 3):
+        best = min(sum(((vs[a:b] - vs[a:b].mean()) ** 2).sum()
+                       for a, b in zip((0,) + cuts, cuts + (n,)))
+                   for cuts in itertools.combinations(range(1, n), k - 1))
+        km = orc.kmeans1d(r.v, k)
+        assert km.cost == pytest.approx(best, rel=1e-9, abs=1e-20)
