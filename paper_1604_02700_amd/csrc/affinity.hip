@@ -582,14 +582,16 @@ template <int MODE>
 hipError_t dispatch(const float *X, int64_t n, int d, float c, float *A,
                     int64_t lda, const double *v, const double *degree_in,
                     double *out, double *partial, StopCtl ctl, int use_ctl,
-                    void *ws, hipStream_t s)
+                    void *ws, hipStream_t s, bool operands_ready = false)
 {
     if (use_mfma(d)) {
         const Ws w = carve(ws, n);
         const int ks = ks_for(d);
         const int64_t np = padded_points(n);
-        hipLaunchKernelGGL(augment_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
-                           dim3(kThreads), 0, s, X, n, np, d, 4 * ks, c, w.xa, w.xb);
+        if (!operands_ready)
+            hipLaunchKernelGGL(augment_kernel,
+                               dim3((unsigned)((np + kThreads - 1) / kThreads)),
+                               dim3(kThreads), 0, s, X, n, np, d, 4 * ks, c, w.xa, w.xb);
         int64_t chunk_cols;
         int nchunks;
         chunking(n, &chunk_cols, &nchunks);
@@ -749,13 +751,25 @@ hipError_t launch_fused_degree(const float *X, int64_t n, int d, float c,
                              nullptr, none, 0, ws, s);
 }
 
+hipError_t launch_fused_prepare(const float *X, int64_t n, int d, float c, void *ws,
+                                hipStream_t s)
+{
+    if (!use_mfma(d))
+        return hipSuccess;
+    const Ws w = carve(ws, n);
+    const int64_t np = padded_points(n);
+    hipLaunchKernelGGL(augment_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, X, n, np, d, 4 * ks_for(d), c, w.xa, w.xb);
+    return hipGetLastError();
+}
+
 hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c,
                               const double *v, const double *degree, double *y,
                               double *partial, StopCtl ctl, bool use_ctl,
-                              void *ws, hipStream_t s)
+                              void *ws, hipStream_t s, bool operands_ready)
 {
     return dispatch<kApply>(X, n, d, c, nullptr, 0, v, degree, y, partial, ctl,
-                            use_ctl ? 1 : 0, ws, s);
+                            use_ctl ? 1 : 0, ws, s, operands_ready);
 }
 
 } // namespace gpic

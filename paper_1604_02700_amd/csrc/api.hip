@@ -243,7 +243,7 @@ struct FusedProduct : Product {
                       hipStream_t s) const override
     {
         return launch_fused_apply(X, n, d, c, v, degree, y, partial, ctl, true,
-                                  scratch, s);
+                                  scratch, s, true);
     }
 };
 
@@ -669,6 +669,9 @@ gpic_status gpic_power_iterate_fused(const float *X, int64_t n, int32_t d,
     gauss_coefficient(sigma, &op.c);
     op.degree = degree;
     op.scratch = static_cast<char *>(ws) + pi_ws(n, fused_nb_bound(n));
+    // the augmented operands are the same for every product of the run
+    CHECK_HIP(launch_fused_prepare(X, n, d, op.c, op.scratch, (hipStream_t)stream),
+              "operands");
     return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
 }
 

@@ -119,10 +119,15 @@ hipError_t launch_affinity_w(const float *X, int64_t n, int d, float c_log2,
                              void *ws, hipStream_t s);
 hipError_t launch_fused_degree(const float *X, int64_t n, int d, float c_log2,
                                double *degree, void *ws, hipStream_t s);
+// Augmented operands for the matrix-core engine, once for a run of
+// products that pass operands_ready = true (no-op below 16 or above 128
+// dimensions).
+hipError_t launch_fused_prepare(const float *X, int64_t n, int d, float c_log2,
+                                void *ws, hipStream_t s);
 hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c_log2,
                               const double *v, const double *degree, double *y,
                               double *partial, StopCtl ctl, bool use_ctl,
-                              void *ws, hipStream_t s);
+                              void *ws, hipStream_t s, bool operands_ready = false);
 // number of |y| partial sums the fused product writes
 int64_t fused_blocks(int64_t n, int d);
 // cosine affinity (1 + cos) / 2, zero diagonal -- ws: cosine_ws(n) bytes
