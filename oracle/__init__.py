@@ -81,6 +81,8 @@ def _declare(lib):
     lib.orc_num_threads.restype = i32
     lib.orc_affinity_rows.argtypes = [p, i64, i32, f64, i64, i64, p]
     lib.orc_affinity_cosine_rows.argtypes = [p, i64, i32, i64, i64, p]
+    lib.orc_knn_graph.argtypes = [p, i64, i32, i32, f64, p, p, p]
+    lib.orc_knn_graph.restype = i64
     lib.orc_degree_rows.argtypes = [p, i64, i32, f64, p, i64, p]
     lib.orc_degree_normalize.argtypes = [p, i64, p, p]
     lib.orc_degree_normalize.restype = i64
@@ -279,6 +281,21 @@ class KMeansResult:
     centroids: np.ndarray   # float64 [k_eff]
     k_eff: int
     cost: float             # total within-cluster sum of squares
+
+
+def knn_graph(X, k, sigma):
+    """Exact kNN graph (self excluded, ties to the smaller index), union
+    symmetrised, Gaussian weights: (row_ptr int64, col int32, val float32)."""
+    X = _f32(X)
+    n, d = X.shape
+    rp = np.empty(n + 1, dtype=np.int64)
+    col = np.empty(2 * n * int(k), dtype=np.int32)
+    val = np.empty(2 * n * int(k), dtype=np.float32)
+    nnz = _L().orc_knn_graph(_ptr(X), n, d, int(k), float(np.float32(sigma)), _ptr(rp),
+                             _ptr(col), _ptr(val))
+    if nnz < 0:
+        raise ValueError("k must be in [1, n-1]")
+    return rp, col[:nnz].copy(), val[:nnz].copy()
 
 
 def kmeans1d(v, k, method="auto") -> KMeansResult:

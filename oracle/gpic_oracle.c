@@ -30,6 +30,10 @@
  *                          equation of section "PIC: an overview"),
  *                          delta_{t+1} = |v_{t+1} - v_t|, stop when
  *                          |delta_{t+1} - delta_t| <= eps for every entry.
+ *   orc_knn_graph          the sparse affinity graph the CSR path takes as
+ *                          input: exact k nearest neighbours, union
+ *                          symmetrised, Gaussian weights (not in the paper;
+ *                          the input of its method in graph form).
  *   orc_kmeans1d           "k-means of v" (Algorithm 1, last step), read as
  *                          the exact minimum within-cluster sum of squares
  *                          partition of the scalars v_i (plain O(k n^2)
@@ -552,4 +556,96 @@ int32_t orc_kmeans1d(const double *v, int64_t n, int32_t k, int32_t method,
     free(run_start);
     free(kv);
     return status;
+}
+
+/* ------------------------------------------------------------------ */
+/* kNN input graph                                                     */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t row, col;
+} edge_t;
+
+static int cmp_edge(const void *a, const void *b)
+{
+    const edge_t *x = (const edge_t *)a, *y = (const edge_t *)b;
+    if (x->row != y->row)
+        return x->row < y->row ? -1 : 1;
+    if (x->col != y->col)
+        return x->col < y->col ? -1 : 1;
+    return 0;
+}
+
+static double sq_dist(const float *X, int32_t d, int64_t i, int64_t j)
+{
+    double s = 0.0;
+    for (int32_t c = 0; c < d; ++c) {
+        double diff = (double)X[i * d + c] - (double)X[j * d + c];
+        s += diff * diff;
+    }
+    return s;
+}
+
+/* Exact k-nearest-neighbour graph: N(i) = the k points j != i with the
+ * smallest (||x_i - x_j||^2, j) (squared distance summed over coordinates
+ * in order; ties to the smaller index); edge {i, j} if j in N(i) or i in
+ * N(j); weight exp(-||x_i - x_j||^2 / (2 sigma^2)) in float64, rounded once
+ * to float32; rows sorted by column.  row_ptr [n+1]; col and val hold up to
+ * 2 n k entries.  Returns nnz, or -1 if k is not in [1, n-1]. */
+int64_t orc_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, double sigma,
+                      int64_t *row_ptr, int32_t *col, float *val)
+{
+    if (k < 1 || (int64_t)k > n - 1)
+        return -1;
+    edge_t *e = (edge_t *)malloc(sizeof(edge_t) * 2 * (size_t)n * (size_t)k);
+#pragma omp parallel
+    {
+        double *bd = (double *)malloc(sizeof(double) * (size_t)k);
+        int64_t *bj = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < n; ++i) {
+            int32_t m = 0;                       /* kept so far, sorted by (dist, j) */
+            for (int64_t j = 0; j < n; ++j) {
+                if (j == i)
+                    continue;
+                double dj = sq_dist(X, d, i, j);
+                if (m == k && !(dj < bd[k - 1]))
+                    continue;                    /* j > kept indices: ties lose */
+                int32_t p = (m < k) ? m++ : k - 1;
+                while (p > 0 && dj < bd[p - 1]) {
+                    bd[p] = bd[p - 1];
+                    bj[p] = bj[p - 1];
+                    --p;
+                }
+                bd[p] = dj;
+                bj[p] = j;
+            }
+            for (int32_t t = 0; t < k; ++t) {
+                e[(2 * i) * (int64_t)k + 2 * t].row = i;
+                e[(2 * i) * (int64_t)k + 2 * t].col = bj[t];
+                e[(2 * i) * (int64_t)k + 2 * t + 1].row = bj[t];
+                e[(2 * i) * (int64_t)k + 2 * t + 1].col = i;
+            }
+        }
+        free(bj);
+        free(bd);
+    }
+    const int64_t m2 = 2 * n * (int64_t)k;
+    qsort(e, (size_t)m2, sizeof(edge_t), cmp_edge);
+    const double two_sigma2 = 2.0 * sigma * sigma;
+    int64_t nnz = 0;
+    for (int64_t i = 0; i <= n; ++i)
+        row_ptr[i] = 0;
+    for (int64_t t = 0; t < m2; ++t) {
+        if (t > 0 && e[t].row == e[t - 1].row && e[t].col == e[t - 1].col)
+            continue;
+        col[nnz] = (int32_t)e[t].col;
+        val[nnz] = (float)exp(-sq_dist(X, d, e[t].row, e[t].col) / two_sigma2);
+        row_ptr[e[t].row + 1]++;
+        ++nnz;
+    }
+    for (int64_t i = 0; i < n; ++i)
+        row_ptr[i + 1] += row_ptr[i];
+    free(e);
+    return nnz;
 }

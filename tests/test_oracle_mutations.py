@@ -37,6 +37,9 @@ MUTATIONS = {
                              "return dot / (sqrt(ni) * sqrt(nj));"),
     "cosine_norm_not_square_rooted": ("return 0.5 * (1.0 + dot / (sqrt(ni) * sqrt(nj)));",
                                       "return 0.5 * (1.0 + dot / (ni * nj));"),
+    "knn_ties_to_larger_index": ("if (m == k && !(dj < bd[k - 1]))", "if (m == k && dj > bd[k - 1])"),
+    "knn_directed_only": ("                e[(2 * i) * (int64_t)k + 2 * t + 1].row = bj[t];\n                e[(2 * i) * (int64_t)k + 2 * t + 1].col = i;\n",
+                          "                e[(2 * i) * (int64_t)k + 2 * t + 1].row = i;\n                e[(2 * i) * (int64_t)k + 2 * t + 1].col = bj[t];\n"),
     "dc_left_bound_too_tight": ("dc_layer(P, run_start, prev, cur, opt, lo, mid - 1, olo, opt[mid]);",
                                 "dc_layer(P, run_start, prev, cur, opt, lo, mid - 1, olo, opt[mid] - 1);"),
 }
@@ -52,6 +55,8 @@ def _pin_suite(orc):
         ("cosine_scipy", lambda: pins.test_cosine_affinity_matches_scipy_distance(orc)),
         ("cosine_closed", lambda: pins.test_cosine_affinity_closed_form_and_invariance(orc)),
         ("brute_gauss", lambda: pins.test_brute_force_fifty_digits(orc, 8, 2, "gauss")),
+        ("knn_ckdtree", lambda: pins.test_knn_graph_matches_ckdtree(orc)),
+        ("knn_ties", lambda: pins.test_knn_graph_ties_and_structure(orc)),
         ("brute_cosine", lambda: pins.test_brute_force_fifty_digits(orc, 7, 3, "cosine")),
         ("row_sums_v0", lambda: pins.test_rows_of_W_sum_to_one_and_v0(orc)),
         ("zero_degree", lambda: pins.test_zero_degree_row_is_counted(orc)),

@@ -483,3 +483,47 @@ def test_brute_force_fifty_digits(orc, n, seed, kind):
                    for cuts in itertools.combinations(range(1, n), k - 1))
         km = orc.kmeans1d(r.v, k)
         assert km.cost == pytest.approx(best, rel=1e-9, abs=1e-20)
+
+
+# ------------------------------------------------------- kNN input graph
+def test_knn_graph_matches_ckdtree(orc):
+    """The exact kNN graph equals one built from scipy's k-d tree (a library
+    kNN routine) with union symmetrisation and the Gaussian weights."""
+    import scipy.sparse as sp
+    from scipy.spatial import cKDTree
+    n, d, k, sigma = 1500, 8, 10, np.float32(1.3)
+    X = _pts(n, d, 71)
+    rp, col, val = orc.knn_graph(X, k, sigma)
+    P = X.astype(np.float64)
+    dist, nb = cKDTree(P).query(P, k=k + 1)
+    assert np.all(nb[:, 0] == np.arange(n))            # no duplicate points here
+    rows = np.repeat(np.arange(n), k)
+    cols = nb[:, 1:].reshape(-1)
+    w = np.exp(-(dist[:, 1:].reshape(-1) ** 2) / (2.0 * float(sigma) ** 2))
+    K = sp.coo_matrix((w, (rows, cols)), shape=(n, n)).tocsr()
+    S = K.maximum(K.T).tocsr()
+    S.sort_indices()
+    assert np.array_equal(rp, S.indptr) and np.array_equal(col, S.indices)
+    np.testing.assert_allclose(val, S.data.astype(np.float32), rtol=2e-7)
+
+
+def test_knn_graph_ties_and_structure(orc):
+    """Integer lattice points (many exact distance ties): ties go to the
+    smaller index; the graph is symmetric with equal weights both ways, has
+    no self loops, sorted columns and at least k entries per row."""
+    g = np.arange(12, dtype=np.float32)
+    X = np.stack(np.meshgrid(g, g), axis=-1).reshape(-1, 2)      # 144 points
+    n, k = X.shape[0], 4
+    rp, col, val = orc.knn_graph(X, k, 1.0)
+    A = np.zeros((n, n), dtype=np.float32)
+    for i in range(n):
+        c = col[rp[i]:rp[i + 1]]
+        assert np.all(np.diff(c) > 0) and i not in c and c.size >= k
+        A[i, c] = val[rp[i]:rp[i + 1]]
+    assert np.array_equal(A, A.T)
+    # corner point 0 = (0, 0): nearest are (1, 0) idx 1 and (0, 1) idx 12 at
+    # distance 1, (1, 1) idx 13 at sqrt 2, then (2, 0) idx 2 and (0, 2) idx
+    # 24 tie at 2 and the smaller index wins; no other point has 0 among
+    # its own 4 nearest, so row 0 is exactly {1, 2, 12, 13}
+    assert list(col[rp[0]:rp[1]]) == [1, 2, 12, 13]
+    assert A[0, 1] == np.float32(np.exp(-0.5)) and A[0, 2] == np.float32(np.exp(-2.0))
