@@ -281,6 +281,17 @@ def other_workload(args):
         val0 = torch.from_numpy(w.val).to(dev)
         nnz = int(val0.numel())
         extra["nnz"] = nnz
+        if w.name.startswith("knn8d") and w.name == "knn8d":
+            # the same input graph built on the GPU (exact kNN, k = 32)
+            g.gpic_knn_graph(X, 32, 1.0)
+            torch.cuda.synchronize()
+            tg = time.perf_counter()
+            grp, gcol, gval = g.gpic_knn_graph(X, 32, 1.0)
+            torch.cuda.synchronize()
+            extra["graph_build_gpu_s"] = round(time.perf_counter() - tg, 4)
+            extra["graph_equal_to_input"] = bool(torch.equal(grp, rp) and torch.equal(gcol, col))
+            del grp, gcol, gval
+            log(f"bench: kNN graph on the GPU in {extra['graph_build_gpu_s']} s")
 
         def step():
             val = val0.clone()

@@ -72,7 +72,8 @@ enum {
     GPIC_OP_AFFINITY_NORMALIZED = 8,
     GPIC_OP_MATVEC_FUSED = 9,
     GPIC_OP_AFFINITY_COSINE = 10,
-    GPIC_OP_AFFINITY_COSINE_NORMALIZED = 11
+    GPIC_OP_AFFINITY_COSINE_NORMALIZED = 11,
+    GPIC_OP_KNN_GRAPH = 12
 };
 
 /* Power-iteration modes. */
@@ -168,6 +169,25 @@ gpic_status gpic_affinity_cosine_normalized(const float *X, int64_t n, int32_t d
                                             float *W, int64_t ldw, double *degree,
                                             double *v0, int64_t *n_zero_rows,
                                             void *ws, size_t ws_bytes, void *stream);
+
+/* The sparse affinity graph the CSR path takes as input (the paper's
+ * affinity of section "Spectral Cluster" restricted to nearest
+ * neighbours): N(i) = the k points j != i with the smallest
+ * (||x_i - x_j||^2, j), ties to the smaller index; edge {i, j} when j is in
+ * N(i) or i in N(j); weight exp(-||x_i - x_j||^2 / (2 sigma^2)) in float64
+ * (squared distance summed over coordinates in order), rounded once to
+ * float32; rows sorted by column.  Exact (float32 distances only narrow
+ * the candidates; the selection uses float64 distances).
+ * X: float32 [n x d], d <= 16; 1 <= k <= min(64, n - 1); 2 n k < 2^32.
+ * Outputs (device, caller-allocated): row_ptr int64 [n+1]; col int32 and
+ * val float32 with room for 2 n k entries; *nnz (host) = row_ptr[n].
+ * Synchronises the stream.  ws: gpic_workspace_bytes(GPIC_OP_KNN_GRAPH, n,
+ * 0, k) bytes (about 8 KiB per point: a 2,048-slot candidate list per row).
+ * Errors: INVALID_ARG for null or misaligned pointers, n < 2, d < 1, k out
+ * of range, sigma <= 0; UNSUPPORTED for d > 16. */
+gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k,
+                           float sigma, int64_t *row_ptr, int32_t *col, float *val,
+                           int64_t *nnz, void *ws, size_t ws_bytes, void *stream);
 
 /* --------------------------------- 2. degrees, W = D^-1 A, v0 = D / sum D */
 

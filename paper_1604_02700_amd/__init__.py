@@ -29,7 +29,7 @@ STATUS = {0: "GPIC_OK", 1: "GPIC_ERR_INVALID_ARG", 2: "GPIC_ERR_WORKSPACE",
 OP = {"affinity": 0, "degree_normalize": 1, "degree_normalize_csr": 2,
       "degree_fused": 3, "pi_dense": 4, "pi_fused": 5, "pi_csr": 6,
       "kmeans1d": 7, "affinity_normalized": 8, "matvec_fused": 9,
-      "affinity_cosine": 10, "affinity_cosine_normalized": 11}
+      "affinity_cosine": 10, "affinity_cosine_normalized": 11, "knn_graph": 12}
 MODES = {"fixed": 0, "converge": 1}
 
 # C entry points declared in include/gpic.h (checked by the tests)
@@ -40,7 +40,7 @@ EXPORTS = (
     "gpic_degree_normalize_csr", "gpic_degree_fused", "gpic_matvec_dense",
     "gpic_matvec_csr", "gpic_matvec_fused", "gpic_power_iterate_dense",
     "gpic_power_iterate_fused", "gpic_power_iterate_csr", "gpic_kmeans1d",
-    "gpic_affinity_cosine", "gpic_affinity_cosine_normalized",
+    "gpic_affinity_cosine", "gpic_affinity_cosine_normalized", "gpic_knn_graph",
 )
 
 
@@ -85,6 +85,7 @@ def lib() -> C.CDLL:
             "gpic_affinity_normalized": [p, i64, i32, f32, p, i64, p, p, p, p, sz, p],
             "gpic_affinity_cosine": [p, i64, i32, p, i64, p, p, sz, p],
             "gpic_affinity_cosine_normalized": [p, i64, i32, p, i64, p, p, p, p, sz, p],
+            "gpic_knn_graph": [p, i64, i32, i32, f32, p, p, p, C.POINTER(i64), p, sz, p],
             "gpic_degree_normalize": [p, i64, i64, p, i32, p, p, p, sz, p],
             "gpic_degree_normalize_csr": [p, p, p, i64, i64, p, p, p, p, sz, p],
             "gpic_degree_fused": [p, i64, i32, f32, p, p, p, p, sz, p],
@@ -237,6 +238,24 @@ def gpic_affinity_cosine_normalized(X: torch.Tensor, W: Optional[torch.Tensor] =
                                                  _ptr(degree), _ptr(v0), _ptr(nz),
                                                  _ptr(ws), nb, _stream(dev)))
     return W, degree, v0, nz
+
+
+def gpic_knn_graph(X: torch.Tensor, k: int, sigma: float):
+    """Exact kNN graph (union symmetrised, Gaussian weights) as device CSR:
+    (row_ptr int64 [n+1], col int32 [nnz], val float32 [nnz])."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    dev = X.device
+    rp = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    col = torch.empty(2 * n * k, dtype=torch.int32, device=dev)
+    val = torch.empty(2 * n * k, dtype=torch.float32, device=dev)
+    nnz = C.c_int64(0)
+    ws, nb = workspace("knn_graph", n, 0, k, device=dev)
+    _check(lib().gpic_knn_graph(_ptr(X), n, d, int(k), float(sigma), _ptr(rp), _ptr(col),
+                                _ptr(val), C.byref(nnz), _ptr(ws), nb, _stream(dev)))
+    m = int(nnz.value)
+    return rp, col[:m], val[:m]
 
 
 # ----------------------------------------------- 2. degrees, W and v0

@@ -370,6 +370,8 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     case GPIC_OP_MATVEC_FUSED: return aff_ws(n);
     case GPIC_OP_AFFINITY_COSINE: return al(cosine_ws(n));
     case GPIC_OP_AFFINITY_COSINE_NORMALIZED: return start_ws(n) + al(cosine_ws(n));
+    case GPIC_OP_KNN_GRAPH:
+        return (k >= 1 && k <= 64 && n >= 2) ? al(knn_graph_ws(n, k)) : 0;
     default: return 0;
     }
 }
@@ -476,6 +478,33 @@ gpic_status gpic_affinity_cosine_normalized(const float *X, int64_t n, int32_t d
     if (bad)
         return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
     CHECK_HIP(launch_cosine_w(X, n, d, W, ldw, degree, cws, s), "W sweep");
+    return GPIC_OK;
+}
+
+gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, float sigma,
+                           int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz,
+                           void *ws, size_t ws_bytes, void *stream)
+{
+    gpic_status st = check_points(X, n, d, sigma);
+    if (st != GPIC_OK)
+        return st;
+    if (d > 16)
+        return fail(GPIC_ERR_UNSUPPORTED, "the kNN graph builder supports d <= 16 (d = %d)", d);
+    CHECK_ARG(k >= 1 && k <= 64 && (int64_t)k <= n - 1, "k = %d must be in [1, min(64, n-1)]",
+              k);
+    CHECK_ARG(2 * n * (int64_t)k < ((int64_t)1 << 32), "2 n k must be below 2^32");
+    CHECK_ARG(row_ptr != nullptr && aligned(row_ptr, 8), "row_ptr null or misaligned");
+    CHECK_ARG(col != nullptr && aligned(col, 4) && val != nullptr && aligned(val, 4),
+              "col / val null or misaligned");
+    CHECK_ARG(nnz != nullptr, "nnz is null");
+    if ((st = check_ws(ws, ws_bytes, al(knn_graph_ws(n, k)))) != GPIC_OK)
+        return st;
+    int status = 0;
+    CHECK_HIP(run_knn_graph(X, n, d, k, sigma, row_ptr, col, val, nnz, &status, ws,
+                            (hipStream_t)stream),
+              "kNN graph");
+    if (status != 0)
+        return fail(GPIC_ERR_NUMERIC, "kNN candidate bounds did not converge");
     return GPIC_OK;
 }
 

@@ -209,6 +209,29 @@ hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
 hipError_t launch_spmv_blocked(const CsrBlocked &B, const double *v, double *y,
                                double *partial, StopCtl ctl, hipStream_t s);
 
+// sort.hip -- stable LSD radix sort of n < 2^32 uint64 keys on their low
+// `bits` bits (a multiple of 8), with an optional int32 payload (idxA and
+// idxB null for keys alone).  The sorted arrays end in keyA / idxA (the
+// pointers are swapped per pass).  hist: radix_hist_bytes(n) bytes, hsum:
+// radix_hsum_bytes(n) bytes.
+size_t radix_hist_bytes(int64_t n);
+size_t radix_hsum_bytes(int64_t n);
+// in-place exclusive scan of m uint32 values (total < 2^32); sums:
+// scan_sums_bytes(m) bytes
+size_t scan_sums_bytes(int64_t m);
+hipError_t exclusive_scan_u32(uint32_t *a, int64_t m, uint32_t *sums, hipStream_t s);
+hipError_t radix_sort_u64(uint64_t *&keyA, int32_t *&idxA, uint64_t *&keyB, int32_t *&idxB,
+                          int64_t n, int bits, uint32_t *hist, uint32_t *hsum,
+                          hipStream_t s);
+
+// knn.hip -- exact kNN graph (d <= 16, k <= 64, 2 n k < 2^32); synchronises.
+// *status_host = 1 when the candidate bounds failed to converge (nothing
+// written).  row_ptr [n+1]; col and val hold up to 2 n k entries.
+size_t knn_graph_ws(int64_t n, int32_t k);
+hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
+                         int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz_host,
+                         int *status_host, void *ws, hipStream_t s);
+
 // kmeans.hip
 size_t kmeans_ws(int64_t n, int32_t k);
 // Runs the whole exact 1-D k-means; synchronises the stream.

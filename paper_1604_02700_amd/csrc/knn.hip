@@ -1,0 +1,664 @@
+// Exact k-nearest-neighbour input graph for the sparse path, on gfx950.
+//
+// N(i) = the k points j != i with the smallest (||x_i - x_j||^2, j); edge
+// {i, j} when j is in N(i) or i in N(j); weight exp(-||x_i - x_j||^2 /
+// (2 sigma^2)) in float64, rounded once to float32; rows sorted by column.
+// This is the graph the CSR power iteration takes as its affinity (the
+// paper's method needs an affinity matrix; a kNN graph is its sparse form).
+//
+// Brute force in four steps, exact in the end:
+//   1. bound: for every row, the k-th smallest float32 squared distance to
+//      a fixed sample of 2^17 points (all points when n is smaller), which
+//      bounds the true k-th neighbour distance from above;
+//   2. collect: all n^2 squared distances on the fp32 matrix cores (Gram
+//      form over the centred points augmented as [x_j, |x_j|^2, 1] .
+//      [-2 x_i, 1, |x_i|^2]),
+//      appending every j that passes the row's bound widened by the float32
+//      error bounds of both forms to a per-row candidate list;
+//   3. select: a wave per row recomputes the candidates' squared distances
+//      in float64 and keeps the k smallest (ties to the smaller index); a
+//      row whose list overflowed gets the k-th distance among the kept
+//      candidates as its new bound and is collected again;
+//   4. symmetrise: both directions of every kept pair as 64-bit keys
+//      (row, column), radix sorted, duplicates dropped, CSR built, weights
+//      from float64 distances.
+// Supports d <= 16 and k <= 64.
+#include "common.h"
+
+namespace gpic {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int64_t kSample = 131072;       // points in the bound's sample
+constexpr int kCap = 2048;                // candidate slots per row
+constexpr int kPerLane = kCap / kWave;    // candidates per lane in the selection
+constexpr int kRowsPerGroup = 64;         // collect: 4 waves x 16 rows
+constexpr int kTileCols = 64;
+constexpr float kEps32 = 5.9604645e-08f;  // 2^-24
+constexpr int kMeanBlocks = 256;
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+int64_t al(int64_t x) { return (x + 255) & ~(int64_t)255; }
+int64_t padded_points(int64_t n) { return (n + kTileCols - 1) / kTileCols * kTileCols; }
+// augmented dimension / 4, rounded up to an instantiated engine (3 or 5)
+int ks_for(int d) { return (d + 2 + 3) / 4 <= 3 ? 3 : 5; }
+
+// float64 squared distance summed over coordinates in order, without
+// fused multiply-adds (the same value a plain C loop gives)
+__device__ __forceinline__ double sq_dist64(const float *__restrict__ X, int d, int64_t i,
+                                            int64_t j)
+{
+    double s = 0.0;
+    for (int c = 0; c < d; ++c) {
+        const double df = __dsub_rn((double)X[i * d + c], (double)X[j * d + c]);
+        s = __dadd_rn(s, __dmul_rn(df, df));
+    }
+    return s;
+}
+
+// ------------------------------------------------------------ 1. bound
+
+__device__ __forceinline__ int64_t sample_point(int64_t t, int64_t n, int64_t m)
+{
+    return (m == n) ? t : (t * n) / m;
+}
+
+// Thread per row: the KT smallest float32 squared distances to the sample
+// (sorted, in registers), then tau_i = the k-th of them.
+template <int D, int KT>
+__global__ __launch_bounds__(kThreads) void knn_bound_kernel(
+    const float *__restrict__ X, int64_t n, int64_t m, int k, float *__restrict__ tau)
+{
+    __shared__ float tile[kThreads * D];
+    __shared__ int64_t tidx[kThreads];
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ic = i < n ? i : n - 1;
+    float xi[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c)
+        xi[c] = X[ic * D + c];
+    float best[KT];
+#pragma unroll
+    for (int p = 0; p < KT; ++p)
+        best[p] = INFINITY;
+    for (int64_t t0 = 0; t0 < m; t0 += kThreads) {
+        __syncthreads();
+        const int64_t t = t0 + threadIdx.x;
+        const int64_t j = (t < m) ? sample_point(t, n, m) : -1;
+        tidx[threadIdx.x] = j;
+#pragma unroll
+        for (int c = 0; c < D; ++c)
+            tile[threadIdx.x * D + c] = (j >= 0) ? X[j * D + c] : 0.0f;
+        __syncthreads();
+        const int cnt = (m - t0 < kThreads) ? (int)(m - t0) : kThreads;
+        for (int u = 0; u < cnt; ++u) {
+            if (tidx[u] == ic)
+                continue;
+            float s = 0.0f;
+#pragma unroll
+            for (int c = 0; c < D; ++c) {
+                const float df = xi[c] - tile[u * D + c];
+                s = fmaf(df, df, s);
+            }
+            if (s < best[KT - 1]) {
+#pragma unroll
+                for (int p = KT - 1; p > 0; --p) {
+                    const float lo = best[p - 1];
+                    best[p] = (s < lo) ? lo : fminf(s, best[p]);
+                }
+                best[0] = fminf(s, best[0]);
+            }
+        }
+    }
+    if (i < n) {
+        float t = best[0];
+#pragma unroll
+        for (int p = 1; p < KT; ++p)
+            if (p == k - 1)
+                t = best[p];
+        tau[i] = t;
+    }
+}
+
+// max_j |x_j|^2 (non-negative floats compare as their bit patterns)
+__global__ __launch_bounds__(kThreads) void max_norm_kernel(const float *__restrict__ norm2,
+                                                            int64_t n,
+                                                            unsigned int *__restrict__ out)
+{
+    unsigned int m = 0;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kThreads)
+        m = max(m, __float_as_uint(norm2[i]));
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1)
+        m = max(m, (unsigned int)__shfl_xor((int)m, o, kWave));
+    if ((threadIdx.x % kWave) == 0)
+        atomicMax(out, m);
+}
+
+// Collection threshold: the exact k-th neighbour distance is at most
+// tau (1 + 4 (d + 2) eps32) (tau is a float32 difference-form value); a
+// Gram-form value over the centred points x' = x - mean (rounded once), a
+// float32 sum of KP terms whose magnitudes add up to at most
+// 2 (|x'_i|^2 + |x'_j|^2), is below the exact squared distance by at most
+// (2 KP + 20) eps32 (|x'_i|^2 + max |x'|^2) with margin (4 of it for the
+// rounding of the centred coordinates).  Formed in float64 and rounded up.
+// Rows not active get -1 (nothing passes).
+__global__ __launch_bounds__(kThreads) void threshold_kernel(
+    const float *__restrict__ tau, const double *__restrict__ kth,
+    const float *__restrict__ norm2, const unsigned int *__restrict__ maxn, int64_t n,
+    int d, int kp, const int *__restrict__ active, float *__restrict__ thr)
+{
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= n)
+        return;
+    if (active != nullptr && !active[i]) {
+        thr[i] = -1.0f;
+        return;
+    }
+    const double eps = (double)kEps32;
+    const double base = (kth != nullptr) ? kth[i] : (double)tau[i];
+    const double t = base * (1.0 + 4.0 * (d + 2) * eps) +
+                     (2 * kp + 20) * eps * ((double)norm2[i] + (double)__uint_as_float(*maxn));
+    float f = (float)t;
+    if ((double)f < t)
+        f = nextafterf(f, INFINITY);
+    thr[i] = f;
+}
+
+// ------------------------------------------------------------ 2. collect
+
+// Mean of the points per coordinate (float64): per-workgroup partial sums,
+// then one workgroup adds them in order.
+__global__ __launch_bounds__(kThreads) void mean_partials_kernel(const float *__restrict__ X,
+                                                                 int64_t n, int d,
+                                                                 double *__restrict__ part)
+{
+    __shared__ double red[kThreads / kWave];
+    for (int c = 0; c < d; ++c) {
+        double s = 0.0;
+        for (int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x; p < n;
+             p += (int64_t)gridDim.x * kThreads)
+            s += (double)X[p * d + c];
+        const double t = block_sum<kThreads>(s, red);
+        if (threadIdx.x == 0)
+            part[(int64_t)blockIdx.x * d + c] = t;
+    }
+}
+
+__global__ void mean_finish_kernel(const double *__restrict__ part, int nb, int d, int64_t n,
+                                   double *__restrict__ mu)
+{
+    const int c = threadIdx.x;
+    if (c >= d)
+        return;
+    double s = 0.0;
+    for (int b = 0; b < nb; ++b)
+        s += part[(int64_t)b * d + c];
+    mu[c] = s / (double)n;
+}
+
+// Augmented operands of the centred points x' = float32(x - mean):
+// column xa[k * np + p] = [x'_p, |x'_p|^2, 1, 0...], row
+// xb[p * KP + k] = [-2 x'_p, 1, |x'_p|^2, 0...]; |x'_p|^2 a float64 sum
+// rounded once (also written to norm2).  Padding points are zeros.
+__global__ __launch_bounds__(kThreads) void knn_augment_kernel(
+    const float *__restrict__ X, const double *__restrict__ mu, int64_t n, int64_t np, int d,
+    int KP, float *__restrict__ xa, float *__restrict__ xb, float *__restrict__ norm2)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= np)
+        return;
+    float xc[16];
+    double s = 0.0;
+    for (int c = 0; c < 16; ++c) {
+        xc[c] = 0.0f;
+        if (c < d && p < n) {
+            xc[c] = (float)((double)X[p * d + c] - mu[c]);
+            s = fma((double)xc[c], (double)xc[c], s);
+        }
+    }
+    const float nrm = (float)s;
+    if (p < n)
+        norm2[p] = nrm;
+    for (int k = 0; k < KP; ++k) {
+        float a = 0.0f, b = 0.0f;
+        if (p < n) {
+            if (k < d) {
+                a = xc[k];
+                b = -2.0f * a;
+            } else if (k == d) {
+                a = nrm;
+                b = 1.0f;
+            } else if (k == d + 1) {
+                a = 1.0f;
+                b = nrm;
+            }
+        }
+        xa[k * np + p] = a;
+        xb[p * KP + k] = b;
+    }
+}
+
+// 4 waves x 16 rows; all columns in tiles of 64 through double-buffered
+// LDS (coordinate-major, XOR-swizzled as in the affinity engine);
+// v_mfma_f32_16x16x4f32 with the A operand on the columns and the B operand
+// on the wave's rows, so lane (m, g) holds row wrow0 + m and columns
+// 16 q + 4 g + r of block q.  Every (i, j != i) whose squared distance
+// passes thr_i is appended to row i's list (an integer atomic counter;
+// slots beyond kCap are counted, not written).
+template <int KS>
+__global__ __launch_bounds__(kThreads) void knn_collect_kernel(
+    const float *__restrict__ xa, int64_t np, const float *__restrict__ xb, int64_t n,
+    const float *__restrict__ thr, int *__restrict__ count, int32_t *__restrict__ cand)
+{
+    constexpr int KP = 4 * KS;
+    constexpr int kRow4 = kTileCols / 4;
+    __shared__ floatx4 xs[2][KP * kRow4];
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    const int g = lane >> 4;
+    const int m = lane & 15;
+    const int64_t wrow0 = (int64_t)blockIdx.x * kRowsPerGroup + wave * 16;
+    const int64_t i = wrow0 + m;
+    const int64_t ic = i < n ? i : n - 1;
+    const float t_i = (i < n) ? thr[i] : -1.0f;
+
+    // a workgroup with no active row has nothing to collect
+    if (__syncthreads_or(t_i >= 0.0f) == 0)
+        return;
+
+    float bop[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+        bop[s] = xb[ic * KP + 4 * s + g];
+
+    constexpr int kPieces = KP * kRow4;
+    constexpr int kPer = (kPieces + kThreads - 1) / kThreads;
+    floatx4 stage[kPer];
+    auto fetch = [&](int64_t jt) {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int f = threadIdx.x + u * kThreads;
+            if (kPieces % kThreads == 0 || f < kPieces)
+                stage[u] = *reinterpret_cast<const floatx4 *>(
+                    xa + (int64_t)(f / kRow4) * np + jt + 4 * (f % kRow4));
+        }
+    };
+    auto commit = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int f = threadIdx.x + u * kThreads;
+            if (kPieces % kThreads == 0 || f < kPieces) {
+                const int k = f / kRow4;
+                xs[buf][k * kRow4 + ((f % kRow4) ^ (4 * (k & 3)))] = stage[u];
+            }
+        }
+    };
+
+    const int64_t ntiles = (n + kTileCols - 1) / kTileCols;
+    fetch(0);
+    commit(0);
+    __syncthreads();
+    for (int64_t t = 0; t < ntiles; ++t) {
+        const int buf = (int)(t & 1);
+        const int64_t jt = t * kTileCols;
+        if (t + 1 < ntiles)
+            fetch(jt + kTileCols);
+        const float *tile = reinterpret_cast<const float *>(xs[buf]) + g * kTileCols;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            floatx4 cacc = {0.0f, 0.0f, 0.0f, 0.0f};
+            const float *ap = tile + ((16 * q + m) ^ (16 * g));
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                cacc = __builtin_amdgcn_mfma_f32_16x16x4f32(ap[4 * s * kTileCols], bop[s],
+                                                            cacc, 0, 0, 0);
+            const int64_t j0 = jt + 16 * q + 4 * g;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t j = j0 + r;
+                if (t_i >= 0.0f && cacc[r] <= t_i && j < n && j != i) {
+                    const int c = atomicAdd(&count[i], 1);
+                    if (c < kCap)
+                        cand[i * kCap + c] = (int32_t)j;
+                }
+            }
+        }
+        if (t + 1 < ntiles) {
+            commit(buf ^ 1);
+            __syncthreads();
+        }
+    }
+}
+
+// ------------------------------------------------------------- 3. select
+
+// A wave per active row: float64 squared distances of the kept candidates
+// (at most kCap, 32 per lane, in registers), then k rounds of a wave
+// argmin over (distance, index).  nbr[i k + t] are the k nearest in order;
+// kth[i] is the k-th distance; a row whose list overflowed is flagged.
+__global__ __launch_bounds__(kThreads) void knn_select_kernel(
+    const float *__restrict__ X, int64_t n, int d, int k, const int *__restrict__ active,
+    int *__restrict__ count, const int32_t *__restrict__ cand, int32_t *__restrict__ nbr,
+    double *__restrict__ kth, int *__restrict__ flags)
+{
+    const int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / kWave;
+    const int lane = threadIdx.x % kWave;
+    if (i >= n || (active != nullptr && !active[i]))
+        return;                                             // uniform per wave
+    const int cnt = count[i];
+    const int kept = cnt < kCap ? cnt : kCap;
+    double dv[kPerLane];
+    int32_t jv[kPerLane];
+#pragma unroll
+    for (int u = 0; u < kPerLane; ++u) {
+        const int e = u * kWave + lane;
+        if (e < kept) {
+            jv[u] = cand[i * kCap + e];
+            dv[u] = sq_dist64(X, d, i, jv[u]);
+        } else {
+            jv[u] = INT32_MAX;
+            dv[u] = INFINITY;
+        }
+    }
+    double last = 0.0;
+    for (int t = 0; t < k; ++t) {
+        double bd = INFINITY;
+        int32_t bj = INT32_MAX;
+#pragma unroll
+        for (int u = 0; u < kPerLane; ++u)
+            if (dv[u] < bd || (dv[u] == bd && jv[u] < bj)) {
+                bd = dv[u];
+                bj = jv[u];
+            }
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) {
+            const double od = __shfl_xor(bd, o, kWave);
+            const int32_t oj = __shfl_xor(bj, o, kWave);
+            if (od < bd || (od == bd && oj < bj)) {
+                bd = od;
+                bj = oj;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kPerLane; ++u)
+            if (jv[u] == bj)
+                dv[u] = INFINITY, jv[u] = INT32_MAX;
+        if (lane == 0)
+            nbr[i * k + t] = bj;
+        last = bd;
+    }
+    if (lane == 0) {
+        kth[i] = last;
+        if (cnt > kCap || last == INFINITY)
+            atomicAdd(&flags[0], 1);
+    }
+}
+
+// rows to collect again (count reset): the overflowed ones, and any with
+// fewer than k candidates (an infinite k-th distance widens its bound to
+// everything, so it overflows next and then shrinks)
+__global__ __launch_bounds__(kThreads) void knn_rearm_kernel(int64_t n, int *__restrict__ count,
+                                                             const double *__restrict__ kth,
+                                                             int *__restrict__ active)
+{
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= n)
+        return;
+    const int again = count[i] > kCap || kth[i] == INFINITY;
+    active[i] = again;
+    if (again)
+        count[i] = 0;
+}
+
+__global__ __launch_bounds__(kThreads) void fill_i32_kernel(int *__restrict__ a, int64_t n,
+                                                            int v)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kThreads)
+        a[i] = v;
+}
+
+// --------------------------------------------------------- 4. symmetrise
+
+__global__ __launch_bounds__(kThreads) void edge_keys_kernel(const int32_t *__restrict__ nbr,
+                                                             int64_t n, int k, int bits,
+                                                             uint64_t *__restrict__ key)
+{
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= n * k)
+        return;
+    const uint64_t a = (uint64_t)(e / k), b = (uint64_t)nbr[e];
+    key[2 * e] = (a << bits) | b;
+    key[2 * e + 1] = (b << bits) | a;
+}
+
+// first[p] = 1 where sorted key p differs from key p - 1
+__global__ __launch_bounds__(kThreads) void first_flags_kernel(const uint64_t *__restrict__ key,
+                                                               int64_t m,
+                                                               uint32_t *__restrict__ first)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p < m)
+        first[p] = (p == 0 || key[p] != key[p - 1]) ? 1u : 0u;
+}
+
+// After an exclusive scan of the flags: column, row start and weight of
+// every distinct key; row_ptr[n] = nnz.
+__global__ __launch_bounds__(kThreads) void build_csr_kernel(
+    const uint64_t *__restrict__ key, const uint32_t *__restrict__ pos, int64_t m, int bits,
+    const float *__restrict__ X, int64_t n, int d, double two_sigma2,
+    int64_t *__restrict__ row_ptr, int32_t *__restrict__ col, float *__restrict__ val)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= m)
+        return;
+    const uint64_t kp = key[p];
+    const bool first = (p == 0 || kp != key[p - 1]);
+    const uint64_t mask = (1ull << bits) - 1;
+    const int64_t r = (int64_t)(kp >> bits), c = (int64_t)(kp & mask);
+    if (p == m - 1)
+        row_ptr[n] = (int64_t)pos[p] + (first ? 1 : 0);
+    if (!first)
+        return;
+    const int64_t q = pos[p];
+    col[q] = (int32_t)c;
+    val[q] = (float)exp(-sq_dist64(X, d, r, c) / two_sigma2);
+    if (p == 0 || (int64_t)(key[p - 1] >> bits) != r)
+        row_ptr[r] = q;
+}
+
+int bits_for(int64_t n)
+{
+    int b = 1;
+    while (((int64_t)1 << b) < n)
+        ++b;
+    return b;
+}
+
+struct KnnLayout {
+    size_t xa, xb, mpart, mu, tau, norm2, maxn, thr, count, active, cand, nbr, kth, flags,
+        keyA, keyB, first, hist, hsum, total;
+};
+
+KnnLayout knn_layout(int64_t n, int32_t k)
+{
+    KnnLayout L{};
+    const int64_t np = padded_points(n);
+    const int64_t m = 2 * n * (int64_t)k;
+    size_t o = 0;
+    auto take = [&](int64_t bytes) {
+        const size_t at = o;
+        o += (size_t)al(bytes);
+        return at;
+    };
+    L.xa = take(np * 20 * 4);               // KP <= 20 for d <= 16
+    L.xb = take(np * 20 * 4);
+    L.mpart = take(kMeanBlocks * 16 * 8);
+    L.mu = take(16 * 8);
+    L.tau = take(n * 4);
+    L.norm2 = take(n * 4);
+    L.maxn = take(4);
+    L.thr = take(n * 4);
+    L.count = take(n * 4);
+    L.active = take(n * 4);
+    L.cand = take(n * (int64_t)kCap * 4);
+    L.nbr = take(n * (int64_t)k * 4);
+    L.kth = take(n * 8);
+    L.flags = take(4);
+    L.keyA = take(m * 8);
+    L.keyB = take(m * 8);
+    L.first = take(m * 4);
+    L.hist = take((int64_t)radix_hist_bytes(m));
+    L.hsum = take((int64_t)(radix_hsum_bytes(m) > scan_sums_bytes(m) ? radix_hsum_bytes(m)
+                                                                      : scan_sums_bytes(m)));
+    L.total = o;
+    return L;
+}
+
+template <int D>
+void launch_bound(int KT, const float *X, int64_t n, int64_t m, int k, float *tau,
+                  hipStream_t s)
+{
+    const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
+    switch (KT) {
+    case 8:
+        hipLaunchKernelGGL((knn_bound_kernel<D, 8>), grid, dim3(kThreads), 0, s, X, n, m, k,
+                           tau);
+        break;
+    case 16:
+        hipLaunchKernelGGL((knn_bound_kernel<D, 16>), grid, dim3(kThreads), 0, s, X, n, m, k,
+                           tau);
+        break;
+    case 32:
+        hipLaunchKernelGGL((knn_bound_kernel<D, 32>), grid, dim3(kThreads), 0, s, X, n, m, k,
+                           tau);
+        break;
+    default:
+        hipLaunchKernelGGL((knn_bound_kernel<D, 64>), grid, dim3(kThreads), 0, s, X, n, m, k,
+                           tau);
+        break;
+    }
+}
+
+} // namespace
+
+size_t knn_graph_ws(int64_t n, int32_t k) { return knn_layout(n, k).total; }
+
+hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
+                         int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz_host,
+                         int *status_host, void *ws, hipStream_t s)
+{
+    const KnnLayout L = knn_layout(n, k);
+    char *w = static_cast<char *>(ws);
+    float *xa = (float *)(w + L.xa), *xb = (float *)(w + L.xb);
+    double *mpart = (double *)(w + L.mpart), *mu = (double *)(w + L.mu);
+    float *tau = (float *)(w + L.tau), *norm2 = (float *)(w + L.norm2);
+    unsigned int *maxn = (unsigned int *)(w + L.maxn);
+    float *thr = (float *)(w + L.thr);
+    int *count = (int *)(w + L.count), *active = (int *)(w + L.active);
+    int32_t *cand = (int32_t *)(w + L.cand), *nbr = (int32_t *)(w + L.nbr);
+    double *kth = (double *)(w + L.kth);
+    int *flags = (int *)(w + L.flags);
+    uint64_t *keyA = (uint64_t *)(w + L.keyA), *keyB = (uint64_t *)(w + L.keyB);
+    uint32_t *first = (uint32_t *)(w + L.first);
+    uint32_t *hist = (uint32_t *)(w + L.hist), *hsum = (uint32_t *)(w + L.hsum);
+    const unsigned rows_grid = (unsigned)((n + kThreads - 1) / kThreads);
+    *status_host = 0;
+
+    // 1. bound
+    const int64_t m = n < kSample ? n : kSample;
+    const int KT = k <= 8 ? 8 : k <= 16 ? 16 : k <= 32 ? 32 : 64;
+#define GPIC_BOUND(D)                                                          \
+    case D:                                                                    \
+        launch_bound<D>(KT, X, n, m, k, tau, s);                               \
+        break;
+    switch (d) {
+        GPIC_BOUND(1) GPIC_BOUND(2) GPIC_BOUND(3) GPIC_BOUND(4) GPIC_BOUND(5) GPIC_BOUND(6)
+        GPIC_BOUND(7) GPIC_BOUND(8) GPIC_BOUND(9) GPIC_BOUND(10) GPIC_BOUND(11)
+        GPIC_BOUND(12) GPIC_BOUND(13) GPIC_BOUND(14) GPIC_BOUND(15) GPIC_BOUND(16)
+    default:
+        return hipErrorInvalidValue;
+    }
+#undef GPIC_BOUND
+    const int KS = ks_for(d);
+    const int64_t np = padded_points(n);
+    hipLaunchKernelGGL(mean_partials_kernel, dim3(kMeanBlocks), dim3(kThreads), 0, s, X, n, d,
+                       mpart);
+    hipLaunchKernelGGL(mean_finish_kernel, dim3(1), dim3(64), 0, s, mpart, kMeanBlocks, d, n,
+                       mu);
+    hipLaunchKernelGGL(knn_augment_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, X, mu, n, np, d, 4 * KS, xa, xb, norm2);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, s, (int *)maxn,
+                       (int64_t)1, 0);
+    hipLaunchKernelGGL(max_norm_kernel, dim3(1024), dim3(kThreads), 0, s, norm2, n, maxn);
+    hipLaunchKernelGGL(threshold_kernel, dim3(rows_grid), dim3(kThreads), 0, s, tau,
+                       (const double *)nullptr, norm2, maxn, n, d, 4 * KS,
+                       (const int *)nullptr, thr);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(4096), dim3(kThreads), 0, s, count, n, 0);
+
+    // 2-3. collect and select, again for overflowed rows
+    const int *act = nullptr;
+    for (int round = 0;; ++round) {
+        const dim3 cgrid((unsigned)((n + kRowsPerGroup - 1) / kRowsPerGroup));
+        if (KS <= 3)
+            hipLaunchKernelGGL(knn_collect_kernel<3>, cgrid, dim3(kThreads), 0, s, xa, np,
+                               xb, n, thr, count, cand);
+        else
+            hipLaunchKernelGGL(knn_collect_kernel<5>, cgrid, dim3(kThreads), 0, s, xa, np,
+                               xb, n, thr, count, cand);
+        hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, s, flags, (int64_t)1,
+                           0);
+        hipLaunchKernelGGL(knn_select_kernel,
+                           dim3((unsigned)((n * kWave + kThreads - 1) / kThreads)),
+                           dim3(kThreads), 0, s, X, n, d, k, act, count, cand, nbr, kth,
+                           flags);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+        int bad = 0;
+        if ((e = hipMemcpyAsync(&bad, flags, sizeof(int), hipMemcpyDeviceToHost, s)) !=
+                hipSuccess ||
+            (e = hipStreamSynchronize(s)) != hipSuccess)
+            return e;
+        if (bad == 0)
+            break;
+        if (round == 8) {                   // bounds that do not shrink: give up
+            *status_host = 1;
+            return hipSuccess;
+        }
+        hipLaunchKernelGGL(knn_rearm_kernel, dim3(rows_grid), dim3(kThreads), 0, s, n,
+                           count, (const double *)kth, active);
+        hipLaunchKernelGGL(threshold_kernel, dim3(rows_grid), dim3(kThreads), 0, s, tau,
+                           (const double *)kth, norm2, maxn, n, d, 4 * KS,
+                           (const int *)active, thr);
+        act = active;
+    }
+
+    // 4. symmetrise
+    const int bits = bits_for(n);
+    const int64_t mm = 2 * n * (int64_t)k;
+    hipLaunchKernelGGL(edge_keys_kernel, dim3((unsigned)((n * k + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, nbr, n, k, bits, keyA);
+    int32_t *none_a = nullptr, *none_b = nullptr;
+    hipError_t e = radix_sort_u64(keyA, none_a, keyB, none_b, mm, (2 * bits + 7) / 8 * 8,
+                                  hist, hsum, s);
+    if (e != hipSuccess)
+        return e;
+    const unsigned egrid = (unsigned)((mm + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(first_flags_kernel, dim3(egrid), dim3(kThreads), 0, s, keyA, mm, first);
+    if ((e = exclusive_scan_u32(first, mm, hsum, s)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(build_csr_kernel, dim3(egrid), dim3(kThreads), 0, s, keyA, first, mm,
+                       bits, X, n, d, 2.0 * (double)sigma * (double)sigma, row_ptr, col, val);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    if ((e = hipMemcpyAsync(nnz_host, row_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost,
+                            s)) != hipSuccess)
+        return e;
+    return hipStreamSynchronize(s);
+}
+
+} // namespace gpic

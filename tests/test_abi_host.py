@@ -40,7 +40,7 @@ def test_workspace_sizes(L):
     import paper_1604_02700_amd as g
     for op in ("affinity", "affinity_normalized", "degree_normalize", "degree_fused",
                "pi_dense", "pi_fused", "pi_csr", "kmeans1d", "matvec_fused",
-               "affinity_cosine", "affinity_cosine_normalized"):
+               "affinity_cosine", "affinity_cosine_normalized", "knn_graph"):
         a = g.workspace_bytes(op, 1000, 5000, 3)
         b = g.workspace_bytes(op, 100000, 500000, 3)
         assert 0 < a < b
@@ -81,6 +81,14 @@ def test_argument_validation_before_launch(L):
     assert fc(dummy, 10, 0, dummy, 12, None, *W, None) == 1              # d < 1
     assert fc(dummy, 10, 2, dummy, 9, None, *W, None) == 1               # lda < n
     assert fc(dummy, 10, 2, dummy, 12, None, dummy, 8, None) == 2        # workspace
+    kg = L.gpic_knn_graph
+    nz = C.c_int64()
+    assert kg(dummy, 100, 17, 8, 1.0, dummy, dummy, dummy, C.byref(nz), *W, None) == 5  # d > 16
+    assert kg(dummy, 100, 8, 0, 1.0, dummy, dummy, dummy, C.byref(nz), *W, None) == 1   # k < 1
+    assert kg(dummy, 100, 8, 65, 1.0, dummy, dummy, dummy, C.byref(nz), *W, None) == 1  # k > 64
+    assert kg(dummy, 10, 8, 10, 1.0, dummy, dummy, dummy, C.byref(nz), *W, None) == 1   # k > n-1
+    assert kg(dummy, 100, 8, 8, 1.0, dummy, dummy, dummy, None, *W, None) == 1          # nnz null
+    assert kg(dummy, 100, 8, 8, 1.0, dummy, dummy, dummy, C.byref(nz), dummy, 8, None) == 2
     fcn = L.gpic_affinity_cosine_normalized
     assert fcn(dummy, 10, 2, dummy, 12, None, dummy, None, *W, None) == 1   # degree null
     assert fcn(dummy, 10, 2, dummy, 12, dummy, dummy, None, dummy, 8, None) == 2

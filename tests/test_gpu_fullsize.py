@@ -13,6 +13,9 @@ benchmark times.
 * 1-D k-means at the kNN workload's full size (n = 2,000,000, k = 50).
 * The paper's Experiment I shape at its largest size: two moons, n = 45,000,
   cosine affinity, at most 3 updates, end to end.
+* The kNN input graph built on the GPU: against the oracle's brute force at
+  n = 200,000 and against the scipy k-d tree graph of the kNN workload at
+  n = 2,000,000.
 """
 import numpy as np
 import pytest
@@ -229,3 +232,29 @@ def test_moons_full_size_cosine(g, orc):
     np.testing.assert_allclose(dg, deg, rtol=1e-5)
     assert it == ref.iterations and conv == ref.converged
     assert rel_l1(vg, ref.v) <= 1e-4
+
+
+def test_knn_graph_200k(g, orc):
+    """n = 200,000 points of the kNN workload's generator, k = 32."""
+    import workloads
+    w = workloads.make("knn8d", n=200000)
+    print(f"gpu: knn graph n={w.n} d={w.d} k=32", flush=True)
+    rp, col, val = g.gpic_knn_graph(_t(w.X), 32, 1.0)
+    rp, col, val = rp.cpu().numpy(), col.cpu().numpy(), val.cpu().numpy()
+    print("oracle: brute-force kNN graph n=200000", flush=True)
+    rpo, colo, valo = orc.knn_graph(w.X, 32, 1.0)
+    assert np.array_equal(rp, rpo) and np.array_equal(col, colo)
+    assert np.all(np.abs(val - valo) <= np.spacing(valo))
+
+
+def test_knn_graph_full_size(g):
+    """n = 2,000,000: the same graph as the workload's (scipy k-d tree, exact
+    kNN, union, float64 weights); weights within one float32 ulp."""
+    import workloads
+    w = workloads.make("knn8d")
+    print(f"gpu: knn graph n={w.n} d={w.d} k=32", flush=True)
+    rp, col, val = g.gpic_knn_graph(_t(w.X), 32, 1.0)
+    assert np.array_equal(rp.cpu().numpy(), w.row_ptr)
+    assert np.array_equal(col.cpu().numpy(), w.col)
+    vg = val.cpu().numpy()
+    assert np.all(np.abs(vg - w.val) <= np.spacing(w.val))

@@ -448,6 +448,40 @@ def test_csr_column_blocked_parity(g, orc, sort_rows, band):
     np.testing.assert_allclose(v.cpu().numpy(), refc.v, rtol=1e-9)
 
 
+def _check_knn(g, orc, X, k, sigma):
+    rp, col, val = g.gpic_knn_graph(_t(X), k, sigma)
+    torch.cuda.synchronize()
+    rpo, colo, valo = orc.knn_graph(X, k, sigma)
+    assert np.array_equal(rp.cpu().numpy(), rpo)
+    assert np.array_equal(col.cpu().numpy(), colo)
+    vg = val.cpu().numpy()
+    # float64 weights rounded once on both sides; exp differs by < 1 ulp
+    # of float64, which can only flip a float32 rounding at a halfway point
+    assert np.all(np.abs(vg - valo) <= np.spacing(valo))
+
+
+@pytest.mark.parametrize("n,d,k,shift", [(3000, 8, 32, 0.0), (40, 3, 39, 0.0),
+                                         (2000, 16, 10, 0.0), (2000, 8, 16, 1000.0),
+                                         (5001, 2, 7, 0.0)])
+def test_knn_graph_parity(g, orc, n, d, k, shift):
+    """The exact kNN graph against the oracle's brute force: same rows,
+    columns and weights (k = n - 1, d = 16, points far from the origin)."""
+    rng = np.random.default_rng(n + d + k)
+    C = 4.0 * rng.standard_normal((10, d))
+    X = (C[rng.integers(0, 10, n)] + rng.standard_normal((n, d)) + shift).astype(np.float32)
+    print(f"knn graph n={n} d={d} k={k} shift={shift}", flush=True)
+    _check_knn(g, orc, X, k, 1.0)
+
+
+def test_knn_graph_ties(g, orc):
+    """Integer lattice (exact distance ties go to the smaller index)."""
+    grid = np.arange(12, dtype=np.float32)
+    X = np.stack(np.meshgrid(grid, grid), axis=-1).reshape(-1, 2)
+    _check_knn(g, orc, X, 4, 1.0)
+    X3 = np.random.default_rng(5).integers(0, 4, size=(3000, 3)).astype(np.float32)
+    _check_knn(g, orc, X3, 10, 0.7)         # many duplicate points and ties
+
+
 def test_csr_full_pattern_equals_dense(g):
     n = 300
     X = _pts(n, 2, 50)
