@@ -40,6 +40,14 @@ def _t(a):
 
 
 @pytest.fixture(scope="module")
+def knn8d():
+    """The full kNN workload (its scipy k-d tree graph takes minutes on the
+    host), built once for the module."""
+    import workloads
+    return workloads.make("knn8d")
+
+
+@pytest.fixture(scope="module")
 def blobs16d():
     import workloads
     return workloads.make("blobs16d")
@@ -193,11 +201,10 @@ def test_kmeans1d_full_size(g, orc):
     _check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))
 
 
-def test_knn_csr_full_size_converge(g, orc):
+def test_knn_csr_full_size_converge(g, orc, knn8d):
     """knn8d at n = 2,000,000 (90M stored entries, random node order): the
     column-blocked product to convergence against the oracle."""
-    import workloads
-    w = workloads.make("knn8d")
+    w = knn8d
     print(f"gpu: knn8d n={w.n} nnz={w.val.shape[0]}", flush=True)
     out = g.pic_csr(_t(w.row_ptr), _t(w.col), _t(w.val.copy()), w.k, "converge",
                     1000, w.eps)
@@ -247,11 +254,10 @@ def test_knn_graph_200k(g, orc):
     assert np.all(np.abs(val - valo) <= np.spacing(valo))
 
 
-def test_knn_graph_full_size(g):
+def test_knn_graph_full_size(g, knn8d):
     """n = 2,000,000: the same graph as the workload's (scipy k-d tree, exact
     kNN, union, float64 weights); weights within one float32 ulp."""
-    import workloads
-    w = workloads.make("knn8d")
+    w = knn8d
     print(f"gpu: knn graph n={w.n} d={w.d} k=32", flush=True)
     rp, col, val = g.gpic_knn_graph(_t(w.X), 32, 1.0)
     assert np.array_equal(rp.cpu().numpy(), w.row_ptr)
