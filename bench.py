@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+FP16_MFMA_PEAK_TFLOPS = 2500.0       # dense fp16 matrix cores, MI355X
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_traffic_blobs16d_n50000.json")
 
 
@@ -342,8 +343,16 @@ def other_workload(args):
         torch.cuda.synchronize()
         pi_ms = e0.elapsed_time(e1)
         flops = 2.0 * w.n * w.n * w.d
+        # executed on the fp16 matrix cores: three part products per
+        # coordinate, coordinates padded to 32-coordinate chunks
+        exec_flops = 3 * 2.0 * w.n * w.n * 32 * ((w.d + 31) // 32)
         rate = {"unit": "TFLOP/s", "value": it * flops / (pi_ms * 1e-3) / 1e12,
-                "flops_per_sweep": flops, "bound": "mfma", "peak": 157.3}
+                "flops_per_sweep": flops, "bound": "mfma",
+                "kernel": "affinity_mfma_kernel (kApply)",
+                "fp16_mfma_flops_per_sweep": exec_flops,
+                "fp16_mfma_tflops": round(it * exec_flops / (pi_ms * 1e-3) / 1e12, 2),
+                "peak": FP16_MFMA_PEAK_TFLOPS}
+        rate["frac_override"] = rate["fp16_mfma_tflops"] / FP16_MFMA_PEAK_TFLOPS
     else:
         W = A
         e0.record(stream)
@@ -355,7 +364,10 @@ def other_workload(args):
         rate = {"unit": "GB/s", "value": it * bytes_it / (pi_ms * 1e-3) / 1e9,
                 "bytes_per_update": bytes_it, "bound": "hbm", "peak": HBM_PEAK_GBS}
     rate["value"] = round(rate["value"], 3)
-    rate["frac"] = round(rate["value"] / rate["peak"], 4)
+    # fused: the fraction of the fp16 matrix-core peak the executed part
+    # products reach; otherwise the rate against its own peak
+    frac = rate.pop("frac_override", rate["value"] / rate["peak"])
+    rate["frac"] = round(frac, 4)
     line = {"metric": f"{w.name}: power-iteration rate ({w.path} operator); "
                       f"end-to-end PIC seconds",
             "value": rate["value"], "unit": rate["unit"], "n_gpus": 1,

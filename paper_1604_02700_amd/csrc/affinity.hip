@@ -8,16 +8,18 @@
 // float64 on the host and rounded once to float32.
 //
 // Two tile engines:
-//   * MFMA, 16 <= d <= 128.  The matrix cores produce c * dist2 directly:
-//     column operands are the augmented points [x_j, |x_j|^2, 1] and row
-//     operands [-2c x_i, c, c |x_i|^2], so one fp32 Gram product gives
-//     c (|x_i|^2 + |x_j|^2 - 2 x_i.x_j); it is clamped at 0 before exp2.
-//     A prologue kernel writes both augmented operand arrays once per call
-//     (squared norms as float64 sums rounded to float32, points padded with
-//     zeros to a multiple of 64); the column operand is stored coordinate-
-//     major, so a column tile is staged into LDS by contiguous 16-byte
-//     copies and every wave reads its matrix-core operands for four column
-//     blocks with one conflict-free 16-byte LDS read.
+//   * MFMA, 16 <= d <= 128.  Squared distances in the Gram form
+//     |x_i|^2 + |x_j|^2 - 2 x_i.x_j, with the dot products on the fp16
+//     matrix cores: every coordinate, scaled by one power of two into
+//     [-1, 1], is split into a half-precision high part and the half-
+//     precision remainder, and three products per pair of parts (hi.hi,
+//     lo.hi, hi.lo, float32 accumulation) reproduce the float32 dot product
+//     to about 2^-22 of |x_i||x_j| per coordinate, at about a fifth of the
+//     fp32 matrix-core time.  A prologue (largest |x|, then the split)
+//     writes the operands once per call in the order the matrix cores take
+//     them, so a column tile is staged into LDS by contiguous 16-byte
+//     copies and every operand read from LDS is one conflict-free 16-byte
+//     read.
 //   * VALU, other d: squared distances from coordinate differences.
 // A workgroup owns a block of rows and a range of columns (a chunk); when
 // the rows alone would not fill the chip the columns are split in chunks,
@@ -35,6 +37,8 @@
 // writes exactly what kStore followed by the row scaling writes.
 #include "common.h"
 
+#include <type_traits>
+
 namespace gpic {
 namespace {
 
@@ -45,6 +49,7 @@ constexpr int kThreads = 256;
 constexpr int kMaxChunks = 16;
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 
 // exp2 on the transcendental unit (1 ulp; results below the smallest
 // normal float flush to zero, far below anything a row sum can notice)
@@ -60,51 +65,6 @@ __device__ __forceinline__ void store4(float *dst, float a, float b, float c, fl
 }
 
 // ------------------------------------------------------------ prologue
-
-// Augmented operands, KP floats per point (KP = 4 KS >= d + 2):
-//   column operand, coordinate-major: xa[k * np + p] = [x_p, |x_p|^2, 1, 0...]_k
-//   row operand, point-major:         xb[p * KP + k] = [-2c x_p, c, c |x_p|^2, 0...]_k
-// |x_p|^2 is a float64 sum rounded once to float32.  Points n .. np-1
-// (padding up to a multiple of the column tile) are all zeros.
-__global__ __launch_bounds__(kThreads) void augment_kernel(
-    const float *__restrict__ X, int64_t n, int64_t np, int d, int KP, float c,
-    float *__restrict__ xa, float *__restrict__ xb)
-{
-    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (p >= np)
-        return;
-    float *a = xa + p;                            // stride np
-    float *b = xb + p * KP;
-    if (p >= n) {
-        for (int k = 0; k < KP; ++k) {
-            a[k * np] = 0.0f;
-            b[k] = 0.0f;
-        }
-        return;
-    }
-    double s = 0.0;
-    for (int k = 0; k < d; ++k) {
-        const double x = (double)X[p * d + k];
-        s = fma(x, x, s);
-    }
-    const float nrm = (float)s;
-    for (int k = 0; k < KP; ++k) {
-        if (k < d) {
-            const float x = X[p * d + k];
-            a[k * np] = x;
-            b[k] = -2.0f * c * x;
-        } else if (k == d) {
-            a[k * np] = nrm;
-            b[k] = c;
-        } else if (k == d + 1) {
-            a[k * np] = 1.0f;
-            b[k] = c * nrm;
-        } else {
-            a[k * np] = 0.0f;
-            b[k] = 0.0f;
-        }
-    }
-}
 
 // rinv[p] = 1 / ||x_p|| (float64, rounded once), 0 for the origin: the
 // cosine affinity (1 + x_i.x_j rinv_i rinv_j) / 2 then gives the origin
@@ -122,6 +82,89 @@ __global__ __launch_bounds__(kThreads) void inv_norm_kernel(const float *__restr
         s = fma(x, x, s);
     }
     rinv[p] = (s > 0.0) ? (float)(1.0 / sqrt(s)) : 0.0f;
+}
+
+// Split-operand prologue of the matrix-core engine (three launches).
+// The largest |x| over every coordinate fixes the scale 2^-S (S the
+// smallest integer with |x| <= 2^S), so that every scaled coordinate
+// x' = x 2^-S lies in [-1, 1]; its two half-precision parts are
+//   hi = fp16(x'),  lo = fp16(x' - hi)   (x' - hi is exact in float32),
+// so hi + lo carries x' to within max(2^-22 |x'|, 2^-25).  Layout, for
+// point p (np padded points, zeros past n), chunk c of 32 coordinates,
+// part h (0 hi, 1 lo) and lane group g:
+//   xh[((c * 2 + h) * 4 + g) * np + p] = the 8 halves of coordinates
+//                                        32 c + 8 g .. 32 c + 8 g + 7
+// (the matrix-core k slots of lane group g), which makes every column
+// tile a set of contiguous 1 KB runs.  Per point also
+//   beta[p] = -|x'_p|^2 / 2 and cn[p] = c |x_p|^2 (float64, rounded once),
+// and scal[1] = m = -2 c 4^S (exact: c times a power of two).
+__global__ void split_clear_kernel(unsigned *__restrict__ scal) { scal[0] = 0u; }
+
+__global__ __launch_bounds__(kThreads) void maxabs_kernel(const float *__restrict__ X,
+                                                          int64_t total,
+                                                          unsigned *__restrict__ scal)
+{
+    __shared__ float red[kThreads / kWave];
+    float mx = 0.0f;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x; t < total; t += stride)
+        mx = fmaxf(mx, fabsf(X[t]));
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1)
+        mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    if ((threadIdx.x % kWave) == 0)
+        red[threadIdx.x / kWave] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kThreads / kWave; ++w)
+            mx = fmaxf(mx, red[w]);
+        // non-negative floats order like their bit patterns
+        atomicMax(scal, __float_as_uint(mx));
+    }
+}
+
+// the scale exponent S from the largest |x| (0 when that is 0 or not finite)
+__device__ __forceinline__ int split_exponent(unsigned bits)
+{
+    const float mx = __uint_as_float(bits);
+    if (!(mx > 0.0f) || !isfinite(mx))
+        return 0;
+    int e;
+    frexpf(mx, &e);                          // mx = f 2^e, f in [0.5, 1)
+    return e;
+}
+
+__global__ __launch_bounds__(kThreads) void split_kernel(
+    const float *__restrict__ X, int64_t n, int64_t np, int d, int nch, float c,
+    unsigned *__restrict__ scal, half8 *__restrict__ xh, float *__restrict__ beta,
+    float *__restrict__ cn)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int S = split_exponent(scal[0]);
+    if (p == 0)
+        scal[1] = __float_as_uint(ldexpf(-2.0f * c, 2 * S));
+    if (p >= np)
+        return;
+    const bool live = p < n;
+    double s = 0.0;
+    for (int ch = 0; ch < nch; ++ch)
+        for (int g = 0; g < 4; ++g) {
+            half8 hi, lo;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int k = 32 * ch + 8 * g + e;
+                const float x = (live && k < d) ? X[p * d + k] : 0.0f;
+                s = fma((double)x, (double)x, s);
+                const float xs = ldexpf(x, -S);
+                const _Float16 h = (_Float16)xs;
+                hi[e] = h;
+                lo[e] = (_Float16)(xs - (float)h);
+            }
+            xh[((int64_t)(ch * 2 + 0) * 4 + g) * np + p] = hi;
+            xh[((int64_t)(ch * 2 + 1) * 4 + g) * np + p] = lo;
+        }
+    beta[p] = (float)(-0.5 * ldexp(s, -2 * S));
+    cn[p] = (float)((double)c * s);
 }
 
 // ---------------------------------------------------- chunk row-sum reduce
@@ -161,43 +204,52 @@ __global__ __launch_bounds__(kThreads) void chunk_reduce_kernel(
 
 // ------------------------------------------------------------------ MFMA
 
-// Workgroup: kMfmaWaves waves x 16 rows; columns [c0, c1) of its chunk in
-// tiles of 64 staged through double-buffered LDS, coordinate-major: tile
-// column c of coordinate k sits at xs[k][c ^ (16 (k % 4))].  The XOR
-// swizzle spreads the four coordinates a wave reads at once over all 64
-// banks (conflict-free 4-byte reads) and keeps 4-column groups contiguous
-// for 16-byte staging writes.
+// Workgroup: W waves, each owning RB blocks of 16 rows; columns [c0, c1)
+// of its chunk in tiles of TC staged through double-buffered LDS.  A tile
+// holds, per (chunk, part, lane group) slot, TC consecutive half8 pieces:
+// xs[buf][slot * TC + col].  Every staged tile feeds 16 W RB rows, so the
+// operand traffic from L2 per pair of points is 4 d / (16 W RB) bytes.
 //
-// v_mfma_f32_16x16x4f32 operand layout (lane l, g = l / 16, m = l % 16):
-//   A operand : element (row m,  k = g)
-//   B operand : element (k = g,  column m)
-//   result    : elements (row 4g + r, column m), r = 0..3
-// The A operand of block q (q = 0..3) carries tile columns 16 q + a and
-// the B operand the wave's 16 rows i.  Lane (m, g) ends with row i and
-// columns 16 q + 4 g + r.  When A or W is written, the wave's 16 x 64
-// tile goes through LDS first and is stored as 4 rows x 256 contiguous
-// bytes per instruction (measured 10 % faster than 16 rows x 64 bytes).
-constexpr int kMfmaWaves = 4;                 // waves (16 rows each) per workgroup
-constexpr int kMfmaThreads = kMfmaWaves * 64;
-constexpr int kRowsPerWave = 16;
-constexpr int kRowsPerGroup = kMfmaWaves * kRowsPerWave;
-constexpr int kTileCols = 64;
+// v_mfma_f32_16x16x32_f16 operand layout (lane l, g = l / 16, m = l % 16;
+// checked on the device):
+//   A operand : row m,      k = 8 g .. 8 g + 7
+//   B operand : column m,   k = 8 g .. 8 g + 7
+//   result    : rows 4 g + r (r = 0..3), column m
+// The A operand carries tile columns 16 q + m and the B operand the wave's
+// rows i, so lane (m, g) ends with row i and columns 16 q + 4 g + r.  Each
+// 32-coordinate chunk takes three products (hi.hi, lo.hi, hi.lo) into one
+// float32 accumulator that starts at beta_j, which leaves
+//   D = x'_i.x'_j - |x'_j|^2 / 2   and   c dist2 = m D + c |x_i|^2
+// for one fused multiply-add; exp2(-c dist2) is clamped to [0, 1] (the
+// output modifier of the exp2 instruction), which equals clamping c dist2
+// at 0.  The matrix-core chain of one 16-column block is issued before the
+// epilogue of the previous block, so the matrix cores and the vector ALUs
+// work at the same time.
+// When A or W is written (W = 4, RB = 1), the wave's 16 x TC tile goes
+// through LDS and is stored as 4 rows x 4 TC contiguous bytes per store.
+constexpr int kChunkRows = 128;               // nominal rows per workgroup (chunking)
+constexpr int kColAlign = 64;                 // chunk and padding granularity
 
-template <int KS, int MODE>
-__global__ __launch_bounds__(kMfmaThreads) void affinity_mfma_kernel(
-    const float *__restrict__ xa, int64_t np, const float *__restrict__ xb, int64_t n,
+template <int NCH, int RB, int TC, int MODE, int W>
+__global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
+    const half8 *__restrict__ xh, int64_t np, const float *__restrict__ beta,
+    const float *__restrict__ cn, const unsigned *__restrict__ scal, int64_t n,
     int64_t chunk_cols, float *__restrict__ A, int64_t lda,
     const double *__restrict__ v, const double *__restrict__ degree_in,
     double *__restrict__ out, double *__restrict__ part,
     double *__restrict__ partial, StopCtl ctl, int use_ctl)
 {
-    constexpr int KP = 4 * KS;               // augmented, padded dimension
-    constexpr int kRow4 = kTileCols / 4;     // 16-byte pieces per coordinate
-    __shared__ floatx4 xs[2][KP * kRow4];
-    __shared__ double vs[2][kTileCols];
-    __shared__ double red[kMfmaThreads / kWave];
-    constexpr int kOutStride = kTileCols + 4;
-    __shared__ float ot[(MODE == kStore || MODE == kStoreW) ? kMfmaWaves : 1][16 * kOutStride];
+    constexpr int NT = W * 64;
+    constexpr int kSlots = NCH * 8;              // (chunk, part, lane group)
+    constexpr int kQ = TC / 16;                  // 16-column blocks per tile
+    constexpr bool kWrites = (MODE == kStore || MODE == kStoreW);
+    constexpr int kOutStride = TC + 4;
+    static_assert(!kWrites || RB == 1, "one staged output tile per wave");
+    __shared__ half8 xs[2][kSlots * TC];
+    __shared__ float bs[2][TC];
+    __shared__ double vs[2][(MODE == kApply) ? TC : 1];
+    __shared__ double red[W];
+    __shared__ float ot[kWrites ? W : 1][kWrites ? 16 * kOutStride : 1];
 
     if (MODE == kApply && use_ctl) {
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
@@ -209,126 +261,192 @@ __global__ __launch_bounds__(kMfmaThreads) void affinity_mfma_kernel(
     const int wave = threadIdx.x / kWave;
     const int g = lane >> 4;
     const int m = lane & 15;
-    const int64_t wrow0 = (int64_t)blockIdx.x * kRowsPerGroup + wave * kRowsPerWave;
-    const int64_t i = wrow0 + m;
-    const bool row_ok = i < n;
-    const int64_t ic = row_ok ? i : n - 1;
+    const int64_t wrow0 = ((int64_t)blockIdx.x * W + wave) * (16 * RB);
     const int64_t c0 = (int64_t)blockIdx.y * chunk_cols;
     const int64_t c1 = (c0 + chunk_cols < n) ? c0 + chunk_cols : n;
+    const float mm = __uint_as_float(scal[1]);
 
-    // B operand: augmented row coordinates 4 s + g of [-2c x_i, c, c |x_i|^2]
-    float bop[KS];
+    // B operands: this lane's rows, hi and lo of every chunk
+    half8 bh[RB][NCH], bl[RB][NCH];
+    float cni[RB], rs[RB];
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-        bop[s] = xb[ic * KP + 4 * s + g];
-    float rs = 0.0f;
-    if (MODE == kStoreW) {
-        const double di = degree_in[ic];
-        rs = (di == 0.0) ? 0.0f : (float)(1.0 / di);
+    for (int rb = 0; rb < RB; ++rb) {
+        const int64_t i = wrow0 + 16 * rb + m;
+        const int64_t ic = i < n ? i : n - 1;
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+            bh[rb][ch] = xh[((int64_t)(ch * 2 + 0) * 4 + g) * np + ic];
+            bl[rb][ch] = xh[((int64_t)(ch * 2 + 1) * 4 + g) * np + ic];
+        }
+        cni[rb] = cn[ic];
+        rs[rb] = 0.0f;
+        if (MODE == kStoreW) {
+            const double di = degree_in[ic];
+            rs[rb] = (di == 0.0) ? 0.0f : (float)(1.0 / di);
+        }
     }
 
-    // staging: piece f = k * 16 + cg holds columns 4 cg .. 4 cg + 3 of
-    // coordinate k (tiles start at multiples of 64 <= np - 64)
-    constexpr int kPieces = KP * kRow4;
-    constexpr int kPer = (kPieces + kMfmaThreads - 1) / kMfmaThreads;
-    floatx4 stage[kPer];
+    // staging: piece f = slot * TC + col (tiles start at multiples of 64
+    // and end at or before np, so every load is in bounds)
+    constexpr int kPieces = kSlots * TC;
+    constexpr int kPer = (kPieces + NT - 1) / NT;
+    half8 stage[kPer];
+    float bstage = 0.0f;
     double vstage = 0.0;
     auto fetch = [&](int64_t jt) {
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
-            const int f = threadIdx.x + u * kMfmaThreads;
-            if (kPieces % kMfmaThreads == 0 || f < kPieces)
-                stage[u] = *reinterpret_cast<const floatx4 *>(
-                    xa + (int64_t)(f / kRow4) * np + jt + 4 * (f % kRow4));
+            const int f = threadIdx.x + u * NT;
+            if (kPieces % NT == 0 || f < kPieces)
+                stage[u] = xh[(int64_t)(f / TC) * np + jt + (f % TC)];
         }
-        if (MODE == kApply && threadIdx.x < kTileCols) {
-            const int64_t j = jt + threadIdx.x;
-            vstage = (j < c1) ? v[j] : 0.0;
+        if (threadIdx.x < TC) {
+            bstage = beta[jt + threadIdx.x];
+            if (MODE == kApply) {
+                const int64_t j = jt + threadIdx.x;
+                vstage = (j < c1) ? v[j] : 0.0;
+            }
         }
     };
     auto commit = [&](int buf) {
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
-            const int f = threadIdx.x + u * kMfmaThreads;
-            if (kPieces % kMfmaThreads == 0 || f < kPieces) {
-                const int k = f / kRow4;
-                xs[buf][k * kRow4 + ((f % kRow4) ^ (4 * (k & 3)))] = stage[u];
-            }
+            const int f = threadIdx.x + u * NT;
+            if (kPieces % NT == 0 || f < kPieces)
+                xs[buf][f] = stage[u];
         }
-        if (MODE == kApply && threadIdx.x < kTileCols)
-            vs[buf][threadIdx.x] = vstage;
+        if (threadIdx.x < TC) {
+            bs[buf][threadIdx.x] = bstage;
+            if (MODE == kApply)
+                vs[buf][threadIdx.x] = vstage;
+        }
     };
 
-    double acc = 0.0;
-    const int64_t ntiles = (c1 - c0 + kTileCols - 1) / kTileCols;
+    // two float64 accumulators per row block (even and odd q), added at the end
+    double acc[RB][2];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+        acc[rb][0] = acc[rb][1] = 0.0;
+
+    auto tile = [&](int buf, int64_t jt, auto masked) {
+        constexpr bool kMask = decltype(masked)::value;
+        // one 16-column block: the matrix-core chain into cc[rb] ...
+        auto chain = [&](int q, floatx4 (&cc)[RB]) {
+            const floatx4 b0 = *reinterpret_cast<const floatx4 *>(&bs[buf][16 * q + 4 * g]);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+                cc[rb] = b0;
+#pragma unroll
+            for (int ch = 0; ch < NCH; ++ch) {
+                const half8 ah = xs[buf][((ch * 2 + 0) * 4 + g) * TC + 16 * q + m];
+                const half8 al = xs[buf][((ch * 2 + 1) * 4 + g) * TC + 16 * q + m];
+                // the row blocks' chains are independent: interleaved, no
+                // product waits for the one before it
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+                    cc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[rb][ch], cc[rb],
+                                                                    0, 0, 0);
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+                    cc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh[rb][ch], cc[rb],
+                                                                    0, 0, 0);
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+                    cc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[rb][ch], cc[rb],
+                                                                    0, 0, 0);
+            }
+        };
+        // ... and its epilogue
+        auto epi = [&](int q, const floatx4 (&cc)[RB]) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                const int64_t i = wrow0 + 16 * rb + m;
+                float a[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    a[r] = __builtin_amdgcn_fmed3f(
+                        exp2_fast(-fmaf(cc[rb][r], mm, cni[rb])), 0.0f, 1.0f);
+                const int64_t j0 = jt + 16 * q + 4 * g;    // this lane's columns
+                if (kMask) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (j0 + r == i || j0 + r >= c1)
+                            a[r] = 0.0f;
+                }
+                if (kWrites) {
+                    float *ow = ot[wave] + m * kOutStride + 16 * q + 4 * g;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        ow[r] = (MODE == kStoreW) ? a[r] * rs[rb] : a[r];
+                }
+                if (MODE == kStore || MODE == kDegree) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        acc[rb][q & 1] += (double)a[r];
+                } else if (MODE == kApply) {
+                    const double *vp = vs[buf] + 16 * q + 4 * g;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        acc[rb][q & 1] = fma((double)a[r], vp[r], acc[rb][q & 1]);
+                }
+            }
+        };
+        floatx4 ca[RB], cb[RB];
+        chain(0, ca);
+#pragma unroll
+        for (int q = 0; q < kQ; q += 2) {
+            if (q + 1 < kQ)
+                chain(q + 1, cb);
+            epi(q, ca);
+            if (q + 2 < kQ)
+                chain(q + 2, ca);
+            if (q + 1 < kQ)
+                epi(q + 1, cb);
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            if (kWrites) {
+                // the wave's 16 x TC tile, 4 rows x 4 TC contiguous bytes per store
+                const int64_t rrow0 = wrow0 + 16 * rb;
+                constexpr int kLanesPerRow = TC / 4;
+                constexpr int kRowsPerStore = kWave / kLanesPerRow;
+#pragma unroll
+                for (int u = 0; u < 16 / kRowsPerStore; ++u) {
+                    const int rr = kRowsPerStore * u + lane / kLanesPerRow;
+                    const int cc = 4 * (lane % kLanesPerRow);
+                    const int64_t ii = rrow0 + rr;
+                    const int64_t jj = jt + cc;
+                    const float *src = ot[wave] + rr * kOutStride + cc;
+                    if (ii < n) {
+                        float *dst = A + ii * lda + jj;
+                        if (!kMask || jj + 3 < c1) {
+                            store4(dst, src[0], src[1], src[2], src[3]);
+                        } else {
+                            for (int e = 0; e < 4 && jj + e < c1; ++e)
+                                dst[e] = src[e];
+                        }
+                    }
+                }
+            }
+        }
+    };
+
+    const int64_t ntiles = (c1 - c0 + TC - 1) / TC;
+    const int64_t rlo = wrow0, rhi = wrow0 + 16 * RB;   // this wave's rows
     fetch(c0);
     commit(0);
     __syncthreads();
     for (int64_t t = 0; t < ntiles; ++t) {
         const int buf = (int)(t & 1);
-        const int64_t jt = c0 + t * kTileCols;
+        const int64_t jt = c0 + t * TC;
         if (t + 1 < ntiles)
-            fetch(jt + kTileCols);                  // in flight during compute
-        const bool diag = (wrow0 >= jt) && (wrow0 < jt + kTileCols);
-        const bool tail = jt + kTileCols > c1;
-        // coordinate 4 s + g, tile column 16 q + m, swizzled by 16 g
-        const float *tile = reinterpret_cast<const float *>(xs[buf]) + g * kTileCols;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            floatx4 cacc = {0.0f, 0.0f, 0.0f, 0.0f};
-            const float *ap = tile + ((16 * q + m) ^ (16 * g));
-#pragma unroll
-            for (int s = 0; s < KS; ++s)
-                cacc = __builtin_amdgcn_mfma_f32_16x16x4f32(ap[4 * s * kTileCols], bop[s],
-                                                            cacc, 0, 0, 0);
-            float a[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                a[r] = exp2_fast(-fmaxf(cacc[r], 0.0f));
-            const int64_t j0 = jt + 16 * q + 4 * g;    // this lane's columns
-            if (diag || tail) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (j0 + r == i || j0 + r >= c1)
-                        a[r] = 0.0f;
-            }
-            if (MODE == kStore || MODE == kStoreW) {
-                float *ow = ot[wave] + m * kOutStride + 16 * q + 4 * g;
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    ow[r] = (MODE == kStoreW) ? a[r] * rs : a[r];
-            }
-            if (MODE == kStore || MODE == kDegree) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    acc += (double)a[r];
-            } else if (MODE == kApply) {
-                const double *vp = vs[buf] + 16 * q + 4 * g;
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    acc = fma((double)a[r], vp[r], acc);
-            }
-        }
-        if (MODE == kStore || MODE == kStoreW) {
-            // the wave's 16 x 64 tile, 4 rows x 256 contiguous bytes per store
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int rr = 4 * u + (lane >> 4);
-                const int cc = 4 * (lane & 15);
-                const int64_t ii = wrow0 + rr;
-                const int64_t jj = jt + cc;
-                const float *src = ot[wave] + rr * kOutStride + cc;
-                if (ii < n) {
-                    float *dst = A + ii * lda + jj;
-                    if (!tail || jj + 3 < c1) {
-                        store4(dst, src[0], src[1], src[2], src[3]);
-                    } else {
-                        for (int e = 0; e < 4 && jj + e < c1; ++e)
-                            dst[e] = src[e];
-                    }
-                }
-            }
-        }
+            fetch(jt + TC);                          // in flight during compute
+        const bool diag = (rlo < jt + TC) && (jt < rhi);
+        const bool tail = jt + TC > c1;
+        if (diag || tail)
+            tile(buf, jt, std::true_type{});
+        else
+            tile(buf, jt, std::false_type{});
         if (t + 1 < ntiles) {
             // the barrier ending the previous iteration ordered every wave's
             // reads of buffer buf ^ 1 before this write; this one orders the
@@ -340,28 +458,30 @@ __global__ __launch_bounds__(kMfmaThreads) void affinity_mfma_kernel(
 
     if (MODE == kStoreW)
         return;
-    // the four lanes sharing a row (g = 0..3) hold disjoint columns
-    acc += __shfl_xor(acc, 16, kWave);
-    acc += __shfl_xor(acc, 32, kWave);
-    if (part != nullptr) {
-        // chunk partial, reduced in chunk order by chunk_reduce_kernel
-        if (g == 0 && row_ok)
-            part[(int64_t)blockIdx.y * n + i] = acc;
-        return;
-    }
     double yabs = 0.0;
-    if (g == 0 && row_ok) {
-        if (MODE == kApply) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int64_t i = wrow0 + 16 * rb + m;
+        double s = acc[rb][0] + acc[rb][1];
+        // the four lanes sharing a row (g = 0..3) hold disjoint columns
+        s += __shfl_xor(s, 16, kWave);
+        s += __shfl_xor(s, 32, kWave);
+        if (g != 0 || i >= n)
+            continue;
+        if (part != nullptr) {
+            // chunk partial, reduced in chunk order by chunk_reduce_kernel
+            part[(int64_t)blockIdx.y * n + i] = s;
+        } else if (MODE == kApply) {
             const double di = degree_in[i];
-            const double yi = (di == 0.0) ? 0.0 : acc / di;
+            const double yi = (di == 0.0) ? 0.0 : s / di;
             out[i] = yi;
-            yabs = fabs(yi);
+            yabs += fabs(yi);
         } else if (out != nullptr) {
-            out[i] = acc;
+            out[i] = s;
         }
     }
-    if (MODE == kApply && partial != nullptr) {
-        const double sum = block_sum<kMfmaThreads>(yabs, red);
+    if (MODE == kApply && part == nullptr && partial != nullptr) {
+        const double sum = block_sum<NT>(yabs, red);
         if (threadIdx.x == 0)
             partial[blockIdx.x] = sum;
     }
@@ -543,53 +663,100 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
 
 bool use_mfma(int d) { return d >= 16 && d <= 128; }
 
-int ks_for(int d)
+constexpr int kMaxNch = 4;                   // 32-coordinate chunks for d <= 128
+
+int nch_for(int d) { return (d + 31) / 32; }
+
+// Row blocking: the sweeps that only sum rows take four 16-row blocks per
+// wave and 8 waves per workgroup (512 rows share every staged column tile,
+// and four independent matrix-core chains per wave hide each other's
+// latency; measured 14.9 ms per product at n = 200,000, d = 64, against
+// 16.4 with 128 rows); the sweeps that write A or W take one block per
+// wave and 4 waves (their bound is the stores).
+constexpr int rb_for(int mode) { return (mode == kApply || mode == kDegree) ? 4 : 1; }
+constexpr int waves_for(int mode) { return (mode == kApply || mode == kDegree) ? 8 : 4; }
+constexpr int64_t rows_per_group(int mode) { return 16 * rb_for(mode) * waves_for(mode); }
+
+int64_t row_groups(int64_t n, int mode)
 {
-    const int need = (d + 2 + 3) / 4;          // augmented dimension / 4
-    static const int sizes[] = {5, 6, 8, 10, 12, 14, 17, 20, 24, 28, 33};
-    for (int s : sizes)
-        if (s >= need)
-            return s;
-    return 33;
+    return (n + rows_per_group(mode) - 1) / rows_per_group(mode);
 }
 
 // Column chunks: enough workgroups to fill the chip when rows are few.
+// The chunk width depends on n alone, so every mode sums a row's columns
+// in the same order.
 void chunking(int64_t n, int64_t *chunk_cols, int *nchunks)
 {
-    const int64_t groups = (n + kRowsPerGroup - 1) / kRowsPerGroup;
+    const int64_t groups = (n + kChunkRows - 1) / kChunkRows;
     int64_t want = (4096 + groups - 1) / groups;     // >= 4 workgroups per CU
     if (want < 1)
         want = 1;
     if (want > kMaxChunks)
         want = kMaxChunks;
     int64_t cols = (n + want - 1) / want;
-    cols = (cols + kTileCols - 1) / kTileCols * kTileCols;
+    cols = (cols + kColAlign - 1) / kColAlign * kColAlign;
     *chunk_cols = cols;
     *nchunks = (int)((n + cols - 1) / cols);
 }
 
-constexpr int kMaxKP = 4 * 33;               // largest augmented dimension
-
-int64_t padded_points(int64_t n) { return (n + kTileCols - 1) / kTileCols * kTileCols; }
+int64_t padded_points(int64_t n) { return (n + kColAlign - 1) / kColAlign * kColAlign; }
 
 int64_t al256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
 struct Ws {
-    float *xa;
-    float *xb;
-    double *part;
+    unsigned *scal;     // [0] largest |x| (float bits), [1] m = -2 c 4^S
+    half8 *xh;          // split operands, kMaxNch * 8 slots of np half8
+    float *beta;        // [np]
+    float *cn;          // [np]
+    double *part;       // per-chunk row sums, kMaxChunks * n
 };
 
-// [xa: np * kMaxKP floats][xb: same][per-chunk row sums: kMaxChunks * n]
 Ws carve(void *ws, int64_t n)
 {
     char *b = static_cast<char *>(ws);
-    const int64_t ob = al256(padded_points(n) * kMaxKP * 4);
+    const int64_t np = padded_points(n);
     Ws w;
-    w.xa = reinterpret_cast<float *>(b);
-    w.xb = reinterpret_cast<float *>(b + ob);
-    w.part = reinterpret_cast<double *>(b + 2 * ob);
+    w.scal = reinterpret_cast<unsigned *>(b);
+    b += 256;
+    w.xh = reinterpret_cast<half8 *>(b);
+    b += al256(np * kMaxNch * 8 * (int64_t)sizeof(half8));
+    w.beta = reinterpret_cast<float *>(b);
+    b += al256(np * 4);
+    w.cn = reinterpret_cast<float *>(b);
+    b += al256(np * 4);
+    w.part = reinterpret_cast<double *>(b);
     return w;
+}
+
+hipError_t launch_split(const float *X, int64_t n, int d, float c, const Ws &w,
+                        hipStream_t s)
+{
+    const int64_t np = padded_points(n);
+    hipLaunchKernelGGL(split_clear_kernel, dim3(1), dim3(1), 0, s, w.scal);
+    const int64_t total = n * (int64_t)d;
+    int64_t blocks = (total + kThreads - 1) / kThreads;
+    if (blocks > 2048)
+        blocks = 2048;
+    hipLaunchKernelGGL(maxabs_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, X,
+                       total, w.scal);
+    hipLaunchKernelGGL(split_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, X, n, np, d, nch_for(d), c, w.scal, w.xh,
+                       w.beta, w.cn);
+    return hipGetLastError();
+}
+
+template <int NCH, int MODE>
+void launch_engine(const Ws &w, int64_t n, int64_t chunk_cols, int nchunks, float *A,
+                   int64_t lda, const double *v, const double *degree_in, double *out,
+                   double *part, double *partial, StopCtl ctl, int use_ctl, hipStream_t s)
+{
+    constexpr int RB = rb_for(MODE);
+    constexpr int W = waves_for(MODE);
+    constexpr int TC = (NCH <= 2) ? 64 : 32;
+    const dim3 grid((unsigned)row_groups(n, MODE), (unsigned)nchunks);
+    hipLaunchKernelGGL((affinity_mfma_kernel<NCH, RB, TC, MODE, W>), grid, dim3(W * 64), 0,
+                       s, w.xh, padded_points(n), w.beta, w.cn, w.scal, n, chunk_cols, A,
+                       lda, v, degree_in, out, part, partial, ctl, use_ctl);
 }
 
 template <int MODE>
@@ -600,35 +767,24 @@ hipError_t dispatch(const float *X, int64_t n, int d, float c, float *A,
 {
     if (use_mfma(d)) {
         const Ws w = carve(ws, n);
-        const int ks = ks_for(d);
-        const int64_t np = padded_points(n);
-        if (!operands_ready)
-            hipLaunchKernelGGL(augment_kernel,
-                               dim3((unsigned)((np + kThreads - 1) / kThreads)),
-                               dim3(kThreads), 0, s, X, n, np, d, 4 * ks, c, w.xa, w.xb);
+        if (!operands_ready) {
+            const hipError_t e = launch_split(X, n, d, c, w, s);
+            if (e != hipSuccess)
+                return e;
+        }
         int64_t chunk_cols;
         int nchunks;
         chunking(n, &chunk_cols, &nchunks);
         const bool sums = (MODE != kStoreW) && (MODE != kStore || out != nullptr);
         double *part = (sums && nchunks > 1) ? w.part : nullptr;
-        const dim3 grid((unsigned)((n + kRowsPerGroup - 1) / kRowsPerGroup),
-                        (unsigned)nchunks);
-#define GPIC_MFMA(KS)                                                          \
-    hipLaunchKernelGGL((affinity_mfma_kernel<KS, MODE>), grid, dim3(kMfmaThreads), 0, \
-                       s, w.xa, np, w.xb, n, chunk_cols, A, lda, v, degree_in,   \
-                       out, part, partial, ctl, use_ctl)
-        switch (ks) {
-        case 5: GPIC_MFMA(5); break;
-        case 6: GPIC_MFMA(6); break;
-        case 8: GPIC_MFMA(8); break;
-        case 10: GPIC_MFMA(10); break;
-        case 12: GPIC_MFMA(12); break;
-        case 14: GPIC_MFMA(14); break;
-        case 17: GPIC_MFMA(17); break;
-        case 20: GPIC_MFMA(20); break;
-        case 24: GPIC_MFMA(24); break;
-        case 28: GPIC_MFMA(28); break;
-        default: GPIC_MFMA(33); break;
+#define GPIC_MFMA(NCH)                                                          \
+    launch_engine<NCH, MODE>(w, n, chunk_cols, nchunks, A, lda, v, degree_in, out, \
+                             part, partial, ctl, use_ctl, s)
+        switch (nch_for(d)) {
+        case 1: GPIC_MFMA(1); break;
+        case 2: GPIC_MFMA(2); break;
+        case 3: GPIC_MFMA(3); break;
+        default: GPIC_MFMA(4); break;
         }
 #undef GPIC_MFMA
         if (part != nullptr) {
@@ -724,8 +880,9 @@ hipError_t launch_cosine_w(const float *X, int64_t n, int d, float *W, int64_t l
 
 size_t affinity_ws(int64_t n)
 {
-    return (size_t)(2 * al256(padded_points(n) * kMaxKP * 4) +
-                    al256((int64_t)kMaxChunks * n * 8));
+    const int64_t np = padded_points(n);
+    return (size_t)(256 + al256(np * kMaxNch * 8 * (int64_t)sizeof(half8)) +
+                    2 * al256(np * 4) + al256((int64_t)kMaxChunks * n * 8));
 }
 
 int64_t fused_blocks(int64_t n, int d)
@@ -737,7 +894,7 @@ int64_t fused_blocks(int64_t n, int d)
     chunking(n, &chunk_cols, &nchunks);
     if (nchunks > 1)
         return (n + kThreads - 1) / kThreads;        // chunk_reduce workgroups
-    return (n + kRowsPerGroup - 1) / kRowsPerGroup;  // tile workgroups
+    return row_groups(n, kApply);                    // tile workgroups
 }
 
 hipError_t launch_affinity(const float *X, int64_t n, int d, float c, float *A,
@@ -770,11 +927,7 @@ hipError_t launch_fused_prepare(const float *X, int64_t n, int d, float c, void 
 {
     if (!use_mfma(d))
         return hipSuccess;
-    const Ws w = carve(ws, n);
-    const int64_t np = padded_points(n);
-    hipLaunchKernelGGL(augment_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, s, X, n, np, d, 4 * ks_for(d), c, w.xa, w.xb);
-    return hipGetLastError();
+    return launch_split(X, n, d, c, carve(ws, n), s);
 }
 
 hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c,

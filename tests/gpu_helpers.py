@@ -42,14 +42,28 @@ def stop_margin(stats, eps, t_star) -> float:
 
 
 def affinity_tolerance(X, sigma, A_ref, gram: bool):
-    """Per-entry bound on |A_gpu - A_ref| from the float32 arithmetic.
+    """Per-entry bound on |A_gpu - A_ref| from the arithmetic of each engine.
 
-    Direct differences: each squared distance carries a relative error of a
-    few float32 ulps.  Gram form: |x_i|^2 + |x_j|^2 - 2 x_i.x_j carries an
-    absolute error up to about (d + 4) eps32 (|x_i|^2 + |x_j|^2), from the
-    norms and the length-d dot product.  Either error e in dist2 moves
-    A = exp(-dist2 / (2 sigma^2)) by A e / (2 sigma^2); exp2 and the final
-    rounding add a few ulps of A.
+    Direct differences (VALU engine): each squared distance carries a
+    relative error of a few float32 ulps, (d + 4) eps32 dist2.
+
+    Gram form (matrix-core engine), u = 2^-24, M = max |x|:
+      * every coordinate is scaled into [-1, 1] by 2^-S (2^S <= 2M) and
+        split into half-precision parts hi + lo, which carry it to within
+        max(2^-22 |x|, 2^-25 2^S) <= 2^-22 |x| + u M;
+      * three of the four part products are summed (lo.lo, at most
+        2^-22 |x_ik||x_jk|, is dropped); part products are exact in
+        float32, so per pair of points the dot product is off by at most
+        12 u sum_k |x_ik||x_jk| + u M (|x_i|_1 + |x_j|_1) from the parts;
+      * the float32 accumulation of 3d products and the start value
+        -|x_j|^2 / 2 adds at most 3d u (|x_i||x_j| + |x_j|^2 / 2);
+      * rounding |x_j|^2 / 2, c |x_i|^2 and the final multiply-add adds
+        u (|x_i|^2 + |x_j|^2 + dist2).
+    With 2 |x_i||x_j| <= |x_i|^2 + |x_j|^2 this gives, in dist2,
+      u [(6d + 16)(|x_i|^2 + |x_j|^2) + 2 M (|x_i|_1 + |x_j|_1)].
+    Either engine: an error e in dist2 moves A = exp(-dist2 / (2 sigma^2))
+    by A e / (2 sigma^2); the float32 coefficient c, exp2 and the final
+    rounding add 4 eps32 dist2 and a few ulps of A.
     """
     X64 = np.asarray(X, dtype=np.float64)
     d = X64.shape[1]
@@ -58,7 +72,11 @@ def affinity_tolerance(X, sigma, A_ref, gram: bool):
     with np.errstate(divide="ignore"):
         dist2 = -np.log(np.where(A_ref > 0, A_ref, 1.0)) * s2
     if gram:
-        e = (d + 4) * EPS32 * (nrm[:, None] + nrm[None, :])
+        u = EPS32 / 2
+        l1 = np.abs(X64).sum(1)
+        M = float(np.abs(X64).max())
+        e = u * ((6 * d + 16) * (nrm[:, None] + nrm[None, :])
+                 + 2 * M * (l1[:, None] + l1[None, :]))
     else:
         e = (d + 4) * EPS32 * dist2
     # the exponent itself is formed in float32: c * dist2 rounds once more
