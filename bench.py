@@ -92,8 +92,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-converge", action="store_true")
     ap.add_argument("--workload", default="blobs16d",
-                    choices=["blobs16d", "blobs64d", "knn8d", "knn8d_rcm", "rings2d",
-                             "blobs2d", "moons", "circles3"],
+                    choices=["blobs16d", "blobs16d_sym", "blobs64d", "knn8d", "knn8d_rcm",
+                             "rings2d", "blobs2d", "moons", "circles3"],
                     help="blobs16d is the headline line; the others measure the "
                          "fused, CSR, small dense and cosine (the paper's "
                          "Experiment I shapes) paths")
@@ -113,6 +113,8 @@ def main():
     import paper_1604_02700_amd as g
     import workloads
 
+    if args.workload == "blobs16d_sym":
+        return sym_workload(args)
     if args.workload != "blobs16d":
         return other_workload(args)
 
@@ -248,6 +250,95 @@ def main():
         "cpu_baseline": cpu,
         "copy_reference": copy_ref,
     }
+    print(json.dumps(line), flush=True)
+
+
+def sym_workload(args):
+    """The headline workload (16-D blobs, n = 50,000, T = 50, k = 10) over the
+    symmetric storage of A (packed upper tiles, 2 n^2 bytes per product):
+    one JSON line, not the headline line."""
+    import torch
+    import paper_1604_02700_amd as g
+    import workloads
+
+    dev = torch.device("cuda:0")
+    w = workloads.make("blobs16d", n=args.n if args.n != 50000 else None)
+    n, T, k = w.n, args.T, w.k
+    log(f"bench: workload blobs16d (symmetric storage) n={n} T={T}")
+    X = torch.from_numpy(w.X).to(dev)
+    As = torch.empty(g.sym_bytes(n) // 4, dtype=torch.float32, device=dev)
+    v = torch.empty(n, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(record):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        As_, deg, v0, nz = g.gpic_affinity_sym(X, w.sigma, As)
+        v.copy_(v0)
+        ev[1].record(stream)
+        g.gpic_power_iterate_sym(As, n, deg, v, None, "fixed", T, record_stats=False)
+        ev[2].record(stream)
+        g.gpic_kmeans1d(v, k)
+        ev[3].record(stream)
+        if record is not None:
+            torch.cuda.synchronize()
+            record.append([ev[i].elapsed_time(ev[i + 1]) for i in range(3)])
+        return deg
+
+    for _ in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    phases = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        deg = step(phases)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ph = np.array(phases)
+    pi_ms = float(ph[:, 1].mean())
+    stored = float(g.sym_bytes(n))
+    # the product alone, one event pair per launch on the library's stream
+    y = torch.empty(n, dtype=torch.float64, device=dev)
+    g.gpic_matvec_sym(As, n, deg, v, y)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.gemv_reps)]
+    for a, b in evs:
+        a.record(stream)
+        g.gpic_matvec_sym(As, n, deg, v, y)
+        b.record(stream)
+    torch.cuda.synchronize()
+    prod_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    nb = (n + 255) // 256
+    part_bytes = 2.0 * 8 * nb * nb * 256          # partial sums written and read back
+    alg = stored + part_bytes + 24.0 * n           # tiles once, partials, v, d, y
+    conv = None
+    if not args.no_converge:
+        tc0 = time.perf_counter()
+        out = g.pic_sym(X, w.sigma, k, "converge", 1000, w.eps, As=As)
+        torch.cuda.synchronize()
+        conv = {"e2e_s": round(time.perf_counter() - tc0, 5),
+                "iterations": out.pi.iterations, "converged": out.pi.converged}
+    line = {"metric": "blobs16d over symmetric storage: power-iteration GB/s of stored "
+                      "A streamed; end-to-end PIC seconds, n=50k",
+            "value": round(T * stored / (pi_ms * 1e-3) / 1e9, 2), "unit": "GB/s",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+            "config": {"workload": f"blobs16d: n={n}, d={w.d}, packed upper tiles of A "
+                                   f"({stored / 1e9:.2f} GB), T={T}, k={k}", "n": n,
+                       "storage": "f32 symmetric tiles", "accumulate": "f64"},
+            "e2e_fixed_T_s": round(ms_step / 1e3, 5),
+            "phases_ms": {"affinity_sym_degree_v0": round(float(ph[:, 0].mean()), 4),
+                          "power_iteration": round(pi_ms, 4),
+                          "kmeans": round(float(ph[:, 2].mean()), 4)},
+            "dense_equivalent_gbs": round(T * 4.0 * n * n / (pi_ms * 1e-3) / 1e9, 2),
+            "to_convergence": conv,
+            "roofline": {"bound": "hbm", "kernel": "sym_gemv_kernel + sym_finalize_kernel",
+                         "achieved": round(alg / (prod_ms * 1e-3) / 1e9, 2),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(alg / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                         "avg_launch_ms": round(prod_ms, 5), "bytes_per_launch": alg,
+                         "traffic": None}}
     print(json.dumps(line), flush=True)
 
 

@@ -73,7 +73,10 @@ enum {
     GPIC_OP_MATVEC_FUSED = 9,
     GPIC_OP_AFFINITY_COSINE = 10,
     GPIC_OP_AFFINITY_COSINE_NORMALIZED = 11,
-    GPIC_OP_KNN_GRAPH = 12
+    GPIC_OP_KNN_GRAPH = 12,
+    GPIC_OP_AFFINITY_SYM = 13,
+    GPIC_OP_MATVEC_SYM = 14,
+    GPIC_OP_PI_SYM = 15
 };
 
 /* Power-iteration modes. */
@@ -189,6 +192,31 @@ gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k,
                            float sigma, int64_t *row_ptr, int32_t *col, float *val,
                            int64_t *nnz, void *ws, size_t ws_bytes, void *stream);
 
+/* Symmetric storage ("packed upper tiles") of the affinity: A is symmetric
+ * (section "Spectral Cluster"), so only its upper block triangle is kept and
+ * the power iteration applies W v = D^-1 (A v), streaming 2 n^2 bytes per
+ * product instead of the 4 n^2 of a dense W.  Layout: the indices are cut
+ * into nb = ceil(n / 256) blocks of 256; tile (I, J), I <= J, is a float32
+ * [256 x 256] row-major array holding A[256 I + r][256 J + c], and the
+ * tiles are stored one after the other in the order (0,0), (0,1), ..,
+ * (0,nb-1), (1,1), .., (nb-1,nb-1).  Diagonal tiles hold the whole block
+ * (zero diagonal).  Entries outside [0, n)^2 are never written or read.
+ * gpic_sym_bytes(n): bytes of that storage (0 for n out of range). */
+size_t gpic_sym_bytes(int64_t n);
+
+/* Affinity A into the symmetric storage As (gpic_sym_bytes(n) bytes,
+ * 16-byte aligned, caller-allocated), with the degrees
+ * d_i = sum_j A_ij (float64, summed over whole rows from the same float32
+ * values the dense path computes), v0 = d / sum(d) and the zero-degree row
+ * count (as gpic_affinity_normalized; GPIC_ERR_NUMERIC when sum(D) is zero
+ * or not finite, a check that synchronises the stream).  Stored entries are
+ * the upper ones: A_ij as computed for row i, for block(i) <= block(j).
+ * ws: gpic_workspace_bytes(GPIC_OP_AFFINITY_SYM, n, 0, 0). */
+gpic_status gpic_affinity_sym(const float *X, int64_t n, int32_t d, float sigma,
+                              float *As, double *degree, double *v0,
+                              int64_t *n_zero_rows, void *ws, size_t ws_bytes,
+                              void *stream);
+
 /* --------------------------------- 2. degrees, W = D^-1 A, v0 = D / sum D */
 
 /* Dense, in place: A becomes W (row i times r_i = float32(1 / d_i)).  If degree_given
@@ -227,6 +255,14 @@ gpic_status gpic_degree_fused(const float *X, int64_t n, int32_t d,
 gpic_status gpic_matvec_dense(const float *W, int64_t n, int64_t ldw,
                               const double *v, double *y, void *stream);
 
+/* One product y_i = (sum_j A_ij v_j) / d_i over the symmetric storage As
+ * (see gpic_sym_bytes; y_i = 0 for d_i = 0), accumulated in float64 in a
+ * fixed order.  ws: gpic_workspace_bytes(GPIC_OP_MATVEC_SYM, n, 0, 0)
+ * (the per-tile partial sums, nb^2 * 256 float64).  Asynchronous. */
+gpic_status gpic_matvec_sym(const float *As, int64_t n, const double *degree,
+                            const double *v, double *y, void *ws, size_t ws_bytes,
+                            void *stream);
+
 /* One product over a CSR W.  Asynchronous. */
 gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
                             const float *val, int64_t n, int64_t nnz,
@@ -256,6 +292,14 @@ gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
                                      const gpic_pi_params *params, double *v,
                                      double *delta, void *ws, size_t ws_bytes,
                                      gpic_pi_result *res, void *stream);
+
+/* The same loop over the symmetric storage As with the degrees d (both
+ * from gpic_affinity_sym): each update's product is y = D^-1 (A v).
+ * ws: gpic_workspace_bytes(GPIC_OP_PI_SYM, n, 0, 0). */
+gpic_status gpic_power_iterate_sym(const float *As, int64_t n, const double *degree,
+                                   const gpic_pi_params *params, double *v,
+                                   double *delta, void *ws, size_t ws_bytes,
+                                   gpic_pi_result *res, void *stream);
 
 /* The same loop with the fused operator (A recomputed every update from X,
  * sigma, and the degrees from gpic_degree_fused).

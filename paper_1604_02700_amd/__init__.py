@@ -29,7 +29,8 @@ STATUS = {0: "GPIC_OK", 1: "GPIC_ERR_INVALID_ARG", 2: "GPIC_ERR_WORKSPACE",
 OP = {"affinity": 0, "degree_normalize": 1, "degree_normalize_csr": 2,
       "degree_fused": 3, "pi_dense": 4, "pi_fused": 5, "pi_csr": 6,
       "kmeans1d": 7, "affinity_normalized": 8, "matvec_fused": 9,
-      "affinity_cosine": 10, "affinity_cosine_normalized": 11, "knn_graph": 12}
+      "affinity_cosine": 10, "affinity_cosine_normalized": 11, "knn_graph": 12,
+      "affinity_sym": 13, "matvec_sym": 14, "pi_sym": 15}
 MODES = {"fixed": 0, "converge": 1}
 
 # C entry points declared in include/gpic.h (checked by the tests)
@@ -41,6 +42,7 @@ EXPORTS = (
     "gpic_matvec_csr", "gpic_matvec_fused", "gpic_power_iterate_dense",
     "gpic_power_iterate_fused", "gpic_power_iterate_csr", "gpic_kmeans1d",
     "gpic_affinity_cosine", "gpic_affinity_cosine_normalized", "gpic_knn_graph",
+    "gpic_sym_bytes", "gpic_affinity_sym", "gpic_matvec_sym", "gpic_power_iterate_sym",
 )
 
 
@@ -80,6 +82,8 @@ def lib() -> C.CDLL:
         L.gpic_last_error.restype = C.c_char_p
         L.gpic_workspace_bytes.restype = sz
         L.gpic_workspace_bytes.argtypes = [i32, i64, i64, i32]
+        L.gpic_sym_bytes.restype = sz
+        L.gpic_sym_bytes.argtypes = [i64]
         sigs = {
             "gpic_affinity": [p, i64, i32, f32, p, i64, p, p, sz, p],
             "gpic_affinity_normalized": [p, i64, i32, f32, p, i64, p, p, p, p, sz, p],
@@ -92,6 +96,10 @@ def lib() -> C.CDLL:
             "gpic_matvec_dense": [p, i64, i64, p, p, p],
             "gpic_matvec_csr": [p, p, p, i64, i64, p, p, p],
             "gpic_matvec_fused": [p, i64, i32, f32, p, p, p, p, sz, p],
+            "gpic_affinity_sym": [p, i64, i32, f32, p, p, p, p, p, sz, p],
+            "gpic_matvec_sym": [p, i64, p, p, p, p, sz, p],
+            "gpic_power_iterate_sym": [p, i64, p, C.POINTER(PiParams), p, p, p, sz,
+                                       C.POINTER(PiResult), p],
             "gpic_power_iterate_dense": [p, i64, i64, C.POINTER(PiParams), p, p, p,
                                          sz, C.POINTER(PiResult), p],
             "gpic_power_iterate_fused": [p, i64, i32, f32, p, C.POINTER(PiParams),
@@ -329,6 +337,45 @@ def gpic_matvec_csr(row_ptr, col, val, v, y=None):
     return y
 
 
+# ------------------------------------------- symmetric (packed upper tiles)
+def sym_bytes(n: int) -> int:
+    """Bytes of the symmetric tile storage of an n x n affinity."""
+    return int(lib().gpic_sym_bytes(int(n)))
+
+
+def gpic_affinity_sym(X: torch.Tensor, sigma: float, As: Optional[torch.Tensor] = None):
+    """A into the packed upper tiles (a flat float32 tensor of sym_bytes(n) / 4
+    entries); returns (As, degree, v0, n_zero_rows tensor)."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    dev = X.device
+    m = sym_bytes(n) // 4
+    if As is None:
+        As = torch.empty(m, dtype=torch.float32, device=dev)
+    _dev(As, torch.float32, "As")
+    if not As.is_contiguous() or As.numel() < m:
+        raise ValueError(f"As must be contiguous with at least {m} entries")
+    degree = torch.empty(n, dtype=torch.float64, device=dev)
+    v0 = torch.empty(n, dtype=torch.float64, device=dev)
+    nz = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws, nb = workspace("affinity_sym", n, device=dev)
+    _check(lib().gpic_affinity_sym(_ptr(X), n, d, float(sigma), _ptr(As), _ptr(degree),
+                                   _ptr(v0), _ptr(nz), _ptr(ws), nb, _stream(dev)))
+    return As, degree, v0, nz
+
+
+def gpic_matvec_sym(As, n, degree, v, y=None):
+    """y = D^-1 (A v) over the symmetric storage."""
+    _dev(As, torch.float32, "As")
+    dev = As.device
+    y = _vec(y, n, "y", dev)
+    ws, nb = workspace("matvec_sym", n, device=dev)
+    _check(lib().gpic_matvec_sym(_ptr(As), int(n), _ptr(degree), _ptr(v), _ptr(y),
+                                 _ptr(ws), nb, _stream(dev)))
+    return y
+
+
 def gpic_matvec_fused(X, sigma, degree, v, y=None):
     _dev(X, torch.float32, "X")
     n, d = X.shape
@@ -385,6 +432,19 @@ def gpic_power_iterate_dense(W, v, delta=None, mode="converge", max_iter=1000, e
     return _run_pi(lib().gpic_power_iterate_dense, (_ptr(W), n, W.stride(0)), n,
                    W.device, v, delta, mode, max_iter, eps, check_every, record_stats,
                    "pi_dense")
+
+
+def gpic_power_iterate_sym(As, n, degree, v, delta=None, mode="converge", max_iter=1000,
+                           eps=0.0, check_every=0, record_stats=True):
+    """Algorithm 1's loop over the symmetric storage (y = D^-1 (A v))."""
+    _dev(As, torch.float32, "As")
+    dev = As.device
+    _vec(v, n, "v", dev)
+    _vec(degree, n, "degree", dev)
+    if delta is not None:
+        _vec(delta, n, "delta", dev)
+    return _run_pi(lib().gpic_power_iterate_sym, (_ptr(As), int(n), _ptr(degree)), n, dev,
+                   v, delta, mode, max_iter, eps, check_every, record_stats, "pi_sym")
 
 
 def gpic_power_iterate_fused(X, sigma, degree, v, delta=None, mode="fixed", max_iter=30,
@@ -464,6 +524,18 @@ def pic_dense(X, sigma, k, mode="converge", max_iter=1000, eps=0.0, check_every=
         W, deg, v0, nz = gpic_degree_normalize(A, n, deg, degree_given=True)
     v = v0.clone()
     pi = gpic_power_iterate_dense(W, v, None, mode, max_iter, eps, check_every, n=n)
+    km = gpic_kmeans1d(pi.v, k)
+    return PICOut(deg, v0, pi, km, int(nz.item()))
+
+
+def pic_sym(X, sigma, k, mode="converge", max_iter=1000, eps=0.0, check_every=0,
+            As: Optional[torch.Tensor] = None) -> PICOut:
+    """The dense path over the symmetric storage: A's upper tiles, the
+    degrees and v0, the power iteration with y = D^-1 (A v), k-means."""
+    n = X.shape[0]
+    As, deg, v0, nz = gpic_affinity_sym(X, sigma, As)
+    v = v0.clone()
+    pi = gpic_power_iterate_sym(As, n, deg, v, None, mode, max_iter, eps, check_every)
     km = gpic_kmeans1d(pi.v, k)
     return PICOut(deg, v0, pi, km, int(nz.item()))
 

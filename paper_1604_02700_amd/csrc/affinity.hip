@@ -31,7 +31,11 @@
 //   kStoreW: write W_ij = A_ij * r_i, r_i = float32(1 / d_i), given d,
 //   kApply : y_i = (sum_j A_ij v_j) / d_i (the Multiply step with the
 //            affinity recomputed; W = D^-1 A is never stored),
-//   kDegree: d_i = sum_j A_ij with nothing of size n^2 written.
+//   kDegree: d_i = sum_j A_ij with nothing of size n^2 written,
+//   kStoreSym: write A (float32) into the packed upper tiles of the
+//            symmetric storage (tiles (I, J), I <= J, of 256 x 256: see
+//            sym.hip); only column tiles at or right of the row's block are
+//            computed, and the storage's tile count nb comes in place of lda.
 // Every mode evaluates the same float32 A_ij and sums rows in the same
 // order, so kDegree reproduces kStore's degrees bit for bit and kStoreW
 // writes exactly what kStore followed by the row scaling writes.
@@ -42,7 +46,7 @@
 namespace gpic {
 namespace {
 
-enum { kStore = 0, kApply = 1, kDegree = 2, kStoreW = 3 };
+enum { kStore = 0, kApply = 1, kDegree = 2, kStoreW = 3, kStoreSym = 4 };
 enum { kGauss = 0, kCosine = 1 };             // affinity kind (VALU engine)
 
 constexpr int kThreads = 256;
@@ -54,6 +58,15 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 // exp2 on the transcendental unit (1 ulp; results below the smallest
 // normal float flush to zero, far below anything a row sum can notice)
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Address of entry (i, j), i <= j rounded to blocks of 256, in the packed
+// upper tiles of the symmetric storage (nb blocks; see sym.hip).
+__device__ __forceinline__ float *sym_entry(float *As, int64_t i, int64_t j, int64_t nb)
+{
+    const int64_t I = i >> 8, J = j >> 8;
+    const int64_t t = I * nb - I * (I - 1) / 2 + (J - I);
+    return As + t * 65536 + (i & 255) * 256 + (j & 255);
+}
 
 // Plain (cached) stores: measured on MI355X, non-temporal stores of this
 // 16-rows-by-64-bytes pattern reach only about 60 % of the bandwidth of
@@ -242,7 +255,7 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     constexpr int NT = W * 64;
     constexpr int kSlots = NCH * 8;              // (chunk, part, lane group)
     constexpr int kQ = TC / 16;                  // 16-column blocks per tile
-    constexpr bool kWrites = (MODE == kStore || MODE == kStoreW);
+    constexpr bool kWrites = (MODE == kStore || MODE == kStoreW || MODE == kStoreSym);
     constexpr int kOutStride = TC + 4;
     static_assert(!kWrites || RB == 1, "one staged output tile per wave");
     __shared__ half8 xs[2][kSlots * TC];
@@ -262,8 +275,17 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     const int g = lane >> 4;
     const int m = lane & 15;
     const int64_t wrow0 = ((int64_t)blockIdx.x * W + wave) * (16 * RB);
-    const int64_t c0 = (int64_t)blockIdx.y * chunk_cols;
+    int64_t c0 = (int64_t)blockIdx.y * chunk_cols;
     const int64_t c1 = (c0 + chunk_cols < n) ? c0 + chunk_cols : n;
+    if (MODE == kStoreSym) {
+        // the workgroup's rows lie in one block of 256: only the tiles at
+        // or right of the diagonal tile are stored
+        const int64_t cs = (((int64_t)blockIdx.x * W * 16 * RB) >> 8) << 8;
+        if (cs > c0)
+            c0 = cs;
+        if (c0 >= c1)
+            return;                                  // uniform over the workgroup
+    }
     const float mm = __uint_as_float(scal[1]);
 
     // B operands: this lane's rows, hi and lo of every chunk
@@ -418,7 +440,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
                     const int64_t jj = jt + cc;
                     const float *src = ot[wave] + rr * kOutStride + cc;
                     if (ii < n) {
-                        float *dst = A + ii * lda + jj;
+                        float *dst = (MODE == kStoreSym) ? sym_entry(A, ii, jj, lda)
+                                                         : A + ii * lda + jj;
                         if (!kMask || jj + 3 < c1) {
                             store4(dst, src[0], src[1], src[2], src[3]);
                         } else {
@@ -456,7 +479,7 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
     }
 
-    if (MODE == kStoreW)
+    if (MODE == kStoreW || MODE == kStoreSym)
         return;
     double yabs = 0.0;
 #pragma unroll
@@ -538,7 +561,10 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
     }
 
     const int64_t ngroups = (n + 3) >> 2;
-    for (int64_t gi = threadIdx.x; gi < ngroups; gi += kThreads) {
+    // kStoreSym: the RB rows lie in one block of 256; columns from that
+    // block's diagonal tile on
+    const int64_t g0 = (MODE == kStoreSym) ? (((row0 >> 8) << 8) >> 2) : 0;
+    for (int64_t gi = g0 + threadIdx.x; gi < ngroups; gi += kThreads) {
         const int64_t j0 = gi << 2;
         float a[RB][4];
         if (D > 0) {
@@ -611,12 +637,12 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
             for (int q = 0; q < 4; ++q)
                 if (i == j0 + q || j0 + q >= n)
                     a[r][q] = 0.0f;
-            if ((MODE == kStore || MODE == kStoreW) && i < n) {
+            if ((MODE == kStore || MODE == kStoreW || MODE == kStoreSym) && i < n) {
                 float o[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     o[q] = (MODE == kStoreW) ? a[r][q] * rs[r] : a[r][q];
-                float *dst = A + i * lda + j0;
+                float *dst = (MODE == kStoreSym) ? sym_entry(A, i, j0, lda) : A + i * lda + j0;
                 if (j0 + 3 < n) {
                     store4(dst, o[0], o[1], o[2], o[3]);
                 } else {
@@ -624,7 +650,7 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
                         dst[q] = o[q];
                 }
             }
-            if (MODE != kStoreW) {
+            if (MODE != kStoreW && MODE != kStoreSym) {
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     acc[r] = fma((double)a[r][q], vj[q], acc[r]);
@@ -632,7 +658,7 @@ __global__ __launch_bounds__(kThreads) void affinity_valu_kernel(
         }
     }
 
-    if (MODE == kStoreW)
+    if (MODE == kStoreW || MODE == kStoreSym)
         return;
     double part = 0.0;
 #pragma unroll
@@ -775,7 +801,8 @@ hipError_t dispatch(const float *X, int64_t n, int d, float c, float *A,
         int64_t chunk_cols;
         int nchunks;
         chunking(n, &chunk_cols, &nchunks);
-        const bool sums = (MODE != kStoreW) && (MODE != kStore || out != nullptr);
+        const bool sums = (MODE != kStoreW) && (MODE != kStoreSym) &&
+                          (MODE != kStore || out != nullptr);
         double *part = (sums && nchunks > 1) ? w.part : nullptr;
 #define GPIC_MFMA(NCH)                                                          \
     launch_engine<NCH, MODE>(w, n, chunk_cols, nchunks, A, lda, v, degree_in, out, \
@@ -912,6 +939,15 @@ hipError_t launch_affinity_w(const float *X, int64_t n, int d, float c,
     StopCtl none{};
     return dispatch<kStoreW>(X, n, d, c, W, ldw, nullptr, degree, nullptr,
                              nullptr, none, 0, ws, s);
+}
+
+hipError_t launch_affinity_sym(const float *X, int64_t n, int d, float c, float *As,
+                               void *ws, hipStream_t s)
+{
+    StopCtl none{};
+    const int64_t nb = (n + 255) / 256;            // tiles per block row (see sym.hip)
+    return dispatch<kStoreSym>(X, n, d, c, As, nb, nullptr, nullptr, nullptr, nullptr,
+                               none, 0, ws, s);
 }
 
 hipError_t launch_fused_degree(const float *X, int64_t n, int d, float c,

@@ -97,6 +97,9 @@ size_t pi_csr_ws(int64_t n, int64_t nnz)
 // the fused product's own scratch follows the power-iteration layout
 size_t pi_fused_ws(int64_t n) { return pi_ws(n, fused_nb_bound(n)) + aff_ws(n); }
 
+// the symmetric product's partial sums follow the power-iteration layout
+size_t pi_sym_ws(int64_t n) { return pi_ws(n, sym_blocks(n)) + al(sym_part_bytes(n)); }
+
 // exp(-x / (2 sigma^2)) = exp2(-c x) with c = log2(e) / (2 sigma^2)
 bool gauss_coefficient(float sigma, float *c)
 {
@@ -247,6 +250,19 @@ struct FusedProduct : Product {
     }
 };
 
+struct SymProduct : Product {
+    const float *As;
+    int64_t n;
+    const double *degree;
+    double *part;
+    int64_t blocks() const override { return sym_blocks(n); }
+    hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
+                      hipStream_t s) const override
+    {
+        return launch_sym_gemv(As, n, degree, v, y, part, partial, ctl, true, s);
+    }
+};
+
 // Algorithm 1's loop on the device; the host only batches launches and
 // reads the statistic slots back every chunk.
 gpic_status run_power_iteration(const Product &op, int64_t n,
@@ -372,6 +388,9 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     case GPIC_OP_AFFINITY_COSINE_NORMALIZED: return start_ws(n) + al(cosine_ws(n));
     case GPIC_OP_KNN_GRAPH:
         return (k >= 1 && k <= 64 && n >= 2) ? al(knn_graph_ws(n, k)) : 0;
+    case GPIC_OP_AFFINITY_SYM: return start_ws(n) + aff_ws(n);
+    case GPIC_OP_MATVEC_SYM: return al(sym_part_bytes(n));
+    case GPIC_OP_PI_SYM: return pi_sym_ws(n);
     default: return 0;
     }
 }
@@ -428,6 +447,42 @@ gpic_status gpic_affinity_normalized(const float *X, int64_t n, int32_t d,
     if (bad)
         return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
     CHECK_HIP(launch_affinity_w(X, n, d, c, W, ldw, degree, aws, s), "W sweep");
+    return GPIC_OK;
+}
+
+size_t gpic_sym_bytes(int64_t n)
+{
+    if (n < 2 || n > kMaxN)
+        return 0;
+    return sym_storage_bytes(n);
+}
+
+gpic_status gpic_affinity_sym(const float *X, int64_t n, int32_t d, float sigma,
+                              float *As, double *degree, double *v0, int64_t *n_zero_rows,
+                              void *ws, size_t ws_bytes, void *stream)
+{
+    gpic_status st = check_points(X, n, d, sigma);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(As != nullptr, "As is null");
+    CHECK_ARG(aligned(As, 16), "As must be 16-byte aligned");
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v0, "v0")) != GPIC_OK)
+        return st;
+    CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
+              "n_zero_rows misaligned");
+    if ((st = check_ws(ws, ws_bytes, start_ws(n) + aff_ws(n))) != GPIC_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    float c;
+    gauss_coefficient(sigma, &c);
+    void *aws = static_cast<char *>(ws) + start_ws(n);
+    CHECK_HIP(launch_fused_degree(X, n, d, c, degree, aws, s), "degree sweep");
+    int bad = 0;
+    CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
+    if (bad)
+        return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
+    CHECK_HIP(launch_affinity_sym(X, n, d, c, As, aws, s), "symmetric A sweep");
     return GPIC_OK;
 }
 
@@ -606,6 +661,25 @@ gpic_status gpic_matvec_dense(const float *W, int64_t n, int64_t ldw,
     return GPIC_OK;
 }
 
+gpic_status gpic_matvec_sym(const float *As, int64_t n, const double *degree,
+                            const double *v, double *y, void *ws, size_t ws_bytes,
+                            void *stream)
+{
+    CHECK_ARG(As != nullptr && aligned(As, 16), "As is null or not 16-byte aligned");
+    CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range", (long long)n);
+    gpic_status st;
+    if ((st = check_vec(degree, "degree")) != GPIC_OK ||
+        (st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
+        return st;
+    if ((st = check_ws(ws, ws_bytes, al(sym_part_bytes(n)))) != GPIC_OK)
+        return st;
+    StopCtl none{};
+    CHECK_HIP(launch_sym_gemv(As, n, degree, v, y, static_cast<double *>(ws), nullptr, none,
+                              false, (hipStream_t)stream),
+              "symmetric product");
+    return GPIC_OK;
+}
+
 gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
                             const float *val, int64_t n, int64_t nnz,
                             const double *v, double *y, void *stream)
@@ -673,6 +747,27 @@ gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
     op.W = W;
     op.n = n;
     op.ldw = ldw;
+    return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
+}
+
+gpic_status gpic_power_iterate_sym(const float *As, int64_t n, const double *degree,
+                                   const gpic_pi_params *params, double *v, double *delta,
+                                   void *ws, size_t ws_bytes, gpic_pi_result *res,
+                                   void *stream)
+{
+    CHECK_ARG(As != nullptr && aligned(As, 16), "As is null or not 16-byte aligned");
+    gpic_status st = check_pi_common(n, params, v, delta, res);
+    if (st != GPIC_OK)
+        return st;
+    if ((st = check_vec(degree, "degree")) != GPIC_OK)
+        return st;
+    if ((st = check_ws(ws, ws_bytes, pi_sym_ws(n))) != GPIC_OK)
+        return st;
+    SymProduct op;
+    op.As = As;
+    op.n = n;
+    op.degree = degree;
+    op.part = reinterpret_cast<double *>(static_cast<char *>(ws) + pi_ws(n, sym_blocks(n)));
     return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
 }
 

@@ -130,6 +130,10 @@ hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c_log2,
                               void *ws, hipStream_t s, bool operands_ready = false);
 // number of |y| partial sums the fused product writes
 int64_t fused_blocks(int64_t n, int d);
+// A into the packed upper tiles of the symmetric storage (sym.hip);
+// ws: affinity_ws(n) bytes
+hipError_t launch_affinity_sym(const float *X, int64_t n, int d, float c_log2,
+                               float *As, void *ws, hipStream_t s);
 // cosine affinity (1 + cos) / 2, zero diagonal -- ws: cosine_ws(n) bytes
 // (reciprocal norms)
 size_t cosine_ws(int64_t n);
@@ -181,6 +185,17 @@ hipError_t launch_tau_update(const double *partial, int64_t nb, double *tau,
 hipError_t launch_init_state(double *ring, int64_t ring_len, int *err,
                              const double *v, double *delta, int64_t n,
                              bool copy_delta, hipStream_t s);
+
+// sym.hip -- y = D^-1 (A v) over the packed upper tiles of a symmetric A:
+// blocks of 256 indices (sym_blocks), storage bytes, the per-product
+// partial sums (sym_part_bytes, caller scratch); two launches, the second
+// writing one |y| partial per block of 256 rows when partial != nullptr
+int64_t sym_blocks(int64_t n);
+size_t sym_storage_bytes(int64_t n);
+size_t sym_part_bytes(int64_t n);
+hipError_t launch_sym_gemv(const float *As, int64_t n, const double *degree,
+                           const double *v, double *y, double *part, double *partial,
+                           StopCtl ctl, bool use_ctl, hipStream_t s);
 
 // spmv_blocked.hip -- column-blocked copy of a CSR W for the product
 struct CsrBlocked {

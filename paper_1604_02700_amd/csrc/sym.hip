@@ -1,0 +1,254 @@
+// Dense product over symmetric tile storage for gfx950: y = D^-1 (A v),
+// the Multiply step of Algorithm 2's loop with W = D^-1 A and the
+// affinity A of section "Spectral Cluster", which is symmetric.  Only the
+// upper block triangle of A is stored, so a product streams 2 n^2 bytes
+// instead of the 4 n^2 bytes of a dense W.
+//
+// Storage ("packed upper tiles"): the indices 0 .. n-1 are cut into
+// nb = ceil(n / 256) blocks of 256; tile (I, J), I <= J, holds
+// A[256 I + r][256 J + c] at r * 256 + c, and the tiles follow each other
+// in the order (0,0), (0,1), .., (0,nb-1), (1,1), .., so tile (I, J)
+// starts at entry 65536 (I nb - I (I - 1) / 2 + J - I).  Diagonal tiles
+// hold the whole block.  Entries outside [0, n)^2 (the last block row and
+// column when 256 does not divide n) are never read.
+//
+// One workgroup per tile.  Tile (I, J) gives the row sums A_IJ v_J to the
+// rows of block I and, when I < J, the column sums A_IJ^T v_I to the rows
+// of block J (A_JI = A_IJ^T), into part[(I nb + J) 256 + r] and
+// part[(J nb + I) 256 + c].  A second launch adds, for every row i of
+// block I, the nb partials part[(I nb + K) 256 + i - 256 I] (four slices
+// of K summed in ascending order, then added in slice order), divides by
+// d_i and writes per-workgroup partial sums of |y_i| for the L1 norm.
+// Every sum runs in a fixed order: bitwise reproducible.
+#include "common.h"
+
+namespace gpic {
+namespace {
+
+constexpr int kTile = 256;                 // tile edge (indices per block)
+constexpr int kThreads = 256;              // one thread per 16 x 16 piece
+constexpr int64_t kTileEntries = (int64_t)kTile * kTile;
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __host__ __forceinline__ int64_t tile_start(int64_t I, int64_t nb)
+{
+    return I * nb - I * (I - 1) / 2;
+}
+
+// (I, J) of the t-th stored tile: I from the quadratic formula, corrected
+// by at most a step either way against rounding.
+__device__ __forceinline__ void tile_of(int64_t t, int64_t nb, int64_t *I, int64_t *J)
+{
+    const double b = (double)(2 * nb + 1);
+    int64_t i = (int64_t)((b - sqrt(b * b - 8.0 * (double)t)) * 0.5);
+    if (i < 0)
+        i = 0;
+    if (i > nb - 1)
+        i = nb - 1;
+    while (i > 0 && tile_start(i, nb) > t)
+        --i;
+    while (i + 1 < nb && tile_start(i + 1, nb) <= t)
+        ++i;
+    *I = i;
+    *J = i + (t - tile_start(i, nb));
+}
+
+// Thread (ty, tx) = (t / 16, t % 16) owns rows 16 ty .. 16 ty + 15 and the
+// columns 64 q + 4 tx + e (q, e = 0..3) of the tile: per row and q the 16
+// lanes of a row group read 256 contiguous bytes (whole cache lines), a
+// wave four rows at a time.  The thread keeps a float64 row partial per
+// row (over its 16 columns, q then e ascending) and a float64 column
+// partial per column (over its 16 rows, ascending).  Row partials are then
+// reduce-scattered over the 16 lanes of a row group, column partials over
+// the 4 row groups of a wave and through LDS over the 4 waves.  EDGE masks
+// entries outside [0, n)^2.
+template <bool EDGE>
+__device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I, int64_t J,
+                                         int64_t n, int64_t nb, const double *vI,
+                                         const double *vJ, double (*cred)[kTile],
+                                         double *__restrict__ part)
+{
+    const int tid = threadIdx.x;
+    const int tx = tid & 15;
+    const int ty = tid >> 4;
+    const int lane = tid % kWave;
+    const int wave = tid / kWave;
+    double vj[16];
+    bool colok[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+        const int col = 64 * (c >> 2) + 4 * tx + (c & 3);
+        vj[c] = vJ[col];
+        colok[c] = !EDGE || (kTile * J + col < n);
+    }
+    double racc[16], cacc[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        racc[k] = cacc[k] = 0.0;
+
+    const floatx4 *base = reinterpret_cast<const floatx4 *>(T) + (16 * ty) * (kTile / 4) + tx;
+#pragma unroll 4
+    for (int k = 0; k < 16; ++k) {
+        const floatx4 *rp = base + k * (kTile / 4);
+        floatx4 w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            w[q] = __builtin_nontemporal_load(rp + 16 * q);
+        const double vi = vI[16 * ty + k];
+        const bool rowok = !EDGE || (kTile * I + 16 * ty + k < n);
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            float af = w[c >> 2][c & 3];
+            if (EDGE && !(rowok && colok[c]))
+                af = 0.0f;
+            const double a = (double)af;
+            racc[k] = fma(a, vj[c], racc[k]);
+            cacc[c] = fma(a, vi, cacc[c]);
+        }
+    }
+
+    // rows: after the steps m = 8, 4, 2, 1 lane tx holds row 16 ty + tx
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) {
+        const bool up = (tx & m) != 0;
+#pragma unroll
+        for (int q = 0; q < m; ++q) {
+            const double send = up ? racc[q] : racc[q + m];
+            const double keep = up ? racc[q + m] : racc[q];
+            racc[q] = keep + __shfl_xor(send, m, kWave);
+        }
+    }
+    part[((I * nb + J) * kTile) + 16 * ty + tx] = racc[0];
+    if (I == J)
+        return;                                  // uniform over the workgroup
+
+    // columns: over the wave's four row groups (lanes 16 and 32 apart) ...
+    const int b1 = (lane >> 5) & 1, b0 = (lane >> 4) & 1;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const double send = b1 ? cacc[q] : cacc[q + 8];
+        const double keep = b1 ? cacc[q + 8] : cacc[q];
+        cacc[q] = keep + __shfl_xor(send, 32, kWave);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const double send = b0 ? cacc[q] : cacc[q + 4];
+        const double keep = b0 ? cacc[q + 4] : cacc[q];
+        cacc[q] = keep + __shfl_xor(send, 16, kWave);
+    }
+    // ... this lane now holds the columns of q = 2 b1 + b0: 64 q + 4 tx + e
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        cred[wave][64 * (2 * b1 + b0) + 4 * tx + e] = cacc[e];
+    __syncthreads();
+    // ... then over the four waves, in wave order
+    const double s = ((cred[0][tid] + cred[1][tid]) + cred[2][tid]) + cred[3][tid];
+    part[((J * nb + I) * kTile) + tid] = s;
+}
+
+__global__ __launch_bounds__(kThreads) void sym_gemv_kernel(
+    const float *__restrict__ As, int64_t n, int64_t nb, const double *__restrict__ v,
+    double *__restrict__ part, StopCtl ctl, int use_ctl)
+{
+    __shared__ double vI[kTile], vJ[kTile];
+    __shared__ double cred[kThreads / kWave][kTile];
+    if (use_ctl) {
+        if (blockIdx.x == 0 && threadIdx.x == 0)
+            *ctl.cur_stat = 0.0;
+        if (stop_reached(ctl))
+            return;
+    }
+    int64_t I, J;
+    tile_of((int64_t)blockIdx.x, nb, &I, &J);
+    const int tid = threadIdx.x;
+    const int64_t gi = kTile * I + tid, gj = kTile * J + tid;
+    vI[tid] = gi < n ? v[gi] : 0.0;
+    vJ[tid] = gj < n ? v[gj] : 0.0;
+    __syncthreads();
+    const float *T = As + (tile_start(I, nb) + (J - I)) * kTileEntries;
+    const bool edge = (kTile * (J + 1) > n);     // J >= I: the last block column
+    if (edge)
+        sym_tile<true>(T, I, J, n, nb, vI, vJ, cred, part);
+    else
+        sym_tile<false>(T, I, J, n, nb, vI, vJ, cred, part);
+}
+
+// y_i = (sum over K of part[(I nb + K) 256 + r]) / d_i; one workgroup of
+// 4 x 256 threads per block of 256 rows: slice s sums K = s, s + 4, ..
+// (eight loads in flight), then the four slices are added in slice order.
+constexpr int kSlices = 4;
+
+__global__ __launch_bounds__(kThreads * kSlices) void sym_finalize_kernel(
+    const double *__restrict__ part, int64_t n, int64_t nb,
+    const double *__restrict__ degree, double *__restrict__ y,
+    double *__restrict__ partial, StopCtl ctl, int use_ctl)
+{
+    __shared__ double sl[kSlices][kThreads];
+    __shared__ double red[kThreads * kSlices / kWave];
+    if (use_ctl && stop_reached(ctl))
+        return;
+    const int r = threadIdx.x % kThreads;
+    const int sidx = threadIdx.x / kThreads;
+    const int64_t I = blockIdx.x;
+    const double *p = part + I * nb * kTile + r;
+    double s = 0.0;
+    int64_t K = sidx;
+    for (; K + 7 * kSlices < nb; K += 8 * kSlices) {
+        double x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            x[u] = p[(K + u * kSlices) * kTile];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            s += x[u];
+    }
+    for (; K < nb; K += kSlices)
+        s += p[K * kTile];
+    sl[sidx][r] = s;
+    __syncthreads();
+    const int64_t i = kTile * I + r;
+    double yabs = 0.0;
+    if (sidx == 0 && i < n) {
+        const double t = ((sl[0][r] + sl[1][r]) + sl[2][r]) + sl[3][r];
+        const double di = degree[i];
+        const double yi = (di == 0.0) ? 0.0 : t / di;
+        y[i] = yi;
+        yabs = fabs(yi);
+    }
+    // every wave takes part; those of slices 1..3 add zeros
+    const double sum = block_sum<kThreads * kSlices>(yabs, red);
+    if (threadIdx.x == 0 && partial != nullptr)
+        partial[blockIdx.x] = sum;
+}
+
+} // namespace
+
+int64_t sym_blocks(int64_t n) { return (n + kTile - 1) / kTile; }
+
+size_t sym_storage_bytes(int64_t n)
+{
+    const int64_t nb = sym_blocks(n);
+    return (size_t)(nb * (nb + 1) / 2) * (size_t)kTileEntries * sizeof(float);
+}
+
+size_t sym_part_bytes(int64_t n)
+{
+    const int64_t nb = sym_blocks(n);
+    return (size_t)(nb * nb * kTile) * sizeof(double);
+}
+
+hipError_t launch_sym_gemv(const float *As, int64_t n, const double *degree,
+                           const double *v, double *y, double *part, double *partial,
+                           StopCtl ctl, bool use_ctl, hipStream_t s)
+{
+    const int64_t nb = sym_blocks(n);
+    hipLaunchKernelGGL(sym_gemv_kernel, dim3((unsigned)(nb * (nb + 1) / 2)), dim3(kThreads),
+                       0, s, As, n, nb, v, part, ctl, use_ctl ? 1 : 0);
+    hipLaunchKernelGGL(sym_finalize_kernel, dim3((unsigned)nb), dim3(kThreads * kSlices), 0,
+                       s, part,
+                       n, nb, degree, y, partial, ctl, use_ctl ? 1 : 0);
+    return hipGetLastError();
+}
+
+} // namespace gpic

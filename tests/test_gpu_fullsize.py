@@ -107,6 +107,25 @@ def test_blobs16d_full_converge(g, blobs16d, blobs16d_oracle):
     assert rel_l1(out.pi.v.cpu().numpy(), conv.v) <= 1e-4
 
 
+def test_blobs16d_full_sym(g, blobs16d, blobs16d_oracle):
+    """The same workload over the symmetric storage (5.06 GB of tiles):
+    T = 50 and to convergence against the oracle."""
+    w, ref = blobs16d, blobs16d_oracle
+    print(f"gpu: blobs16d n={w.n} symmetric storage", flush=True)
+    out = g.pic_sym(_t(w.X), w.sigma, w.k, "fixed", 50)
+    np.testing.assert_allclose(out.degree.cpu().numpy(), ref["deg"], rtol=1e-5)
+    vg = out.pi.v.cpu().numpy()
+    err = rel_l1(vg, ref["fixed"].v)
+    print(f"  rel_l1 = {err:.3e}", flush=True)
+    assert out.pi.iterations == 50 and err <= 1e-4
+    np.testing.assert_allclose(out.pi.stats, ref["fixed"].stats, rtol=1e-3,
+                               atol=1e-3 * w.eps)
+    del out
+    conv = g.pic_sym(_t(w.X), w.sigma, w.k, "converge", 1000, w.eps)
+    assert conv.pi.converged and conv.pi.iterations == ref["conv"].iterations
+    assert rel_l1(conv.pi.v.cpu().numpy(), ref["conv"].v) <= 1e-4
+
+
 def test_blobs64d_full_size_sampled(g, orc):
     """n = 200,000, d = 64, fused operator, T = 30: sampled rows one by one."""
     import workloads

@@ -511,3 +511,113 @@ def test_csr_invalid_structure_rejected(g):
     col = torch.tensor([1, 2, 0, 9], dtype=torch.int32, device=DEV)      # column >= n
     with pytest.raises(g.GpicError):
         g.gpic_degree_normalize_csr(rp, col, val)
+
+
+# ------------------------------------- symmetric storage (packed upper tiles)
+def _unpack_sym(As, n):
+    """Dense float64 n x n matrix from the packed upper tiles (tile (I, J),
+    I <= J, of 256 x 256, row-major; lower tiles mirrored)."""
+    a = As.cpu().numpy()
+    nb = (n + 255) // 256
+    full = np.zeros((nb * 256, nb * 256))
+    t = 0
+    for I in range(nb):
+        for J in range(I, nb):
+            blk = a[t * 65536:(t + 1) * 65536].reshape(256, 256).astype(np.float64)
+            full[256 * I:256 * I + 256, 256 * J:256 * J + 256] = blk
+            if I != J:
+                full[256 * J:256 * J + 256, 256 * I:256 * I + 256] = blk.T
+            t += 1
+    return full[:n, :n]
+
+
+def _upper_mask(n):
+    b = np.arange(n) // 256
+    return b[:, None] <= b[None, :]
+
+
+@pytest.mark.parametrize("n,d", [(2, 2), (255, 3), (256, 2), (300, 16), (513, 64),
+                                 (777, 17), (1000, 2), (130, 140)])
+def test_sym_affinity_equals_dense(g, n, d):
+    """Stored entries are bitwise the dense affinity's (same engine and
+    operands); degrees and v0 equal the dense one-call path's."""
+    X = _pts(n, d, 4000 + n + d, scale=1.4)
+    sigma = np.float32(np.sqrt(d))
+    As, deg, v0, nz = g.gpic_affinity_sym(_t(X), sigma)
+    A, degA = g.gpic_affinity(_t(X), sigma)
+    W1, deg1, v01, _ = g.gpic_affinity_normalized(_t(X), sigma)
+    torch.cuda.synchronize()
+    assert As.numel() * 4 == g.sym_bytes(n)
+    full = _unpack_sym(As, n)
+    Ad = A[:, :n].cpu().numpy().astype(np.float64)
+    up = _upper_mask(n)
+    assert np.array_equal(full[up], Ad[up])
+    assert np.all(np.diag(full) == 0.0)
+    assert torch.equal(deg, deg1) and torch.equal(v0, v01) and torch.equal(deg, degA)
+    assert int(nz.item()) == 0
+
+
+@pytest.mark.parametrize("n", [2, 255, 256, 257, 700, 2050])
+def test_sym_matvec_stage_isolation(g, n):
+    """y = D^-1 (A v) from the stored float32 tiles: only summation order
+    differs from a float64 product with the unpacked matrix."""
+    X = _pts(n, 3, 60 + n)
+    As, deg, v0, _ = g.gpic_affinity_sym(_t(X), 0.9)
+    rng = np.random.default_rng(n)
+    v = rng.random(n)
+    y = g.gpic_matvec_sym(As, n, deg, _t(v)).cpu().numpy()
+    full = _unpack_sym(As, n)
+    ref = (full @ v) / deg.cpu().numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-12)
+    y2 = g.gpic_matvec_sym(As, n, deg, _t(v)).cpu().numpy()
+    assert np.array_equal(y, y2)
+
+
+@pytest.mark.parametrize("name", ["blobs2d", "rings2d"])
+def test_pic_sym_converge_parity(g, orc, name):
+    import workloads
+    w = workloads.make(name)
+    out = g.pic_sym(_t(w.X), w.sigma, w.k, "converge", w.max_iter, w.eps)
+    torch.cuda.synchronize()
+    ref = orc.pic_dense(w.X, w.sigma, w.k, "converge", w.max_iter, w.eps)
+    v = out.pi.v.cpu().numpy()
+    mu = stop_margin(ref.pi.stats, w.eps, ref.pi.iterations)
+    print(f"  sym {name}: iterations gpu={out.pi.iterations} oracle={ref.pi.iterations} "
+          f"margin={mu:.3g} rel_l1={rel_l1(v, ref.pi.v):.3e}", flush=True)
+    assert out.pi.converged and ref.pi.converged
+    assert out.pi.iterations == ref.pi.iterations
+    assert rel_l1(v, ref.pi.v) <= 1e-4
+    np.testing.assert_allclose(out.pi.stats, ref.pi.stats, rtol=1e-3, atol=1e-3 * w.eps)
+    assert out.km.k_eff == ref.km.k_eff == w.k
+    if separation_ok(ref.pi.v, v, ref.km.labels):
+        assert matched_agreement(out.km.labels.cpu().numpy(), ref.km.labels) >= 0.999
+
+
+@pytest.mark.parametrize("n", [3000, 4099])
+def test_pic_sym_fixed_T_parity_16d(g, orc, n):
+    import workloads
+    w = workloads.make("blobs16d", n=n)
+    out = g.pic_sym(_t(w.X), w.sigma, w.k, "fixed", 50)
+    ref = orc.pic_dense(w.X, w.sigma, w.k, "fixed", 50)
+    v = out.pi.v.cpu().numpy()
+    assert out.pi.iterations == 50
+    assert rel_l1(v, ref.pi.v) <= 1e-4
+    np.testing.assert_allclose(out.degree.cpu().numpy(), ref.A_degree, rtol=1e-5)
+    np.testing.assert_allclose(out.pi.stats, ref.pi.stats, rtol=1e-3, atol=1e-3 * w.eps)
+    # resume: 20 + 30 updates equal 50, bitwise
+    As, deg, v0, _ = g.gpic_affinity_sym(_t(w.X), w.sigma)
+    a, da = v0.clone(), v0.clone()
+    g.gpic_power_iterate_sym(As, n, deg, a, da, "fixed", 20)
+    g.gpic_power_iterate_sym(As, n, deg, a, da, "fixed", 30)
+    assert torch.equal(a, out.pi.v)
+
+
+def test_sym_uniform_fixed_point(g):
+    """Pin P3 through the symmetric operator: v = 1/n stops after 2 products."""
+    n = 600
+    X = _pts(n, 2, 34)
+    As, deg, _, _ = g.gpic_affinity_sym(_t(X), 1.0)
+    v = torch.full((n,), 1.0 / n, dtype=torch.float64, device=DEV)
+    out = g.gpic_power_iterate_sym(As, n, deg, v, None, "converge", 100, 1e-9)
+    assert out.converged and out.iterations == 2
+    np.testing.assert_allclose(v.cpu().numpy(), 1.0 / n, rtol=1e-6)
