@@ -92,8 +92,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-converge", action="store_true")
     ap.add_argument("--workload", default="blobs16d",
-                    choices=["blobs16d", "blobs16d_sym", "blobs64d", "knn8d", "knn8d_rcm",
-                             "rings2d", "blobs2d", "moons", "circles3"],
+                    choices=["blobs16d", "blobs16d_sym", "blobs16d_host", "blobs64d", "knn8d",
+                             "knn8d_rcm", "rings2d", "blobs2d", "moons", "circles3"],
                     help="blobs16d is the headline line; the others measure the "
                          "fused, CSR, small dense and cosine (the paper's "
                          "Experiment I shapes) paths")
@@ -115,6 +115,8 @@ def main():
 
     if args.workload == "blobs16d_sym":
         return sym_workload(args)
+    if args.workload == "blobs16d_host":
+        return host_workload(args)
     if args.workload != "blobs16d":
         return other_workload(args)
 
@@ -339,6 +341,46 @@ def sym_workload(args):
                          "frac": round(alg / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                          "avg_launch_ms": round(prod_ms, 5), "bytes_per_launch": alg,
                          "traffic": None}}
+    print(json.dumps(line), flush=True)
+
+
+def host_workload(args):
+    """The headline workload's dense W kept in pinned host memory and
+    streamed to the device in row panels every update (the out-of-core
+    path): a few fixed updates, one JSON line with the PCIe-inclusive rate."""
+    import torch
+    import paper_1604_02700_amd as g
+    import workloads
+
+    dev = torch.device("cuda:0")
+    w = workloads.make("blobs16d", n=args.n if args.n != 50000 else None)
+    n = w.n
+    T = min(args.T, 3)
+    log(f"bench: workload blobs16d, W in pinned host memory, n={n} T={T}")
+    X = torch.from_numpy(w.X).to(dev)
+    W, deg, v0, _ = g.gpic_affinity_normalized(X, w.sigma)
+    Wh = torch.empty(W.shape, dtype=torch.float32, pin_memory=True)
+    Wh.copy_(W)
+    del W
+    torch.cuda.synchronize()
+    v = v0.clone()
+    g.gpic_power_iterate_dense_host(Wh, v, None, "fixed", 1, record_stats=False, n=n)
+    torch.cuda.synchronize()
+    v.copy_(v0)
+    t0 = time.perf_counter()
+    g.gpic_power_iterate_dense_host(Wh, v, None, "fixed", T, record_stats=False, n=n)
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    wbytes = 4.0 * n * n
+    line = {"metric": "blobs16d with W in host memory: power-iteration GB/s of W streamed "
+                      "over PCIe", "value": round(T * wbytes / t / 1e9, 2), "unit": "GB/s",
+            "n_gpus": 1, "steps": T, "warmup": 1, "ms_per_step": round(t * 1e3 / T, 3),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+            "data": "synthetic",
+            "config": {"workload": f"blobs16d: n={n}, dense float32 W ({wbytes / 1e9:.1f} GB) "
+                                   "in pinned host memory, two 64 MiB device panels",
+                       "n": n, "T": T, "storage": "f32, host"},
+            "note": "one step = one update; the W stream crosses PCIe every update"}
     print(json.dumps(line), flush=True)
 
 

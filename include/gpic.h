@@ -76,7 +76,8 @@ enum {
     GPIC_OP_KNN_GRAPH = 12,
     GPIC_OP_AFFINITY_SYM = 13,
     GPIC_OP_MATVEC_SYM = 14,
-    GPIC_OP_PI_SYM = 15
+    GPIC_OP_PI_SYM = 15,
+    GPIC_OP_PI_DENSE_HOST = 16
 };
 
 /* Power-iteration modes. */
@@ -292,6 +293,29 @@ gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
                                      const gpic_pi_params *params, double *v,
                                      double *delta, void *ws, size_t ws_bytes,
                                      gpic_pi_result *res, void *stream);
+
+/* Out-of-core: the same loop over a dense W that stays in HOST memory
+ * (W_host: host pointer, float32 [n x ldw] row-major, ldw >= n; allocate it
+ * pinned, e.g. with hipHostMalloc, so that copies overlap the products).
+ * For a W larger than the device memory: section "Our Approach GPIC"
+ * divides the data into chunks copied to the device one after another;
+ * on 288 GB of HBM every workload here fits, so this path serves larger n.  Every update streams
+ * W to the device in panels of P rows through two staging buffers in ws
+ * (copy of panel k on an internal copy stream, product of panel k-1 on
+ * `stream`); results are bitwise those of gpic_power_iterate_dense.  P is
+ * the largest multiple of 4 whose two buffers (P rows of n floats rounded
+ * up to 4) fit in ws after the power-iteration state:
+ * gpic_workspace_bytes(GPIC_OP_PI_DENSE_HOST, n, 0, 0) gives two 64 MiB
+ * panels; a smaller ws (at least two 4-row panels) gives smaller panels,
+ * a larger one larger panels.  In CONVERGE mode check_every = 0 means 1
+ * here (an update queued past the stop costs a full pass of W over PCIe).
+ * Creates and destroys one stream and four events per call; synchronises
+ * at the end.  Errors: as gpic_power_iterate_dense; WORKSPACE when ws holds
+ * no two 4-row panels. */
+gpic_status gpic_power_iterate_dense_host(const float *W_host, int64_t n, int64_t ldw,
+                                          const gpic_pi_params *params, double *v,
+                                          double *delta, void *ws, size_t ws_bytes,
+                                          gpic_pi_result *res, void *stream);
 
 /* The same loop over the symmetric storage As with the degrees d (both
  * from gpic_affinity_sym): each update's product is y = D^-1 (A v).

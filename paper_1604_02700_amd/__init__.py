@@ -30,7 +30,7 @@ OP = {"affinity": 0, "degree_normalize": 1, "degree_normalize_csr": 2,
       "degree_fused": 3, "pi_dense": 4, "pi_fused": 5, "pi_csr": 6,
       "kmeans1d": 7, "affinity_normalized": 8, "matvec_fused": 9,
       "affinity_cosine": 10, "affinity_cosine_normalized": 11, "knn_graph": 12,
-      "affinity_sym": 13, "matvec_sym": 14, "pi_sym": 15}
+      "affinity_sym": 13, "matvec_sym": 14, "pi_sym": 15, "pi_dense_host": 16}
 MODES = {"fixed": 0, "converge": 1}
 
 # C entry points declared in include/gpic.h (checked by the tests)
@@ -43,6 +43,7 @@ EXPORTS = (
     "gpic_power_iterate_fused", "gpic_power_iterate_csr", "gpic_kmeans1d",
     "gpic_affinity_cosine", "gpic_affinity_cosine_normalized", "gpic_knn_graph",
     "gpic_sym_bytes", "gpic_affinity_sym", "gpic_matvec_sym", "gpic_power_iterate_sym",
+    "gpic_power_iterate_dense_host",
 )
 
 
@@ -100,6 +101,8 @@ def lib() -> C.CDLL:
             "gpic_matvec_sym": [p, i64, p, p, p, p, sz, p],
             "gpic_power_iterate_sym": [p, i64, p, C.POINTER(PiParams), p, p, p, sz,
                                        C.POINTER(PiResult), p],
+            "gpic_power_iterate_dense_host": [p, i64, i64, C.POINTER(PiParams), p, p, p,
+                                              sz, C.POINTER(PiResult), p],
             "gpic_power_iterate_dense": [p, i64, i64, C.POINTER(PiParams), p, p, p,
                                          sz, C.POINTER(PiResult), p],
             "gpic_power_iterate_fused": [p, i64, i32, f32, p, C.POINTER(PiParams),
@@ -432,6 +435,36 @@ def gpic_power_iterate_dense(W, v, delta=None, mode="converge", max_iter=1000, e
     return _run_pi(lib().gpic_power_iterate_dense, (_ptr(W), n, W.stride(0)), n,
                    W.device, v, delta, mode, max_iter, eps, check_every, record_stats,
                    "pi_dense")
+
+
+def gpic_power_iterate_dense_host(W_host, v, delta=None, mode="converge", max_iter=1000,
+                                  eps=0.0, check_every=0, record_stats=True, n=None,
+                                  ws_bytes=None):
+    """Algorithm 1's loop over a dense W kept in host memory (a pinned CPU
+    float32 tensor [n, >= n]), streamed to the device in row panels every
+    update; ws_bytes (default: two 64 MiB panels) sets the panel size."""
+    if not isinstance(W_host, torch.Tensor) or W_host.is_cuda or W_host.dtype != torch.float32:
+        raise TypeError("W_host must be a float32 CPU tensor")
+    if W_host.dim() != 2 or W_host.stride(1) != 1:
+        raise ValueError("W_host must be 2-D with unit column stride")
+    dev = v.device
+    n = W_host.shape[0] if n is None else n
+    _vec(v, n, "v", dev)
+    if delta is not None:
+        _vec(delta, n, "delta", dev)
+    stats = np.zeros(max(int(max_iter), 1)) if record_stats else None
+    p = _params(mode, max_iter, eps, check_every, stats)
+    r = PiResult()
+    nb = workspace_bytes("pi_dense_host", n) if ws_bytes is None else int(ws_bytes)
+    buf = torch.empty(nb + 256, dtype=torch.uint8, device=dev)
+    off = (-buf.data_ptr()) % 256
+    ws = buf[off:off + nb]
+    _check(lib().gpic_power_iterate_dense_host(C.c_void_p(W_host.data_ptr()), n,
+                                               W_host.stride(0), C.byref(p), _ptr(v),
+                                               _ptr(delta), _ptr(ws), nb, C.byref(r),
+                                               _stream(dev)))
+    st = stats[: r.iterations].copy() if record_stats else np.zeros(0)
+    return PIOut(v, delta, int(r.iterations), bool(r.converged), float(r.last_stat), st)
 
 
 def gpic_power_iterate_sym(As, n, degree, v, delta=None, mode="converge", max_iter=1000,

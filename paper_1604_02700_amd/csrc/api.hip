@@ -100,6 +100,26 @@ size_t pi_fused_ws(int64_t n) { return pi_ws(n, fused_nb_bound(n)) + aff_ws(n); 
 // the symmetric product's partial sums follow the power-iteration layout
 size_t pi_sym_ws(int64_t n) { return pi_ws(n, sym_blocks(n)) + al(sym_part_bytes(n)); }
 
+// Out-of-core dense path: two staging buffers of P rows (P a multiple of
+// 4, the dense product's rows per workgroup) with a row pitch of n rounded
+// up to 4 floats follow the power-iteration layout.
+constexpr int64_t kHostPanelBytes = 64ll << 20;     // default panel: 64 MiB
+int64_t host_pitch(int64_t n) { return (n + 3) & ~(int64_t)3; }
+size_t host_panel_bytes(int64_t n, int64_t P) { return al((size_t)(P * host_pitch(n)) * 4); }
+int64_t host_default_rows(int64_t n)
+{
+    int64_t P = kHostPanelBytes / (host_pitch(n) * 4) / 4 * 4;
+    const int64_t all = (n + 3) & ~(int64_t)3;
+    if (P < 4)
+        P = 4;
+    return P < all ? P : all;
+}
+size_t pi_host_base(int64_t n) { return pi_ws(n, gemv_blocks(n)); }
+size_t pi_host_ws(int64_t n)
+{
+    return pi_host_base(n) + 2 * host_panel_bytes(n, host_default_rows(n));
+}
+
 // exp(-x / (2 sigma^2)) = exp2(-c x) with c = log2(e) / (2 sigma^2)
 bool gauss_coefficient(float sigma, float *c)
 {
@@ -263,6 +283,69 @@ struct SymProduct : Product {
     }
 };
 
+// Out-of-core product: W stays in host memory and every product streams it
+// to the device in panels of P rows, alternating between two staging
+// buffers: panel k is copied on a copy stream (waiting until the product
+// that last read its buffer is done) and multiplied on the caller's stream
+// (waiting for its copy), so the copy of one panel overlaps the product of
+// the previous one.  Each panel's product writes its rows of y and its
+// workgroups' |y| partials at their whole-matrix positions, so the results
+// are bitwise those of the device-resident dense product.
+struct HostDenseProduct : Product {
+    const float *Wh;                 // host
+    int64_t n, ldw, P, pitch;
+    float *buf[2];
+    hipStream_t cs;
+    hipEvent_t copied[2], consumed[2];
+    mutable int64_t seq = 0;         // panels issued so far
+    int64_t blocks() const override { return gemv_blocks(n); }
+    hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
+                      hipStream_t s) const override
+    {
+        for (int64_t r0 = 0; r0 < n; r0 += P) {
+            const int64_t rows = (r0 + P < n) ? P : n - r0;
+            const int b = (int)(seq & 1);
+            hipError_t e;
+            if (seq >= 2 && (e = hipStreamWaitEvent(cs, consumed[b], 0)) != hipSuccess)
+                return e;
+            if ((e = hipMemcpy2DAsync(buf[b], (size_t)pitch * 4, Wh + r0 * ldw,
+                                      (size_t)ldw * 4, (size_t)n * 4, (size_t)rows,
+                                      hipMemcpyHostToDevice, cs)) != hipSuccess ||
+                (e = hipEventRecord(copied[b], cs)) != hipSuccess ||
+                (e = hipStreamWaitEvent(s, copied[b], 0)) != hipSuccess ||
+                (e = launch_gemv_panel(buf[b], rows, n, pitch, v, y + r0, partial + r0 / 4,
+                                       ctl, true, s)) != hipSuccess ||
+                (e = hipEventRecord(consumed[b], s)) != hipSuccess)
+                return e;
+            ++seq;
+        }
+        return hipSuccess;
+    }
+};
+
+// the copy stream and events of one out-of-core call, released on return
+struct HostStreams {
+    hipStream_t cs = nullptr;
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    hipError_t create()
+    {
+        hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+        for (int i = 0; i < 4 && e == hipSuccess; ++i)
+            e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
+        return e;
+    }
+    ~HostStreams()
+    {
+        if (cs != nullptr)
+            (void)hipStreamSynchronize(cs);
+        for (hipEvent_t e : ev)
+            if (e != nullptr)
+                (void)hipEventDestroy(e);
+        if (cs != nullptr)
+            (void)hipStreamDestroy(cs);
+    }
+};
+
 // Algorithm 1's loop on the device; the host only batches launches and
 // reads the statistic slots back every chunk.
 gpic_status run_power_iteration(const Product &op, int64_t n,
@@ -391,6 +474,7 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     case GPIC_OP_AFFINITY_SYM: return start_ws(n) + aff_ws(n);
     case GPIC_OP_MATVEC_SYM: return al(sym_part_bytes(n));
     case GPIC_OP_PI_SYM: return pi_sym_ws(n);
+    case GPIC_OP_PI_DENSE_HOST: return (n >= 2 && n <= kMaxN) ? pi_host_ws(n) : 0;
     default: return 0;
     }
 }
@@ -748,6 +832,55 @@ gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
     op.n = n;
     op.ldw = ldw;
     return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
+}
+
+gpic_status gpic_power_iterate_dense_host(const float *W_host, int64_t n, int64_t ldw,
+                                          const gpic_pi_params *params, double *v,
+                                          double *delta, void *ws, size_t ws_bytes,
+                                          gpic_pi_result *res, void *stream)
+{
+    CHECK_ARG(W_host != nullptr && aligned(W_host, 4), "W_host is null or misaligned");
+    gpic_status st = check_pi_common(n, params, v, delta, res);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(ldw >= n, "ldw must be >= n");
+    const size_t base = pi_host_base(n);
+    CHECK_ARG(ws != nullptr && aligned(ws, 256), "workspace is null or not 256-byte aligned");
+    if (ws_bytes < base + 2 * host_panel_bytes(n, 4))
+        return fail(GPIC_ERR_WORKSPACE, "workspace of %zu bytes holds no two 4-row panels "
+                    "(need at least %zu)", ws_bytes, base + 2 * host_panel_bytes(n, 4));
+    // the panel: the largest multiple of 4 rows whose two buffers fit
+    int64_t P = (int64_t)((ws_bytes - base) / 2 / 256 * 256 / 4) / host_pitch(n) / 4 * 4;
+    const int64_t all = (n + 3) & ~(int64_t)3;
+    if (P > all)
+        P = all;
+    while (P > 4 && base + 2 * host_panel_bytes(n, P) > ws_bytes)
+        P -= 4;
+    if (P < 4)
+        P = 4;                                   // the size check above allows 4
+    HostStreams hs;
+    CHECK_HIP(hs.create(), "copy stream");
+    HostDenseProduct op;
+    op.Wh = W_host;
+    op.n = n;
+    op.ldw = ldw;
+    op.P = P;
+    op.pitch = host_pitch(n);
+    char *w = static_cast<char *>(ws) + base;
+    op.buf[0] = reinterpret_cast<float *>(w);
+    op.buf[1] = reinterpret_cast<float *>(w + host_panel_bytes(n, P));
+    op.cs = hs.cs;
+    op.copied[0] = hs.ev[0];
+    op.copied[1] = hs.ev[1];
+    op.consumed[0] = hs.ev[2];
+    op.consumed[1] = hs.ev[3];
+    // in CONVERGE mode the stop state is read after every update unless the
+    // caller asks otherwise: each update queued past a stop costs a full
+    // pass of W over PCIe
+    gpic_pi_params p = *params;
+    if (p.mode == GPIC_MODE_CONVERGE && p.check_every == 0)
+        p.check_every = 1;
+    return run_power_iteration(op, n, &p, v, delta, ws, res, (hipStream_t)stream);
 }
 
 gpic_status gpic_power_iterate_sym(const float *As, int64_t n, const double *degree,

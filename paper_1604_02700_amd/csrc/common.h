@@ -168,6 +168,10 @@ int64_t spmv_blocks(int64_t n);
 hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
                        double *y, double *partial, StopCtl ctl, bool use_ctl,
                        hipStream_t s);
+// the same over a panel of m rows (n columns): y[0..m), partial[0..m/4)
+hipError_t launch_gemv_panel(const float *W, int64_t m, int64_t n, int64_t ldw,
+                             const double *v, double *y, double *partial, StopCtl ctl,
+                             bool use_ctl, hipStream_t s);
 hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
                        const float *val, int64_t n, const double *v, double *y,
                        double *partial, StopCtl ctl, bool use_ctl,

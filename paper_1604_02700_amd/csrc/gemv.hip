@@ -14,16 +14,17 @@ constexpr int kGemvThreads = 512;   // threads per workgroup of the dense produc
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// Dense product.  A workgroup owns kGemvRows consecutive rows; every thread
+// Dense product over m rows of n columns (m = n for a whole W; m < n for a
+// row panel of it).  A workgroup owns kGemvRows consecutive rows; every thread
 // takes 16-byte column groups c, c + NT, ... and keeps one float64
 // accumulator per row, so each 32-byte slice of v it loads is reused across
 // all rows of the block.  W is streamed exactly once per product, so its
 // loads are non-temporal (they do not displace v, which every workgroup
-// re-reads, from the caches).  Rows past n are clamped for loading and
+// re-reads, from the caches).  Rows past m are clamped for loading and
 // never written.
 template <int R, int NT>
 __global__ __launch_bounds__(NT) void gemv_kernel(
-    const float *__restrict__ W, int64_t n, int64_t ldw,
+    const float *__restrict__ W, int64_t m, int64_t n, int64_t ldw,
     const double *__restrict__ v, double *__restrict__ y,
     double *__restrict__ partial, StopCtl ctl, int use_ctl)
 {
@@ -38,7 +39,7 @@ __global__ __launch_bounds__(NT) void gemv_kernel(
     const floatx4 *rp[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int64_t i = (row0 + r < n) ? row0 + r : n - 1;
+        const int64_t i = (row0 + r < m) ? row0 + r : m - 1;
         rp[r] = reinterpret_cast<const floatx4 *>(W + i * ldw);
     }
     double acc[R];
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(NT) void gemv_kernel(
 #pragma unroll
             for (int w = 0; w < NT / kWave; ++w)
                 t += red[r][w];
-            if (row0 + r < n) {
+            if (row0 + r < m) {
                 y[row0 + r] = t;
                 part += fabs(t);
             }
@@ -108,9 +109,16 @@ hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
                        double *y, double *partial, StopCtl ctl, bool use_ctl,
                        hipStream_t s)
 {
+    return launch_gemv_panel(W, n, n, ldw, v, y, partial, ctl, use_ctl, s);
+}
+
+hipError_t launch_gemv_panel(const float *W, int64_t m, int64_t n, int64_t ldw,
+                             const double *v, double *y, double *partial, StopCtl ctl,
+                             bool use_ctl, hipStream_t s)
+{
     hipLaunchKernelGGL((gemv_kernel<kGemvRows, kGemvThreads>),
-                       dim3((unsigned)gemv_blocks(n)), dim3(kGemvThreads), 0, s, W,
-                       n, ldw, v, y, partial, ctl, use_ctl ? 1 : 0);
+                       dim3((unsigned)gemv_blocks(m)), dim3(kGemvThreads), 0, s, W,
+                       m, n, ldw, v, y, partial, ctl, use_ctl ? 1 : 0);
     return hipGetLastError();
 }
 

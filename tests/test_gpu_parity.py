@@ -621,3 +621,50 @@ def test_sym_uniform_fixed_point(g):
     out = g.gpic_power_iterate_sym(As, n, deg, v, None, "converge", 100, 1e-9)
     assert out.converged and out.iterations == 2
     np.testing.assert_allclose(v.cpu().numpy(), 1.0 / n, rtol=1e-6)
+
+
+# --------------------------------------------- out-of-core dense (host W)
+def _host_copy(W, n):
+    Wh = torch.empty((n, W.shape[1]), dtype=torch.float32, pin_memory=True)
+    Wh.copy_(W[:n].cpu())
+    return Wh
+
+
+@pytest.mark.parametrize("n,rows", [(1003, 12), (3000, 64), (4099, None)])
+def test_dense_host_equals_device(g, n, rows):
+    """W streamed from pinned host memory in row panels gives bitwise the
+    device-resident path's v, statistics and stop update."""
+    import workloads
+    w = workloads.make("blobs16d", n=n)
+    W, deg, v0, _ = g.gpic_affinity_normalized(_t(w.X), w.sigma)
+    torch.cuda.synchronize()
+    Wh = _host_copy(W, n)
+    ws_bytes = None
+    if rows is not None:
+        pitch = (n + 3) // 4 * 4
+        panel = (rows * pitch * 4 + 255) // 256 * 256
+        ws_bytes = g.workspace_bytes("pi_dense", n) + 2 * panel
+    a = v0.clone()
+    ra = g.gpic_power_iterate_dense(W, a, None, "fixed", 20, n=n)
+    b = v0.clone()
+    rb = g.gpic_power_iterate_dense_host(Wh, b, None, "fixed", 20, ws_bytes=ws_bytes)
+    assert rb.iterations == 20 and torch.equal(a, b)
+    assert np.array_equal(ra.stats, rb.stats)
+    eps = 1e-5 / n
+    a = v0.clone()
+    ra = g.gpic_power_iterate_dense(W, a, None, "converge", 1000, eps, n=n)
+    b = v0.clone()
+    rb = g.gpic_power_iterate_dense_host(Wh, b, None, "converge", 1000, eps,
+                                         ws_bytes=ws_bytes)
+    assert ra.converged and rb.converged and ra.iterations == rb.iterations
+    assert torch.equal(a, b)
+
+
+def test_dense_host_workspace_too_small(g):
+    n = 100
+    Wh = torch.zeros((n, n), dtype=torch.float32, pin_memory=True)
+    v = torch.full((n,), 1.0 / n, dtype=torch.float64, device=DEV)
+    with pytest.raises(g.GpicError) as ei:
+        g.gpic_power_iterate_dense_host(Wh, v, None, "fixed", 1,
+                                        ws_bytes=g.workspace_bytes("pi_dense", n) + 256)
+    assert ei.value.status == 2
