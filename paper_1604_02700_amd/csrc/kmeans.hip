@@ -235,35 +235,44 @@ __global__ __launch_bounds__(kThreads) void first_layer_kernel(
 // Each layer is solved by F-ary divide and conquer: an interval of rows
 // [lo, hi] whose neighbours' optimal split points are known takes F evenly
 // spaced sample rows (all its rows if it has at most F) and computes their
-// leftmost argmins in parallel, each over the interval's bounds
-// [opt(lo-1), opt(hi+1)]; the F+1 gaps between samples are the next
-// level's intervals.  ceil(log_{F+1} n) levels replace the log2 n of a
-// binary split, which matters because every level is a dependent step; in
-// exchange every candidate of a level is scanned by F samples.  F = 64 up
-// to 2^18 rows (few dependent steps), F = 8 above (less redundant work).
+// leftmost argmins in parallel, over the interval's bounds
+// [opt(lo-1), opt(hi+1)] (and j <= r for row r); the F+1 gaps between
+// samples are the next level's intervals.  ceil(log_{F+1} n) levels replace
+// the log2 n of a binary split, which matters because every level is a
+// dependent step.  F = 64 up to 2^18 rows, F = 8 above.
+//
+// All samples of an interval share its candidates, so an interval whose
+// range is long is queued as parts of kChunk candidates, and one wave per
+// part reads each candidate once and evaluates it for every sample (in
+// groups of 8 samples); short ranges are scanned by a thread per sample.
+// Node digits and sample rows use 32-bit arithmetic (n <= 2^30).
 constexpr int kFSmall = 64;
 constexpr int kFLarge = 8;
 constexpr int64_t kFLargeFrom = (int64_t)1 << 18;
 constexpr int kMaxLevels = 16;
 constexpr int kShortScan = 32;        // longer ranges go to the work queue
 constexpr int kChunk = 1024;          // candidates per queued part (16 per lane)
+constexpr int kGroup = 8;             // samples evaluated per pass over a part
 
 // Sample f of interval [lo, hi] (m = hi - lo + 1 rows): every row if m <= F,
-// else lo + (f + 1)(m + 1) / (F + 1) - 1; returns -1 if there is none.
+// else lo + (f + 1)(m + 1) / (F + 1) - 1 (evaluated as (f + 1) a +
+// (f + 1) b / (F + 1) with m + 1 = (F + 1) a + b); -1 if there is none.
 template <int F>
-__device__ __forceinline__ int64_t sample_row(int64_t lo, int64_t hi, int f)
+__device__ __forceinline__ int32_t sample_row(int32_t lo, int32_t hi, int f)
 {
-    const int64_t m = hi - lo + 1;
-    if (m <= F)
-        return (f < m) ? lo + f : -1;
-    return lo + ((int64_t)(f + 1) * (m + 1)) / (F + 1) - 1;
+    const uint32_t m = (uint32_t)(hi - lo + 1);
+    if (m <= (uint32_t)F)
+        return (f < (int)m) ? lo + f : -1;
+    const uint32_t a = (m + 1) / (F + 1), b = (m + 1) % (F + 1);
+    const uint32_t f1 = (uint32_t)(f + 1);
+    return lo + (int32_t)(f1 * a + (f1 * b) / (F + 1)) - 1;
 }
 
 // Interval of node q at level L (digits of q in base F + 1, most significant
 // first, choose the gap between samples); false if the node does not exist.
 template <int F>
-__device__ __forceinline__ bool fary_node(int64_t n, int L, int64_t q, int64_t &lo,
-                                          int64_t &hi)
+__device__ __forceinline__ bool fary_node(int32_t n, int L, uint32_t q, int32_t &lo,
+                                          int32_t &hi)
 {
     int dig[kMaxLevels];
     for (int l = 0; l < L; ++l) {
@@ -276,8 +285,8 @@ __device__ __forceinline__ bool fary_node(int64_t n, int L, int64_t q, int64_t &
         if (hi - lo + 1 <= F)
             return false;                     // a leaf interval has no gaps
         const int c = dig[l];
-        const int64_t nlo = (c == 0) ? lo : sample_row<F>(lo, hi, c - 1) + 1;
-        const int64_t nhi = (c == F) ? hi : sample_row<F>(lo, hi, c) - 1;
+        const int32_t nlo = (c == 0) ? lo : sample_row<F>(lo, hi, c - 1) + 1;
+        const int32_t nhi = (c == F) ? hi : sample_row<F>(lo, hi, c) - 1;
         lo = nlo;
         hi = nhi;
         if (lo > hi)
@@ -328,15 +337,14 @@ __device__ __forceinline__ void wave_argmin(double &best, int64_t &arg)
     }
 }
 
-// Row r of interval [lo, hi]: candidate split points [alo, ahi].
-__device__ __forceinline__ void row_bounds(const int32_t *__restrict__ opt, int64_t n,
-                                           int64_t lo, int64_t hi, int64_t r,
-                                           int64_t &alo, int64_t &ahi)
+// Candidate bounds of interval [lo, hi]: [alo, ohi]; row r takes j <= r.
+__device__ __forceinline__ void interval_bounds(const int32_t *__restrict__ opt, int32_t n,
+                                                int32_t lo, int32_t hi, int32_t &alo,
+                                                int32_t &ohi)
 {
-    const int64_t olo = (lo > 0) ? (int64_t)opt[lo - 1] : 1;
-    const int64_t ohi = (hi < n - 1) ? (int64_t)opt[hi + 1] : n - 1;
+    const int32_t olo = (lo > 0) ? opt[lo - 1] : 1;
+    ohi = (hi < n - 1) ? opt[hi + 1] : n - 1;
     alo = olo < 1 ? 1 : olo;
-    ahi = ohi < r ? ohi : r;
 }
 
 __device__ __forceinline__ void store_result(double *__restrict__ Dcur,
@@ -347,56 +355,62 @@ __device__ __forceinline__ void store_result(double *__restrict__ Dcur,
     opt[r] = (int32_t)((arg == INT64_MAX) ? alo : arg);
 }
 
-// A queued part: candidates [alo, ahi] of row r; head is the slot of the
-// row's first part (its part count lives there).  r < 0
-// marks a slot that holds no work.
+// A queued part: candidates [plo, phi] of interval [lo, hi] with bounds
+// [alo, ohi]; head is the slot of the interval's first part (its part count
+// lives there).  lo < 0 marks a slot that holds no work.
 struct QueuePart {
-    int32_t r, alo, ahi, head;
+    int32_t lo, hi, plo, phi, alo, ohi, head, pad;
 };
 
 struct LevelQueue {
     QueuePart *part;
     int32_t *nparts;                     // indexed by head
-    int32_t *heads;                      // heads of rows with more than one part
-    double *pbest;                       // per part
+    int32_t *heads;                      // heads of intervals with more than one part
+    double *pbest;                       // per part and sample: [e * F + f]
     int32_t *parg;
-    unsigned long long *qlen;            // parts: [g & 1]; rows: [2 + (g & 1)]
+    unsigned long long *qlen;            // parts: [g & 1]; intervals: [2 + (g & 1)]
     int64_t cap;
 };
 
-// One recursion level: a thread per (node, sample).  A short range is
-// scanned by the thread itself; a long one is cut into parts of kChunk
-// candidates appended to the queue (the order of appends does not matter:
-// every row's parts are merged by an order-independent minimum).  Item 0
-// clears the other pair of counters, whose level has finished.
+// One recursion level: a thread per (node, sample); the F threads of a
+// node sit in one wave (F divides 64).  Sample 0 of a node whose range is
+// long reserves the node's parts (the order of appends does not matter:
+// every row's minimum is order-independent); otherwise, or when the queue
+// is full, every sample thread scans its own row.  Item 0 clears the other
+// pair of counters, whose level has finished.
 template <int F>
 __global__ __launch_bounds__(kThreads) void fary_level_kernel(
     const double *__restrict__ S1, const double *__restrict__ S2,
     const int32_t *__restrict__ run, const double *__restrict__ Dprev,
-    double *__restrict__ Dcur, int32_t *__restrict__ opt, int64_t n, int L,
+    double *__restrict__ Dcur, int32_t *__restrict__ opt, int32_t n, int L,
     int64_t items, LevelQueue Q, int g)
 {
+    static_assert(kWave % F == 0, "a node's samples share a wave");
     const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (item == 0) {
         Q.qlen[(g + 1) & 1] = 0ull;
         Q.qlen[2 + ((g + 1) & 1)] = 0ull;
     }
-    int64_t lo = 0, hi = -1, r = -1, alo = 1, ahi = 0;
-    if (item < items && fary_node<F>(n, L, item / F, lo, hi)) {
-        r = sample_row<F>(lo, hi, (int)(item % F));
-        if (r >= 0)
-            row_bounds(opt, n, lo, hi, r, alo, ahi);
+    const int f = (int)(item % F);
+    int32_t lo = 0, hi = -1, r = -1, alo = 1, ohi = 0;
+    bool has = item < items && fary_node<F>(n, L, (uint32_t)(item / F), lo, hi);
+    int64_t len = 0;
+    if (has) {
+        r = sample_row<F>(lo, hi, f);
+        interval_bounds(opt, n, lo, hi, alo, ohi);
+        const int32_t rlast = (hi - lo + 1 <= F) ? hi : sample_row<F>(lo, hi, F - 1);
+        len = (int64_t)(ohi < rlast ? ohi : rlast) - alo + 1;
     }
-    const int64_t len = ahi - alo + 1;
-    // long ranges: reserve parts; up to 64 parts are written by their own
-    // thread, more by the whole wave, one such lane after the other
-    bool queued = false;
+    // the node's leader (sample 0) reserves its parts
+    const int lane = threadIdx.x % kWave;
+    const int leader = lane - f;
     int64_t e0 = 0, C = 0;
-    if (r >= 0 && len > kShortScan) {
+    int ok = 0;
+    if (has && f == 0 && len > kShortScan) {
         C = (len + kChunk - 1) / kChunk;
         e0 = (int64_t)atomicAdd(&Q.qlen[g & 1], (unsigned long long)C);
-        queued = e0 + C <= Q.cap;
-        if (queued) {
+        ok = e0 + C <= Q.cap;
+        if (ok) {
             Q.nparts[e0] = (int32_t)C;
             if (C > 1) {
                 const unsigned long long h = atomicAdd(&Q.qlen[2 + (g & 1)], 1ull);
@@ -404,99 +418,150 @@ __global__ __launch_bounds__(kThreads) void fary_level_kernel(
             }
         } else {
             // no room left (only if split points were far from monotone):
-            // void the reserved slots below the capacity and scan here
+            // void the reserved slots below the capacity; the samples scan
             for (int64_t e = e0; e < e0 + C && e < Q.cap; ++e)
-                Q.part[e] = QueuePart{-1, 0, -1, 0};
+                Q.part[e] = QueuePart{-1, 0, 0, -1, 0, 0, 0, 0};
         }
     }
-    if (queued && C <= kWave) {
+    const bool queued = __shfl(ok, leader, kWave) != 0;
+    const int32_t aend = alo + (int32_t)len - 1;    // end of the longest sample range
+    if (ok && C <= kWave) {
         for (int64_t p = 0; p < C; ++p) {
-            const int64_t plo = alo + p * kChunk;
-            const int64_t phi = plo + kChunk - 1 < ahi ? plo + kChunk - 1 : ahi;
-            Q.part[e0 + p] = QueuePart{(int32_t)r, (int32_t)plo, (int32_t)phi,
-                                       (int32_t)e0};
+            const int32_t plo = alo + (int32_t)(p * kChunk);
+            const int32_t phi = plo + kChunk - 1 < aend ? plo + kChunk - 1 : aend;
+            Q.part[e0 + p] = QueuePart{lo, hi, plo, phi, alo, ohi, (int32_t)e0, 0};
         }
     }
-    const int lane = threadIdx.x % kWave;
-    unsigned long long mask = __ballot(queued && C > kWave);
+    unsigned long long mask = __ballot(ok && C > kWave);
     while (mask) {
         const int src = __ffsll((long long)mask) - 1;
         mask &= mask - 1;
         const long long qe0 = __shfl((long long)e0, src, kWave);
         const long long qC = __shfl((long long)C, src, kWave);
-        const long long qr = __shfl((long long)r, src, kWave);
-        const long long qalo = __shfl((long long)alo, src, kWave);
-        const long long qahi = __shfl((long long)ahi, src, kWave);
+        const int qlo = __shfl(lo, src, kWave), qhi = __shfl(hi, src, kWave);
+        const int qalo = __shfl(alo, src, kWave), qohi = __shfl(ohi, src, kWave);
+        const int qend = __shfl(aend, src, kWave);
         for (long long p = lane; p < qC; p += kWave) {
-            const long long plo = qalo + p * kChunk;
-            const long long phi = plo + kChunk - 1 < qahi ? plo + kChunk - 1 : qahi;
-            Q.part[qe0 + p] = QueuePart{(int32_t)qr, (int32_t)plo, (int32_t)phi,
-                                        (int32_t)qe0};
+            const int32_t plo = qalo + (int32_t)(p * kChunk);
+            const int32_t phi = plo + kChunk - 1 < qend ? plo + kChunk - 1 : qend;
+            Q.part[qe0 + p] = QueuePart{qlo, qhi, plo, phi, qalo, qohi, (int32_t)qe0, 0};
         }
     }
     if (r < 0 || queued)
         return;
     double best = INFINITY;
     int64_t arg = INT64_MAX;
-    scan_range(S1, S2, run, Dprev, r, alo, ahi, 1, best, arg);
+    scan_range(S1, S2, run, Dprev, r, alo, ohi < r ? ohi : r, 1, best, arg);
     store_result(Dcur, opt, r, best, arg, alo);
 }
 
-// The level's queued parts: wave w of the grid takes parts w, w + waves, ...
-// and scans each with its 64 lanes.  A row with one part is finished here;
-// otherwise the part leaves its minimum for fary_merge_kernel.
+// The level's queued parts: a wave per (part, group of kGroup samples);
+// its lanes read each candidate of the part once and evaluate it for the
+// group's samples (candidate j counts for row r if j <= r and j <= ohi).  An interval with one part is finished here; otherwise
+// the part leaves each sample's minimum for fary_merge_kernel.
+template <int F>
 __global__ __launch_bounds__(kThreads) void fary_queue_kernel(
     const double *__restrict__ S1, const double *__restrict__ S2,
     const int32_t *__restrict__ run, const double *__restrict__ Dprev,
     double *__restrict__ Dcur, int32_t *__restrict__ opt, LevelQueue Q, int g)
 {
+    constexpr int kGroups = (F + kGroup - 1) / kGroup;
     const int64_t total = (int64_t)Q.qlen[g & 1];
     const int64_t len = total < Q.cap ? total : Q.cap;
     const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
     const int lane = threadIdx.x % kWave;
-    for (int64_t e = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
-         e < len; e += waves) {
+    // work item t: part t / kGroups, samples kGroup (t % kGroups) ..
+    for (int64_t t = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
+         t < len * kGroups; t += waves) {
+        const int64_t e = t / kGroups;
         const QueuePart q = Q.part[e];
-        if (q.r < 0)
+        if (q.lo < 0)
             continue;                                   // uniform per wave
-        double best = INFINITY;
-        int64_t arg = INT64_MAX;
-        scan_range(S1, S2, run, Dprev, q.r, (int64_t)q.alo + lane, q.ahi, kWave, best,
-                   arg);
-        wave_argmin(best, arg);
-        if (lane == 0) {
-            if (Q.nparts[q.head] == 1) {
-                store_result(Dcur, opt, q.r, best, arg, q.alo);
-            } else {
-                Q.pbest[e] = best;
-                Q.parg[e] = (arg == INT64_MAX) ? INT32_MAX : (int32_t)arg;
+        const int m = q.hi - q.lo + 1;
+        const int ns = m < F ? m : F;
+        const bool single = Q.nparts[q.head] == 1;
+        const int g0 = (int)(t % kGroups) * kGroup;
+        if (g0 < ns) {
+            int64_t rr[kGroup], lim[kGroup];
+            double s1e[kGroup], s2e[kGroup], best[kGroup];
+            int64_t arg[kGroup];
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) {
+                rr[u] = (g0 + u < ns) ? (int64_t)sample_row<F>(q.lo, q.hi, g0 + u) : -1;
+                lim[u] = (rr[u] < q.ohi) ? rr[u] : q.ohi;
+                s1e[u] = (rr[u] >= 0) ? S1[rr[u] + 1] : 0.0;
+                s2e[u] = (rr[u] >= 0) ? S2[rr[u] + 1] : 0.0;
+                best[u] = INFINITY;
+                arg[u] = INT64_MAX;
+            }
+            for (int64_t j = (int64_t)q.plo + lane; j <= q.phi; j += kWave) {
+                const double dp = Dprev[j - 1];
+                const double a1 = S1[j], a2 = S2[j];
+                const bool st = run[j] != 0;
+#pragma unroll
+                for (int u = 0; u < kGroup; ++u) {
+                    // the cost of seg_cost(S1, S2, j, rr[u]), term by term
+                    const double mm = (double)(rr[u] - j + 1);
+                    const double s1 = s1e[u] - a1;
+                    const double s2 = s2e[u] - a2;
+                    const double c0 = s2 - s1 * s1 / mm;
+                    const double cst = dp + (c0 > 0.0 ? c0 : 0.0);
+                    const double c = st ? cst : INFINITY;
+                    if (j <= lim[u] && c < best[u]) {
+                        best[u] = c;
+                        arg[u] = j;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) {
+                if (g0 + u >= ns)
+                    break;                                  // uniform per wave
+                wave_argmin(best[u], arg[u]);
+                if (lane == 0) {
+                    if (single) {
+                        store_result(Dcur, opt, rr[u], best[u], arg[u], q.alo);
+                    } else {
+                        Q.pbest[e * F + g0 + u] = best[u];
+                        Q.parg[e * F + g0 + u] =
+                            (arg[u] == INT64_MAX) ? INT32_MAX : (int32_t)arg[u];
+                    }
+                }
             }
         }
     }
 }
 
-// Rows with several parts: a wave per row merges its parts' minima.
+// Intervals with several parts: a wave per (interval, sample) merges the
+// parts' minima in an order-independent leftmost minimum.
+template <int F>
 __global__ __launch_bounds__(kThreads) void fary_merge_kernel(
     double *__restrict__ Dcur, int32_t *__restrict__ opt, LevelQueue Q, int g)
 {
     const int64_t nh = (int64_t)Q.qlen[2 + (g & 1)];
     const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
     const int lane = threadIdx.x % kWave;
-    for (int64_t h = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
-         h < nh; h += waves) {
-        const int64_t head = Q.heads[h];
+    // work item t: interval t / F, sample t % F
+    for (int64_t t = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
+         t < nh * F; t += waves) {
+        const int64_t head = Q.heads[t / F];
+        const int f = (int)(t % F);
         const QueuePart q = Q.part[head];
         const int C = Q.nparts[head];
-        double best = INFINITY;
-        int64_t arg = INT64_MAX;
-        for (int p = lane; p < C; p += kWave) {
-            const int32_t a = Q.parg[head + p];
-            amin_merge(best, arg, Q.pbest[head + p],
-                       a == INT32_MAX ? INT64_MAX : (int64_t)a);
+        const int m = q.hi - q.lo + 1;
+        const int ns = m < F ? m : F;
+        if (f < ns) {
+            double best = INFINITY;
+            int64_t arg = INT64_MAX;
+            for (int p = lane; p < C; p += kWave) {
+                const int32_t a = Q.parg[(head + p) * F + f];
+                amin_merge(best, arg, Q.pbest[(head + p) * F + f],
+                           a == INT32_MAX ? INT64_MAX : (int64_t)a);
+            }
+            wave_argmin(best, arg);
+            if (lane == 0)
+                store_result(Dcur, opt, sample_row<F>(q.lo, q.hi, f), best, arg, q.alo);
         }
-        wave_argmin(best, arg);
-        if (lane == 0)
-            store_result(Dcur, opt, q.r, best, arg, q.alo);
     }
 }
 
@@ -563,11 +628,13 @@ struct KmLayout {
         qpart, qnparts, qheads, qbest, qarg, qlen, sc, first, costs, total;
 };
 
-// Queue slots per level.  With monotone split points the ranges of one
-// level overlap only at their ends, so they hold at most 2 F n candidates
-// and at most n + 2 F n / kChunk parts; a level that would need more
-// scans the excess in place.
-int64_t queue_cap(int64_t n) { return n + (2 * kFSmall * n) / kChunk + 1024; }
+// Queue slots per level.  With monotone split points the interval ranges
+// of one level overlap only at their ends (at most 2n candidates in all)
+// and a queued range is longer than kShortScan, so a level holds at most
+// 2n / kShortScan intervals and 2n / kChunk + 2n / kShortScan parts; a
+// level that would need more scans the excess in place.
+int64_t queue_cap(int64_t n) { return 2 * n / kShortScan + 2 * n / kChunk + 1024; }
+int fary_f(int64_t n) { return (n >= kFLargeFrom) ? kFLarge : kFSmall; }
 
 KmLayout layout(int64_t n, int32_t k)
 {
@@ -598,8 +665,8 @@ KmLayout layout(int64_t n, int32_t k)
     L.qpart = take(cap * sizeof(QueuePart));
     L.qnparts = take(cap * 4);
     L.qheads = take(cap * 4);
-    L.qbest = take(cap * 8);
-    L.qarg = take(cap * 4);
+    L.qbest = take(cap * fary_f(n) * 8);
+    L.qarg = take(cap * fary_f(n) * 4);
     L.qlen = take(4 * 8);
     L.sc = take(sizeof(KmScalars));
     L.first = take((size_t)(k + 1) * 8);
@@ -675,7 +742,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     // 3. layers
     hipLaunchKernelGGL(first_layer_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
                        S1, S2, n, Da, Q.qlen);
-    const int F = (n >= kFLargeFrom) ? kFLarge : kFSmall;
+    const int F = fary_f(n);
     // levels of the F-ary recursion: until every interval has <= F rows
     int levels = 1;
     for (int64_t m = n; m > F; m /= (F + 1))       // gaps hold <= m / (F+1) rows
@@ -690,16 +757,21 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
         for (int Lv = 0; Lv < levels; ++Lv, nodes *= (F + 1), ++g) {
             const int64_t items = nodes * F;
             const dim3 grid((unsigned)((items + kThreads - 1) / kThreads));
-            if (F == kFSmall)
+            if (F == kFSmall) {
                 hipLaunchKernelGGL(fary_level_kernel<kFSmall>, grid, dim3(kThreads), 0, s,
-                                   S1, S2, run, Dprev, Dcur, oc, n, Lv, items, Q, g);
-            else
+                                   S1, S2, run, Dprev, Dcur, oc, (int32_t)n, Lv, items, Q, g);
+                hipLaunchKernelGGL(fary_queue_kernel<kFSmall>, dim3(2048), dim3(kThreads), 0,
+                                   s, S1, S2, run, Dprev, Dcur, oc, Q, g);
+                hipLaunchKernelGGL(fary_merge_kernel<kFSmall>, dim3(512), dim3(kThreads), 0,
+                                   s, Dcur, oc, Q, g);
+            } else {
                 hipLaunchKernelGGL(fary_level_kernel<kFLarge>, grid, dim3(kThreads), 0, s,
-                                   S1, S2, run, Dprev, Dcur, oc, n, Lv, items, Q, g);
-            hipLaunchKernelGGL(fary_queue_kernel, dim3(2048), dim3(kThreads), 0, s, S1,
-                               S2, run, Dprev, Dcur, oc, Q, g);
-            hipLaunchKernelGGL(fary_merge_kernel, dim3(512), dim3(kThreads), 0, s, Dcur,
-                               oc, Q, g);
+                                   S1, S2, run, Dprev, Dcur, oc, (int32_t)n, Lv, items, Q, g);
+                hipLaunchKernelGGL(fary_queue_kernel<kFLarge>, dim3(2048), dim3(kThreads), 0,
+                                   s, S1, S2, run, Dprev, Dcur, oc, Q, g);
+                hipLaunchKernelGGL(fary_merge_kernel<kFLarge>, dim3(512), dim3(kThreads), 0,
+                                   s, Dcur, oc, Q, g);
+            }
         }
         double *tmp = Dprev; Dprev = Dcur; Dcur = tmp;
     }
