@@ -202,6 +202,7 @@ gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k,
  * tiles are stored one after the other in the order (0,0), (0,1), ..,
  * (0,nb-1), (1,1), .., (nb-1,nb-1).  Diagonal tiles hold the whole block
  * (zero diagonal).  Entries outside [0, n)^2 are never written or read.
+ * 2 <= n <= 2^24 for every symmetric entry point (INVALID_ARG otherwise).
  * gpic_sym_bytes(n): bytes of that storage (0 for n out of range). */
 size_t gpic_sym_bytes(int64_t n);
 

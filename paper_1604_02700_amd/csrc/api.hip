@@ -40,6 +40,7 @@ namespace {
 constexpr int64_t kMaxN = 2147483647LL;     // indices are int32 in places
 constexpr int64_t kMaxKmeansN = 1LL << 30;  // keeps the split-point recursion within 5 levels
 constexpr int64_t kRing = 1024;             // statistic slots on the device
+constexpr int64_t kMaxSymN = 1LL << 24;     // one workgroup per stored tile: < 2^31 tiles
 constexpr size_t kCtlBytes = 256;           // err @0, tau @8, csr flag @16
 
 inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -536,7 +537,7 @@ gpic_status gpic_affinity_normalized(const float *X, int64_t n, int32_t d,
 
 size_t gpic_sym_bytes(int64_t n)
 {
-    if (n < 2 || n > kMaxN)
+    if (n < 2 || n > kMaxSymN)
         return 0;
     return sym_storage_bytes(n);
 }
@@ -548,6 +549,8 @@ gpic_status gpic_affinity_sym(const float *X, int64_t n, int32_t d, float sigma,
     gpic_status st = check_points(X, n, d, sigma);
     if (st != GPIC_OK)
         return st;
+    CHECK_ARG(n <= kMaxSymN, "n = %lld exceeds the symmetric storage's limit 2^24",
+              (long long)n);
     CHECK_ARG(As != nullptr, "As is null");
     CHECK_ARG(aligned(As, 16), "As must be 16-byte aligned");
     if ((st = check_vec(degree, "degree")) != GPIC_OK ||
@@ -750,7 +753,7 @@ gpic_status gpic_matvec_sym(const float *As, int64_t n, const double *degree,
                             void *stream)
 {
     CHECK_ARG(As != nullptr && aligned(As, 16), "As is null or not 16-byte aligned");
-    CHECK_ARG(n >= 2 && n <= kMaxN, "n = %lld out of range", (long long)n);
+    CHECK_ARG(n >= 2 && n <= kMaxSymN, "n = %lld out of range [2, 2^24]", (long long)n);
     gpic_status st;
     if ((st = check_vec(degree, "degree")) != GPIC_OK ||
         (st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
@@ -889,6 +892,8 @@ gpic_status gpic_power_iterate_sym(const float *As, int64_t n, const double *deg
                                    void *stream)
 {
     CHECK_ARG(As != nullptr && aligned(As, 16), "As is null or not 16-byte aligned");
+    CHECK_ARG(n <= kMaxSymN, "n = %lld exceeds the symmetric storage's limit 2^24",
+              (long long)n);
     gpic_status st = check_pi_common(n, params, v, delta, res);
     if (st != GPIC_OK)
         return st;

@@ -110,3 +110,47 @@ def test_argument_validation_before_launch(L):
     assert km(dummy, 5, 0, dummy, dummy, C.byref(ke), None, dummy, 1 << 20, None) == 1
     assert km(dummy, 5, 2, dummy, dummy, None, None, dummy, 1 << 20, None) == 1
     assert km(dummy, 5, 2, dummy, dummy, C.byref(ke), None, dummy, 8, None) == 2
+
+
+def test_sym_bytes_limits():
+    """The symmetric storage's size: nb(nb+1)/2 tiles of 256 x 256 float32,
+    nb = ceil(n / 256); 0 outside 2 <= n <= 2^24."""
+    import paper_1604_02700_amd as g
+    for n in (2, 255, 256, 257, 50000):
+        nb = (n + 255) // 256
+        assert g.sym_bytes(n) == nb * (nb + 1) // 2 * 65536 * 4
+    assert g.sym_bytes(1) == 0 and g.sym_bytes((1 << 24) + 1) == 0
+
+
+def test_sym_and_host_validation(L):
+    """The symmetric and out-of-core entry points reject bad arguments on
+    the host before any launch."""
+    import paper_1604_02700_amd as g
+    for op in ("affinity_sym", "matvec_sym", "pi_sym", "pi_dense_host"):
+        a = g.workspace_bytes(op, 1000)
+        b = g.workspace_bytes(op, 100000)
+        assert 0 < a < b
+    dummy = C.c_void_p(4096)
+    W = (dummy, 1 << 30)
+    fa = L.gpic_affinity_sym
+    assert fa(None, 10, 2, 1.0, dummy, dummy, dummy, None, *W, None) == 1      # X null
+    assert fa(dummy, 10, 2, 1.0, None, dummy, dummy, None, *W, None) == 1      # As null
+    assert fa(dummy, 10, 2, 1.0, C.c_void_p(4100), dummy, dummy, None, *W, None) == 1
+    assert fa(dummy, 10, 2, 0.0, dummy, dummy, dummy, None, *W, None) == 1     # sigma
+    assert fa(dummy, (1 << 24) + 1, 2, 1.0, dummy, dummy, dummy, None, *W, None) == 1
+    assert fa(dummy, 10, 2, 1.0, dummy, dummy, dummy, None, dummy, 8, None) == 2
+    mv = L.gpic_matvec_sym
+    assert mv(dummy, 1, dummy, dummy, dummy, *W, None) == 1                   # n < 2
+    assert mv(dummy, 10, None, dummy, dummy, *W, None) == 1                   # degree null
+    assert mv(dummy, 10, dummy, dummy, dummy, dummy, 8, None) == 2            # workspace
+    p = g.PiParams()
+    p.mode, p.max_iter, p.eps, p.check_every, p.reserved = 0, 5, 0.0, 0, 0
+    r = g.PiResult()
+    ps = L.gpic_power_iterate_sym
+    assert ps(dummy, 10, None, C.byref(p), dummy, None, *W, C.byref(r), None) == 1
+    assert ps(dummy, 10, dummy, C.byref(p), dummy, None, dummy, 8, C.byref(r), None) == 2
+    ph = L.gpic_power_iterate_dense_host
+    assert ph(None, 10, 10, C.byref(p), dummy, None, *W, C.byref(r), None) == 1
+    assert ph(dummy, 10, 9, C.byref(p), dummy, None, *W, C.byref(r), None) == 1   # ldw < n
+    small = g.workspace_bytes("pi_dense", 10)
+    assert ph(dummy, 10, 10, C.byref(p), dummy, None, dummy, small, C.byref(r), None) == 2

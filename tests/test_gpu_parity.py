@@ -660,6 +660,23 @@ def test_dense_host_equals_device(g, n, rows):
     assert torch.equal(a, b)
 
 
+def test_dense_host_pageable_memory(g):
+    """W in ordinary (pageable) host memory: slower copies, same bits."""
+    import workloads
+    n = 1500
+    w = workloads.make("rings2d", n=n)
+    W, deg, v0, _ = g.gpic_affinity_normalized(_t(w.X), w.sigma)
+    torch.cuda.synchronize()
+    Wh = W[:n].cpu().contiguous()
+    assert not Wh.is_pinned()
+    a = v0.clone()
+    g.gpic_power_iterate_dense(W, a, None, "fixed", 9, n=n)
+    b = v0.clone()
+    g.gpic_power_iterate_dense_host(Wh, b, None, "fixed", 9,
+                                    ws_bytes=g.workspace_bytes("pi_dense", n) + 2 * 256 * 1024)
+    assert torch.equal(a, b)
+
+
 def test_dense_host_workspace_too_small(g):
     n = 100
     Wh = torch.zeros((n, n), dtype=torch.float32, pin_memory=True)
