@@ -760,9 +760,10 @@ hipError_t launch_split(const float *X, int64_t n, int d, float c, const Ws &w,
     const int64_t np = padded_points(n);
     hipLaunchKernelGGL(split_clear_kernel, dim3(1), dim3(1), 0, s, w.scal);
     const int64_t total = n * (int64_t)d;
+    // few workgroups: each ends with one atomic on the same word
     int64_t blocks = (total + kThreads - 1) / kThreads;
-    if (blocks > 2048)
-        blocks = 2048;
+    if (blocks > 256)
+        blocks = 256;
     hipLaunchKernelGGL(maxabs_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, X,
                        total, w.scal);
     hipLaunchKernelGGL(split_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
