@@ -31,26 +31,28 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 FP16_MFMA_PEAK_TFLOPS = 2500.0       # dense fp16 matrix cores, MI355X
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_traffic_blobs16d_n50000.json")
+SYM_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sym_traffic_blobs16d_n50000.json")
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    with open(os.path.join(ROOT, "paper_1604_02700_amd", "csrc", "gemv.hip"), "rb") as f:
+def kernel_source_hash(source: str = "gemv.hip") -> str:
+    with open(os.path.join(ROOT, "paper_1604_02700_amd", "csrc", source), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(path: str = TRAFFIC_FILE, source: str = "gemv.hip",
+                     key: str = "gemv_hip_sha"):
     """HBM bytes per product launch from the committed rocprofv3 counter
     runs, if they were taken on the current kernel source; else None."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("gemv_hip_sha") != kernel_source_hash():
+    if t.get(key) != kernel_source_hash(source):
         return None
     return t.get("bytes_per_launch")
 
@@ -346,7 +348,8 @@ def sym_workload(args):
                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(alg / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                          "avg_launch_ms": round(prod_ms, 5), "bytes_per_launch": alg,
-                         "traffic": None}}
+                         "traffic": measured_traffic(SYM_TRAFFIC_FILE, "sym.hip",
+                                                     "sym_hip_sha")}}
     print(json.dumps(line), flush=True)
 
 

@@ -26,7 +26,7 @@ namespace gpic {
 namespace {
 
 constexpr int kTile = 256;                 // tile edge (indices per block)
-constexpr int kThreads = 256;              // one thread per 16 x 16 piece
+constexpr int kThreads = 256;              // four waves; a thread covers 32 rows x 8 columns
 constexpr int64_t kTileEntries = (int64_t)kTile * kTile;
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -54,93 +54,100 @@ __device__ __forceinline__ void tile_of(int64_t t, int64_t nb, int64_t *I, int64
     *J = i + (t - tile_start(i, nb));
 }
 
-// Thread (ty, tx) = (t / 16, t % 16) owns rows 16 ty .. 16 ty + 15 and the
-// columns 64 q + 4 tx + e (q, e = 0..3) of the tile: per row and q the 16
-// lanes of a row group read 256 contiguous bytes (whole cache lines), a
-// wave four rows at a time.  The thread keeps a float64 row partial per
-// row (over its 16 columns, q then e ascending) and a float64 column
-// partial per column (over its 16 rows, ascending).  Row partials are then
-// reduce-scattered over the 16 lanes of a row group, column partials over
-// the 4 row groups of a wave and through LDS over the 4 waves.  EDGE masks
-// entries outside [0, n)^2.
+// Thread (ty, tx) = (t / 32, t % 32) owns the columns 128 q + 4 tx + e
+// (q = 0, 1; e = 0..3) of the tile and, in pass p = 0..3, the rows
+// 64 p + 8 ty + k (k = 0..7): per row and q the 32 lanes of a row group
+// read 512 contiguous bytes.  Row partials (over the thread's 8 columns,
+// q then e ascending) are reduce-scattered over the 32 lanes after each
+// pass; column partials (over the thread's 32 rows, ascending) are carried
+// over the passes and reduced once at the end, over the wave's two row
+// groups and through LDS over the 4 waves.  v is read from global memory
+// (it stays in the caches), so the first loads of the tile issue at once.
+// Two rows in flight per step keep the kernel at 126 registers, four
+// workgroups per compute unit.
 template <bool EDGE>
 __device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I, int64_t J,
-                                         int64_t n, int64_t nb, const double *vI,
-                                         const double *vJ, double (*cred)[kTile],
-                                         double *__restrict__ part)
+                                         int64_t n, int64_t nb, const double *__restrict__ v,
+                                         double (*cred)[kTile], double *__restrict__ part)
 {
     const int tid = threadIdx.x;
-    const int tx = tid & 15;
-    const int ty = tid >> 4;
+    const int tx = tid & 31;
+    const int ty = tid >> 5;
     const int lane = tid % kWave;
     const int wave = tid / kWave;
-    double vj[16];
-    bool colok[16];
+    const int64_t cI = kTile * I, cJ = kTile * J;
+    double vj[8];
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-        const int col = 64 * (c >> 2) + 4 * tx + (c & 3);
-        vj[c] = vJ[col];
-        colok[c] = !EDGE || (kTile * J + col < n);
+    for (int c = 0; c < 8; ++c) {
+        const int64_t col = cJ + 128 * (c >> 2) + 4 * tx + (c & 3);
+        vj[c] = (!EDGE || col < n) ? v[col] : 0.0;
     }
-    double racc[16], cacc[16];
+    double cacc[8];
 #pragma unroll
-    for (int k = 0; k < 16; ++k)
-        racc[k] = cacc[k] = 0.0;
-
-    const floatx4 *base = reinterpret_cast<const floatx4 *>(T) + (16 * ty) * (kTile / 4) + tx;
-#pragma unroll 4
-    for (int k = 0; k < 16; ++k) {
-        const floatx4 *rp = base + k * (kTile / 4);
-        floatx4 w[4];
+    for (int c = 0; c < 8; ++c)
+        cacc[c] = 0.0;
+    const floatx4 *base = reinterpret_cast<const floatx4 *>(T) + (8 * ty) * (kTile / 4) + tx;
+    double *prow = part + (I * nb + J) * kTile;
+#pragma unroll 1
+    for (int p = 0; p < 4; ++p) {
+        double racc[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            w[q] = __builtin_nontemporal_load(rp + 16 * q);
-        const double vi = vI[16 * ty + k];
-        const bool rowok = !EDGE || (kTile * I + 16 * ty + k < n);
+        for (int k = 0; k < 8; ++k)
+            racc[k] = 0.0;
+#pragma unroll 2
+        for (int k = 0; k < 8; ++k) {
+            const floatx4 *rp = base + (64 * p + k) * (kTile / 4);
+            const floatx4 w0 = __builtin_nontemporal_load(rp);
+            const floatx4 w1 = __builtin_nontemporal_load(rp + 32);
+            const int64_t row = cI + 64 * p + 8 * ty + k;
+            const bool rowok = !EDGE || row < n;
+            const double vi = rowok ? v[row] : 0.0;
 #pragma unroll
-        for (int c = 0; c < 16; ++c) {
-            float af = w[c >> 2][c & 3];
-            if (EDGE && !(rowok && colok[c]))
-                af = 0.0f;
-            const double a = (double)af;
-            racc[k] = fma(a, vj[c], racc[k]);
-            cacc[c] = fma(a, vi, cacc[c]);
+            for (int c = 0; c < 8; ++c) {
+                float af = (c < 4) ? w0[c & 3] : w1[c & 3];
+                if (EDGE && !(rowok && cJ + 128 * (c >> 2) + 4 * tx + (c & 3) < n))
+                    af = 0.0f;
+                const double a = (double)af;
+                racc[k] = fma(a, vj[c], racc[k]);
+                cacc[c] = fma(a, vi, cacc[c]);
+            }
+        }
+        // rows: after m = 16, 8, 4 lane tx holds row 4 b4 + 2 b3 + b2 of the
+        // group (b = the bits of tx), summed over the 8 lanes sharing those
+        // bits; m = 2, 1 add the remaining 4 lanes
+#pragma unroll
+        for (int m = 16, h = 4; m >= 4; m >>= 1, h >>= 1) {
+            const bool up = (tx & m) != 0;
+#pragma unroll
+            for (int q = 0; q < h; ++q) {
+                const double send = up ? racc[q] : racc[q + h];
+                const double keep = up ? racc[q + h] : racc[q];
+                racc[q] = keep + __shfl_xor(send, m, kWave);
+            }
+        }
+        double rs = racc[0];
+        rs = rs + __shfl_xor(rs, 2, kWave);
+        rs = rs + __shfl_xor(rs, 1, kWave);
+        if ((tx & 3) == 0) {
+            const int r = 4 * ((tx >> 4) & 1) + 2 * ((tx >> 3) & 1) + ((tx >> 2) & 1);
+            prow[64 * p + 8 * ty + r] = rs;
         }
     }
-
-    // rows: after the steps m = 8, 4, 2, 1 lane tx holds row 16 ty + tx
-#pragma unroll
-    for (int m = 8; m >= 1; m >>= 1) {
-        const bool up = (tx & m) != 0;
-#pragma unroll
-        for (int q = 0; q < m; ++q) {
-            const double send = up ? racc[q] : racc[q + m];
-            const double keep = up ? racc[q + m] : racc[q];
-            racc[q] = keep + __shfl_xor(send, m, kWave);
-        }
-    }
-    part[((I * nb + J) * kTile) + 16 * ty + tx] = racc[0];
     if (I == J)
         return;                                  // uniform over the workgroup
 
-    // columns: over the wave's four row groups (lanes 16 and 32 apart) ...
-    const int b1 = (lane >> 5) & 1, b0 = (lane >> 4) & 1;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const double send = b1 ? cacc[q] : cacc[q + 8];
-        const double keep = b1 ? cacc[q + 8] : cacc[q];
-        cacc[q] = keep + __shfl_xor(send, 32, kWave);
-    }
+    // columns: over the wave's two row groups (lanes 32 apart) ...
+    const int b1 = (lane >> 5) & 1;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        const double send = b0 ? cacc[q] : cacc[q + 4];
-        const double keep = b0 ? cacc[q + 4] : cacc[q];
-        cacc[q] = keep + __shfl_xor(send, 16, kWave);
+        const double send = b1 ? cacc[q] : cacc[q + 4];
+        const double keep = b1 ? cacc[q + 4] : cacc[q];
+        cacc[q] = keep + __shfl_xor(send, 32, kWave);
     }
-    // ... this lane now holds the columns of q = 2 b1 + b0: 64 q + 4 tx + e
+    // ... this lane now holds the columns 128 b1 + 4 tx + e
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-        cred[wave][64 * (2 * b1 + b0) + 4 * tx + e] = cacc[e];
+        cred[wave][128 * b1 + 4 * tx + e] = cacc[e];
     __syncthreads();
     // ... then over the four waves, in wave order
     const double s = ((cred[0][tid] + cred[1][tid]) + cred[2][tid]) + cred[3][tid];
@@ -151,7 +158,6 @@ __global__ __launch_bounds__(kThreads) void sym_gemv_kernel(
     const float *__restrict__ As, int64_t n, int64_t nb, const double *__restrict__ v,
     double *__restrict__ part, StopCtl ctl, int use_ctl)
 {
-    __shared__ double vI[kTile], vJ[kTile];
     __shared__ double cred[kThreads / kWave][kTile];
     if (use_ctl) {
         if (blockIdx.x == 0 && threadIdx.x == 0)
@@ -161,17 +167,12 @@ __global__ __launch_bounds__(kThreads) void sym_gemv_kernel(
     }
     int64_t I, J;
     tile_of((int64_t)blockIdx.x, nb, &I, &J);
-    const int tid = threadIdx.x;
-    const int64_t gi = kTile * I + tid, gj = kTile * J + tid;
-    vI[tid] = gi < n ? v[gi] : 0.0;
-    vJ[tid] = gj < n ? v[gj] : 0.0;
-    __syncthreads();
     const float *T = As + (tile_start(I, nb) + (J - I)) * kTileEntries;
     const bool edge = (kTile * (J + 1) > n);     // J >= I: the last block column
     if (edge)
-        sym_tile<true>(T, I, J, n, nb, vI, vJ, cred, part);
+        sym_tile<true>(T, I, J, n, nb, v, cred, part);
     else
-        sym_tile<false>(T, I, J, n, nb, vI, vJ, cred, part);
+        sym_tile<false>(T, I, J, n, nb, v, cred, part);
 }
 
 // y_i = (sum over K of part[(I nb + K) 256 + r]) / d_i; one workgroup of
