@@ -484,13 +484,25 @@ def other_workload(args):
         e1.record(stream)
         torch.cuda.synchronize()
         pi_ms = e0.elapsed_time(e1)
+        # algorithmic: the operator's 2 n^2 d flop per sweep (every ordered
+        # pair), whatever the kernel evaluates
         flops = 2.0 * w.n * w.n * w.d
-        # executed on the fp16 matrix cores: three part products per
-        # coordinate, coordinates padded to 32-coordinate chunks
-        exec_flops = 3 * 2.0 * w.n * w.n * 32 * ((w.d + 31) // 32)
+        # evaluated: up to 2^19 points each pair once, in row groups of 256
+        # (group R covers the columns from its own first row on), else every
+        # ordered pair; three fp16 part products per coordinate, coordinates
+        # padded to 32-coordinate chunks
+        G = 256
+        if w.n <= (1 << 19):
+            groups = (w.n + G - 1) // G
+            pairs = float(sum(G * (w.n - G * r) for r in range(groups)))
+            kernel = "affinity_mfma_kernel (kApplySym) + fused_sym_reduce_kernel"
+        else:
+            pairs = float(w.n) * w.n
+            kernel = "affinity_mfma_kernel (kApply)"
+        exec_flops = 3 * 2.0 * pairs * 32 * ((w.d + 31) // 32)
         rate = {"unit": "TFLOP/s", "value": it * flops / (pi_ms * 1e-3) / 1e12,
-                "flops_per_sweep": flops, "bound": "mfma",
-                "kernel": "affinity_mfma_kernel (kApply)",
+                "flops_per_sweep": flops, "bound": "mfma", "kernel": kernel,
+                "pairs_evaluated_per_sweep": pairs,
                 "fp16_mfma_flops_per_sweep": exec_flops,
                 "fp16_mfma_tflops": round(it * exec_flops / (pi_ms * 1e-3) / 1e12, 2),
                 "peak": FP16_MFMA_PEAK_TFLOPS}

@@ -244,7 +244,13 @@ gpic_status gpic_degree_normalize_csr(const int64_t *row_ptr,
 
 /* Fused (W never stored): d_i = sum_{j != i} A_ij with A recomputed from the
  * points as in gpic_affinity, and v0 = D / sum D.  Nothing of size n^2 is
- * written.  ws: gpic_workspace_bytes(GPIC_OP_DEGREE_FUSED, n, 0, 0). */
+ * written.  For 16 <= d <= 128 and n <= 2^19 the fused operator evaluates
+ * each pair {i, j} once (A = A^T, section "Spectral Cluster") and uses that
+ * one float32 value for both A_ij and A_ji; the degrees are the row sums of
+ * that same symmetric A (so W's rows sum to 1 up to float64 rounding), and
+ * may differ from gpic_affinity's row sums in the last float32 bits of
+ * individual entries.  ws: gpic_workspace_bytes(GPIC_OP_DEGREE_FUSED, n, 0, 0)
+ * (for n <= 2^19 it includes about n^2 / 64 bytes of column partial sums). */
 gpic_status gpic_degree_fused(const float *X, int64_t n, int32_t d,
                               float sigma, double *degree, double *v0,
                               int64_t *n_zero_rows, void *ws, size_t ws_bytes,
@@ -272,8 +278,11 @@ gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
 
 /* One product y_i = (sum_{j != i} A_ij v_j) / d_i with A recomputed from X
  * (the fused operator; W = D^-1 A is never stored).  A zero-degree row gives
- * y_i = 0.  ws: gpic_workspace_bytes(GPIC_OP_MATVEC_FUSED, n, 0, 0).
- * Asynchronous. */
+ * y_i = 0.  For 16 <= d <= 128 and n <= 2^19 each pair is evaluated once
+ * (see gpic_degree_fused): the rows of 256-point groups give their row sums
+ * and, beyond their own group, column sums to later groups, added per row
+ * in a fixed order by a second launch.
+ * ws: gpic_workspace_bytes(GPIC_OP_MATVEC_FUSED, n, 0, 0).  Asynchronous. */
 gpic_status gpic_matvec_fused(const float *X, int64_t n, int32_t d,
                               float sigma, const double *degree,
                               const double *v, double *y, void *ws,

@@ -36,9 +36,18 @@
 //            symmetric storage (tiles (I, J), I <= J, of 256 x 256: see
 //            sym.hip); only column tiles at or right of the row's block are
 //            computed, and the storage's tile count nb comes in place of lda.
-// Every mode evaluates the same float32 A_ij and sums rows in the same
-// order, so kDegree reproduces kStore's degrees bit for bit and kStoreW
-// writes exactly what kStore followed by the row scaling writes.
+//   kApplySym: the fused product with each pair evaluated once (A = A^T):
+//            a workgroup's 256 rows take the columns from their own first
+//            row on; the row sums go to its rows, and for columns past its
+//            rows A_ij v_i also goes to column sums that a second kernel
+//            adds to the later rows (fused_sym_reduce_kernel).  With v = 1
+//            and no division it is the degree sweep of that same A.
+// Every mode evaluates the same float32 A_ij for a (row i, column j) pair
+// and sums rows in the same order, so kDegree reproduces kStore's degrees
+// bit for bit and kStoreW writes exactly what kStore followed by the row
+// scaling writes.  A_ij and A_ji can differ in the last float32 bits (the
+// two points play different parts in the Gram form); the symmetric modes
+// use the value computed with the earlier point as the row.
 #include "common.h"
 
 #include <type_traits>
@@ -46,7 +55,7 @@
 namespace gpic {
 namespace {
 
-enum { kStore = 0, kApply = 1, kDegree = 2, kStoreW = 3, kStoreSym = 4 };
+enum { kStore = 0, kApply = 1, kDegree = 2, kStoreW = 3, kStoreSym = 4, kApplySym = 5 };
 enum { kGauss = 0, kCosine = 1 };             // affinity kind (VALU engine)
 
 constexpr int kThreads = 256;
@@ -215,6 +224,65 @@ __global__ __launch_bounds__(kThreads) void chunk_reduce_kernel(
     }
 }
 
+// Column partial sums of the symmetric fused product: row group R (rows
+// R G .. R G + G - 1) holds one float64 per column j >= (R + 1) G, packed
+// group after group, so group R starts at sum over R' < R of
+// n - (R' + 1) G = R n - G R (R + 1) / 2 (every earlier group ends before n).
+__device__ __host__ __forceinline__ int64_t colpart_offset(int64_t R, int64_t n, int64_t G)
+{
+    return R * n - G * R * (R + 1) / 2;
+}
+
+// y_i for the symmetric fused product: the row sums of row i's group (its
+// chunk partials, chunks from the one holding the group's first row on, in
+// chunk order), then the column sums that every earlier row group left for
+// column i (in group order), divided by d_i; per-workgroup partial sums of
+// |y_i| for the L1 norm.  With degree_in null (the degree sweep, v = 1) the
+// sum itself is written.
+__global__ __launch_bounds__(kThreads) void fused_sym_reduce_kernel(
+    const double *__restrict__ part, int nchunks, int64_t chunk_cols,
+    const double *__restrict__ colpart, int64_t n, int64_t G,
+    const double *__restrict__ degree_in, double *__restrict__ out,
+    double *__restrict__ partial, StopCtl ctl, int use_ctl)
+{
+    __shared__ double red[kThreads / kWave];
+    if (use_ctl && stop_reached(ctl))
+        return;
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    double yabs = 0.0;
+    if (i < n) {
+        const int64_t R = i / G;
+        double s = 0.0;
+        for (int c = (int)((R * G) / chunk_cols); c < nchunks; ++c)
+            s += part[(int64_t)c * n + i];
+        int64_t Rp = 0;
+        for (; Rp + 4 <= R; Rp += 4) {
+            double x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                x[u] = colpart[colpart_offset(Rp + u, n, G) + i - (Rp + u + 1) * G];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                s += x[u];
+        }
+        for (; Rp < R; ++Rp)
+            s += colpart[colpart_offset(Rp, n, G) + i - (Rp + 1) * G];
+        if (degree_in == nullptr) {
+            out[i] = s;
+        } else {
+            const double di = degree_in[i];
+            const double yi = (di == 0.0) ? 0.0 : s / di;
+            out[i] = yi;
+            yabs = fabs(yi);
+        }
+    }
+    if (partial != nullptr) {
+        const double t = block_sum<kThreads>(yabs, red);
+        if (threadIdx.x == 0)
+            partial[blockIdx.x] = t;
+    }
+}
+
 // ------------------------------------------------------------------ MFMA
 
 // Workgroup: W waves, each owning RB blocks of 16 rows; columns [c0, c1)
@@ -249,10 +317,13 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     const float *__restrict__ cn, const unsigned *__restrict__ scal, int64_t n,
     int64_t chunk_cols, float *__restrict__ A, int64_t lda,
     const double *__restrict__ v, const double *__restrict__ degree_in,
-    double *__restrict__ out, double *__restrict__ part,
+    double *__restrict__ out, double *__restrict__ part, double *__restrict__ colpart,
     double *__restrict__ partial, StopCtl ctl, int use_ctl)
 {
     constexpr int NT = W * 64;
+    constexpr bool kApplyAny = (MODE == kApply || MODE == kApplySym);
+    constexpr bool kSymA = (MODE == kApplySym);
+    constexpr int64_t kGroupRows = (int64_t)W * 16 * RB;
     constexpr int kSlots = NCH * 8;              // (chunk, part, lane group)
     constexpr int kQ = TC / 16;                  // 16-column blocks per tile
     constexpr bool kWrites = (MODE == kStore || MODE == kStoreW || MODE == kStoreSym);
@@ -260,11 +331,12 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     static_assert(!kWrites || RB == 1, "one staged output tile per wave");
     __shared__ half8 xs[2][kSlots * TC];
     __shared__ float bs[2][TC];
-    __shared__ double vs[2][(MODE == kApply) ? TC : 1];
+    __shared__ double vs[2][kApplyAny ? TC : 1];
+    __shared__ double cred[kSymA ? 2 : 1][kSymA ? W : 1][kSymA ? TC : 1];
     __shared__ double red[W];
     __shared__ float ot[kWrites ? W : 1][kWrites ? 16 * kOutStride : 1];
 
-    if (MODE == kApply && use_ctl) {
+    if (kApplyAny && use_ctl) {
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
             *ctl.cur_stat = 0.0;
         if (stop_reached(ctl))
@@ -286,11 +358,22 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         if (c0 >= c1)
             return;                                  // uniform over the workgroup
     }
+    // kApplySym: columns from the workgroup's first row on; tiles from its
+    // last row + 1 on are off the diagonal block and give column sums too
+    const int64_t grow0 = (int64_t)blockIdx.x * kGroupRows;
+    const int64_t grow1 = grow0 + kGroupRows;
+    if (kSymA) {
+        if (grow0 > c0)
+            c0 = grow0;
+        if (c0 >= c1)
+            return;                                  // uniform over the workgroup
+    }
     const float mm = __uint_as_float(scal[1]);
 
     // B operands: this lane's rows, hi and lo of every chunk
     half8 bh[RB][NCH], bl[RB][NCH];
     float cni[RB], rs[RB];
+    __shared__ double vrow[kSymA ? kGroupRows : 1];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int64_t i = wrow0 + 16 * rb + m;
@@ -302,6 +385,7 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
         cni[rb] = cn[ic];
         rs[rb] = 0.0f;
+
         if (MODE == kStoreW) {
             const double di = degree_in[ic];
             rs[rb] = (di == 0.0) ? 0.0f : (float)(1.0 / di);
@@ -324,9 +408,9 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
         if (threadIdx.x < TC) {
             bstage = beta[jt + threadIdx.x];
-            if (MODE == kApply) {
+            if (kApplyAny) {
                 const int64_t j = jt + threadIdx.x;
-                vstage = (j < c1) ? v[j] : 0.0;
+                vstage = (j < c1) ? (v != nullptr ? v[j] : 1.0) : 0.0;
             }
         }
     };
@@ -339,7 +423,7 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
         if (threadIdx.x < TC) {
             bs[buf][threadIdx.x] = bstage;
-            if (MODE == kApply)
+            if (kApplyAny)
                 vs[buf][threadIdx.x] = vstage;
         }
     };
@@ -349,9 +433,16 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
         acc[rb][0] = acc[rb][1] = 0.0;
+    if (kSymA) {
+        // v of the workgroup's rows for the column sums (read after the
+        // barrier that follows the first staged tile)
+        for (int t = threadIdx.x; t < kGroupRows; t += NT)
+            vrow[t] = (grow0 + t < n) ? (v != nullptr ? v[grow0 + t] : 1.0) : 0.0;
+    }
 
-    auto tile = [&](int buf, int64_t jt, auto masked) {
+    auto tile = [&](int buf, int64_t jt, auto masked, auto offdiag) {
         constexpr bool kMask = decltype(masked)::value;
+        constexpr bool kOff = kSymA && decltype(offdiag)::value;
         // one 16-column block: the matrix-core chain into cc[rb] ...
         auto chain = [&](int q, floatx4 (&cc)[RB]) {
             const floatx4 b0 = *reinterpret_cast<const floatx4 *>(&bs[buf][16 * q + 4 * g]);
@@ -380,6 +471,7 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         };
         // ... and its epilogue
         auto epi = [&](int q, const floatx4 (&cc)[RB]) {
+            double cq[4] = {0.0, 0.0, 0.0, 0.0};     // kOff: column sums
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) {
                 const int64_t i = wrow0 + 16 * rb + m;
@@ -405,12 +497,45 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
                         acc[rb][q & 1] += (double)a[r];
-                } else if (MODE == kApply) {
+                } else if (kApplyAny) {
                     const double *vp = vs[buf] + 16 * q + 4 * g;
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
-                        acc[rb][q & 1] = fma((double)a[r], vp[r], acc[rb][q & 1]);
+                        acc[rb][kSymA ? 0 : (q & 1)] =
+                            fma((double)a[r], vp[r], acc[rb][kSymA ? 0 : (q & 1)]);
                 }
+                if (kOff) {
+                    const double vi = vrow[wave * 16 * RB + 16 * rb + m];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        cq[r] = fma((double)a[r], vi, cq[r]);
+                }
+            }
+            if (kOff) {
+                // column 16 q + 4 g + r over the wave's 16 RB rows: reduce-
+                // scatter over the 16 lanes of a lane group (m = 8, 4), then
+                // add the 4 lanes that share the column (m = 2, 1); lane m
+                // ends with r = 2 b3 + b2 (b = the bits of m)
+                {
+                    const bool up = (m & 8) != 0;
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const double send = up ? cq[h] : cq[h + 2];
+                        const double keep = up ? cq[h + 2] : cq[h];
+                        cq[h] = keep + __shfl_xor(send, 8, kWave);
+                    }
+                }
+                {
+                    const bool up = (m & 4) != 0;
+                    const double send = up ? cq[0] : cq[1];
+                    const double keep = up ? cq[1] : cq[0];
+                    cq[0] = keep + __shfl_xor(send, 4, kWave);
+                }
+                cq[0] += __shfl_xor(cq[0], 2, kWave);
+                cq[0] += __shfl_xor(cq[0], 1, kWave);
+                if ((m & 3) == 0)
+                    cred[buf][wave][16 * q + 4 * g + 2 * ((m >> 3) & 1) + ((m >> 2) & 1)] =
+                        cq[0];
             }
         };
         floatx4 ca[RB], cb[RB];
@@ -466,16 +591,37 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
             fetch(jt + TC);                          // in flight during compute
         const bool diag = (rlo < jt + TC) && (jt < rhi);
         const bool tail = jt + TC > c1;
-        if (diag || tail)
-            tile(buf, jt, std::true_type{});
-        else
-            tile(buf, jt, std::false_type{});
+        const bool off = kSymA && jt >= grow1;
+        if (off) {
+            if (tail)
+                tile(buf, jt, std::true_type{}, std::true_type{});
+            else
+                tile(buf, jt, std::false_type{}, std::true_type{});
+        } else if (diag || tail) {
+            tile(buf, jt, std::true_type{}, std::false_type{});
+        } else {
+            tile(buf, jt, std::false_type{}, std::false_type{});
+        }
         if (t + 1 < ntiles) {
             // the barrier ending the previous iteration ordered every wave's
             // reads of buffer buf ^ 1 before this write; this one orders the
             // write before the next tile's reads
             commit(buf ^ 1);
             __syncthreads();
+        } else if (kSymA) {
+            __syncthreads();
+        }
+        if (off && threadIdx.x < TC) {
+            // the tile's column sums over the workgroup's rows, in wave order
+            // (cred[buf] is written again two tiles on, after the next barrier)
+            const int64_t j = jt + threadIdx.x;
+            if (j < c1) {
+                double cs = 0.0;
+#pragma unroll
+                for (int w = 0; w < W; ++w)
+                    cs += cred[buf][w][threadIdx.x];
+                colpart[colpart_offset(blockIdx.x, n, kGroupRows) + (j - grow1)] = cs;
+            }
         }
     }
 
@@ -697,10 +843,16 @@ int nch_for(int d) { return (d + 31) / 32; }
 // wave and 8 waves per workgroup (512 rows share every staged column tile,
 // and four independent matrix-core chains per wave hide each other's
 // latency; measured 14.9 ms per product at n = 200,000, d = 64, against
-// 16.4 with 128 rows); the sweeps that write A or W take one block per
-// wave and 4 waves (their bound is the stores).
-constexpr int rb_for(int mode) { return (mode == kApply || mode == kDegree) ? 4 : 1; }
-constexpr int waves_for(int mode) { return (mode == kApply || mode == kDegree) ? 8 : 4; }
+// 16.4 with 128 rows); the symmetric product, which also keeps column sums
+// and v of its rows, takes two blocks per wave (256 rows) to stay within
+// 256 registers; the sweeps that write A or W take one block per wave and
+// 4 waves (their bound is the stores).
+constexpr bool sums_rows(int mode)
+{
+    return mode == kApply || mode == kDegree || mode == kApplySym;
+}
+constexpr int rb_for(int mode) { return mode == kApplySym ? 2 : (sums_rows(mode) ? 4 : 1); }
+constexpr int waves_for(int mode) { return sums_rows(mode) ? 8 : 4; }
 constexpr int64_t rows_per_group(int mode) { return 16 * rb_for(mode) * waves_for(mode); }
 
 int64_t row_groups(int64_t n, int mode)
@@ -726,6 +878,31 @@ void chunking(int64_t n, int64_t *chunk_cols, int *nchunks)
 }
 
 int64_t padded_points(int64_t n) { return (n + kColAlign - 1) / kColAlign * kColAlign; }
+
+// The symmetric fused product (each pair once: row sums for the row's
+// group, column sums for the column's) up to this many points; its column
+// partial sums take about n^2 / 64 bytes (4.3 GB at the limit).  Above it
+// the product sums whole rows.
+constexpr int64_t kFusedSymMaxN = 1 << 19;
+constexpr int64_t kSymGroupRows = rows_per_group(kApplySym);
+
+bool fused_sym(int64_t n, int d) { return use_mfma(d) && n <= kFusedSymMaxN; }
+
+int64_t colpart_entries(int64_t n)
+{
+    const int64_t groups = (n + kSymGroupRows - 1) / kSymGroupRows;
+    return colpart_offset(groups - 1, n, kSymGroupRows);
+}
+
+// Column chunks of the symmetric product: kMaxChunks chunks, so that the
+// triangle of (row group, chunk) pieces spreads over many workgroups.
+void sym_chunking(int64_t n, int64_t *chunk_cols, int *nchunks)
+{
+    int64_t cols = (n + kMaxChunks - 1) / kMaxChunks;
+    cols = (cols + kColAlign - 1) / kColAlign * kColAlign;
+    *chunk_cols = cols;
+    *nchunks = (int)((n + cols - 1) / cols);
+}
 
 int64_t al256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
@@ -775,7 +952,8 @@ hipError_t launch_split(const float *X, int64_t n, int d, float c, const Ws &w,
 template <int NCH, int MODE>
 void launch_engine(const Ws &w, int64_t n, int64_t chunk_cols, int nchunks, float *A,
                    int64_t lda, const double *v, const double *degree_in, double *out,
-                   double *part, double *partial, StopCtl ctl, int use_ctl, hipStream_t s)
+                   double *part, double *partial, StopCtl ctl, int use_ctl, hipStream_t s,
+                   double *colpart = nullptr)
 {
     constexpr int RB = rb_for(MODE);
     constexpr int W = waves_for(MODE);
@@ -783,7 +961,7 @@ void launch_engine(const Ws &w, int64_t n, int64_t chunk_cols, int nchunks, floa
     const dim3 grid((unsigned)row_groups(n, MODE), (unsigned)nchunks);
     hipLaunchKernelGGL((affinity_mfma_kernel<NCH, RB, TC, MODE, W>), grid, dim3(W * 64), 0,
                        s, w.xh, padded_points(n), w.beta, w.cn, w.scal, n, chunk_cols, A,
-                       lda, v, degree_in, out, part, partial, ctl, use_ctl);
+                       lda, v, degree_in, out, part, colpart, partial, ctl, use_ctl);
 }
 
 template <int MODE>
@@ -917,6 +1095,8 @@ int64_t fused_blocks(int64_t n, int d)
 {
     if (!use_mfma(d))
         return (n + 7) / 8;
+    if (fused_sym(n, d))
+        return (n + kThreads - 1) / kThreads;        // fused_sym_reduce workgroups
     int64_t chunk_cols;
     int nchunks;
     chunking(n, &chunk_cols, &nchunks);
@@ -972,8 +1152,54 @@ hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c,
                               double *partial, StopCtl ctl, bool use_ctl,
                               void *ws, hipStream_t s, bool operands_ready)
 {
-    return dispatch<kApply>(X, n, d, c, nullptr, 0, v, degree, y, partial, ctl,
-                            use_ctl ? 1 : 0, ws, s, operands_ready);
+    if (!fused_sym(n, d))
+        return dispatch<kApply>(X, n, d, c, nullptr, 0, v, degree, y, partial, ctl,
+                                use_ctl ? 1 : 0, ws, s, operands_ready);
+    const Ws w = carve(ws, n);
+    if (!operands_ready) {
+        const hipError_t e = launch_split(X, n, d, c, w, s);
+        if (e != hipSuccess)
+            return e;
+    }
+    double *colpart = reinterpret_cast<double *>(static_cast<char *>(ws) + affinity_ws(n));
+    int64_t chunk_cols;
+    int nchunks;
+    sym_chunking(n, &chunk_cols, &nchunks);
+    const int uc = use_ctl ? 1 : 0;
+#define GPIC_MFMA(NCH)                                                                \
+    launch_engine<NCH, kApplySym>(w, n, chunk_cols, nchunks, nullptr, 0, v, degree,   \
+                                  nullptr, w.part, nullptr, ctl, uc, s, colpart)
+    switch (nch_for(d)) {
+    case 1: GPIC_MFMA(1); break;
+    case 2: GPIC_MFMA(2); break;
+    case 3: GPIC_MFMA(3); break;
+    default: GPIC_MFMA(4); break;
+    }
+#undef GPIC_MFMA
+    hipLaunchKernelGGL(fused_sym_reduce_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, w.part, nchunks, chunk_cols, colpart, n,
+                       kSymGroupRows, degree, y, partial, ctl, uc);
+    return hipGetLastError();
+}
+
+hipError_t launch_fused_operator_degree(const float *X, int64_t n, int d, float c,
+                                       double *degree, void *ws, hipStream_t s)
+{
+    if (!fused_sym(n, d))
+        return launch_fused_degree(X, n, d, c, degree, ws, s);
+    // the symmetric product with v = 1 and no division: the degrees of the
+    // same symmetric A the products use, so W's rows sum to 1 up to rounding
+    StopCtl none{};
+    return launch_fused_apply(X, n, d, c, nullptr, nullptr, degree, nullptr, none, false,
+                              ws, s, false);
+}
+
+size_t fused_ws(int64_t n)
+{
+    size_t b = affinity_ws(n);
+    if (n <= kFusedSymMaxN)                          // whatever d the product gets
+        b += (size_t)colpart_entries(n) * sizeof(double);
+    return b;
 }
 
 } // namespace gpic

@@ -96,7 +96,7 @@ size_t pi_csr_ws(int64_t n, int64_t nnz)
 }
 
 // the fused product's own scratch follows the power-iteration layout
-size_t pi_fused_ws(int64_t n) { return pi_ws(n, fused_nb_bound(n)) + aff_ws(n); }
+size_t pi_fused_ws(int64_t n) { return pi_ws(n, fused_nb_bound(n)) + al(fused_ws(n)); }
 
 // the symmetric product's partial sums follow the power-iteration layout
 size_t pi_sym_ws(int64_t n) { return pi_ws(n, sym_blocks(n)) + al(sym_part_bytes(n)); }
@@ -461,13 +461,13 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     case GPIC_OP_AFFINITY: return aff_ws(n);
     case GPIC_OP_DEGREE_NORMALIZE: return start_ws(n);
     case GPIC_OP_DEGREE_NORMALIZE_CSR: return kCtlBytes + start_ws(n);
-    case GPIC_OP_DEGREE_FUSED: return start_ws(n) + aff_ws(n);
+    case GPIC_OP_DEGREE_FUSED: return start_ws(n) + al(fused_ws(n));
     case GPIC_OP_PI_DENSE: return pi_ws(n, gemv_blocks(n));
     case GPIC_OP_PI_FUSED: return pi_fused_ws(n);
     case GPIC_OP_PI_CSR: return pi_csr_ws(n, nnz);
     case GPIC_OP_KMEANS1D: return kmeans_ws(n, k < 1 ? 1 : k);
     case GPIC_OP_AFFINITY_NORMALIZED: return start_ws(n) + aff_ws(n);
-    case GPIC_OP_MATVEC_FUSED: return aff_ws(n);
+    case GPIC_OP_MATVEC_FUSED: return al(fused_ws(n));
     case GPIC_OP_AFFINITY_COSINE: return al(cosine_ws(n));
     case GPIC_OP_AFFINITY_COSINE_NORMALIZED: return start_ws(n) + al(cosine_ws(n));
     case GPIC_OP_KNN_GRAPH:
@@ -718,13 +718,13 @@ gpic_status gpic_degree_fused(const float *X, int64_t n, int32_t d, float sigma,
         return st;
     CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
               "n_zero_rows misaligned");
-    if ((st = check_ws(ws, ws_bytes, start_ws(n) + aff_ws(n))) != GPIC_OK)
+    if ((st = check_ws(ws, ws_bytes, start_ws(n) + al(fused_ws(n)))) != GPIC_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
     float c;
     gauss_coefficient(sigma, &c);
-    CHECK_HIP(launch_fused_degree(X, n, d, c, degree,
-                                  static_cast<char *>(ws) + start_ws(n), s),
+    CHECK_HIP(launch_fused_operator_degree(X, n, d, c, degree,
+                                           static_cast<char *>(ws) + start_ws(n), s),
               "fused degree");
     int bad = 0;
     CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
@@ -793,7 +793,7 @@ gpic_status gpic_matvec_fused(const float *X, int64_t n, int32_t d, float sigma,
     if ((st = check_vec(degree, "degree")) != GPIC_OK ||
         (st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
         return st;
-    if ((st = check_ws(ws, ws_bytes, aff_ws(n))) != GPIC_OK)
+    if ((st = check_ws(ws, ws_bytes, al(fused_ws(n)))) != GPIC_OK)
         return st;
     float c;
     gauss_coefficient(sigma, &c);

@@ -124,12 +124,21 @@ hipError_t launch_fused_degree(const float *X, int64_t n, int d, float c_log2,
 // dimensions).
 hipError_t launch_fused_prepare(const float *X, int64_t n, int d, float c_log2,
                                 void *ws, hipStream_t s);
+// ws: fused_ws(n) bytes
 hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c_log2,
                               const double *v, const double *degree, double *y,
                               double *partial, StopCtl ctl, bool use_ctl,
                               void *ws, hipStream_t s, bool operands_ready = false);
 // number of |y| partial sums the fused product writes
 int64_t fused_blocks(int64_t n, int d);
+// the fused product's ws: affinity_ws(n) bytes, then (n <= 2^19, where the
+// product takes each pair once) the column partial sums
+size_t fused_ws(int64_t n);
+// the degrees of the fused operator's A (ws: fused_ws(n) bytes): where the
+// product takes each pair once, the same sweep with v = 1, else the
+// row-sum sweep of launch_fused_degree
+hipError_t launch_fused_operator_degree(const float *X, int64_t n, int d, float c_log2,
+                                       double *degree, void *ws, hipStream_t s);
 // A into the packed upper tiles of the symmetric storage (sym.hip);
 // ws: affinity_ws(n) bytes
 hipError_t launch_affinity_sym(const float *X, int64_t n, int d, float c_log2,

@@ -378,6 +378,42 @@ def test_fused_parity(g, orc, n, d):
     assert rel_l1(v.cpu().numpy(), vd.cpu().numpy()) <= 1e-6
 
 
+@pytest.mark.parametrize("n,d", [(255, 16), (256, 20), (257, 64), (513, 100),
+                                 (2050, 33), (4099, 16)])
+def test_fused_symmetric_edges(g, orc, n, d):
+    """The fused operator evaluates each pair once (256-point row groups:
+    row sums for the group, column sums for later groups): sizes around the
+    group and chunk edges, every coordinate-chunk count (d = 16, 20, 33,
+    64, 100), one product against the oracle's on-the-fly rows."""
+    X = _pts(n, d, 50 + d, scale=1.2)
+    sigma = np.float32(np.sqrt(d))
+    deg, v0, nz = g.gpic_degree_fused(_t(X), sigma)
+    dr, v0r, _ = orc.degree_onthefly(X, sigma)
+    np.testing.assert_allclose(deg.cpu().numpy(), dr, rtol=1e-5)
+    v = np.random.default_rng(n + d).uniform(0.5, 1.5, size=n)
+    y = g.gpic_matvec_fused(_t(X), sigma, deg, _t(v)).cpu().numpy()
+    rows = np.arange(n, dtype=np.int64)
+    yr = orc.matvec_onthefly_rows(X, sigma, dr, v, rows)
+    np.testing.assert_allclose(y, yr, rtol=1e-5)
+
+
+@pytest.mark.parametrize("n,d", [(700, 16), (3000, 64)])
+def test_fused_rows_sum_to_one(g, n, d):
+    """Pin P3 through the fused operator: its degrees are the row sums of
+    the same symmetric A its products use, so W 1 = 1 up to float64
+    rounding and v = 1/n stops after two products."""
+    X = _pts(n, d, 60 + d)
+    sigma = np.float32(np.sqrt(d))
+    deg, _, _ = g.gpic_degree_fused(_t(X), sigma)
+    ones = torch.ones(n, dtype=torch.float64, device=DEV)
+    y = g.gpic_matvec_fused(_t(X), sigma, deg, ones).cpu().numpy()
+    np.testing.assert_allclose(y, 1.0, rtol=1e-12)
+    v = torch.full((n,), 1.0 / n, dtype=torch.float64, device=DEV)
+    out = g.gpic_power_iterate_fused(_t(X), sigma, deg, v, None, "converge", 100, 1e-15)
+    assert out.converged and out.iterations == 2
+    np.testing.assert_allclose(v.cpu().numpy(), 1.0 / n, rtol=1e-12)
+
+
 # ---------------------------------------------------------------- CSR path
 def test_csr_parity_knn(g, orc):
     import workloads
