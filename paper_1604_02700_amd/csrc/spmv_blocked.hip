@@ -10,6 +10,9 @@
 // One launch then walks (block, row tile) pairs block-major, so the
 // workgroups in flight on every XCD gather from one 2 MB slice of v, and
 // writes per-block row sums; a second launch adds them in block order.
+// When rows hold few entries per block (one lane per row would do), the
+// tile's entries are gathered by all lanes in storage order and staged in
+// LDS before a thread per row adds them (spmv_blocked_staged_kernel).
 //
 // The copy needs every row's columns in ascending order (checked on the
 // device) and at most 32 blocks (n <= 2^23), and it is made only when at
@@ -269,6 +272,74 @@ __global__ __launch_bounds__(kThreads) void spmv_blocked_kernel(
         ypart[b * n + i] = s;
 }
 
+// The product for one lane per row, staged: a row holds few entries per
+// block (about 5.6 for a 32-NN graph), so a lane per row leaves most lanes
+// of a gather instruction idle while the wave finishes its longest row.
+// Here the 256 threads first walk the tile's entries in storage order
+// (every lane busy: coalesced column and value loads, then the gathers,
+// kUnroll in flight per thread) and stage w and v[col] in LDS; after a
+// barrier a thread per row adds its entries in entry order with the same
+// multiply-adds as the lane-per-row kernel, so the sums are bitwise the
+// same.  Tiles with more entries than the stage go round by round.
+constexpr int kStage = 2048;             // staged entries per round
+
+__global__ __launch_bounds__(kThreads) void spmv_blocked_staged_kernel(
+    const int64_t *__restrict__ base, const int32_t *__restrict__ rpb,
+    const int32_t *__restrict__ colb, const float *__restrict__ valb, int64_t n,
+    int64_t tiles, const double *__restrict__ v, double *__restrict__ ypart, StopCtl ctl)
+{
+    constexpr int R = kThreads;                  // rows per tile
+    __shared__ int32_t rp[R + 1];
+    __shared__ double xs[kStage];
+    __shared__ float ws[kStage];
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        *ctl.cur_stat = 0.0;
+    if (stop_reached(ctl))
+        return;
+    const int64_t b = blockIdx.x / tiles;
+    const int64_t row0 = (blockIdx.x % tiles) * R;
+    const int32_t *rb = rpb + b * (n + 1);
+    for (int t = threadIdx.x; t <= R; t += kThreads)
+        rp[t] = rb[row0 + t < n ? row0 + t : n];
+    __syncthreads();
+    const int32_t *cb = colb + base[b];
+    const float *vb = valb + base[b];
+    const int32_t e0 = rp[0], e1 = rp[R];
+    const int li = threadIdx.x;
+    const int64_t i = row0 + li;
+    const int32_t rs = rp[li], re = rp[li + 1];  // this thread's row (empty past n)
+    double s = 0.0;
+    for (int32_t r0 = e0; r0 < e1; r0 += kStage) {
+        const int32_t r1 = (r0 + kStage < e1) ? r0 + kStage : e1;
+        for (int32_t p0 = r0 + threadIdx.x; p0 < r1; p0 += kThreads * kUnroll) {
+            int32_t c[kUnroll];
+            float w[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int32_t p = p0 + u * kThreads;
+                c[u] = p < r1 ? cb[p] : -1;
+                w[u] = p < r1 ? vb[p] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                if (c[u] >= 0) {
+                    const int32_t q = p0 + u * kThreads - r0;
+                    xs[q] = v[c[u]];
+                    ws[q] = w[u];
+                }
+            }
+        }
+        __syncthreads();
+        const int32_t a = (rs > r0) ? rs : r0;
+        const int32_t z = (re < r1) ? re : r1;
+        for (int32_t p = a; p < z; ++p)
+            s = fma((double)ws[p - r0], xs[p - r0], s);
+        __syncthreads();                         // before the next round's stage
+    }
+    if (i < n)
+        ypart[b * n + i] = s;
+}
+
 // y_i = sum over blocks of the block sums (block order); per-workgroup
 // partial sums of |y_i| for the L1 norm.
 __global__ __launch_bounds__(kThreads) void spmv_finalize_kernel(
@@ -408,7 +479,13 @@ hipError_t launch_spmv_blocked(const CsrBlocked &B, const double *v, double *y,
                            tiles, v, B.ypart, ctl);                            \
     }
     switch (B.lanes) {
-    case 1: GPIC_BLOCKED(1); break;
+    case 1: {
+        const int64_t tiles = (B.n + kThreads - 1) / kThreads;
+        hipLaunchKernelGGL(spmv_blocked_staged_kernel, dim3((unsigned)(B.nb * tiles)),
+                           dim3(kThreads), 0, s, B.base, B.rpb, B.colb, B.valb, B.n, tiles,
+                           v, B.ypart, ctl);
+        break;
+    }
     case 2: GPIC_BLOCKED(2); break;
     case 4: GPIC_BLOCKED(4); break;
     case 8: GPIC_BLOCKED(8); break;
