@@ -93,6 +93,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=50000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-converge", action="store_true")
+    ap.add_argument("--no-sym", action="store_true",
+                    help="skip the symmetric-storage figures of the headline line")
     ap.add_argument("--workload", default="blobs16d",
                     choices=["blobs16d", "blobs16d_sym", "blobs16d_host", "blobs64d", "knn8d",
                              "knn8d_rcm", "rings2d", "blobs2d", "moons", "circles3"],
@@ -201,6 +203,19 @@ def main():
                 "converged": out.pi.converged, "eps": w.eps, "runs": 3, "statistic": "median"}
         log(f"bench: to convergence {out.pi.iterations} updates, {tc:.4f} s")
 
+    sym = None
+    if not args.no_sym:
+        # the same job with A stored once as its upper tiles (half the bytes
+        # per update); a secondary figure, not the headline value
+        r = measure_sym(g, w, X, T, k, args.steps, args.warmup, args.gemv_reps,
+                        not args.no_converge)
+        sym = {"e2e_fixed_T_s": round(r["ms_step"] / 1e3, 5),
+               "ms_per_update": round(r["pi_ms"] / T, 5),
+               "stored_bytes": r["stored_bytes"], "phases_ms": r["phases_ms"],
+               "product_ms": round(r["prod_ms"], 5),
+               "to_convergence": r["to_convergence"]}
+        log(f"bench: symmetric storage {sym['e2e_fixed_T_s']} s per fixed-T job")
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"bench: cpu baseline (oracle) on {args.cpu_sample} points ...")
@@ -257,25 +272,21 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "avg_launch_ms": round(gemv_ms, 5),
                      "bytes_per_launch": alg_bytes},
+        "symmetric_storage": sym,
         "cpu_baseline": cpu,
         "copy_reference": copy_ref,
     }
     print(json.dumps(line), flush=True)
 
 
-def sym_workload(args):
-    """The headline workload (16-D blobs, n = 50,000, T = 50, k = 10) over the
-    symmetric storage of A (packed upper tiles, 2 n^2 bytes per product):
-    one JSON line, not the headline line."""
+def measure_sym(g, w, X, T, k, steps, warmup, gemv_reps, converge):
+    """The 16-D blobs job over the symmetric storage of A (packed upper tiles,
+    2 n^2 bytes per product): the fixed-T pipeline timed over `steps`, the
+    product alone, and (if asked) the to-convergence run, median of three
+    after an untimed one."""
     import torch
-    import paper_1604_02700_amd as g
-    import workloads
-
-    dev = torch.device("cuda:0")
-    w = workloads.make("blobs16d", n=args.n if args.n != 50000 else None)
-    n, T, k = w.n, args.T, w.k
-    log(f"bench: workload blobs16d (symmetric storage) n={n} T={T}")
-    X = torch.from_numpy(w.X).to(dev)
+    dev = X.device
+    n = w.n
     As = torch.empty(g.sym_bytes(n) // 4, dtype=torch.float32, device=dev)
     v = torch.empty(n, dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream(dev)
@@ -295,15 +306,15 @@ def sym_workload(args):
             record.append([ev[i].elapsed_time(ev[i + 1]) for i in range(3)])
         return deg
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step(None)
     torch.cuda.synchronize()
     phases = []
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         deg = step(phases)
     torch.cuda.synchronize()
-    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
     ph = np.array(phases)
     pi_ms = float(ph[:, 1].mean())
     stored = float(g.sym_bytes(n))
@@ -311,7 +322,7 @@ def sym_workload(args):
     y = torch.empty(n, dtype=torch.float64, device=dev)
     g.gpic_matvec_sym(As, n, deg, v, y)
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.gemv_reps)]
+           for _ in range(gemv_reps)]
     for a, b in evs:
         a.record(stream)
         g.gpic_matvec_sym(As, n, deg, v, y)
@@ -322,27 +333,54 @@ def sym_workload(args):
     part_bytes = 2.0 * 8 * nb * nb * 256          # partial sums written and read back
     alg = stored + part_bytes + 24.0 * n           # tiles once, partials, v, d, y
     conv = None
-    if not args.no_converge:
-        tc0 = time.perf_counter()
+    if converge:
         out = g.pic_sym(X, w.sigma, k, "converge", 1000, w.eps, As=As)
         torch.cuda.synchronize()
-        conv = {"e2e_s": round(time.perf_counter() - tc0, 5),
-                "iterations": out.pi.iterations, "converged": out.pi.converged}
+        tcs = []
+        for _ in range(3):
+            tc0 = time.perf_counter()
+            out = g.pic_sym(X, w.sigma, k, "converge", 1000, w.eps, As=As)
+            torch.cuda.synchronize()
+            tcs.append(time.perf_counter() - tc0)
+        conv = {"e2e_s": round(float(np.median(tcs)), 5), "iterations": out.pi.iterations,
+                "converged": out.pi.converged, "runs": 3, "statistic": "median"}
+    del As
+    return {"stored_bytes": stored, "ms_step": ms_step, "pi_ms": pi_ms,
+            "phases_ms": {"affinity_sym_degree_v0": round(float(ph[:, 0].mean()), 4),
+                          "power_iteration": round(pi_ms, 4),
+                          "kmeans": round(float(ph[:, 2].mean()), 4)},
+            "prod_ms": prod_ms, "alg_bytes": alg, "to_convergence": conv}
+
+
+def sym_workload(args):
+    """The headline workload (16-D blobs, n = 50,000, T = 50, k = 10) over the
+    symmetric storage of A (packed upper tiles, 2 n^2 bytes per product):
+    one JSON line, not the headline line."""
+    import torch
+    import paper_1604_02700_amd as g
+    import workloads
+
+    dev = torch.device("cuda:0")
+    w = workloads.make("blobs16d", n=args.n if args.n != 50000 else None)
+    n, T, k = w.n, args.T, w.k
+    log(f"bench: workload blobs16d (symmetric storage) n={n} T={T}")
+    X = torch.from_numpy(w.X).to(dev)
+    r = measure_sym(g, w, X, T, k, args.steps, args.warmup, args.gemv_reps,
+                    not args.no_converge)
+    stored, pi_ms, prod_ms, alg = r["stored_bytes"], r["pi_ms"], r["prod_ms"], r["alg_bytes"]
     line = {"metric": "blobs16d over symmetric storage: power-iteration GB/s of stored "
                       "A streamed; end-to-end PIC seconds, n=50k",
             "value": round(T * stored / (pi_ms * 1e-3) / 1e9, 2), "unit": "GB/s",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-            "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
-            "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+            "ms_per_step": round(r["ms_step"], 4), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
             "config": {"workload": f"blobs16d: n={n}, d={w.d}, packed upper tiles of A "
                                    f"({stored / 1e9:.2f} GB), T={T}, k={k}", "n": n,
                        "storage": "f32 symmetric tiles", "accumulate": "f64"},
-            "e2e_fixed_T_s": round(ms_step / 1e3, 5),
-            "phases_ms": {"affinity_sym_degree_v0": round(float(ph[:, 0].mean()), 4),
-                          "power_iteration": round(pi_ms, 4),
-                          "kmeans": round(float(ph[:, 2].mean()), 4)},
+            "e2e_fixed_T_s": round(r["ms_step"] / 1e3, 5),
+            "phases_ms": r["phases_ms"],
             "dense_equivalent_gbs": round(T * 4.0 * n * n / (pi_ms * 1e-3) / 1e9, 2),
-            "to_convergence": conv,
+            "to_convergence": r["to_convergence"],
             "roofline": {"bound": "hbm", "kernel": "sym_gemv_kernel + sym_finalize_kernel",
                          "achieved": round(alg / (prod_ms * 1e-3) / 1e9, 2),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
