@@ -357,7 +357,7 @@ def test_kmeans1d_special_values(g, orc):
 
 
 # -------------------------------------------------------------- fused path
-@pytest.mark.parametrize("n,d", [(300, 2), (1000, 64), (1025, 16)])
+@pytest.mark.parametrize("n,d", [(300, 2), (1000, 64), (1025, 16), (500, 140)])
 def test_fused_parity(g, orc, n, d):
     X = _pts(n, d, 40 + d, scale=1.5)
     sigma = np.float32(np.sqrt(d))
@@ -395,6 +395,26 @@ def test_fused_symmetric_edges(g, orc, n, d):
     rows = np.arange(n, dtype=np.int64)
     yr = orc.matvec_onthefly_rows(X, sigma, dr, v, rows)
     np.testing.assert_allclose(y, yr, rtol=1e-5)
+
+
+def test_fused_full_rows_above_symmetric_limit(g, orc):
+    """Above 2^19 points the fused operator sums every ordered pair (row
+    sweep for the degrees, row products): n = 2^19 + 1, sampled rows
+    against the oracle, one by one."""
+    n, d = (1 << 19) + 1, 16
+    X = _pts(n, d, 77, scale=2.0)
+    sigma = np.float32(4.0)
+    print(f"gpu: fused full rows n={n} d={d}", flush=True)
+    deg, v0, nz = g.gpic_degree_fused(_t(X), sigma)
+    rows = np.array([0, 1, 255, 256, 511, 512, n // 3, n - 2, n - 1], dtype=np.int64)
+    dr = orc.degree_rows(X, sigma, rows)
+    np.testing.assert_allclose(deg.cpu().numpy()[rows], dr, rtol=1e-5)
+    v = np.random.default_rng(5).uniform(0.5, 1.5, size=n)
+    y = g.gpic_matvec_fused(_t(X), sigma, deg, _t(v)).cpu().numpy()
+    dfull = np.zeros(n)
+    dfull[rows] = dr
+    yr = orc.matvec_onthefly_rows(X, sigma, dfull, v, rows)
+    np.testing.assert_allclose(y[rows], yr, rtol=1e-5)
 
 
 @pytest.mark.parametrize("n,d", [(700, 16), (3000, 64)])
