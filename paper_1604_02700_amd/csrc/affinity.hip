@@ -9,13 +9,16 @@
 //
 // Two tile engines:
 //   * MFMA, 16 <= d <= 128.  Squared distances in the Gram form
-//     |x_i|^2 + |x_j|^2 - 2 x_i.x_j, with the dot products on the fp16
-//     matrix cores: every coordinate, scaled by one power of two into
-//     [-1, 1], is split into a half-precision high part and the half-
-//     precision remainder, and three products per pair of parts (hi.hi,
-//     lo.hi, hi.lo, float32 accumulation) reproduce the float32 dot product
-//     to about 2^-22 of |x_i||x_j| per coordinate, at about a fifth of the
-//     fp32 matrix-core time.  A prologue (largest |x|, then the split)
+//     |x_i|^2 + |x_j|^2 - 2 x_i.x_j over the centred points x - mean
+//     (distances are unchanged; the cancellation then scales with the
+//     spread of the points, not their offset from the origin), with the dot
+//     products on the fp16 matrix cores: every coordinate, scaled by one
+//     power of two into [-1, 1], is split into a half-precision high part
+//     and the half-precision remainder, and three products per pair of
+//     parts (hi.hi, lo.hi, hi.lo, float32 accumulation) reproduce the
+//     float32 dot product to about 2^-22 of |x_i||x_j| per coordinate, at
+//     about a fifth of the fp32 matrix-core time.  A prologue (column
+//     means, largest |x - mean|, then the split)
 //     writes the operands once per call in the order the matrix cores take
 //     them, so a column tile is staged into LDS by contiguous 16-byte
 //     copies and every operand read from LDS is one conflict-free 16-byte
@@ -122,15 +125,65 @@ __global__ __launch_bounds__(kThreads) void inv_norm_kernel(const float *__restr
 // and scal[1] = m = -2 c 4^S (exact: c times a power of two).
 __global__ void split_clear_kernel(unsigned *__restrict__ scal) { scal[0] = 0u; }
 
+// Column means of X in float64 (the Gram form works on centred points:
+// distances do not change, and the cancellation in |x_i|^2 + |x_j|^2 -
+// 2 x_i.x_j scales with |x - mean|, not with |x|).  A workgroup takes
+// kThreads / d rows per pass (whole rows, coalesced) and leaves one float64
+// partial per column; one workgroup adds the partials in order.
+constexpr int kMeanBlocks = 256;
+
+__global__ __launch_bounds__(kThreads) void col_mean_partials_kernel(
+    const float *__restrict__ X, int64_t n, int d, double *__restrict__ part)
+{
+    __shared__ double red[kThreads];
+    const int rows = kThreads / d;               // 16 <= d <= 128: 2 to 16 rows
+    const int t = threadIdx.x;
+    const int r = t / d, c = t % d;
+    double sum = 0.0;
+    if (r < rows) {
+        for (int64_t p = (int64_t)blockIdx.x * rows + r; p < n;
+             p += (int64_t)gridDim.x * rows)
+            sum += (double)X[p * d + c];
+    }
+    red[t] = sum;
+    __syncthreads();
+    if (t < d) {
+        double a = 0.0;
+        for (int q = 0; q < rows; ++q)
+            a += red[q * d + t];
+        part[(int64_t)blockIdx.x * d + t] = a;
+    }
+}
+
+__global__ void col_mean_finish_kernel(const double *__restrict__ part, int nb, int d,
+                                       int64_t n, double *__restrict__ mu)
+{
+    const int c = threadIdx.x;
+    if (c >= d)
+        return;
+    double sum = 0.0;
+    for (int b = 0; b < nb; ++b)
+        sum += part[(int64_t)b * d + c];
+    mu[c] = sum / (double)n;
+}
+
+// The centred coordinate x - mean, rounded once to float32 (the same
+// expression wherever it is formed).
+__device__ __forceinline__ float centred(float x, double mu)
+{
+    return (float)((double)x - mu);
+}
+
 __global__ __launch_bounds__(kThreads) void maxabs_kernel(const float *__restrict__ X,
-                                                          int64_t total,
+                                                          int64_t total, int d,
+                                                          const double *__restrict__ mu,
                                                           unsigned *__restrict__ scal)
 {
     __shared__ float red[kThreads / kWave];
     float mx = 0.0f;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x; t < total; t += stride)
-        mx = fmaxf(mx, fabsf(X[t]));
+        mx = fmaxf(mx, fabsf(centred(X[t], mu[t % d])));
 #pragma unroll
     for (int o = kWave / 2; o > 0; o >>= 1)
         mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
@@ -157,9 +210,9 @@ __device__ __forceinline__ int split_exponent(unsigned bits)
 }
 
 __global__ __launch_bounds__(kThreads) void split_kernel(
-    const float *__restrict__ X, int64_t n, int64_t np, int d, int nch, float c,
-    unsigned *__restrict__ scal, half8 *__restrict__ xh, float *__restrict__ beta,
-    float *__restrict__ cn)
+    const float *__restrict__ X, const double *__restrict__ mu, int64_t n, int64_t np, int d,
+    int nch, float c, unsigned *__restrict__ scal, half8 *__restrict__ xh,
+    float *__restrict__ beta, float *__restrict__ cn)
 {
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int S = split_exponent(scal[0]);
@@ -175,7 +228,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int k = 32 * ch + 8 * g + e;
-                const float x = (live && k < d) ? X[p * d + k] : 0.0f;
+                const float x = (live && k < d) ? centred(X[p * d + k], mu[k]) : 0.0f;
                 s = fma((double)x, (double)x, s);
                 const float xs = ldexpf(x, -S);
                 const _Float16 h = (_Float16)xs;
@@ -907,10 +960,12 @@ void sym_chunking(int64_t n, int64_t *chunk_cols, int *nchunks)
 int64_t al256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
 struct Ws {
-    unsigned *scal;     // [0] largest |x| (float bits), [1] m = -2 c 4^S
+    unsigned *scal;     // [0] largest |x - mean| (float bits), [1] m = -2 c 4^S
     half8 *xh;          // split operands, kMaxNch * 8 slots of np half8
     float *beta;        // [np]
     float *cn;          // [np]
+    double *mu;         // column means [32 kMaxNch]
+    double *mpart;      // their per-workgroup partials [kMeanBlocks][32 kMaxNch]
     double *part;       // per-chunk row sums, kMaxChunks * n
 };
 
@@ -927,6 +982,10 @@ Ws carve(void *ws, int64_t n)
     b += al256(np * 4);
     w.cn = reinterpret_cast<float *>(b);
     b += al256(np * 4);
+    w.mu = reinterpret_cast<double *>(b);
+    b += al256(32 * kMaxNch * 8);
+    w.mpart = reinterpret_cast<double *>(b);
+    b += al256((int64_t)kMeanBlocks * 32 * kMaxNch * 8);
     w.part = reinterpret_cast<double *>(b);
     return w;
 }
@@ -936,15 +995,19 @@ hipError_t launch_split(const float *X, int64_t n, int d, float c, const Ws &w,
 {
     const int64_t np = padded_points(n);
     hipLaunchKernelGGL(split_clear_kernel, dim3(1), dim3(1), 0, s, w.scal);
+    hipLaunchKernelGGL(col_mean_partials_kernel, dim3(kMeanBlocks), dim3(kThreads), 0, s, X, n,
+                       d, w.mpart);
+    hipLaunchKernelGGL(col_mean_finish_kernel, dim3(1), dim3(32 * kMaxNch), 0, s, w.mpart,
+                       kMeanBlocks, d, n, w.mu);
     const int64_t total = n * (int64_t)d;
     // few workgroups: each ends with one atomic on the same word
     int64_t blocks = (total + kThreads - 1) / kThreads;
     if (blocks > 256)
         blocks = 256;
     hipLaunchKernelGGL(maxabs_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, X,
-                       total, w.scal);
+                       total, d, w.mu, w.scal);
     hipLaunchKernelGGL(split_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, s, X, n, np, d, nch_for(d), c, w.scal, w.xh,
+                       dim3(kThreads), 0, s, X, w.mu, n, np, d, nch_for(d), c, w.scal, w.xh,
                        w.beta, w.cn);
     return hipGetLastError();
 }
@@ -1088,7 +1151,9 @@ size_t affinity_ws(int64_t n)
 {
     const int64_t np = padded_points(n);
     return (size_t)(256 + al256(np * kMaxNch * 8 * (int64_t)sizeof(half8)) +
-                    2 * al256(np * 4) + al256((int64_t)kMaxChunks * n * 8));
+                    2 * al256(np * 4) + al256(32 * kMaxNch * 8) +
+                    al256((int64_t)kMeanBlocks * 32 * kMaxNch * 8) +
+                    al256((int64_t)kMaxChunks * n * 8));
 }
 
 int64_t fused_blocks(int64_t n, int d)

@@ -47,7 +47,11 @@ def affinity_tolerance(X, sigma, A_ref, gram: bool):
     Direct differences (VALU engine): each squared distance carries a
     relative error of a few float32 ulps, (d + 4) eps32 dist2.
 
-    Gram form (matrix-core engine), u = 2^-24, M = max |x|:
+    Gram form (matrix-core engine), u = 2^-24, over the centred points
+    x = float32(x_raw - mean) (each centred coordinate rounded once: the
+    difference x_i - x_j is off by at most u (|x_ik| + |x_jk|) per
+    coordinate, which adds at most 4 u (|x_i|^2 + |x_j|^2) to dist2 for
+    the distances that matter here), M = max |x|:
       * every coordinate is scaled into [-1, 1] by 2^-S (2^S <= 2M) and
         split into half-precision parts hi + lo, which carry it to within
         max(2^-22 |x|, 2^-25 2^S) <= 2^-22 |x| + u M;
@@ -60,7 +64,7 @@ def affinity_tolerance(X, sigma, A_ref, gram: bool):
       * rounding |x_j|^2 / 2, c |x_i|^2 and the final multiply-add adds
         u (|x_i|^2 + |x_j|^2 + dist2).
     With 2 |x_i||x_j| <= |x_i|^2 + |x_j|^2 this gives, in dist2,
-      u [(6d + 16)(|x_i|^2 + |x_j|^2) + 2 M (|x_i|_1 + |x_j|_1)].
+      u [(6d + 20)(|x_i|^2 + |x_j|^2) + 2 M (|x_i|_1 + |x_j|_1)].
     Either engine: an error e in dist2 moves A = exp(-dist2 / (2 sigma^2))
     by A e / (2 sigma^2); the float32 coefficient c, exp2 and the final
     rounding add 4 eps32 dist2 and a few ulps of A.
@@ -73,9 +77,11 @@ def affinity_tolerance(X, sigma, A_ref, gram: bool):
         dist2 = -np.log(np.where(A_ref > 0, A_ref, 1.0)) * s2
     if gram:
         u = EPS32 / 2
-        l1 = np.abs(X64).sum(1)
-        M = float(np.abs(X64).max())
-        e = u * ((6 * d + 16) * (nrm[:, None] + nrm[None, :])
+        Xc = (X64 - X64.mean(0)).astype(np.float32).astype(np.float64)
+        nrmc = (Xc * Xc).sum(1)
+        l1 = np.abs(Xc).sum(1)
+        M = float(np.abs(Xc).max())
+        e = u * ((6 * d + 20) * (nrmc[:, None] + nrmc[None, :])
                  + 2 * M * (l1[:, None] + l1[None, :]))
     else:
         e = (d + 4) * EPS32 * dist2

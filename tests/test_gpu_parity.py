@@ -57,6 +57,28 @@ def test_affinity_parity(g, orc, n, d):
     np.testing.assert_allclose(deg.cpu().numpy(), Ag.sum(1), rtol=1e-13)
 
 
+@pytest.mark.parametrize("n,d,offset", [(700, 16, 1.0e4), (300, 64, -3.0e3), (257, 33, 250.0)])
+def test_affinity_offset_points(g, orc, n, d, offset):
+    """Points far from the origin (a common offset much larger than their
+    spread): the Gram form runs on centred coordinates, so its error scales
+    with the spread; against the oracle's difference form, the same bound
+    as for centred data, and the fused operator's degrees to 1e-5."""
+    X = (_pts(n, d, 3000 + d, scale=1.0) + np.float32(offset)).astype(np.float32)
+    sigma = np.float32(np.sqrt(d))
+    print(f"affinity offset n={n} d={d} offset={offset}", flush=True)
+    A, deg = g.gpic_affinity(_t(X), sigma)
+    torch.cuda.synchronize()
+    Ag = A[:, :n].cpu().numpy().astype(np.float64)
+    Ar = orc.affinity(X, sigma)
+    tol = affinity_tolerance(X, sigma, Ar, True)
+    err = np.abs(Ag - Ar)
+    assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
+    assert np.max(err) <= 1e-5 * np.max(Ar)
+    degf, _, _ = g.gpic_degree_fused(_t(X), sigma)
+    dr, _, _ = orc.degree_onthefly(X, sigma)
+    np.testing.assert_allclose(degf.cpu().numpy(), dr, rtol=1e-5)
+
+
 @pytest.mark.parametrize("n,d", [(2, 2), (3, 1), (64, 2), (1000, 2), (1023, 5),
                                  (300, 16), (257, 17), (99, 40)])
 def test_cosine_affinity_parity(g, orc, n, d):
