@@ -7,14 +7,20 @@
 // paper's method needs an affinity matrix; a kNN graph is its sparse form).
 //
 // Brute force in four steps, exact in the end:
-//   1. bound: for every row, the k-th smallest float32 squared distance to
-//      a fixed sample of 2^17 points (all points when n is smaller), which
-//      bounds the true k-th neighbour distance from above;
-//   2. collect: all n^2 squared distances on the fp32 matrix cores (Gram
-//      form over the centred points augmented as [x_j, |x_j|^2, 1] .
-//      [-2 x_i, 1, |x_i|^2]),
-//      appending every j that passes the row's bound widened by the float32
-//      error bounds of both forms to a per-row candidate list;
+//   1. bound: the points are put in Morton order of their quantised centred
+//      coordinates; for every row, the k-th smallest float32 squared
+//      distance to the points within 256 positions of it in that order and
+//      to a fixed sample of 65,536 positions, which bounds the true k-th
+//      neighbour distance from above;
+//   2. collect: squared distances on the fp32 matrix cores (Gram form over
+//      the centred points augmented as [x_j, |x_j|^2, 1] .
+//      [-2 x_i, 1, |x_i|^2]), appending every j that passes the row's bound
+//      widened by the float32 error bounds of both forms to a per-row
+//      candidate list.  In Morton order a tile of 64 consecutive points is
+//      spatially compact; a pair of tiles whose bounding boxes are farther
+//      apart than every bound of the row tile is skipped whole (no pair in
+//      it can be a neighbour: its true distance exceeds the row's bound,
+//      which is at least the true k-th neighbour distance);
 //   3. select: a wave per row recomputes the candidates' squared distances
 //      in float64 and keeps the k smallest (ties to the smaller index); a
 //      row whose list overflowed gets the k-th distance among the kept
@@ -29,7 +35,6 @@ namespace gpic {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int64_t kSample = 131072;       // points in the bound's sample
 constexpr int kCap = 2048;                // candidate slots per row
 constexpr int kPerLane = kCap / kWave;    // candidates per lane in the selection
 constexpr int kRowsPerGroup = 64;         // collect: 4 waves x 16 rows
@@ -59,64 +64,102 @@ __device__ __forceinline__ double sq_dist64(const float *__restrict__ X, int d, 
 
 // ------------------------------------------------------------ 1. bound
 
+// Thread per Morton position p, row i = perm[p]: the KT smallest float32
+// squared distances from x_i to the points at positions p - kWindow ..
+// p + kWindow and at the sample positions outside that window (every
+// n / kSample-th position, all of them when n is smaller; each point is
+// counted once), then tau_i = the k-th of them.  The k-th distance to any k
+// other points bounds the true k-th neighbour distance from above: Morton
+// neighbours are mostly near (a tight bound), the sample caps the bound
+// where the Morton order jumps.  Both sets go through LDS 256 points at a
+// time.
+constexpr int kWindow = 256;           // Morton positions on each side
+constexpr int64_t kSample = 65536;     // sample positions
+
 __device__ __forceinline__ int64_t sample_point(int64_t t, int64_t n, int64_t m)
 {
     return (m == n) ? t : (t * n) / m;
 }
 
-// Thread per row: the KT smallest float32 squared distances to the sample
-// (sorted, in registers), then tau_i = the k-th of them.
 template <int D, int KT>
 __global__ __launch_bounds__(kThreads) void knn_bound_kernel(
-    const float *__restrict__ X, int64_t n, int64_t m, int k, float *__restrict__ tau)
+    const float *__restrict__ X, const int32_t *__restrict__ perm, int64_t n, int k,
+    float *__restrict__ tau)
 {
     __shared__ float tile[kThreads * D];
-    __shared__ int64_t tidx[kThreads];
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    const int64_t ic = i < n ? i : n - 1;
+    __shared__ int64_t tid_[kThreads];
+    const int64_t p0 = (int64_t)blockIdx.x * kThreads;
+    const int64_t p = p0 + threadIdx.x;
+    const int64_t pc = p < n ? p : n - 1;
+    const int64_t i = perm[pc];
     float xi[D];
 #pragma unroll
     for (int c = 0; c < D; ++c)
-        xi[c] = X[ic * D + c];
+        xi[c] = X[i * D + c];
     float best[KT];
 #pragma unroll
-    for (int p = 0; p < KT; ++p)
-        best[p] = INFINITY;
+    for (int u = 0; u < KT; ++u)
+        best[u] = INFINITY;
+    auto consider = [&](const float *xj) {
+        float s = 0.0f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) {
+            const float df = xi[c] - xj[c];
+            s = fmaf(df, df, s);
+        }
+        if (s < best[KT - 1]) {
+#pragma unroll
+            for (int u = KT - 1; u > 0; --u) {
+                const float lo = best[u - 1];
+                best[u] = (s < lo) ? lo : fminf(s, best[u]);
+            }
+            best[0] = fminf(s, best[0]);
+        }
+    };
+    // the Morton window (positions, skipping p and anything beyond kWindow)
+    for (int64_t q0 = p0 - kWindow; q0 < p0 + kThreads + kWindow; q0 += kThreads) {
+        __syncthreads();
+        const int64_t q = q0 + threadIdx.x;
+        const bool ok = q >= 0 && q < n;
+        const int64_t pt = ok ? (int64_t)perm[q] : 0;
+#pragma unroll
+        for (int c = 0; c < D; ++c)
+            tile[threadIdx.x * D + c] = ok ? X[pt * D + c] : 0.0f;
+        __syncthreads();
+        for (int u = 0; u < kThreads; ++u) {
+            const int64_t qq = q0 + u;
+            if (qq < 0 || qq >= n || qq == pc || qq < pc - kWindow || qq > pc + kWindow)
+                continue;
+            consider(tile + u * D);
+        }
+    }
+    // the sample positions outside the window (the window already holds
+    // the others, and the row itself)
+    const int64_t m = n < kSample ? n : kSample;
     for (int64_t t0 = 0; t0 < m; t0 += kThreads) {
         __syncthreads();
         const int64_t t = t0 + threadIdx.x;
-        const int64_t j = (t < m) ? sample_point(t, n, m) : -1;
-        tidx[threadIdx.x] = j;
+        const int64_t q = (t < m) ? sample_point(t, n, m) : -1;
+        tid_[threadIdx.x] = q;
+        const int64_t pt = (q >= 0) ? (int64_t)perm[q] : 0;
 #pragma unroll
         for (int c = 0; c < D; ++c)
-            tile[threadIdx.x * D + c] = (j >= 0) ? X[j * D + c] : 0.0f;
+            tile[threadIdx.x * D + c] = (q >= 0) ? X[pt * D + c] : 0.0f;
         __syncthreads();
         const int cnt = (m - t0 < kThreads) ? (int)(m - t0) : kThreads;
         for (int u = 0; u < cnt; ++u) {
-            if (tidx[u] == ic)
+            const int64_t qq = tid_[u];
+            if (qq >= pc - kWindow && qq <= pc + kWindow)
                 continue;
-            float s = 0.0f;
-#pragma unroll
-            for (int c = 0; c < D; ++c) {
-                const float df = xi[c] - tile[u * D + c];
-                s = fmaf(df, df, s);
-            }
-            if (s < best[KT - 1]) {
-#pragma unroll
-                for (int p = KT - 1; p > 0; --p) {
-                    const float lo = best[p - 1];
-                    best[p] = (s < lo) ? lo : fminf(s, best[p]);
-                }
-                best[0] = fminf(s, best[0]);
-            }
+            consider(tile + u * D);
         }
     }
-    if (i < n) {
+    if (p < n) {
         float t = best[0];
 #pragma unroll
-        for (int p = 1; p < KT; ++p)
-            if (p == k - 1)
-                t = best[p];
+        for (int u = 1; u < KT; ++u)
+            if (u == k - 1)
+                t = best[u];
         tau[i] = t;
     }
 }
@@ -203,25 +246,28 @@ __global__ void mean_finish_kernel(const double *__restrict__ part, int nb, int 
 // column xa[k * np + p] = [x'_p, |x'_p|^2, 1, 0...], row
 // xb[p * KP + k] = [-2 x'_p, 1, |x'_p|^2, 0...]; |x'_p|^2 a float64 sum
 // rounded once (also written to norm2).  Padding points are zeros.
+// With perm, position p holds point perm[p] (norm2 stays indexed by point).
 __global__ __launch_bounds__(kThreads) void knn_augment_kernel(
-    const float *__restrict__ X, const double *__restrict__ mu, int64_t n, int64_t np, int d,
-    int KP, float *__restrict__ xa, float *__restrict__ xb, float *__restrict__ norm2)
+    const float *__restrict__ X, const double *__restrict__ mu, const int32_t *__restrict__ perm,
+    int64_t n, int64_t np, int d, int KP, float *__restrict__ xa, float *__restrict__ xb,
+    float *__restrict__ norm2)
 {
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (p >= np)
         return;
+    const int64_t pt = (p < n && perm != nullptr) ? (int64_t)perm[p] : p;
     float xc[16];
     double s = 0.0;
     for (int c = 0; c < 16; ++c) {
         xc[c] = 0.0f;
         if (c < d && p < n) {
-            xc[c] = (float)((double)X[p * d + c] - mu[c]);
+            xc[c] = (float)((double)X[pt * d + c] - mu[c]);
             s = fma((double)xc[c], (double)xc[c], s);
         }
     }
     const float nrm = (float)s;
     if (p < n)
-        norm2[p] = nrm;
+        norm2[pt] = nrm;
     for (int k = 0; k < KP; ++k) {
         float a = 0.0f, b = 0.0f;
         if (p < n) {
@@ -241,6 +287,59 @@ __global__ __launch_bounds__(kThreads) void knn_augment_kernel(
     }
 }
 
+// Morton key of point p: its centred coordinates quantised to b = min(64 / d,
+// 32) bits over [-R, R] (R^2 = the largest |x - mean|^2), bits interleaved
+// from the most significant down; the payload is the point's index.
+__global__ __launch_bounds__(kThreads) void morton_key_kernel(
+    const float *__restrict__ X, const double *__restrict__ mu,
+    const unsigned int *__restrict__ maxn, int64_t n, int d, uint64_t *__restrict__ key,
+    int32_t *__restrict__ idx)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= n)
+        return;
+    const double R = sqrt((double)__uint_as_float(*maxn));
+    const int b = (64 / d < 32) ? 64 / d : 32;
+    const double levels = ldexp(1.0, b);
+    uint32_t q[16];
+    for (int c = 0; c < d; ++c) {
+        const double xc = (double)(float)((double)X[p * d + c] - mu[c]);
+        double u = (R > 0.0) ? (xc + R) / (2.0 * R) * levels : 0.0;
+        u = u < 0.0 ? 0.0 : (u > levels - 1.0 ? levels - 1.0 : u);
+        q[c] = (uint32_t)u;
+    }
+    uint64_t k = 0;
+    for (int l = b - 1; l >= 0; --l)
+        for (int c = 0; c < d; ++c)
+            k = (k << 1) | ((q[c] >> l) & 1u);
+    key[p] = k;
+    idx[p] = (int32_t)p;
+}
+
+// Bounding box of the raw coordinates of every tile of kTileCols
+// consecutive positions: box[t][c] = min, box[t][16 + c] = max.  A thread
+// per (tile, coordinate); padding positions are left out.
+__global__ __launch_bounds__(kThreads) void tile_box_kernel(
+    const float *__restrict__ X, const int32_t *__restrict__ perm, int64_t n, int d,
+    int64_t ntiles, float *__restrict__ box)
+{
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= ntiles * 16)
+        return;
+    const int64_t t = e / 16;
+    const int c = (int)(e % 16);
+    if (c >= d)
+        return;
+    float lo = INFINITY, hi = -INFINITY;
+    for (int64_t p = t * kTileCols; p < (t + 1) * kTileCols && p < n; ++p) {
+        const float x = X[(int64_t)perm[p] * d + c];
+        lo = fminf(lo, x);
+        hi = fmaxf(hi, x);
+    }
+    box[t * 32 + c] = lo;
+    box[t * 32 + 16 + c] = hi;
+}
+
 // 4 waves x 16 rows; all columns in tiles of 64 through double-buffered
 // LDS (coordinate-major, XOR-swizzled as in the affinity engine);
 // v_mfma_f32_16x16x4f32 with the A operand on the columns and the B operand
@@ -250,24 +349,49 @@ __global__ __launch_bounds__(kThreads) void knn_augment_kernel(
 // slots beyond kCap are counted, not written).
 template <int KS>
 __global__ __launch_bounds__(kThreads) void knn_collect_kernel(
-    const float *__restrict__ xa, int64_t np, const float *__restrict__ xb, int64_t n,
+    const float *__restrict__ xa, int64_t np, const float *__restrict__ xb, int64_t n, int d,
+    const int32_t *__restrict__ perm, const float *__restrict__ box,
     const float *__restrict__ thr, int *__restrict__ count, int32_t *__restrict__ cand)
 {
     constexpr int KP = 4 * KS;
     constexpr int kRow4 = kTileCols / 4;
+    static_assert(kRowsPerGroup == kTileCols, "a row group is one tile");
     __shared__ floatx4 xs[2][KP * kRow4];
+    __shared__ int tl[kThreads];                 // column tiles of the current chunk
+    __shared__ int wcnt[kThreads / kWave];
+    __shared__ float wmax[kThreads / kWave];
+    __shared__ float rbox[32];
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
     const int g = lane >> 4;
     const int m = lane & 15;
     const int64_t wrow0 = (int64_t)blockIdx.x * kRowsPerGroup + wave * 16;
-    const int64_t i = wrow0 + m;
+    const int64_t i = wrow0 + m;                 // position in Morton order
     const int64_t ic = i < n ? i : n - 1;
-    const float t_i = (i < n) ? thr[i] : -1.0f;
+    const int64_t io = (i < n) ? (int64_t)perm[i] : -1;   // the point it holds
+    const float t_i = (i < n) ? thr[io] : -1.0f;
 
     // a workgroup with no active row has nothing to collect
     if (__syncthreads_or(t_i >= 0.0f) == 0)
         return;
+
+    // the largest bound among the workgroup's rows, and their box
+    float tm = t_i;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1)
+        tm = fmaxf(tm, __shfl_xor(tm, o, kWave));
+    if (lane == 0)
+        wmax[wave] = tm;
+    if (threadIdx.x < 32)
+        rbox[threadIdx.x] = box[(int64_t)blockIdx.x * 32 + threadIdx.x];
+    __syncthreads();
+    float tmax = wmax[0];
+#pragma unroll
+    for (int w = 1; w < kThreads / kWave; ++w)
+        tmax = fmaxf(tmax, wmax[w]);
+    // a tile is skipped when the squared gap between the boxes (float64,
+    // exact differences of float32 coordinates) exceeds every bound
+    const double cut = (double)tmax * (1.0 + 1e-12);
 
     float bop[KS];
 #pragma unroll
@@ -298,14 +422,45 @@ __global__ __launch_bounds__(kThreads) void knn_collect_kernel(
     };
 
     const int64_t ntiles = (n + kTileCols - 1) / kTileCols;
-    fetch(0);
+    for (int64_t c0 = 0; c0 < ntiles; c0 += kThreads) {
+    // this chunk's tiles that may hold neighbours, in order
+    bool pass = false;
+    const int64_t tt = c0 + threadIdx.x;
+    if (tt < ntiles) {
+        const float *bx = box + tt * 32;
+        double lb = 0.0;
+        for (int c = 0; c < d; ++c) {
+            double gap = (double)bx[c] - (double)rbox[16 + c];
+            const double g2 = (double)rbox[c] - (double)bx[16 + c];
+            gap = gap > g2 ? gap : g2;
+            if (gap > 0.0)
+                lb += gap * gap;
+        }
+        pass = !(lb > cut);
+    }
+    const unsigned long long bal = __ballot(pass);
+    if (lane == 0)
+        wcnt[wave] = __popcll(bal);
+    __syncthreads();
+    int before = 0, cnt = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / kWave; ++w) {
+        before += (w < wave) ? wcnt[w] : 0;
+        cnt += wcnt[w];
+    }
+    if (pass)
+        tl[before + __popcll(bal & ((lane == 0) ? 0ull : (~0ull >> (kWave - lane))))] = (int)tt;
+    __syncthreads();
+    if (cnt == 0)
+        continue;                                // uniform over the workgroup
+    fetch((int64_t)tl[0] * kTileCols);
     commit(0);
     __syncthreads();
-    for (int64_t t = 0; t < ntiles; ++t) {
-        const int buf = (int)(t & 1);
-        const int64_t jt = t * kTileCols;
-        if (t + 1 < ntiles)
-            fetch(jt + kTileCols);
+    for (int u = 0; u < cnt; ++u) {
+        const int buf = u & 1;
+        const int64_t jt = (int64_t)tl[u] * kTileCols;
+        if (u + 1 < cnt)
+            fetch((int64_t)tl[u + 1] * kTileCols);
         const float *tile = reinterpret_cast<const float *>(xs[buf]) + g * kTileCols;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -320,16 +475,18 @@ __global__ __launch_bounds__(kThreads) void knn_collect_kernel(
             for (int r = 0; r < 4; ++r) {
                 const int64_t j = j0 + r;
                 if (t_i >= 0.0f && cacc[r] <= t_i && j < n && j != i) {
-                    const int c = atomicAdd(&count[i], 1);
+                    const int c = atomicAdd(&count[io], 1);
                     if (c < kCap)
-                        cand[i * kCap + c] = (int32_t)j;
+                        cand[io * kCap + c] = perm[j];
                 }
             }
         }
-        if (t + 1 < ntiles) {
+        if (u + 1 < cnt) {
             commit(buf ^ 1);
             __syncthreads();
         }
+    }
+    __syncthreads();                             // tl and xs are refilled next chunk
     }
 }
 
@@ -480,7 +637,7 @@ int bits_for(int64_t n)
 
 struct KnnLayout {
     size_t xa, xb, mpart, mu, tau, norm2, maxn, thr, count, active, cand, nbr, kth, flags,
-        keyA, keyB, first, hist, hsum, total;
+        keyA, keyB, first, hist, hsum, permA, permB, box, total;
 };
 
 KnnLayout knn_layout(int64_t n, int32_t k)
@@ -514,31 +671,34 @@ KnnLayout knn_layout(int64_t n, int32_t k)
     L.hist = take((int64_t)radix_hist_bytes(m));
     L.hsum = take((int64_t)(radix_hsum_bytes(m) > scan_sums_bytes(m) ? radix_hsum_bytes(m)
                                                                       : scan_sums_bytes(m)));
+    L.permA = take(n * 4);
+    L.permB = take(n * 4);
+    L.box = take(np / kTileCols * 32 * 4);
     L.total = o;
     return L;
 }
 
 template <int D>
-void launch_bound(int KT, const float *X, int64_t n, int64_t m, int k, float *tau,
+void launch_bound(int KT, const float *X, const int32_t *perm, int64_t n, int k, float *tau,
                   hipStream_t s)
 {
     const dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
     switch (KT) {
     case 8:
-        hipLaunchKernelGGL((knn_bound_kernel<D, 8>), grid, dim3(kThreads), 0, s, X, n, m, k,
+        hipLaunchKernelGGL((knn_bound_kernel<D, 8>), grid, dim3(kThreads), 0, s, X, perm, n, k,
                            tau);
         break;
     case 16:
-        hipLaunchKernelGGL((knn_bound_kernel<D, 16>), grid, dim3(kThreads), 0, s, X, n, m, k,
-                           tau);
+        hipLaunchKernelGGL((knn_bound_kernel<D, 16>), grid, dim3(kThreads), 0, s, X, perm, n,
+                           k, tau);
         break;
     case 32:
-        hipLaunchKernelGGL((knn_bound_kernel<D, 32>), grid, dim3(kThreads), 0, s, X, n, m, k,
-                           tau);
+        hipLaunchKernelGGL((knn_bound_kernel<D, 32>), grid, dim3(kThreads), 0, s, X, perm, n,
+                           k, tau);
         break;
     default:
-        hipLaunchKernelGGL((knn_bound_kernel<D, 64>), grid, dim3(kThreads), 0, s, X, n, m, k,
-                           tau);
+        hipLaunchKernelGGL((knn_bound_kernel<D, 64>), grid, dim3(kThreads), 0, s, X, perm, n,
+                           k, tau);
         break;
     }
 }
@@ -568,12 +728,40 @@ hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
     const unsigned rows_grid = (unsigned)((n + kThreads - 1) / kThreads);
     *status_host = 0;
 
-    // 1. bound
-    const int64_t m = n < kSample ? n : kSample;
+    if (d < 1 || d > 16)
+        return hipErrorInvalidValue;
+    const int KS = ks_for(d);
+    const int64_t np = padded_points(n);
+    hipLaunchKernelGGL(mean_partials_kernel, dim3(kMeanBlocks), dim3(kThreads), 0, s, X, n, d,
+                       mpart);
+    hipLaunchKernelGGL(mean_finish_kernel, dim3(1), dim3(64), 0, s, mpart, kMeanBlocks, d, n,
+                       mu);
+    const unsigned pgrid = (unsigned)((np + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(knn_augment_kernel, dim3(pgrid), dim3(kThreads), 0, s, X, mu,
+                       (const int32_t *)nullptr, n, np, d, 4 * KS, xa, xb, norm2);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, s, (int *)maxn,
+                       (int64_t)1, 0);
+    hipLaunchKernelGGL(max_norm_kernel, dim3(1024), dim3(kThreads), 0, s, norm2, n, maxn);
+    // Morton order of the points, the operands in that order, tile boxes
+    int32_t *perm = (int32_t *)(w + L.permA), *permB = (int32_t *)(w + L.permB);
+    uint64_t *mkA = keyA, *mkB = keyB;
+    hipLaunchKernelGGL(morton_key_kernel, dim3(rows_grid), dim3(kThreads), 0, s, X, mu,
+                       (const unsigned int *)maxn, n, d, mkA, perm);
+    hipError_t e0 = radix_sort_u64(mkA, perm, mkB, permB, n, 64, hist, hsum, s);
+    if (e0 != hipSuccess)
+        return e0;
+    hipLaunchKernelGGL(knn_augment_kernel, dim3(pgrid), dim3(kThreads), 0, s, X, mu,
+                       (const int32_t *)perm, n, np, d, 4 * KS, xa, xb, norm2);
+    const int64_t ntiles = np / kTileCols;
+    float *box = (float *)(w + L.box);
+    hipLaunchKernelGGL(tile_box_kernel, dim3((unsigned)((ntiles * 16 + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, X, (const int32_t *)perm, n, d, ntiles, box);
+
+    // 1. bound, over the Morton neighbours
     const int KT = k <= 8 ? 8 : k <= 16 ? 16 : k <= 32 ? 32 : 64;
 #define GPIC_BOUND(D)                                                          \
     case D:                                                                    \
-        launch_bound<D>(KT, X, n, m, k, tau, s);                               \
+        launch_bound<D>(KT, X, perm, n, k, tau, s);                            \
         break;
     switch (d) {
         GPIC_BOUND(1) GPIC_BOUND(2) GPIC_BOUND(3) GPIC_BOUND(4) GPIC_BOUND(5) GPIC_BOUND(6)
@@ -583,17 +771,6 @@ hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
         return hipErrorInvalidValue;
     }
 #undef GPIC_BOUND
-    const int KS = ks_for(d);
-    const int64_t np = padded_points(n);
-    hipLaunchKernelGGL(mean_partials_kernel, dim3(kMeanBlocks), dim3(kThreads), 0, s, X, n, d,
-                       mpart);
-    hipLaunchKernelGGL(mean_finish_kernel, dim3(1), dim3(64), 0, s, mpart, kMeanBlocks, d, n,
-                       mu);
-    hipLaunchKernelGGL(knn_augment_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, s, X, mu, n, np, d, 4 * KS, xa, xb, norm2);
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, s, (int *)maxn,
-                       (int64_t)1, 0);
-    hipLaunchKernelGGL(max_norm_kernel, dim3(1024), dim3(kThreads), 0, s, norm2, n, maxn);
     hipLaunchKernelGGL(threshold_kernel, dim3(rows_grid), dim3(kThreads), 0, s, tau,
                        (const double *)nullptr, norm2, maxn, n, d, 4 * KS,
                        (const int *)nullptr, thr);
@@ -605,10 +782,12 @@ hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
         const dim3 cgrid((unsigned)((n + kRowsPerGroup - 1) / kRowsPerGroup));
         if (KS <= 3)
             hipLaunchKernelGGL(knn_collect_kernel<3>, cgrid, dim3(kThreads), 0, s, xa, np,
-                               xb, n, thr, count, cand);
+                               xb, n, d, (const int32_t *)perm, (const float *)box, thr, count,
+                               cand);
         else
             hipLaunchKernelGGL(knn_collect_kernel<5>, cgrid, dim3(kThreads), 0, s, xa, np,
-                               xb, n, thr, count, cand);
+                               xb, n, d, (const int32_t *)perm, (const float *)box, thr, count,
+                               cand);
         hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, s, flags, (int64_t)1,
                            0);
         hipLaunchKernelGGL(knn_select_kernel,
