@@ -540,7 +540,8 @@ def _check_knn(g, orc, X, k, sigma):
 
 @pytest.mark.parametrize("n,d,k,shift", [(3000, 8, 32, 0.0), (40, 3, 39, 0.0),
                                          (2000, 16, 10, 0.0), (2000, 8, 16, 1000.0),
-                                         (5001, 2, 7, 0.0)])
+                                         (5001, 2, 7, 0.0), (3000, 1, 5, 0.0),
+                                         (1500, 4, 64, 0.0)])
 def test_knn_graph_parity(g, orc, n, d, k, shift):
     """The exact kNN graph against the oracle's brute force: same rows,
     columns and weights (k = n - 1, d = 16, points far from the origin)."""
