@@ -207,13 +207,14 @@ gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k,
 size_t gpic_sym_bytes(int64_t n);
 
 /* Affinity A into the symmetric storage As (gpic_sym_bytes(n) bytes,
- * 16-byte aligned, caller-allocated), with the degrees
- * d_i = sum_j A_ij (float64, summed over whole rows from the same float32
- * values the dense path computes), v0 = d / sum(d) and the zero-degree row
- * count (as gpic_affinity_normalized; GPIC_ERR_NUMERIC when sum(D) is zero
- * or not finite, a check that synchronises the stream).  Stored entries are
- * the upper ones: A_ij as computed for row i, for block(i) <= block(j).
- * ws: gpic_workspace_bytes(GPIC_OP_AFFINITY_SYM, n, 0, 0). */
+ * 16-byte aligned, caller-allocated), with the degrees d_i = sum_j A_ij
+ * (float64 row sums of the stored symmetric A, taken by the symmetric
+ * product with v = 1, so the rows of D^-1 A sum to 1 up to float64
+ * rounding), v0 = d / sum(d) and the zero-degree row count (as
+ * gpic_affinity_normalized; GPIC_ERR_NUMERIC when sum(D) is zero or not
+ * finite, a check that synchronises the stream).  Stored entries are the
+ * upper ones: A_ij as computed for row i, for block(i) <= block(j), used
+ * for A_ji as well.  ws: gpic_workspace_bytes(GPIC_OP_AFFINITY_SYM, n, 0, 0). */
 gpic_status gpic_affinity_sym(const float *X, int64_t n, int32_t d, float sigma,
                               float *As, double *degree, double *v0,
                               int64_t *n_zero_rows, void *ws, size_t ws_bytes,

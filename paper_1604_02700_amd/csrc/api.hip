@@ -98,6 +98,14 @@ size_t pi_csr_ws(int64_t n, int64_t nnz)
 // the fused product's own scratch follows the power-iteration layout
 size_t pi_fused_ws(int64_t n) { return pi_ws(n, fused_nb_bound(n)) + al(fused_ws(n)); }
 
+// A into the symmetric storage, then its row sums by the symmetric product:
+// the affinity scratch, reused for the product's partial sums
+size_t sym_aff_ws(int64_t n)
+{
+    const size_t a = aff_ws(n), b = al(sym_part_bytes(n));
+    return a > b ? a : b;
+}
+
 // the symmetric product's partial sums follow the power-iteration layout
 size_t pi_sym_ws(int64_t n) { return pi_ws(n, sym_blocks(n)) + al(sym_part_bytes(n)); }
 
@@ -472,7 +480,7 @@ size_t gpic_workspace_bytes(int32_t op, int64_t n, int64_t nnz, int32_t k)
     case GPIC_OP_AFFINITY_COSINE_NORMALIZED: return start_ws(n) + al(cosine_ws(n));
     case GPIC_OP_KNN_GRAPH:
         return (k >= 1 && k <= 64 && n >= 2) ? al(knn_graph_ws(n, k)) : 0;
-    case GPIC_OP_AFFINITY_SYM: return start_ws(n) + aff_ws(n);
+    case GPIC_OP_AFFINITY_SYM: return start_ws(n) + sym_aff_ws(n);
     case GPIC_OP_MATVEC_SYM: return al(sym_part_bytes(n));
     case GPIC_OP_PI_SYM: return pi_sym_ws(n);
     case GPIC_OP_PI_DENSE_HOST: return (n >= 2 && n <= kMaxN) ? pi_host_ws(n) : 0;
@@ -558,18 +566,23 @@ gpic_status gpic_affinity_sym(const float *X, int64_t n, int32_t d, float sigma,
         return st;
     CHECK_ARG(n_zero_rows == nullptr || aligned(n_zero_rows, 8),
               "n_zero_rows misaligned");
-    if ((st = check_ws(ws, ws_bytes, start_ws(n) + aff_ws(n))) != GPIC_OK)
+    if ((st = check_ws(ws, ws_bytes, start_ws(n) + sym_aff_ws(n))) != GPIC_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
     float c;
     gauss_coefficient(sigma, &c);
     void *aws = static_cast<char *>(ws) + start_ws(n);
-    CHECK_HIP(launch_fused_degree(X, n, d, c, degree, aws, s), "degree sweep");
+    CHECK_HIP(launch_affinity_sym(X, n, d, c, As, aws, s), "symmetric A sweep");
+    // the degrees are the row sums of the stored symmetric A (the product
+    // with v = 1, no division), so the rows of D^-1 A sum to 1
+    StopCtl none{};
+    CHECK_HIP(launch_sym_gemv(As, n, nullptr, nullptr, degree, static_cast<double *>(aws),
+                              nullptr, none, false, s),
+              "degrees");
     int bad = 0;
     CHECK_HIP(launch_start_vector(degree, n, v0, n_zero_rows, ws, s, &bad), "v0");
     if (bad)
         return fail(GPIC_ERR_NUMERIC, "sum of degrees is zero or not finite");
-    CHECK_HIP(launch_affinity_sym(X, n, d, c, As, aws, s), "symmetric A sweep");
     return GPIC_OK;
 }
 

@@ -202,7 +202,9 @@ hipError_t launch_init_state(double *ring, int64_t ring_len, int *err,
 // sym.hip -- y = D^-1 (A v) over the packed upper tiles of a symmetric A:
 // blocks of 256 indices (sym_blocks), storage bytes, the per-product
 // partial sums (sym_part_bytes, caller scratch); two launches, the second
-// writing one |y| partial per block of 256 rows when partial != nullptr
+// writing one |y| partial per block of 256 rows when partial != nullptr;
+// v == nullptr stands for v = 1 and degree == nullptr for no division
+// (then y holds the row sums A v)
 int64_t sym_blocks(int64_t n);
 size_t sym_storage_bytes(int64_t n);
 size_t sym_part_bytes(int64_t n);

@@ -80,7 +80,7 @@ __device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I,
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
         const int64_t col = cJ + 128 * (c >> 2) + 4 * tx + (c & 3);
-        vj[c] = (!EDGE || col < n) ? v[col] : 0.0;
+        vj[c] = (!EDGE || col < n) ? (v != nullptr ? v[col] : 1.0) : 0.0;
     }
     double cacc[8];
 #pragma unroll
@@ -101,7 +101,7 @@ __device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I,
             const floatx4 w1 = __builtin_nontemporal_load(rp + 32);
             const int64_t row = cI + 64 * p + 8 * ty + k;
             const bool rowok = !EDGE || row < n;
-            const double vi = rowok ? v[row] : 0.0;
+            const double vi = rowok ? (v != nullptr ? v[row] : 1.0) : 0.0;
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
                 float af = (c < 4) ? w0[c & 3] : w1[c & 3];
@@ -212,10 +212,14 @@ __global__ __launch_bounds__(kThreads * kSlices) void sym_finalize_kernel(
     double yabs = 0.0;
     if (sidx == 0 && i < n) {
         const double t = ((sl[0][r] + sl[1][r]) + sl[2][r]) + sl[3][r];
-        const double di = degree[i];
-        const double yi = (di == 0.0) ? 0.0 : t / di;
-        y[i] = yi;
-        yabs = fabs(yi);
+        if (degree == nullptr) {
+            y[i] = t;                            // the row sums themselves
+        } else {
+            const double di = degree[i];
+            const double yi = (di == 0.0) ? 0.0 : t / di;
+            y[i] = yi;
+            yabs = fabs(yi);
+        }
     }
     // every wave takes part; those of slices 1..3 add zeros
     const double sum = block_sum<kThreads * kSlices>(yabs, red);
