@@ -250,7 +250,7 @@ constexpr int kFSmall = 64;
 constexpr int kFLarge = 8;
 constexpr int64_t kFLargeFrom = (int64_t)1 << 18;
 constexpr int kMaxLevels = 16;
-constexpr int kShortScan = 32;        // longer ranges go to the work queue
+constexpr int kShortScan = 64;        // longer ranges go to the work queue
 // candidates per queued part and samples evaluated per pass over it: F = 8
 // (large n) shares each candidate read among all 8 samples; F = 64 (small
 // n) keeps more, smaller work items, since the grid would otherwise be
