@@ -28,11 +28,17 @@
  *     Arguments are validated on the host before any launch.  On an error
  *     the outputs are unspecified; gpic_last_error() gives the text
  *     (thread-local).
- *   - Layouts: points X are float32 [n x d] row-major (16-byte aligned);
+ *   - Layouts: points X are float32 [n x d] row-major (4-byte aligned);
  *     dense A / W are float32 [n x lda] row-major, only the first n columns
  *     of each row are read or written, lda % 4 == 0, base 16-byte aligned.
  *     Vectors v, delta, degree, v0 are float64 [n], 16-byte aligned.
  *     CSR graphs: row_ptr int64 [n+1], col int32 [nnz], val float32 [nnz].
+ *     gpic_degree_normalize_csr and gpic_power_iterate_csr check the
+ *     structure on the device before any kernel indexes through it (row_ptr
+ *     nondecreasing from 0 to nnz, every column in [0, n); otherwise
+ *     GPIC_ERR_INVALID_ARG, a check that synchronises the stream);
+ *     gpic_matvec_csr, which takes no workspace, relies on a graph one of
+ *     those calls has accepted.
  *   - Floating point: stored matrices and points are float32; every
  *     accumulation and all iteration state (v, delta, the L1 norm, the stop
  *     statistic, degrees) are float64.  Reductions are deterministic (fixed
@@ -272,7 +278,9 @@ gpic_status gpic_matvec_sym(const float *As, int64_t n, const double *degree,
                             const double *v, double *y, void *ws, size_t ws_bytes,
                             void *stream);
 
-/* One product over a CSR W.  Asynchronous. */
+/* One product over a CSR W, rows in storage order, accumulated in float64.
+ * The structure is not checked here (see the layout notes at the top).
+ * Asynchronous. */
 gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
                             const float *val, int64_t n, int64_t nnz,
                             const double *v, double *y, void *stream);

@@ -38,7 +38,7 @@ using namespace gpic;
 namespace {
 
 constexpr int64_t kMaxN = 2147483647LL;     // indices are int32 in places
-constexpr int64_t kMaxKmeansN = 1LL << 30;  // keeps the split-point recursion within 5 levels
+constexpr int64_t kMaxKmeansN = 1LL << 30;  // the split-point recursion indexes nodes in 32 bits
 constexpr int64_t kRing = 1024;             // statistic slots on the device
 constexpr int64_t kMaxSymN = 1LL << 24;     // one workgroup per stored tile: < 2^31 tiles
 constexpr size_t kCtlBytes = 256;           // err @0, tau @8, csr flag @16
