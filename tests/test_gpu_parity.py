@@ -602,7 +602,8 @@ def _unpack_sym(As, n):
     t = 0
     for I in range(nb):
         for J in range(I, nb):
-            blk = a[t * 65536:(t + 1) * 65536].reshape(256, 256).astype(np.float64)
+            with np.errstate(invalid="ignore"):      # padding past n is never written
+                blk = a[t * 65536:(t + 1) * 65536].reshape(256, 256).astype(np.float64)
             full[256 * I:256 * I + 256, 256 * J:256 * J + 256] = blk
             if I != J:
                 full[256 * J:256 * J + 256, 256 * I:256 * I + 256] = blk.T
