@@ -11,8 +11,10 @@ Prints one JSON line.  `value` is the power-iteration rate in GB/s of W
 streamed (4 bytes per stored entry, 50 updates per step, divided by the
 power-iteration time); `ms_per_step` is the end-to-end step.  The roofline
 object is for the dominant kernel (the dense product), timed with HIP events
-on the library's stream; cpu_baseline is the float64 oracle on a bounded
-sample of the same workload on the host cores.
+on the library's stream, and also as a fraction of the plain read stream
+the device reaches over the same buffer in the same run (read_stream);
+cpu_baseline is the float64 oracle on a bounded sample of the same workload
+on the host cores.
 """
 from __future__ import annotations
 
@@ -174,18 +176,39 @@ def main():
     W = A
     y = torch.empty(n, dtype=torch.float64, device=dev)
     g.gpic_matvec_dense(W, v, y, n=n)
-    # one event pair around every launch, on the library's stream
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.gemv_reps)]
-    for a, b in evs:
-        a.record(stream)
-        g.gpic_matvec_dense(W, v, y, n=n)
-        b.record(stream)
+    # back-to-back launches between one event pair on the library's stream:
+    # the average launch duration (events around every launch would add the
+    # recording itself to each)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    gemv_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    ev0.record(stream)
+    for _ in range(args.gemv_reps):
+        g.gpic_matvec_dense(W, v, y, n=n)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    gemv_ms = ev0.elapsed_time(ev1) / args.gemv_reps
     alg_bytes = wbytes + 16.0 * n            # W once, v read, y written
     achieved = alg_bytes / (gemv_ms * 1e-3) / 1e9
     log(f"bench: product {gemv_ms:.4f} ms/launch, {achieved:.1f} GB/s")
+
+    # the plain read stream over the same buffer: the read ceiling this
+    # device reaches in the same run, timed like the product
+    rs_n = W.numel() // 4 * 4
+    sink = g.gpic_read_stream(W, rs_n)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.gemv_reps):
+        g.gpic_read_stream(W, rs_n, sink)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    rs_ms = ev0.elapsed_time(ev1) / args.gemv_reps
+    rs_gbs = 4.0 * rs_n / (rs_ms * 1e-3) / 1e9
+    read_stream = {"kernel": "read_stream_kernel", "bytes_per_launch": 4 * rs_n,
+                   "avg_launch_ms": round(rs_ms, 5), "gbs": round(rs_gbs, 1),
+                   "frac_of_peak": round(rs_gbs / HBM_PEAK_GBS, 4)}
+    log(f"bench: read stream {rs_ms:.4f} ms/launch, {rs_gbs:.1f} GB/s")
+    del sink
 
     conv = None
     if not args.no_converge:
@@ -271,7 +294,9 @@ def main():
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "avg_launch_ms": round(gemv_ms, 5),
-                     "bytes_per_launch": alg_bytes},
+                     "bytes_per_launch": alg_bytes,
+                     "frac_of_read_stream": round(achieved / rs_gbs, 4)},
+        "read_stream": read_stream,
         "symmetric_storage": sym,
         "cpu_baseline": cpu,
         "copy_reference": copy_ref,

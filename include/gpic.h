@@ -377,6 +377,19 @@ gpic_status gpic_kmeans1d(const double *v, int64_t n, int32_t k,
                           double *cost, void *ws, size_t ws_bytes,
                           void *stream);
 
+/* ------------------------------------------- 6. bandwidth reference */
+
+/* Length of the sink gpic_read_stream writes. */
+#define GPIC_READ_STREAM_SINK 1536
+
+/* Reads the n floats of x (device, 16-byte aligned, n a positive multiple
+ * of 4) once with 16-byte non-temporal loads over GPIC_READ_STREAM_SINK
+ * workgroups, each writing the float64 sum of what it read to sink (device,
+ * float64 [GPIC_READ_STREAM_SINK], 16-byte aligned).  Not a step of the
+ * method: the plain read stream the dense product (a pure HBM read of W) is
+ * compared with, timed on the same buffer.  Asynchronous. */
+gpic_status gpic_read_stream(const float *x, int64_t n, double *sink, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -43,7 +43,7 @@ EXPORTS = (
     "gpic_power_iterate_fused", "gpic_power_iterate_csr", "gpic_kmeans1d",
     "gpic_affinity_cosine", "gpic_affinity_cosine_normalized", "gpic_knn_graph",
     "gpic_sym_bytes", "gpic_affinity_sym", "gpic_matvec_sym", "gpic_power_iterate_sym",
-    "gpic_power_iterate_dense_host",
+    "gpic_power_iterate_dense_host", "gpic_read_stream",
 )
 
 
@@ -111,6 +111,7 @@ def lib() -> C.CDLL:
                                        p, sz, C.POINTER(PiResult), p],
             "gpic_kmeans1d": [p, i64, i32, p, p, C.POINTER(i32), C.POINTER(C.c_double),
                               p, sz, p],
+            "gpic_read_stream": [p, i64, p, p],
         }
         for name, args in sigs.items():
             fn = getattr(L, name)
@@ -517,6 +518,23 @@ class KMOut:
     centroids: torch.Tensor     # float64 [k_eff]
     k_eff: int
     cost: float
+
+
+READ_STREAM_SINK = 1536
+
+
+def gpic_read_stream(x: torch.Tensor, n: Optional[int] = None,
+                     sink: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Read the first n floats of x once (a bandwidth reference, not a step
+    of the method); returns the per-workgroup float64 sums."""
+    _dev(x, torch.float32, "x")
+    n = x.numel() if n is None else n
+    if n > x.numel() or not x.is_contiguous():
+        raise ValueError("x must be contiguous and hold n floats")
+    if sink is None:
+        sink = torch.empty(READ_STREAM_SINK, dtype=torch.float64, device=x.device)
+    _check(lib().gpic_read_stream(_ptr(x), n, _ptr(sink), _stream(x.device)))
+    return sink
 
 
 def gpic_kmeans1d(v: torch.Tensor, k: int) -> KMOut:

@@ -984,6 +984,18 @@ gpic_status gpic_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
     return run_power_iteration(op, n, params, v, delta, ws, res, s);
 }
 
+gpic_status gpic_read_stream(const float *x, int64_t n, double *sink, void *stream)
+{
+    CHECK_ARG(x != nullptr && aligned(x, 16), "x is null or not 16-byte aligned");
+    CHECK_ARG(n >= 4 && n % 4 == 0, "n = %lld must be a positive multiple of 4", (long long)n);
+    gpic_status st;
+    if ((st = check_vec(sink, "sink")) != GPIC_OK)
+        return st;
+    static_assert(kReadStreamBlocks == GPIC_READ_STREAM_SINK, "sink length");
+    CHECK_HIP(launch_read_stream(x, n, sink, (hipStream_t)stream), "read stream");
+    return GPIC_OK;
+}
+
 gpic_status gpic_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
                           double *centroids, int32_t *k_eff, double *cost, void *ws,
                           size_t ws_bytes, void *stream)

@@ -262,6 +262,12 @@ hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
                          int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz_host,
                          int *status_host, void *ws, hipStream_t s);
 
+// stream.hip -- read-bandwidth reference (not a step of the method):
+// kReadStreamBlocks workgroups read n floats (n % 4 == 0, 16-byte aligned)
+// once and write one float64 sum each to sink.
+constexpr int kReadStreamBlocks = 1536;
+hipError_t launch_read_stream(const float *x, int64_t n, double *sink, hipStream_t s);
+
 // kmeans.hip
 size_t kmeans_ws(int64_t n, int32_t k);
 // Runs the whole exact 1-D k-means; synchronises the stream.

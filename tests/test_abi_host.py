@@ -154,3 +154,14 @@ def test_sym_and_host_validation(L):
     assert ph(dummy, 10, 9, C.byref(p), dummy, None, *W, C.byref(r), None) == 1   # ldw < n
     small = g.workspace_bytes("pi_dense", 10)
     assert ph(dummy, 10, 10, C.byref(p), dummy, None, dummy, small, C.byref(r), None) == 2
+
+
+def test_read_stream_validation(L):
+    """The read-bandwidth reference rejects bad buffers on the host."""
+    dummy = C.c_void_p(4096)
+    rs = L.gpic_read_stream
+    assert rs(None, 16, dummy, None) == 1                      # x null
+    assert rs(C.c_void_p(4100), 16, dummy, None) == 1          # x misaligned
+    assert rs(dummy, 18, dummy, None) == 1                     # n % 4 != 0
+    assert rs(dummy, 0, dummy, None) == 1                      # empty
+    assert rs(dummy, 16, None, None) == 1                      # sink null

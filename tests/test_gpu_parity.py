@@ -777,3 +777,14 @@ def test_dense_host_workspace_too_small(g):
         g.gpic_power_iterate_dense_host(Wh, v, None, "fixed", 1,
                                         ws_bytes=g.workspace_bytes("pi_dense", n) + 256)
     assert ei.value.status == 2
+
+
+@pytest.mark.parametrize("n", [4, 4 * 1536 * 256 * 3 + 12])
+def test_read_stream_reads_every_float(g, n):
+    """The bandwidth reference reads each float once: the sink's sums add up
+    to the buffer's sum (ones, so every partial sum is exact)."""
+    x = torch.ones(n + 8, dtype=torch.float32, device=DEV)
+    x[n:] = 1e6                                   # past n: never read
+    sink = g.gpic_read_stream(x, n)
+    assert sink.numel() == g.READ_STREAM_SINK
+    assert float(sink.sum().item()) == float(n)
