@@ -788,3 +788,17 @@ def test_read_stream_reads_every_float(g, n):
     sink = g.gpic_read_stream(x, n)
     assert sink.numel() == g.READ_STREAM_SINK
     assert float(sink.sum().item()) == float(n)
+
+
+@pytest.mark.parametrize("n", [2047, 3001, 4103, 6150])
+def test_dense_matvec_prefetch_edges(g, n):
+    """Column-group counts around one, two and three passes of the 512
+    threads (n/4 = 511, 750, 1025, 1537) with ragged tails: the loads issued
+    two groups ahead stay in the row and every entry is used once."""
+    rng = np.random.default_rng(n)
+    W32 = rng.random((n, n), dtype=np.float32)
+    Wd = torch.full((n, g.padded_ld(n)), float("nan"), dtype=torch.float32, device=DEV)
+    Wd[:, :n] = _t(W32)                       # padding past n must never be read
+    v = rng.random(n)
+    y = g.gpic_matvec_dense(Wd, _t(v), n=n).cpu().numpy()
+    np.testing.assert_allclose(y, W32.astype(np.float64) @ v, rtol=1e-12)
