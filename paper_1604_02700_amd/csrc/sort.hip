@@ -2,8 +2,10 @@
 // gfx950: 8-bit digits; per pass a histogram per tile of 4,096 keys, an
 // exclusive scan of the digit-major counts (three launches when they are
 // many), and a stable scatter that ranks keys inside each wave with ballots
-// over the digit bits.  Shared by the 1-D k-means (sorting v) and the kNN
-// graph builder (sorting edges).
+// over the digit bits.  Up to 4,096 keys are sorted instead by one
+// workgroup in LDS (a bitonic network over (key, input position), the same
+// order).  Shared by the 1-D k-means (sorting v) and the kNN graph builder
+// (sorting edges).
 #include "common.h"
 
 namespace gpic {
@@ -179,6 +181,51 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     }
 }
 
+// Up to kSmallSort keys: one workgroup sorts (low `bits` of the key, input
+// position) pairs with a bitonic network in LDS, so equal keys keep their
+// input order exactly as the radix passes do; one launch instead of three
+// per 8-bit pass.  P is n rounded up to a power of two; the padding sorts
+// last.
+constexpr int kSmallSort = 4096;
+constexpr int kSmallThreads = 1024;
+
+__global__ __launch_bounds__(kSmallThreads) void small_sort_kernel(
+    const uint64_t *__restrict__ key, const int32_t *__restrict__ idx,
+    uint64_t *__restrict__ okey, int32_t *__restrict__ oidx, int n, int P, uint64_t mask)
+{
+    __shared__ uint64_t k[kSmallSort];
+    __shared__ int32_t pos[kSmallSort];
+    for (int i = threadIdx.x; i < P; i += kSmallThreads) {
+        k[i] = (i < n) ? (key[i] & mask) : ~0ull;
+        pos[i] = i;
+    }
+    __syncthreads();
+    for (int size = 2; size <= P; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int t = threadIdx.x; t < P / 2; t += kSmallThreads) {
+                const int lo = 2 * t - (t & (stride - 1));
+                const int hi = lo + stride;
+                const bool up = (lo & size) == 0;
+                const uint64_t a = k[lo], b = k[hi];
+                const int32_t pa = pos[lo], pb = pos[hi];
+                const bool gt = (a > b) || (a == b && pa > pb);
+                if (gt == up) {
+                    k[lo] = b;
+                    k[hi] = a;
+                    pos[lo] = pb;
+                    pos[hi] = pa;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int i = threadIdx.x; i < n; i += kSmallThreads) {
+        okey[i] = key[pos[i]];
+        if (oidx != nullptr && idx != nullptr)
+            oidx[i] = idx[pos[i]];
+    }
+}
+
 } // namespace
 
 size_t radix_hist_bytes(int64_t n) { return (size_t)kRadix * tiles(n) * 4; }
@@ -202,6 +249,19 @@ hipError_t radix_sort_u64(uint64_t *&keyA, int32_t *&idxA, uint64_t *&keyB, int3
                           int64_t n, int bits, uint32_t *hist, uint32_t *hsum,
                           hipStream_t s)
 {
+    if (n <= 0)
+        return hipSuccess;
+    if (n <= kSmallSort) {
+        int P = 1;
+        while (P < n)
+            P <<= 1;
+        const uint64_t mask = (bits >= 64) ? ~0ull : ((1ull << bits) - 1);
+        hipLaunchKernelGGL(small_sort_kernel, dim3(1), dim3(kSmallThreads), 0, s, keyA,
+                           idxA, keyB, idxB, (int)n, P, mask);
+        uint64_t *tk = keyA; keyA = keyB; keyB = tk;
+        int32_t *ti = idxA; idxA = idxB; idxB = ti;
+        return hipGetLastError();
+    }
     const int64_t nt = tiles(n);
     for (int shift = 0; shift < bits; shift += 8) {
         hipLaunchKernelGGL(radix_hist_kernel, dim3((unsigned)nt), dim3(kThreads), 0, s,
