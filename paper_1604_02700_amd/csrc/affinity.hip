@@ -9,16 +9,19 @@
 //
 // Two tile engines:
 //   * MFMA, 16 <= d <= 128.  Squared distances in the Gram form
-//     |x_i|^2 + |x_j|^2 - 2 x_i.x_j over the centred points x - mean
-//     (distances are unchanged; the cancellation then scales with the
-//     spread of the points, not their offset from the origin), with the dot
-//     products on the fp16 matrix cores: every coordinate, scaled by one
-//     power of two into [-1, 1], is split into a half-precision high part
-//     and the half-precision remainder, and three products per pair of
-//     parts (hi.hi, lo.hi, hi.lo, float32 accumulation) reproduce the
-//     float32 dot product to about 2^-22 of |x_i||x_j| per coordinate, at
-//     about a fifth of the fp32 matrix-core time.  A prologue (column
-//     means, largest |x - mean|, then the split)
+//     |x_i|^2 + |x_j|^2 - 2 x_i.x_j over the centred points x - centre
+//     (a per-coordinate median of a sample; distances are unchanged, and
+//     the cancellation then scales with the spread of the points, not
+//     their offset from the origin), with the dot
+//     products on the fp16 matrix cores: every point, scaled by its own
+//     power of two into [-1, 1], has each coordinate split into a
+//     half-precision high part and the half-precision remainder, and three
+//     products per pair of parts (hi.hi, lo.hi, hi.lo, float32
+//     accumulation) reproduce the float32 dot product to about 2^-22 of
+//     |x_i||x_j| per coordinate, at about a fifth of the fp32 matrix-core
+//     time.  With a median centre and a scale per point, a point far from
+//     the others coarsens only its own rows and columns.  A prologue (the
+//     centre, then the split)
 //     writes the operands once per call in the order the matrix cores take
 //     them, so a column tile is staged into LDS by contiguous 16-byte
 //     copies and every operand read from LDS is one conflict-free 16-byte
@@ -109,118 +112,93 @@ __global__ __launch_bounds__(kThreads) void inv_norm_kernel(const float *__restr
     rinv[p] = (s > 0.0) ? (float)(1.0 / sqrt(s)) : 0.0f;
 }
 
-// Split-operand prologue of the matrix-core engine (three launches).
-// The largest |x| over every coordinate fixes the scale 2^-S (S the
-// smallest integer with |x| <= 2^S), so that every scaled coordinate
-// x' = x 2^-S lies in [-1, 1]; its two half-precision parts are
-//   hi = fp16(x'),  lo = fp16(x' - hi)   (x' - hi is exact in float32),
-// so hi + lo carries x' to within max(2^-22 |x'|, 2^-25).  Layout, for
-// point p (np padded points, zeros past n), chunk c of 32 coordinates,
-// part h (0 hi, 1 lo) and lane group g:
-//   xh[((c * 2 + h) * 4 + g) * np + p] = the 8 halves of coordinates
-//                                        32 c + 8 g .. 32 c + 8 g + 7
-// (the matrix-core k slots of lane group g), which makes every column
-// tile a set of contiguous 1 KB runs.  Per point also
-//   beta[p] = -|x'_p|^2 / 2 and cn[p] = c |x_p|^2 (float64, rounded once),
-// and scal[1] = m = -2 c 4^S (exact: c times a power of two).
-__global__ void split_clear_kernel(unsigned *__restrict__ scal) { scal[0] = 0u; }
+// The centre the Gram form works on (distances do not change under a
+// shift, and the cancellation in |x_i|^2 + |x_j|^2 - 2 x_i.x_j scales with
+// |x - centre|): per coordinate, the lower median of a sample of
+// m = min(n, 1024) points at the evenly spaced indices floor(t n / m).  A
+// median, unlike the mean, does not move with a few far points, so such
+// points coarsen only their own rows and columns.  One workgroup per
+// coordinate: every sampled value gets its rank in the order of (value,
+// sample position), compared as integers that order like the floats, and
+// the value of rank (m - 1) / 2 is the centre (exact, a float32 value).
+constexpr int kCentreSample = 1024;
 
-// Column means of X in float64 (the Gram form works on centred points:
-// distances do not change, and the cancellation in |x_i|^2 + |x_j|^2 -
-// 2 x_i.x_j scales with |x - mean|, not with |x|).  A workgroup takes
-// kThreads / d rows per pass (whole rows, coalesced) and leaves one float64
-// partial per column; one workgroup adds the partials in order.
-constexpr int kMeanBlocks = 256;
-
-__global__ __launch_bounds__(kThreads) void col_mean_partials_kernel(
-    const float *__restrict__ X, int64_t n, int d, double *__restrict__ part)
+__device__ __forceinline__ unsigned float_order_key(float x)
 {
-    __shared__ double red[kThreads];
-    const int rows = kThreads / d;               // 16 <= d <= 128: 2 to 16 rows
-    const int t = threadIdx.x;
-    const int r = t / d, c = t % d;
-    double sum = 0.0;
-    if (r < rows) {
-        for (int64_t p = (int64_t)blockIdx.x * rows + r; p < n;
-             p += (int64_t)gridDim.x * rows)
-            sum += (double)X[p * d + c];
+    const unsigned b = __float_as_uint(x);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__global__ __launch_bounds__(kThreads) void centre_kernel(const float *__restrict__ X,
+                                                          int64_t n, int d,
+                                                          double *__restrict__ mu)
+{
+    __shared__ unsigned key[kCentreSample];
+    __shared__ float val[kCentreSample];
+    const int k = blockIdx.x;                    // coordinate
+    const int m = (n < kCentreSample) ? (int)n : kCentreSample;
+    for (int t = threadIdx.x; t < m; t += kThreads) {
+        const float x = X[((int64_t)t * n / m) * d + k];
+        val[t] = x;
+        key[t] = float_order_key(x);
     }
-    red[t] = sum;
     __syncthreads();
-    if (t < d) {
-        double a = 0.0;
-        for (int q = 0; q < rows; ++q)
-            a += red[q * d + t];
-        part[(int64_t)blockIdx.x * d + t] = a;
+    const int target = (m - 1) / 2;
+    for (int t = threadIdx.x; t < m; t += kThreads) {
+        const unsigned kt = key[t];
+        int rank = 0;
+        for (int u = 0; u < m; ++u) {
+            const unsigned ku = key[u];
+            rank += (ku < kt || (ku == kt && u < t)) ? 1 : 0;
+        }
+        if (rank == target)                      // exactly one sample position
+            mu[k] = (double)val[t];
     }
 }
 
-__global__ void col_mean_finish_kernel(const double *__restrict__ part, int nb, int d,
-                                       int64_t n, double *__restrict__ mu)
-{
-    const int c = threadIdx.x;
-    if (c >= d)
-        return;
-    double sum = 0.0;
-    for (int b = 0; b < nb; ++b)
-        sum += part[(int64_t)b * d + c];
-    mu[c] = sum / (double)n;
-}
-
-// The centred coordinate x - mean, rounded once to float32 (the same
+// The centred coordinate x - centre, rounded once to float32 (the same
 // expression wherever it is formed).
 __device__ __forceinline__ float centred(float x, double mu)
 {
     return (float)((double)x - mu);
 }
 
-__global__ __launch_bounds__(kThreads) void maxabs_kernel(const float *__restrict__ X,
-                                                          int64_t total, int d,
-                                                          const double *__restrict__ mu,
-                                                          unsigned *__restrict__ scal)
-{
-    __shared__ float red[kThreads / kWave];
-    float mx = 0.0f;
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x; t < total; t += stride)
-        mx = fmaxf(mx, fabsf(centred(X[t], mu[t % d])));
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1)
-        mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
-    if ((threadIdx.x % kWave) == 0)
-        red[threadIdx.x / kWave] = mx;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        for (int w = 1; w < kThreads / kWave; ++w)
-            mx = fmaxf(mx, red[w]);
-        // non-negative floats order like their bit patterns
-        atomicMax(scal, __float_as_uint(mx));
-    }
-}
-
-// the scale exponent S from the largest |x| (0 when that is 0 or not finite)
-__device__ __forceinline__ int split_exponent(unsigned bits)
-{
-    const float mx = __uint_as_float(bits);
-    if (!(mx > 0.0f) || !isfinite(mx))
-        return 0;
-    int e;
-    frexpf(mx, &e);                          // mx = f 2^e, f in [0.5, 1)
-    return e;
-}
-
+// Split-operand prologue of the matrix-core engine.  Every point p gets
+// its own scale 2^-S_p (S_p the smallest integer with |x_pk| < 2^S_p for
+// every coordinate k of the centred point; 0 for the centre itself), so
+// that its scaled coordinates x'_p = x_p 2^-S_p lie in [-1, 1] whatever
+// the spread of the other points; their two half-precision parts are
+//   hi = fp16(x'),  lo = fp16(x' - hi)   (x' - hi is exact in float32),
+// so hi + lo carries x' to within max(2^-22 |x'|, 2^-25), i.e. each
+// coordinate of x_p to within max(2^-22 |x_pk|, 2^-25 2^S_p).  Layout, for
+// point p (np padded points, zeros past n), chunk c of 32 coordinates,
+// part h (0 hi, 1 lo) and lane group g:
+//   xh[((c * 2 + h) * 4 + g) * np + p] = the 8 halves of coordinates
+//                                        32 c + 8 g .. 32 c + 8 g + 7
+// (the matrix-core k slots of lane group g), which makes every column
+// tile a set of contiguous 1 KB runs.  Per point also (float64, each
+// rounded once to float32)
+//   cn[p]  = c |x_p|^2,       gam[p] = c |x_p|^2 2^-S_p,
+//   sc[p]  = 2^S_p,           mr[p]  = -2 c 2^S_p,
+// so that with D = x'_i . x'_j
+//   c dist2(i, j) = sc_j (mr_i D + gam_j) + cn_i.
 __global__ __launch_bounds__(kThreads) void split_kernel(
     const float *__restrict__ X, const double *__restrict__ mu, int64_t n, int64_t np, int d,
-    int nch, float c, unsigned *__restrict__ scal, half8 *__restrict__ xh,
-    float *__restrict__ beta, float *__restrict__ cn)
+    int nch, float c, half8 *__restrict__ xh, float *__restrict__ cn,
+    float *__restrict__ gam, float *__restrict__ sc, float *__restrict__ mr)
 {
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    const int S = split_exponent(scal[0]);
-    if (p == 0)
-        scal[1] = __float_as_uint(ldexpf(-2.0f * c, 2 * S));
     if (p >= np)
         return;
     const bool live = p < n;
+    // the point's largest centred coordinate fixes its exponent
+    float mx = 0.0f;
+    if (live)
+        for (int k = 0; k < d; ++k)
+            mx = fmaxf(mx, fabsf(centred(X[p * d + k], mu[k])));
+    int S = 0;
+    if (mx > 0.0f && isfinite(mx))
+        frexpf(mx, &S);                          // mx = f 2^S, f in [0.5, 1)
     double s = 0.0;
     for (int ch = 0; ch < nch; ++ch)
         for (int g = 0; g < 4; ++g) {
@@ -238,8 +216,11 @@ __global__ __launch_bounds__(kThreads) void split_kernel(
             xh[((int64_t)(ch * 2 + 0) * 4 + g) * np + p] = hi;
             xh[((int64_t)(ch * 2 + 1) * 4 + g) * np + p] = lo;
         }
-    beta[p] = (float)(-0.5 * ldexp(s, -2 * S));
-    cn[p] = (float)((double)c * s);
+    const double cs = (double)c * s;
+    cn[p] = (float)cs;
+    gam[p] = (float)ldexp(cs, -S);
+    sc[p] = ldexpf(1.0f, S);
+    mr[p] = ldexpf(-2.0f * c, S);
 }
 
 // ---------------------------------------------------- chunk row-sum reduce
@@ -352,11 +333,11 @@ __global__ __launch_bounds__(kThreads) void fused_sym_reduce_kernel(
 // The A operand carries tile columns 16 q + m and the B operand the wave's
 // rows i, so lane (m, g) ends with row i and columns 16 q + 4 g + r.  Each
 // 32-coordinate chunk takes three products (hi.hi, lo.hi, hi.lo) into one
-// float32 accumulator that starts at beta_j, which leaves
-//   D = x'_i.x'_j - |x'_j|^2 / 2   and   c dist2 = m D + c |x_i|^2
-// for one fused multiply-add; exp2(-c dist2) is clamped to [0, 1] (the
-// output modifier of the exp2 instruction), which equals clamping c dist2
-// at 0.  The matrix-core chain of one 16-column block is issued before the
+// float32 accumulator, which leaves D = x'_i.x'_j (each point in its own
+// scale), and two fused multiply-adds give
+//   c dist2 = sc_j (mr_i D + gam_j) + cn_i
+// (row values in registers, column values staged with the tile);
+// exp2(-c dist2) is clamped to [0, 1], which equals clamping c dist2 at 0.  The matrix-core chain of one 16-column block is issued before the
 // epilogue of the previous block, so the matrix cores and the vector ALUs
 // work at the same time.
 // When A or W is written (W = 4, RB = 1), the wave's 16 x TC tile goes
@@ -366,8 +347,9 @@ constexpr int kColAlign = 64;                 // chunk and padding granularity
 
 template <int NCH, int RB, int TC, int MODE, int W>
 __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
-    const half8 *__restrict__ xh, int64_t np, const float *__restrict__ beta,
-    const float *__restrict__ cn, const unsigned *__restrict__ scal, int64_t n,
+    const half8 *__restrict__ xh, int64_t np, const float *__restrict__ cn,
+    const float *__restrict__ gam, const float *__restrict__ sc,
+    const float *__restrict__ mr, int64_t n,
     int64_t chunk_cols, float *__restrict__ A, int64_t lda,
     const double *__restrict__ v, const double *__restrict__ degree_in,
     double *__restrict__ out, double *__restrict__ part, double *__restrict__ colpart,
@@ -383,7 +365,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     constexpr int kOutStride = TC + 4;
     static_assert(!kWrites || RB == 1, "one staged output tile per wave");
     __shared__ half8 xs[2][kSlots * TC];
-    __shared__ float bs[2][TC];
+    __shared__ float gs[2][TC];                  // gam_j of the staged columns
+    __shared__ float ss[2][TC];                  // sc_j
     __shared__ double vs[2][kApplyAny ? TC : 1];
     __shared__ double cred[kSymA ? 2 : 1][kSymA ? W : 1][kSymA ? TC : 1];
     __shared__ double red[W];
@@ -421,11 +404,9 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         if (c0 >= c1)
             return;                                  // uniform over the workgroup
     }
-    const float mm = __uint_as_float(scal[1]);
-
     // B operands: this lane's rows, hi and lo of every chunk
     half8 bh[RB][NCH], bl[RB][NCH];
-    float cni[RB], rs[RB];
+    float cni[RB], mri[RB], rs[RB];
     __shared__ double vrow[kSymA ? kGroupRows : 1];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -437,6 +418,7 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
             bl[rb][ch] = xh[((int64_t)(ch * 2 + 1) * 4 + g) * np + ic];
         }
         cni[rb] = cn[ic];
+        mri[rb] = mr[ic];
         rs[rb] = 0.0f;
 
         if (MODE == kStoreW) {
@@ -450,7 +432,7 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     constexpr int kPieces = kSlots * TC;
     constexpr int kPer = (kPieces + NT - 1) / NT;
     half8 stage[kPer];
-    float bstage = 0.0f;
+    float gstage = 0.0f, sstage = 0.0f;
     double vstage = 0.0;
     auto fetch = [&](int64_t jt) {
 #pragma unroll
@@ -460,7 +442,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
                 stage[u] = xh[(int64_t)(f / TC) * np + jt + (f % TC)];
         }
         if (threadIdx.x < TC) {
-            bstage = beta[jt + threadIdx.x];
+            gstage = gam[jt + threadIdx.x];
+            sstage = sc[jt + threadIdx.x];
             if (kApplyAny) {
                 const int64_t j = jt + threadIdx.x;
                 vstage = (j < c1) ? (v != nullptr ? v[j] : 1.0) : 0.0;
@@ -475,7 +458,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
                 xs[buf][f] = stage[u];
         }
         if (threadIdx.x < TC) {
-            bs[buf][threadIdx.x] = bstage;
+            gs[buf][threadIdx.x] = gstage;
+            ss[buf][threadIdx.x] = sstage;
             if (kApplyAny)
                 vs[buf][threadIdx.x] = vstage;
         }
@@ -498,10 +482,9 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         constexpr bool kOff = kSymA && decltype(offdiag)::value;
         // one 16-column block: the matrix-core chain into cc[rb] ...
         auto chain = [&](int q, floatx4 (&cc)[RB]) {
-            const floatx4 b0 = *reinterpret_cast<const floatx4 *>(&bs[buf][16 * q + 4 * g]);
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
-                cc[rb] = b0;
+                cc[rb] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int ch = 0; ch < NCH; ++ch) {
                 const half8 ah = xs[buf][((ch * 2 + 0) * 4 + g) * TC + 16 * q + m];
@@ -525,6 +508,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         // ... and its epilogue
         auto epi = [&](int q, const floatx4 (&cc)[RB]) {
             double cq[4] = {0.0, 0.0, 0.0, 0.0};     // kOff: column sums
+            const floatx4 gj = *reinterpret_cast<const floatx4 *>(&gs[buf][16 * q + 4 * g]);
+            const floatx4 sj = *reinterpret_cast<const floatx4 *>(&ss[buf][16 * q + 4 * g]);
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) {
                 const int64_t i = wrow0 + 16 * rb + m;
@@ -532,7 +517,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                     a[r] = __builtin_amdgcn_fmed3f(
-                        exp2_fast(-fmaf(cc[rb][r], mm, cni[rb])), 0.0f, 1.0f);
+                        exp2_fast(-fmaf(fmaf(cc[rb][r], mri[rb], gj[r]), sj[r], cni[rb])),
+                        0.0f, 1.0f);
                 const int64_t j0 = jt + 16 * q + 4 * g;    // this lane's columns
                 if (kMask) {
 #pragma unroll
@@ -960,12 +946,12 @@ void sym_chunking(int64_t n, int64_t *chunk_cols, int *nchunks)
 int64_t al256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
 struct Ws {
-    unsigned *scal;     // [0] largest |x - mean| (float bits), [1] m = -2 c 4^S
     half8 *xh;          // split operands, kMaxNch * 8 slots of np half8
-    float *beta;        // [np]
-    float *cn;          // [np]
-    double *mu;         // column means [32 kMaxNch]
-    double *mpart;      // their per-workgroup partials [kMeanBlocks][32 kMaxNch]
+    float *cn;          // [np] c |x|^2
+    float *gam;         // [np] c |x|^2 2^-S
+    float *sc;          // [np] 2^S
+    float *mr;          // [np] -2 c 2^S
+    double *mu;         // the centre [32 kMaxNch]
     double *part;       // per-chunk row sums, kMaxChunks * n
 };
 
@@ -974,18 +960,18 @@ Ws carve(void *ws, int64_t n)
     char *b = static_cast<char *>(ws);
     const int64_t np = padded_points(n);
     Ws w;
-    w.scal = reinterpret_cast<unsigned *>(b);
-    b += 256;
     w.xh = reinterpret_cast<half8 *>(b);
     b += al256(np * kMaxNch * 8 * (int64_t)sizeof(half8));
-    w.beta = reinterpret_cast<float *>(b);
-    b += al256(np * 4);
     w.cn = reinterpret_cast<float *>(b);
+    b += al256(np * 4);
+    w.gam = reinterpret_cast<float *>(b);
+    b += al256(np * 4);
+    w.sc = reinterpret_cast<float *>(b);
+    b += al256(np * 4);
+    w.mr = reinterpret_cast<float *>(b);
     b += al256(np * 4);
     w.mu = reinterpret_cast<double *>(b);
     b += al256(32 * kMaxNch * 8);
-    w.mpart = reinterpret_cast<double *>(b);
-    b += al256((int64_t)kMeanBlocks * 32 * kMaxNch * 8);
     w.part = reinterpret_cast<double *>(b);
     return w;
 }
@@ -994,21 +980,10 @@ hipError_t launch_split(const float *X, int64_t n, int d, float c, const Ws &w,
                         hipStream_t s)
 {
     const int64_t np = padded_points(n);
-    hipLaunchKernelGGL(split_clear_kernel, dim3(1), dim3(1), 0, s, w.scal);
-    hipLaunchKernelGGL(col_mean_partials_kernel, dim3(kMeanBlocks), dim3(kThreads), 0, s, X, n,
-                       d, w.mpart);
-    hipLaunchKernelGGL(col_mean_finish_kernel, dim3(1), dim3(32 * kMaxNch), 0, s, w.mpart,
-                       kMeanBlocks, d, n, w.mu);
-    const int64_t total = n * (int64_t)d;
-    // few workgroups: each ends with one atomic on the same word
-    int64_t blocks = (total + kThreads - 1) / kThreads;
-    if (blocks > 256)
-        blocks = 256;
-    hipLaunchKernelGGL(maxabs_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, X,
-                       total, d, w.mu, w.scal);
+    hipLaunchKernelGGL(centre_kernel, dim3((unsigned)d), dim3(kThreads), 0, s, X, n, d, w.mu);
     hipLaunchKernelGGL(split_kernel, dim3((unsigned)((np + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, s, X, w.mu, n, np, d, nch_for(d), c, w.scal, w.xh,
-                       w.beta, w.cn);
+                       dim3(kThreads), 0, s, X, w.mu, n, np, d, nch_for(d), c, w.xh, w.cn,
+                       w.gam, w.sc, w.mr);
     return hipGetLastError();
 }
 
@@ -1023,7 +998,7 @@ void launch_engine(const Ws &w, int64_t n, int64_t chunk_cols, int nchunks, floa
     constexpr int TC = (NCH <= 2) ? 64 : 32;
     const dim3 grid((unsigned)row_groups(n, MODE), (unsigned)nchunks);
     hipLaunchKernelGGL((affinity_mfma_kernel<NCH, RB, TC, MODE, W>), grid, dim3(W * 64), 0,
-                       s, w.xh, padded_points(n), w.beta, w.cn, w.scal, n, chunk_cols, A,
+                       s, w.xh, padded_points(n), w.cn, w.gam, w.sc, w.mr, n, chunk_cols, A,
                        lda, v, degree_in, out, part, colpart, partial, ctl, use_ctl);
 }
 
@@ -1150,9 +1125,8 @@ hipError_t launch_cosine_w(const float *X, int64_t n, int d, float *W, int64_t l
 size_t affinity_ws(int64_t n)
 {
     const int64_t np = padded_points(n);
-    return (size_t)(256 + al256(np * kMaxNch * 8 * (int64_t)sizeof(half8)) +
-                    2 * al256(np * 4) + al256(32 * kMaxNch * 8) +
-                    al256((int64_t)kMeanBlocks * 32 * kMaxNch * 8) +
+    return (size_t)(al256(np * kMaxNch * 8 * (int64_t)sizeof(half8)) +
+                    4 * al256(np * 4) + al256(32 * kMaxNch * 8) +
                     al256((int64_t)kMaxChunks * n * 8));
 }
 

@@ -18,3 +18,14 @@ def orc():
     import oracle
     oracle._L()
     return oracle
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Whether each end-to-end label comparison ran under the separation
+    guard (agreement) or not (k-means of the GPU's own v)."""
+    helpers = sys.modules.get("gpu_helpers")
+    lines = getattr(helpers, "LABEL_GUARD", None)
+    if lines:
+        terminalreporter.section("label parity guard")
+        for line in lines:
+            terminalreporter.write_line(line)

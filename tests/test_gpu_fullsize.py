@@ -20,7 +20,7 @@ benchmark times.
 import numpy as np
 import pytest
 
-from gpu_helpers import matched_agreement, rel_l1, separation_ok, stop_margin
+from gpu_helpers import check_kmeans, check_labels, rel_l1, stop_margin
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -82,11 +82,11 @@ def test_blobs16d_full_fixed_T(g, orc, blobs16d, blobs16d_oracle):
                                atol=1e-3 * w.eps)
     assert np.all(vg >= 0) and abs(vg.sum() - 1.0) < 1e-12
     km = g.gpic_kmeans1d(v, w.k)
-    lab = km.labels.cpu().numpy()
     assert km.k_eff == ref["km"].k_eff == w.k
-    if separation_ok(ref["fixed"].v, vg, ref["km"].labels):
-        assert matched_agreement(lab, ref["km"].labels) >= 0.999
-    # k-means parity on the same (GPU) embedding: identical optimum
+    check_labels(orc, f"blobs16d n={w.n} T=50", ref["fixed"].v, ref["km"].labels, vg, km,
+                 w.k)
+    # k-means parity on the same (GPU) embedding, whatever the guard: the
+    # identical optimum
     kmo = orc.kmeans1d(vg, w.k, "dc")
     assert km.cost == pytest.approx(kmo.cost, rel=1e-9)
     # determinism at full size
@@ -166,8 +166,7 @@ def test_blobs64d_reduced_end_to_end(g, orc):
     vg = out.pi.v.cpu().numpy()
     assert rel_l1(vg, ref.v) <= 1e-4
     km = orc.kmeans1d(ref.v, w.k)
-    if separation_ok(ref.v, vg, km.labels):
-        assert matched_agreement(out.km.labels.cpu().numpy(), km.labels) >= 0.999
+    check_labels(orc, f"blobs64d fused n={w.n}", ref.v, km.labels, vg, out.km, w.k)
 
 
 def test_knn_csr_relabelled_matches_original(g):
@@ -205,19 +204,21 @@ def test_knn_csr_reduced_end_to_end(g, orc):
     np.testing.assert_allclose(out.degree.cpu().numpy(), dr, rtol=1e-12)
     assert ref.converged == out.pi.converged
     assert out.pi.iterations == ref.iterations
-    assert rel_l1(out.pi.v.cpu().numpy(), ref.v) <= 1e-4
+    vg = out.pi.v.cpu().numpy()
+    assert rel_l1(vg, ref.v) <= 1e-4
+    check_labels(orc, f"knn8d csr n={w.n}", ref.v, orc.kmeans1d(ref.v, w.k, "dc").labels,
+                 vg, out.km, w.k)
 
 
 def test_kmeans1d_full_size(g, orc):
     """n = 2,000,000 scalars into k = 50 clusters: the exact optimum."""
-    from test_gpu_parity import _check_kmeans
     rng = np.random.default_rng(2_000_050)
     n, k = 2_000_000, 50
     centres = np.sort(rng.uniform(0, 100, size=k))
     v = centres[rng.integers(0, k, size=n)] + rng.standard_normal(n) * 0.5
     print(f"gpu: kmeans1d n={n} k={k}", flush=True)
     out = g.gpic_kmeans1d(_t(v), k)
-    _check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))
+    check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))
 
 
 def test_knn_csr_full_size_converge(g, orc, knn8d):
@@ -235,7 +236,10 @@ def test_knn_csr_full_size_converge(g, orc, knn8d):
     np.testing.assert_allclose(out.degree.cpu().numpy(), dr, rtol=1e-12)
     assert ref.converged and out.pi.converged
     assert out.pi.iterations == ref.iterations
-    assert rel_l1(out.pi.v.cpu().numpy(), ref.v) <= 1e-4
+    vg = out.pi.v.cpu().numpy()
+    assert rel_l1(vg, ref.v) <= 1e-4
+    check_labels(orc, f"knn8d csr n={w.n}", ref.v, orc.kmeans1d(ref.v, w.k, "dc").labels,
+                 vg, out.km, w.k)
 
 
 def test_moons_full_size_cosine(g, orc):
@@ -248,6 +252,7 @@ def test_moons_full_size_cosine(g, orc):
     vg = out.pi.v.cpu().numpy()
     dg = out.degree.cpu().numpy()
     it, conv = out.pi.iterations, out.pi.converged
+    km = out.km
     del out
     torch.cuda.empty_cache()
     print("oracle: moons n=45000 (cosine affinity, normalise, <= 3 updates)", flush=True)
@@ -258,6 +263,8 @@ def test_moons_full_size_cosine(g, orc):
     np.testing.assert_allclose(dg, deg, rtol=1e-5)
     assert it == ref.iterations and conv == ref.converged
     assert rel_l1(vg, ref.v) <= 1e-4
+    check_labels(orc, f"moons cosine n={w.n}", ref.v, orc.kmeans1d(ref.v, w.k).labels, vg,
+                 km, w.k)
 
 
 def test_knn_graph_200k(g, orc):

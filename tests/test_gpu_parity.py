@@ -7,8 +7,8 @@ state in float64; the oracle is float64 throughout.
 import numpy as np
 import pytest
 
-from gpu_helpers import (cosine_tolerance, EPS32, affinity_tolerance, matched_agreement, rel_l1,
-                         separation_ok, stop_margin)
+from gpu_helpers import (cosine_tolerance, EPS32, affinity_tolerance, check_kmeans,
+                         check_labels, matched_agreement, rel_l1, stop_margin)
 
 pytestmark = pytest.mark.gpu
 
@@ -77,6 +77,75 @@ def test_affinity_offset_points(g, orc, n, d, offset):
     degf, _, _ = g.gpic_degree_fused(_t(X), sigma)
     dr, _, _ = orc.degree_onthefly(X, sigma)
     np.testing.assert_allclose(degf.cpu().numpy(), dr, rtol=1e-5)
+
+
+def _with_outlier(X, far):
+    """X plus one point `far` away from the first point along every
+    coordinate (a single far point among clustered ones)."""
+    return np.vstack([X, (X[0] + np.float32(far))[None, :]]).astype(np.float32)
+
+
+@pytest.mark.parametrize("n,d,far", [(700, 16, 1.0e4), (700, 16, 1.0e5), (300, 64, 1.0e4),
+                                     (257, 33, -3.0e4)])
+def test_affinity_outlier_points(g, orc, n, d, far):
+    """One point far from all others: each point is split in its own scale
+    around a median centre, so the far point coarsens only its own row and
+    column.  Every entry within the per-pair bound (which carries only the
+    pair's own norms), and the entries among the other points within 1e-5
+    of the largest entry."""
+    X = _with_outlier(_pts(n, d, 3100 + d, scale=1.0), far)
+    sigma = np.float32(np.sqrt(d))
+    print(f"affinity outlier n={n}+1 d={d} far={far}", flush=True)
+    A, deg = g.gpic_affinity(_t(X), sigma)
+    torch.cuda.synchronize()
+    Ag = A[:, :n + 1].cpu().numpy().astype(np.float64)
+    Ar = orc.affinity(X, sigma)
+    tol = affinity_tolerance(X, sigma, Ar, True)
+    err = np.abs(Ag - Ar)
+    assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
+    assert np.max(err[:n, :n]) <= 1e-5 * np.max(Ar)
+    np.testing.assert_allclose(deg.cpu().numpy(), Ag.sum(1), rtol=1e-13)
+
+
+@pytest.mark.parametrize("far", [1.0e4, 1.0e5])
+@pytest.mark.parametrize("sigma_kind", ["one", "median"])
+def test_affinity_outlier_end_to_end(g, orc, far, sigma_kind):
+    """The 16-D blob shape at n = 4,099 plus one point far from all others
+    (at sigma = 1 its row of A underflows to zero: a zero-degree row): v
+    after T = 50 within relative L1 1e-4 and the same stop update as the
+    oracle, through the matrix-core affinity."""
+    import workloads
+    w = workloads.make("blobs16d", n=4099)
+    X = _with_outlier(w.X, far)
+    sigma = np.float32(1.0) if sigma_kind == "one" else w.sigma
+    n = X.shape[0]
+    eps = 1e-5 / n
+    print(f"pic_dense blobs16d n=4099+1 far={far} sigma={float(sigma)}", flush=True)
+    out = g.pic_dense(_t(X), sigma, w.k, "fixed", 50)
+    conv = g.pic_dense(_t(X), sigma, w.k, "converge", 1000, eps)
+    torch.cuda.synchronize()
+    Ar = orc.affinity(X, sigma)
+    # degrees: within the sum of their entries' bounds (at sigma = 1 every
+    # entry is tiny and its relative error is the Gram form's absolute
+    # error in dist2 over 2 sigma^2)
+    dtol = affinity_tolerance(X, sigma, Ar, True).sum(1)
+    Wr, dr, v0r, nzr = orc.degree_normalize(Ar, copy=False)
+    del Ar
+    ref = orc.power_iterate_dense(Wr, v0r, "fixed", 50)
+    refc = orc.power_iterate_dense(Wr, v0r, "converge", 1000, eps)
+    del Wr
+    assert out.n_zero_rows == nzr
+    derr = np.abs(out.degree.cpu().numpy() - dr)
+    assert np.all(derr <= dtol), f"degree err/tol {np.max(derr / dtol):.3g}"
+    v = out.pi.v.cpu().numpy()
+    err = rel_l1(v, ref.v)
+    mu = stop_margin(refc.stats, eps, refc.iterations)
+    print(f"  rel_l1 = {err:.3e}; iterations gpu={conv.pi.iterations} "
+          f"oracle={refc.iterations} margin={mu:.3g}", flush=True)
+    assert out.pi.iterations == 50 and err <= 1e-4
+    assert conv.pi.converged == refc.converged
+    assert conv.pi.iterations == refc.iterations
+    assert rel_l1(conv.pi.v.cpu().numpy(), refc.v) <= 1e-4
 
 
 @pytest.mark.parametrize("n,d", [(2, 2), (3, 1), (64, 2), (1000, 2), (1023, 5),
@@ -270,10 +339,9 @@ def test_pic_dense_converge_parity(g, orc, name):
     assert out.pi.iterations == ref.pi.iterations
     assert rel_l1(v, ref.pi.v) <= 1e-4
     np.testing.assert_allclose(out.pi.stats, ref.pi.stats, rtol=1e-3, atol=1e-3 * w.eps)
-    lab = out.km.labels.cpu().numpy()
     assert out.km.k_eff == ref.km.k_eff == w.k
-    if separation_ok(ref.pi.v, v, ref.km.labels):
-        assert matched_agreement(lab, ref.km.labels) >= 0.999
+    check_labels(orc, f"dense {name}", ref.pi.v, ref.km.labels, v, out.km, w.k,
+                 expect_separated=True)
 
 
 @pytest.mark.parametrize("n", [3000, 4099])
@@ -308,39 +376,10 @@ def test_pic_cosine_parity(g, orc, name):
     vg = out.pi.v.cpu().numpy()
     assert rel_l1(vg, ref.v) <= 1e-4
     km = orc.kmeans1d(ref.v, w.k)
-    if separation_ok(ref.v, vg, km.labels):
-        assert matched_agreement(out.km.labels.cpu().numpy(), km.labels) >= 0.999
+    check_labels(orc, f"cosine {name} n={w.n}", ref.v, km.labels, vg, out.km, w.k)
 
 
 # ------------------------------------------------------------------ k-means
-def _partition_cost(v, labels, k_eff):
-    """Within-cluster sum of squares of a labelling, from its members."""
-    return float(sum(((v[labels == c] - v[labels == c].mean()) ** 2).sum()
-                     for c in range(k_eff)))
-
-
-def _check_kmeans(v, out, ref):
-    """Unique: k_eff and the optimal cost.  The labels must equal the
-    oracle's, or (exact cost ties) form an equally optimal partition into
-    contiguous runs of the sorted values, numbered by ascending centroid,
-    that never splits equal values."""
-    assert out.k_eff == ref.k_eff
-    assert out.cost == pytest.approx(ref.cost, rel=1e-9, abs=1e-12)
-    lab = out.labels.cpu().numpy()
-    if np.array_equal(lab, ref.labels):
-        np.testing.assert_allclose(out.centroids.cpu().numpy(), ref.centroids,
-                                   rtol=1e-10, atol=1e-300)
-        return
-    order = np.argsort(v, kind="stable")
-    ls = lab[order]
-    assert np.all(np.diff(ls) >= 0) and set(ls) == set(range(out.k_eff))
-    vs = v[order]
-    same = vs[1:] == vs[:-1]
-    assert np.all(ls[1:][same] == ls[:-1][same])
-    assert _partition_cost(v, lab, out.k_eff) == pytest.approx(ref.cost, rel=1e-9,
-                                                                abs=1e-12)
-
-
 @pytest.mark.parametrize("n,k,dup", [(1, 1, False), (2, 2, False), (5, 3, False),
                                      (64, 8, False), (65, 8, False), (66, 8, True),
                                      (1000, 4, False), (4097, 10, False),
@@ -359,7 +398,7 @@ def test_kmeans1d_parity(g, orc, n, k, dup):
         v = np.round(v, 0)
     out = g.gpic_kmeans1d(_t(v), k)
     ref = orc.kmeans1d(v, k, "dc" if n > 2000 else "plain")
-    _check_kmeans(v, out, ref)
+    check_kmeans(v, out, ref)
 
 
 @pytest.mark.parametrize("n,k", [(30000, 50), (100000, 17)])
@@ -367,7 +406,7 @@ def test_kmeans1d_unclustered(g, orc, n, k):
     """Uniform values (no cluster structure): split points move smoothly."""
     v = np.random.default_rng(n).uniform(-1.0, 1.0, size=n)
     out = g.gpic_kmeans1d(_t(v), k)
-    _check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))
+    check_kmeans(v, out, orc.kmeans1d(v, k, "dc"))
 
 
 def test_kmeans1d_special_values(g, orc):
@@ -375,7 +414,7 @@ def test_kmeans1d_special_values(g, orc):
     for k in (1, 3, 6, 8):
         out = g.gpic_kmeans1d(_t(v), k)
         ref = orc.kmeans1d(v, k, "plain")
-        _check_kmeans(v, out, ref)
+        check_kmeans(v, out, ref)
 
 
 # -------------------------------------------------------------- fused path
@@ -675,8 +714,8 @@ def test_pic_sym_converge_parity(g, orc, name):
     assert rel_l1(v, ref.pi.v) <= 1e-4
     np.testing.assert_allclose(out.pi.stats, ref.pi.stats, rtol=1e-3, atol=1e-3 * w.eps)
     assert out.km.k_eff == ref.km.k_eff == w.k
-    if separation_ok(ref.pi.v, v, ref.km.labels):
-        assert matched_agreement(out.km.labels.cpu().numpy(), ref.km.labels) >= 0.999
+    check_labels(orc, f"sym {name}", ref.pi.v, ref.km.labels, v, out.km, w.k,
+                 expect_separated=True)
 
 
 @pytest.mark.parametrize("n", [3000, 4099])
@@ -750,6 +789,47 @@ def test_dense_host_equals_device(g, n, rows):
                                          ws_bytes=ws_bytes)
     assert ra.converged and rb.converged and ra.iterations == rb.iterations
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("mode", ["fixed", "converge"])
+def test_dense_host_oracle_parity(g, orc, mode):
+    """The out-of-core path against the oracle, n = 3,000 (16-D blobs):
+    (1) the whole path, W built on the GPU and streamed from pinned host
+    memory in row panels, against the oracle's float64 chain: v within
+    relative L1 1e-4 and the identical stop update; (2) stage isolation:
+    the oracle's W rounded to float32 streamed the same way, against the
+    oracle's iteration over that same float32 W, to 1e-11."""
+    import workloads
+    n = 3000
+    w = workloads.make("blobs16d", n=n)
+    eps = 1e-5 / n
+    T = 20 if mode == "fixed" else 1000
+    pitch = (n + 3) // 4 * 4
+    panel = (256 * pitch * 4 + 255) // 256 * 256            # 256-row panels
+    ws_bytes = g.workspace_bytes("pi_dense", n) + 2 * panel
+    print(f"dense_host oracle parity n={n} mode={mode}", flush=True)
+    W, deg, v0, _ = g.gpic_affinity_normalized(_t(w.X), w.sigma)
+    torch.cuda.synchronize()
+    Wh = _host_copy(W, n)
+    del W
+    v = v0.clone()
+    r = g.gpic_power_iterate_dense_host(Wh, v, None, mode, T, eps, ws_bytes=ws_bytes)
+    Wr, dr, v0r, _ = orc.degree_normalize(orc.affinity(w.X, w.sigma), copy=False)
+    ref = orc.power_iterate_dense(Wr, v0r, mode, T, eps)
+    print(f"  iterations gpu={r.iterations} oracle={ref.iterations} "
+          f"rel_l1={rel_l1(v.cpu().numpy(), ref.v):.3e}", flush=True)
+    assert r.iterations == ref.iterations and r.converged == ref.converged
+    assert rel_l1(v.cpu().numpy(), ref.v) <= 1e-4
+    np.testing.assert_allclose(r.stats, ref.stats, rtol=1e-3, atol=1e-3 * eps)
+    # stage isolation over the oracle's own W in float32
+    W32 = Wr.astype(np.float32)
+    ref32 = orc.power_iterate_dense(W32.astype(np.float64), v0r, mode, T, eps)
+    Wh32 = torch.empty((n, n), dtype=torch.float32, pin_memory=True)
+    Wh32.copy_(torch.from_numpy(W32))
+    v = _t(v0r)
+    r = g.gpic_power_iterate_dense_host(Wh32, v, None, mode, T, eps, ws_bytes=ws_bytes)
+    assert r.iterations == ref32.iterations and r.converged == ref32.converged
+    np.testing.assert_allclose(v.cpu().numpy(), ref32.v, rtol=1e-11)
 
 
 def test_dense_host_pageable_memory(g):
