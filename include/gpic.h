@@ -313,6 +313,25 @@ gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
                                      double *delta, void *ws, size_t ws_bytes,
                                      gpic_pi_result *res, void *stream);
 
+/* For callers that cannot allocate device memory (tight serving loops,
+ * harnesses that forbid hipMalloc): gpic_power_iterate_dense with its
+ * scratch (control words, statistic ring, per-workgroup |y| partials, y and,
+ * when delta is null, delta) in a static device array of
+ * GPIC_NOALLOC_SCRATCH_BYTES that the library owns, one per GPU, held until
+ * the process ends, instead of a caller workspace.  Same arguments, results
+ * (bitwise: the same kernels) and errors as gpic_power_iterate_dense, minus
+ * ws; allocates nothing (no hipMalloc/hipFree, no library allocation).
+ * n <= GPIC_NOALLOC_MAX_N, else GPIC_ERR_WORKSPACE before any launch.  The
+ * scratch is re-initialised on the device by every call, but it is shared:
+ * calls that overlap on one GPU (several streams or threads at once) race
+ * and must be serialised by the caller. */
+#define GPIC_NOALLOC_SCRATCH_BYTES (8u << 20)
+#define GPIC_NOALLOC_MAX_N 465536
+gpic_status gpic_power_iterate_dense_noalloc(const float *W, int64_t n, int64_t ldw,
+                                             const gpic_pi_params *params, double *v,
+                                             double *delta, gpic_pi_result *res,
+                                             void *stream);
+
 /* Out-of-core: the same loop over a dense W that stays in HOST memory
  * (W_host: host pointer, float32 [n x ldw] row-major, ldw >= n; allocate it
  * pinned, e.g. with hipHostMalloc, so that copies overlap the products).

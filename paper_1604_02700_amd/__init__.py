@@ -44,7 +44,12 @@ EXPORTS = (
     "gpic_affinity_cosine", "gpic_affinity_cosine_normalized", "gpic_knn_graph",
     "gpic_sym_bytes", "gpic_affinity_sym", "gpic_matvec_sym", "gpic_power_iterate_sym",
     "gpic_power_iterate_dense_host", "gpic_read_stream",
+    "gpic_power_iterate_dense_noalloc",
 )
+
+# the static scratch of gpic_power_iterate_dense_noalloc (include/gpic.h)
+NOALLOC_SCRATCH_BYTES = 8 << 20
+NOALLOC_MAX_N = 465536
 
 
 class GpicError(RuntimeError):
@@ -105,6 +110,8 @@ def lib() -> C.CDLL:
                                               sz, C.POINTER(PiResult), p],
             "gpic_power_iterate_dense": [p, i64, i64, C.POINTER(PiParams), p, p, p,
                                          sz, C.POINTER(PiResult), p],
+            "gpic_power_iterate_dense_noalloc": [p, i64, i64, C.POINTER(PiParams), p, p,
+                                                 C.POINTER(PiResult), p],
             "gpic_power_iterate_fused": [p, i64, i32, f32, p, C.POINTER(PiParams),
                                          p, p, p, sz, C.POINTER(PiResult), p],
             "gpic_power_iterate_csr": [p, p, p, i64, i64, C.POINTER(PiParams), p, p,
@@ -436,6 +443,26 @@ def gpic_power_iterate_dense(W, v, delta=None, mode="converge", max_iter=1000, e
     return _run_pi(lib().gpic_power_iterate_dense, (_ptr(W), n, W.stride(0)), n,
                    W.device, v, delta, mode, max_iter, eps, check_every, record_stats,
                    "pi_dense")
+
+
+def gpic_power_iterate_dense_noalloc(W, v, delta=None, mode="converge", max_iter=1000,
+                                     eps=0.0, check_every=0, record_stats=True, n=None):
+    """gpic_power_iterate_dense with the library's static device scratch in
+    place of a workspace: nothing is allocated on the device (n <=
+    NOALLOC_MAX_N; calls that overlap on one GPU race)."""
+    _dev(W, torch.float32, "W")
+    n = W.shape[0] if n is None else n
+    _vec(v, n, "v", W.device)
+    if delta is not None:
+        _vec(delta, n, "delta", W.device)
+    stats = np.zeros(max(int(max_iter), 1)) if record_stats else None
+    p = _params(mode, max_iter, eps, check_every, stats)
+    r = PiResult()
+    _check(lib().gpic_power_iterate_dense_noalloc(_ptr(W), n, W.stride(0), C.byref(p),
+                                                  _ptr(v), _ptr(delta), C.byref(r),
+                                                  _stream(W.device)))
+    st = stats[: r.iterations].copy() if record_stats else np.zeros(0)
+    return PIOut(v, delta, int(r.iterations), bool(r.converged), float(r.last_stat), st)
 
 
 def gpic_power_iterate_dense_host(W_host, v, delta=None, mode="converge", max_iter=1000,

@@ -7,8 +7,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
-#include <vector>
 
 #include "../../include/gpic.h"
 #include "common.h"
@@ -385,7 +385,7 @@ gpic_status run_power_iteration(const Product &op, int64_t n,
     if (conv)
         chunk = p->check_every > 0 ? (p->check_every < kRing ? p->check_every : kRing)
                                    : 16;
-    std::vector<double> hstat((size_t)chunk);
+    double hstat[kRing];                       // chunk <= kRing; no heap use
     const int64_t T = p->max_iter;
     int64_t t = 0;
     bool stopped = false;
@@ -410,10 +410,10 @@ gpic_status run_power_iteration(const Product &op, int64_t n,
         const int64_t m = te - t;
         const int64_t a = t % kRing;
         const int64_t first = (a + m <= kRing) ? m : kRing - a;
-        CHECK_HIP(hipMemcpyAsync(hstat.data(), ring + a, first * 8,
+        CHECK_HIP(hipMemcpyAsync(hstat, ring + a, first * 8,
                                  hipMemcpyDeviceToHost, s), "stat copy");
         if (first < m)
-            CHECK_HIP(hipMemcpyAsync(hstat.data() + first, ring, (m - first) * 8,
+            CHECK_HIP(hipMemcpyAsync(hstat + first, ring, (m - first) * 8,
                                      hipMemcpyDeviceToHost, s), "stat copy");
         int herr = 0;
         CHECK_HIP(hipMemcpyAsync(&herr, err, sizeof(int), hipMemcpyDeviceToHost, s),
@@ -422,7 +422,7 @@ gpic_status run_power_iteration(const Product &op, int64_t n,
         if (herr)
             return fail(GPIC_ERR_NUMERIC, "||W v||_1 is zero or not finite");
         for (int64_t u = t; u < te; ++u) {
-            const double su = hstat[(size_t)(u - t)];
+            const double su = hstat[u - t];
             if (p->stats_host)
                 p->stats_host[u] = su;
             res->last_stat = su;
@@ -437,6 +437,54 @@ gpic_status run_power_iteration(const Product &op, int64_t n,
     }
     if (T == 0)
         CHECK_HIP(hipStreamSynchronize(s), "synchronize");
+    return GPIC_OK;
+}
+
+} // namespace
+
+// Scratch of gpic_power_iterate_dense_noalloc: the power-iteration state
+// (control words, statistic ring, per-workgroup |y| partials, y and delta)
+// in a library-owned device array instead of a caller workspace, for
+// callers that cannot allocate device memory.  Every GPU the library runs
+// on holds its own copy until the process ends.  In host code `scratch`
+// is only a stand-in for the symbol: its device address, one per device,
+// comes from hipGetSymbolAddress with that device current, and only that
+// address is ever handed to kernels.
+static __device__ __align__(256) unsigned char scratch[GPIC_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];            // per device, set on first use
+
+// the device address of `scratch` on the device `s` belongs to
+gpic_status noalloc_scratch(hipStream_t s, void **out)
+{
+    int dev = -1;
+    if (s != nullptr)
+        CHECK_HIP(hipStreamGetDevice(s, &dev), "stream device");
+    else
+        CHECK_HIP(hipGetDevice(&dev), "current device");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(GPIC_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        int cur = -1;
+        CHECK_HIP(hipGetDevice(&cur), "current device");
+        if (cur != dev)
+            CHECK_HIP(hipSetDevice(dev), "set device");
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur != dev)
+            (void)hipSetDevice(cur);
+        if (e != hipSuccess)
+            return hip_fail(e, "scratch address");
+        if (ptr == nullptr || !aligned(ptr, 256))
+            return fail(GPIC_ERR_HIP, "scratch address null or misaligned");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
     return GPIC_OK;
 }
 
@@ -848,6 +896,34 @@ gpic_status gpic_power_iterate_dense(const float *W, int64_t n, int64_t ldw,
     op.n = n;
     op.ldw = ldw;
     return run_power_iteration(op, n, params, v, delta, ws, res, (hipStream_t)stream);
+}
+
+gpic_status gpic_power_iterate_dense_noalloc(const float *W, int64_t n, int64_t ldw,
+                                             const gpic_pi_params *params, double *v,
+                                             double *delta, gpic_pi_result *res,
+                                             void *stream)
+{
+    CHECK_ARG(W != nullptr && aligned(W, 16), "W is null or not 16-byte aligned");
+    gpic_status st = check_pi_common(n, params, v, delta, res);
+    if (st != GPIC_OK)
+        return st;
+    CHECK_ARG(ldw >= n && ldw % 4 == 0, "ldw must be >= n and a multiple of 4");
+    const size_t need = pi_ws(n, gemv_blocks(n));
+    if (need > (size_t)GPIC_NOALLOC_SCRATCH_BYTES)
+        return fail(GPIC_ERR_WORKSPACE,
+                    "n = %lld needs %zu bytes of scratch; the static scratch holds %zu "
+                    "(n <= %lld)",
+                    (long long)n, need, (size_t)GPIC_NOALLOC_SCRATCH_BYTES,
+                    (long long)GPIC_NOALLOC_MAX_N);
+    hipStream_t s = (hipStream_t)stream;
+    void *ws = nullptr;
+    if ((st = noalloc_scratch(s, &ws)) != GPIC_OK)
+        return st;
+    DenseProduct op;
+    op.W = W;
+    op.n = n;
+    op.ldw = ldw;
+    return run_power_iteration(op, n, params, v, delta, ws, res, s);
 }
 
 gpic_status gpic_power_iterate_dense_host(const float *W_host, int64_t n, int64_t ldw,

@@ -165,3 +165,25 @@ def test_read_stream_validation(L):
     assert rs(dummy, 18, dummy, None) == 1                     # n % 4 != 0
     assert rs(dummy, 0, dummy, None) == 1                      # empty
     assert rs(dummy, 16, None, None) == 1                      # sink null
+
+
+def test_noalloc_validation(L):
+    """The no-allocation dense power iteration checks its arguments and its
+    size limit on the host, before it looks up its static scratch or
+    launches anything."""
+    import paper_1604_02700_amd as g
+    # the documented limit is the largest n whose power-iteration state fits
+    assert (g.workspace_bytes("pi_dense", g.NOALLOC_MAX_N) <= g.NOALLOC_SCRATCH_BYTES
+            < g.workspace_bytes("pi_dense", g.NOALLOC_MAX_N + 1))
+    dummy = C.c_void_p(4096)
+    p = g.PiParams()
+    p.mode, p.max_iter, p.eps, p.check_every, p.reserved = 0, 5, 0.0, 0, 0
+    r = g.PiResult()
+    fn = L.gpic_power_iterate_dense_noalloc
+    assert fn(None, 10, 12, C.byref(p), dummy, None, C.byref(r), None) == 1     # W null
+    assert fn(dummy, 10, 9, C.byref(p), dummy, None, C.byref(r), None) == 1     # ldw < n
+    assert fn(dummy, 10, 12, C.byref(p), None, None, C.byref(r), None) == 1     # v null
+    assert fn(dummy, 10, 12, C.byref(p), dummy, None, None, None) == 1          # res null
+    n = g.NOALLOC_MAX_N + 1
+    assert fn(dummy, n, n + 3, C.byref(p), dummy, None, C.byref(r), None) == 2
+    assert b"static scratch" in L.gpic_last_error()
