@@ -25,11 +25,12 @@
  *   orc_degree_normalize   d_ii = sum_j a_ij and W = D^-1 A ("Spectral
  *                          Cluster"); v0 = D / sum(D) (Algorithm 2, the
  *                          Reduction and Norm steps before the loop).
- *   orc_power_iterate_*    Algorithm 1: delta_0 = v_0; each step
- *                          v_{t+1} = W v_t / ||W v_t||_1 (the update
- *                          equation of section "PIC: an overview"),
- *                          delta_{t+1} = |v_{t+1} - v_t|, stop when
- *                          |delta_{t+1} - delta_t| <= eps for every entry.
+ *   orc_power_iterate_*    the update equation of section "PIC: an
+ *                          overview" (W v scaled to unit L1 norm) with the
+ *                          acceleration stop of Algorithm 1 (velocity
+ *                          |v_new - v| per entry, the first velocity
+ *                          compared against v_0; stop once no entry's
+ *                          velocity changes by more than eps).
  *   orc_knn_graph          the sparse affinity graph the CSR path takes as
  *                          input: exact k nearest neighbours, union
  *                          symmetrised, Gaussian weights (not in the paper;
@@ -267,15 +268,22 @@ static void op_apply(const orc_op *op, const double *v, double *y)
 }
 
 /* ------------------------------------------------------------------ */
-/* Algorithm 1                                                          */
+/* Power iteration with the acceleration stop (section "PIC: an         */
+/* overview", update equation; stopping rule of Algorithm 1)            */
 /* ------------------------------------------------------------------ */
 
-/* mode 0: run exactly max_iter updates and record the statistic;
- * mode 1: stop at the first t with max_i |delta_{t+1,i} - delta_{t,i}| <= eps.
- * v (in: v_t, out: the newest iterate) and delta (in: delta_t, out: the
- * newest velocity) carry the state, so a run can be resumed.  stats[t]
- * receives the statistic of update t.  Returns the number of matrix-vector
- * products performed, or -1 when ||W v||_1 is zero or not finite. */
+/* Every update applies the operator, y = W v, scales y by its L1 norm
+ * tau = sum_i |y_i| to give the next iterate, and measures the velocity
+ * of each coordinate as the absolute change of v.  Its statistic is the
+ * largest absolute change of that velocity between consecutive updates;
+ * the velocity the first update compares against is whatever delta holds
+ * on entry (v_0 itself by the paper's convention, set by the caller).
+ * mode 0 runs exactly max_iter updates and records the statistic; mode 1
+ * stops after the first update whose statistic is <= eps.  v and delta
+ * carry the state in and out (the newest iterate and velocity), so a run
+ * can be resumed.  stats[t] receives the statistic of update t.  Returns
+ * the number of operator applications performed, or -1 when the L1 norm
+ * is zero or not finite. */
 static int32_t power_iterate(const orc_op *op, int32_t mode, int32_t max_iter,
                              double eps, double *v, double *delta,
                              double *stats, int32_t *converged)
@@ -285,8 +293,8 @@ static int32_t power_iterate(const orc_op *op, int32_t mode, int32_t max_iter,
     *converged = 0;
     int32_t done = max_iter;
     for (int32_t t = 0; t < max_iter; ++t) {
-        op_apply(op, v, y);                            /* W v_t            */
-        double tau = 0.0;                              /* ||W v_t||_1      */
+        op_apply(op, v, y);
+        double tau = 0.0;
         for (int64_t i = 0; i < n; ++i)
             tau += fabs(y[i]);
         if (!(tau > 0.0) || !isfinite(tau)) {
@@ -295,13 +303,13 @@ static int32_t power_iterate(const orc_op *op, int32_t mode, int32_t max_iter,
         }
         double s = 0.0;
         for (int64_t i = 0; i < n; ++i) {
-            double v_next = y[i] / tau;                /* v_{t+1}          */
-            double d_next = fabs(v_next - v[i]);       /* delta_{t+1}      */
-            double acc = fabs(d_next - delta[i]);      /* |d_{t+1} - d_t|  */
-            if (acc > s)
-                s = acc;
-            v[i] = v_next;
-            delta[i] = d_next;
+            const double v_new = y[i] / tau;
+            const double vel = fabs(v_new - v[i]);
+            const double change = fabs(vel - delta[i]);
+            if (change > s)
+                s = change;
+            v[i] = v_new;
+            delta[i] = vel;
         }
         if (stats)
             stats[t] = s;

@@ -10,7 +10,11 @@
 // in the order (0,0), (0,1), .., (0,nb-1), (1,1), .., so tile (I, J)
 // starts at entry 65536 (I nb - I (I - 1) / 2 + J - I).  Diagonal tiles
 // hold the whole block.  Entries outside [0, n)^2 (the last block row and
-// column when 256 does not divide n) are never read.
+// column when 256 does not divide n) are never written by the affinity
+// and may hold anything, NaN included: the product of the last block row
+// or column still loads whole tile rows, but replaces every value outside
+// [0, n)^2 by 0 with a select (never a multiply by a mask) before it is
+// used, so such padding cannot reach a sum.
 //
 // One workgroup per tile.  Tile (I, J) gives the row sums A_IJ v_J to the
 // rows of block I and, when I < J, the column sums A_IJ^T v_I to the rows

@@ -27,9 +27,9 @@ MUTATIONS = {
     "csr_gathers_own_entry": ("y += op->w[p] * v[op->col[p]];", "y += op->w[p] * v[i];"),
     "onthefly_column_degree": ("y += (gauss_affinity(op->X, op->d, i, j, two_sigma2) / di) * v[j];",
                                "y += (gauss_affinity(op->X, op->d, i, j, two_sigma2) / op->degree[j]) * v[j];"),
-    "statistic_without_previous_velocity": ("double acc = fabs(d_next - delta[i]);",
-                                            "double acc = fabs(d_next);"),
-    "velocity_not_carried": ("            delta[i] = d_next;\n", ""),
+    "statistic_without_previous_velocity": ("const double change = fabs(vel - delta[i]);",
+                                            "const double change = fabs(vel);"),
+    "velocity_not_carried": ("            delta[i] = vel;\n", ""),
     "strict_stop_test": ("if (mode == 1 && s <= eps)", "if (mode == 1 && s < eps)"),
     "iterations_off_by_one": ("done = t + 1;", "done = t;"),
     "segment_size_off_by_one": ("double m = (double)(i - j + 1);", "double m = (double)(i - j + 2);"),
