@@ -199,6 +199,21 @@ gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k,
                            float sigma, int64_t *row_ptr, int32_t *col, float *val,
                            int64_t *nnz, void *ws, size_t ws_bytes, void *stream);
 
+/* The same graph with its nodes numbered in the Morton order of the points
+ * (their quantised centred coordinates, the order the builder sorts them
+ * by): node p is point perm[p] (perm: int32 [n], device, written), rows
+ * and columns use node numbers, rows sorted by node number, weights from
+ * the points as above.  The affinity graph is the same whatever the
+ * numbering (section "Spectral Cluster"); this one keeps graph neighbours
+ * at nearby numbers, so the CSR product's gathers of v stay in cache.  A
+ * result v over the nodes maps back to the points as v_point[perm[p]] =
+ * v_node[p].  Arguments, workspace and errors as gpic_knn_graph, plus
+ * INVALID_ARG for a null or misaligned perm. */
+gpic_status gpic_knn_graph_local(const float *X, int64_t n, int32_t d, int32_t k,
+                                 float sigma, int64_t *row_ptr, int32_t *col, float *val,
+                                 int64_t *nnz, int32_t *perm, void *ws, size_t ws_bytes,
+                                 void *stream);
+
 /* Symmetric storage ("packed upper tiles") of the affinity: A is symmetric
  * (section "Spectral Cluster"), so only its upper block triangle is kept and
  * the power iteration applies W v = D^-1 (A v), streaming 2 n^2 bytes per
@@ -207,7 +222,8 @@ gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k,
  * [256 x 256] row-major array holding A[256 I + r][256 J + c], and the
  * tiles are stored one after the other in the order (0,0), (0,1), ..,
  * (0,nb-1), (1,1), .., (nb-1,nb-1).  Diagonal tiles hold the whole block
- * (zero diagonal).  Entries outside [0, n)^2 are never written or read.
+ * (zero diagonal).  Entries outside [0, n)^2 are never written and may hold
+ * anything: the product loads whole tile rows but replaces them by 0.
  * 2 <= n <= 2^24 for every symmetric entry point (INVALID_ARG otherwise).
  * gpic_sym_bytes(n): bytes of that storage (0 for n out of range). */
 size_t gpic_sym_bytes(int64_t n);

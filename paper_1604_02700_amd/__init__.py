@@ -44,7 +44,7 @@ EXPORTS = (
     "gpic_affinity_cosine", "gpic_affinity_cosine_normalized", "gpic_knn_graph",
     "gpic_sym_bytes", "gpic_affinity_sym", "gpic_matvec_sym", "gpic_power_iterate_sym",
     "gpic_power_iterate_dense_host", "gpic_read_stream",
-    "gpic_power_iterate_dense_noalloc",
+    "gpic_power_iterate_dense_noalloc", "gpic_knn_graph_local",
 )
 
 # the static scratch of gpic_power_iterate_dense_noalloc (include/gpic.h)
@@ -96,6 +96,8 @@ def lib() -> C.CDLL:
             "gpic_affinity_cosine": [p, i64, i32, p, i64, p, p, sz, p],
             "gpic_affinity_cosine_normalized": [p, i64, i32, p, i64, p, p, p, p, sz, p],
             "gpic_knn_graph": [p, i64, i32, i32, f32, p, p, p, C.POINTER(i64), p, sz, p],
+            "gpic_knn_graph_local": [p, i64, i32, i32, f32, p, p, p, C.POINTER(i64), p, p, sz,
+                                     p],
             "gpic_degree_normalize": [p, i64, i64, p, i32, p, p, p, sz, p],
             "gpic_degree_normalize_csr": [p, p, p, i64, i64, p, p, p, p, sz, p],
             "gpic_degree_fused": [p, i64, i32, f32, p, p, p, p, sz, p],
@@ -275,6 +277,26 @@ def gpic_knn_graph(X: torch.Tensor, k: int, sigma: float):
                                 _ptr(val), C.byref(nnz), _ptr(ws), nb, _stream(dev)))
     m = int(nnz.value)
     return rp, col[:m], val[:m]
+
+
+def gpic_knn_graph_local(X: torch.Tensor, k: int, sigma: float):
+    """The same graph with its nodes numbered in the Morton order of the
+    points: (row_ptr, col, val, perm), node p being point perm[p] (int32)."""
+    _dev(X, torch.float32, "X")
+    X = X.contiguous()
+    n, d = X.shape
+    dev = X.device
+    rp = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    col = torch.empty(2 * n * k, dtype=torch.int32, device=dev)
+    val = torch.empty(2 * n * k, dtype=torch.float32, device=dev)
+    perm = torch.empty(n, dtype=torch.int32, device=dev)
+    nnz = C.c_int64(0)
+    ws, nb = workspace("knn_graph", n, 0, k, device=dev)
+    _check(lib().gpic_knn_graph_local(_ptr(X), n, d, int(k), float(sigma), _ptr(rp),
+                                      _ptr(col), _ptr(val), C.byref(nnz), _ptr(perm),
+                                      _ptr(ws), nb, _stream(dev)))
+    m = int(nnz.value)
+    return rp, col[:m], val[:m], perm
 
 
 # ----------------------------------------------- 2. degrees, W and v0

@@ -244,12 +244,12 @@ struct CsrProduct : Product {
     const int64_t *row_ptr;
     const int32_t *col;
     const float *val;
-    int64_t n;
-    int64_t blocks() const override { return spmv_blocks(n); }
+    int64_t n, nnz;
+    int64_t blocks() const override { return spmv_partials(n, nnz); }
     hipError_t launch(const double *v, double *y, double *partial, StopCtl ctl,
                       hipStream_t s) const override
     {
-        return launch_spmv(row_ptr, col, val, n, v, y, partial, ctl, true, s);
+        return launch_spmv(row_ptr, col, val, n, nnz, v, y, partial, ctl, true, s);
     }
 };
 
@@ -684,9 +684,10 @@ gpic_status gpic_affinity_cosine_normalized(const float *X, int64_t n, int32_t d
     return GPIC_OK;
 }
 
-gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, float sigma,
-                           int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz,
-                           void *ws, size_t ws_bytes, void *stream)
+static gpic_status knn_graph_common(const float *X, int64_t n, int32_t d, int32_t k,
+                                    float sigma, int64_t *row_ptr, int32_t *col, float *val,
+                                    int64_t *nnz, int32_t *perm, void *ws, size_t ws_bytes,
+                                    void *stream)
 {
     gpic_status st = check_points(X, n, d, sigma);
     if (st != GPIC_OK)
@@ -704,11 +705,29 @@ gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, floa
         return st;
     int status = 0;
     CHECK_HIP(run_knn_graph(X, n, d, k, sigma, row_ptr, col, val, nnz, &status, ws,
-                            (hipStream_t)stream),
+                            (hipStream_t)stream, perm),
               "kNN graph");
     if (status != 0)
         return fail(GPIC_ERR_NUMERIC, "kNN candidate bounds did not converge");
     return GPIC_OK;
+}
+
+gpic_status gpic_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, float sigma,
+                           int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz,
+                           void *ws, size_t ws_bytes, void *stream)
+{
+    return knn_graph_common(X, n, d, k, sigma, row_ptr, col, val, nnz, nullptr, ws, ws_bytes,
+                            stream);
+}
+
+gpic_status gpic_knn_graph_local(const float *X, int64_t n, int32_t d, int32_t k,
+                                 float sigma, int64_t *row_ptr, int32_t *col, float *val,
+                                 int64_t *nnz, int32_t *perm, void *ws, size_t ws_bytes,
+                                 void *stream)
+{
+    CHECK_ARG(perm != nullptr && aligned(perm, 4), "perm null or misaligned");
+    return knn_graph_common(X, n, d, k, sigma, row_ptr, col, val, nnz, perm, ws, ws_bytes,
+                            stream);
 }
 
 gpic_status gpic_degree_normalize(float *A, int64_t n, int64_t lda, double *degree,
@@ -838,7 +857,7 @@ gpic_status gpic_matvec_csr(const int64_t *row_ptr, const int32_t *col,
     if ((st = check_vec(v, "v")) != GPIC_OK || (st = check_vec(y, "y")) != GPIC_OK)
         return st;
     StopCtl none{};
-    CHECK_HIP(launch_spmv(row_ptr, col, val, n, v, y, nullptr, none, false,
+    CHECK_HIP(launch_spmv(row_ptr, col, val, n, nnz, v, y, nullptr, none, false,
                           (hipStream_t)stream),
               "spmv");
     return GPIC_OK;
@@ -1057,6 +1076,7 @@ gpic_status gpic_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
     op.col = col;
     op.val = val;
     op.n = n;
+    op.nnz = nnz;
     return run_power_iteration(op, n, params, v, delta, ws, res, s);
 }
 

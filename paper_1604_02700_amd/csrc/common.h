@@ -181,9 +181,15 @@ hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
 hipError_t launch_gemv_panel(const float *W, int64_t m, int64_t n, int64_t ldw,
                              const double *v, double *y, double *partial, StopCtl ctl,
                              bool use_ctl, hipStream_t s);
+// CSR product: up to 64 entries per row on average, the staged product
+// (tiles of 256 rows, entries staged in LDS by all lanes, a thread per row
+// summing in entry order), else 16 lanes per row; spmv_partials(n, nnz)
+// |y| partial sums either way
+bool spmv_staged(int64_t n, int64_t nnz);
+int64_t spmv_partials(int64_t n, int64_t nnz);
 hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
-                       const float *val, int64_t n, const double *v, double *y,
-                       double *partial, StopCtl ctl, bool use_ctl,
+                       const float *val, int64_t n, int64_t nnz, const double *v,
+                       double *y, double *partial, StopCtl ctl, bool use_ctl,
                        hipStream_t s);
 hipError_t launch_reduce_tau(const double *partial, int64_t nb, double *tau,
                              StopCtl ctl, hipStream_t s);
@@ -256,11 +262,14 @@ hipError_t radix_sort_u64(uint64_t *&keyA, int32_t *&idxA, uint64_t *&keyB, int3
 
 // knn.hip -- exact kNN graph (d <= 16, k <= 64, 2 n k < 2^32); synchronises.
 // *status_host = 1 when the candidate bounds failed to converge (nothing
-// written).  row_ptr [n+1]; col and val hold up to 2 n k entries.
+// written).  row_ptr [n+1]; col and val hold up to 2 n k entries.  With
+// perm_out (int32 [n], device) the nodes are numbered in the Morton order
+// of the points: node p is point perm_out[p].
 size_t knn_graph_ws(int64_t n, int32_t k);
 hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
                          int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz_host,
-                         int *status_host, void *ws, hipStream_t s);
+                         int *status_host, void *ws, hipStream_t s,
+                         int32_t *perm_out = nullptr);
 
 // stream.hip -- read-bandwidth reference (not a step of the method):
 // kReadStreamBlocks workgroups read n floats (n % 4 == 0, 16-byte aligned)

@@ -580,16 +580,33 @@ __global__ __launch_bounds__(kThreads) void fill_i32_kernel(int *__restrict__ a,
 
 // --------------------------------------------------------- 4. symmetrise
 
+// Both directions of every kNN edge as (row, column) keys; with rank, in
+// the node numbering rank[point] (the Morton position) instead of point
+// indices.
 __global__ __launch_bounds__(kThreads) void edge_keys_kernel(const int32_t *__restrict__ nbr,
                                                              int64_t n, int k, int bits,
+                                                             const int32_t *__restrict__ rank,
                                                              uint64_t *__restrict__ key)
 {
     const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (e >= n * k)
         return;
-    const uint64_t a = (uint64_t)(e / k), b = (uint64_t)nbr[e];
+    uint64_t a = (uint64_t)(e / k), b = (uint64_t)nbr[e];
+    if (rank != nullptr) {
+        a = (uint64_t)rank[a];
+        b = (uint64_t)rank[b];
+    }
     key[2 * e] = (a << bits) | b;
     key[2 * e + 1] = (b << bits) | a;
+}
+
+// rank[perm[p]] = p: the node number of every point in Morton numbering
+__global__ __launch_bounds__(kThreads) void rank_kernel(const int32_t *__restrict__ perm,
+                                                        int64_t n, int32_t *__restrict__ rank)
+{
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p < n)
+        rank[perm[p]] = (int32_t)p;
 }
 
 // first[p] = 1 where sorted key p differs from key p - 1
@@ -603,11 +620,13 @@ __global__ __launch_bounds__(kThreads) void first_flags_kernel(const uint64_t *_
 }
 
 // After an exclusive scan of the flags: column, row start and weight of
-// every distinct key; row_ptr[n] = nnz.
+// every distinct key; row_ptr[n] = nnz.  With perm, node r is point
+// perm[r] (the weight comes from the points' coordinates).
 __global__ __launch_bounds__(kThreads) void build_csr_kernel(
     const uint64_t *__restrict__ key, const uint32_t *__restrict__ pos, int64_t m, int bits,
     const float *__restrict__ X, int64_t n, int d, double two_sigma2,
-    int64_t *__restrict__ row_ptr, int32_t *__restrict__ col, float *__restrict__ val)
+    const int32_t *__restrict__ perm, int64_t *__restrict__ row_ptr,
+    int32_t *__restrict__ col, float *__restrict__ val)
 {
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (p >= m)
@@ -622,7 +641,9 @@ __global__ __launch_bounds__(kThreads) void build_csr_kernel(
         return;
     const int64_t q = pos[p];
     col[q] = (int32_t)c;
-    val[q] = (float)exp(-sq_dist64(X, d, r, c) / two_sigma2);
+    const int64_t pr = (perm != nullptr) ? (int64_t)perm[r] : r;
+    const int64_t pc = (perm != nullptr) ? (int64_t)perm[c] : c;
+    val[q] = (float)exp(-sq_dist64(X, d, pr, pc) / two_sigma2);
     if (p == 0 || (int64_t)(key[p - 1] >> bits) != r)
         row_ptr[r] = q;
 }
@@ -709,7 +730,7 @@ size_t knn_graph_ws(int64_t n, int32_t k) { return knn_layout(n, k).total; }
 
 hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
                          int64_t *row_ptr, int32_t *col, float *val, int64_t *nnz_host,
-                         int *status_host, void *ws, hipStream_t s)
+                         int *status_host, void *ws, hipStream_t s, int32_t *perm_out)
 {
     const KnnLayout L = knn_layout(n, k);
     char *w = static_cast<char *>(ws);
@@ -816,11 +837,18 @@ hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
         act = active;
     }
 
-    // 4. symmetrise
+    // 4. symmetrise (in Morton numbering when the caller takes the order:
+    // the sort's spare index buffer holds the ranks)
     const int bits = bits_for(n);
     const int64_t mm = 2 * n * (int64_t)k;
+    int32_t *rank = nullptr;
+    if (perm_out != nullptr) {
+        rank = permB;
+        hipLaunchKernelGGL(rank_kernel, dim3(rows_grid), dim3(kThreads), 0, s,
+                           (const int32_t *)perm, n, rank);
+    }
     hipLaunchKernelGGL(edge_keys_kernel, dim3((unsigned)((n * k + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, s, nbr, n, k, bits, keyA);
+                       dim3(kThreads), 0, s, nbr, n, k, bits, (const int32_t *)rank, keyA);
     int32_t *none_a = nullptr, *none_b = nullptr;
     hipError_t e = radix_sort_u64(keyA, none_a, keyB, none_b, mm, (2 * bits + 7) / 8 * 8,
                                   hist, hsum, s);
@@ -831,8 +859,14 @@ hipError_t run_knn_graph(const float *X, int64_t n, int d, int k, float sigma,
     if ((e = exclusive_scan_u32(first, mm, hsum, s)) != hipSuccess)
         return e;
     hipLaunchKernelGGL(build_csr_kernel, dim3(egrid), dim3(kThreads), 0, s, keyA, first, mm,
-                       bits, X, n, d, 2.0 * (double)sigma * (double)sigma, row_ptr, col, val);
+                       bits, X, n, d, 2.0 * (double)sigma * (double)sigma,
+                       perm_out != nullptr ? (const int32_t *)perm : nullptr, row_ptr, col,
+                       val);
     if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    if (perm_out != nullptr &&
+        (e = hipMemcpyAsync(perm_out, perm, (size_t)n * 4, hipMemcpyDeviceToDevice, s)) !=
+            hipSuccess)
         return e;
     if ((e = hipMemcpyAsync(nnz_host, row_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost,
                             s)) != hipSuccess)

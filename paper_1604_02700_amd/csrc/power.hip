@@ -24,6 +24,11 @@ constexpr int kSpmvLanes = 16;      // lanes per CSR row
 constexpr int kSpmvRows = 32;       // rows per workgroup of the CSR product
 constexpr int kSpmvUnroll = 4;      // independent gathers in flight per lane
 constexpr int64_t kTauUpdateMaxN = 16384;   // one launch for tau and the update
+constexpr int kStagedRows = 256;    // rows per tile of the staged CSR product
+constexpr int kStageK = 24;         // entries per thread per round of the staged product
+constexpr int kStage = kStageK * kThreads;   // entries staged in LDS per round (48 KB)
+constexpr int64_t kStagedMaxAvg = 64;   // mean entries per row up to which it is used
+constexpr int kXcds = 8;            // workgroups go round-robin to the 8 XCDs
 
 // CSR product: 16 lanes per row, lane l summing entries l, l + 16, ... of
 // its row in that order, then a 16-lane butterfly.  The workgroup's row
@@ -88,6 +93,96 @@ __global__ __launch_bounds__(kThreads) void spmv_kernel(
         partial[blockIdx.x] = t;
 }
 
+// CSR product for short rows (a kNN graph holds about 45 entries per row):
+// with 16 lanes per row, most lanes of a gather instruction sit idle while
+// the wave finishes its longest row.  Here a workgroup owns a tile of 256
+// consecutive rows and walks the tile's entries in storage order in rounds
+// of kStage: every thread loads kStageK columns and weights (coalesced, all
+// in flight at once), gathers v at those columns (all in flight), and
+// stages the float64 products w_p v[col_p] in LDS; after a barrier a thread
+// per row adds its row's products in entry order -- the oracle's own
+// arithmetic, a product rounded then added -- carrying its sum across
+// rounds.  The next round's columns and weights are loaded while the
+// current round's rows are summed.  Tiles are numbered XCD-major: the
+// workgroups one XCD runs hold a contiguous eighth of the rows, so with a
+// numbering that keeps graph neighbours close, the v entries an XCD
+// gathers stay in its L2.
+__global__ __launch_bounds__(kThreads) void spmv_staged_kernel(
+    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    const float *__restrict__ val, int64_t n, int64_t tiles, int64_t per_xcd,
+    const double *__restrict__ v, double *__restrict__ y, double *__restrict__ partial,
+    StopCtl ctl, int use_ctl)
+{
+    __shared__ int64_t rp[kStagedRows + 1];
+    __shared__ double ps[kStage];
+    __shared__ double red[kThreads / kWave];
+    if (use_ctl) {
+        if (blockIdx.x == 0 && threadIdx.x == 0)
+            *ctl.cur_stat = 0.0;
+        if (stop_reached(ctl))
+            return;
+    }
+    const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (tile >= tiles)
+        return;                                      // uniform over the workgroup
+    const int64_t row0 = tile * kStagedRows;
+    for (int t = threadIdx.x; t <= kStagedRows; t += kThreads)
+        rp[t] = row_ptr[row0 + t < n ? row0 + t : n];
+    __syncthreads();
+    const int64_t e0 = rp[0], e1 = rp[kStagedRows];
+    const int li = threadIdx.x;
+    const int64_t i = row0 + li;
+    const int64_t rs = rp[li], re = rp[li + 1];      // this thread's row (empty past n)
+    int32_t c[kStageK];
+    float w[kStageK];
+    auto load = [&](int64_t r0) {
+#pragma unroll
+        for (int u = 0; u < kStageK; ++u) {
+            const int64_t p = r0 + threadIdx.x + (int64_t)u * kThreads;
+            c[u] = p < e1 ? col[p] : -1;
+            w[u] = p < e1 ? val[p] : 0.0f;
+        }
+    };
+    double s = 0.0;
+    load(e0);
+    for (int64_t r0 = e0; r0 < e1; r0 += kStage) {
+        double x[kStageK];
+#pragma unroll
+        for (int u = 0; u < kStageK; ++u)
+            x[u] = c[u] >= 0 ? v[c[u]] : 0.0;
+#pragma unroll
+        for (int u = 0; u < kStageK; ++u)
+            ps[threadIdx.x + u * kThreads] = (double)w[u] * x[u];   // 0 past the tile
+        __syncthreads();
+        if (r0 + kStage < e1)
+            load(r0 + kStage);                       // in flight during the sums
+        const int64_t r1 = (r0 + kStage < e1) ? r0 + kStage : e1;
+        const int a = (int)(((rs > r0) ? rs : r0) - r0);
+        const int z = (int)(((re < r1) ? re : r1) - r0);
+        int p = a;
+        for (; p + 4 <= z; p += 4) {
+            double q[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                q[u] = ps[p + u];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                s = s + q[u];
+        }
+        for (; p < z; ++p)
+            s = s + ps[p];
+        __syncthreads();                             // before the next round's stage
+    }
+    double yabs = 0.0;
+    if (i < n) {
+        y[i] = s;
+        yabs = fabs(s);
+    }
+    const double t = block_sum<kThreads>(yabs, red);
+    if (threadIdx.x == 0 && partial != nullptr)
+        partial[tile] = t;
+}
+
 // tau = sum of the block partials, by one workgroup in a fixed order.
 __global__ __launch_bounds__(1024) void reduce_tau_kernel(
     const double *__restrict__ partial, int64_t nb, double *__restrict__ tau,
@@ -118,13 +213,30 @@ __global__ __launch_bounds__(kThreads) void update_kernel(
     const double t = *tau;
     double s = 0.0;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
-         i += stride) {
-        const double vn = y[i] / t;
-        const double dn = fabs(vn - v[i]);
-        s = fmax(s, fabs(dn - delta[i]));
-        v[i] = vn;
-        delta[i] = dn;
+    // four rows per thread per step, their loads all in flight (the max
+    // is order-free, so the result does not depend on the grouping)
+    constexpr int U = 4;
+    for (int64_t i0 = (int64_t)blockIdx.x * kThreads + threadIdx.x; i0 < n;
+         i0 += U * stride) {
+        double yy[U], vv[U], dd[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + u * stride;
+            yy[u] = i < n ? y[i] : 0.0;
+            vv[u] = i < n ? v[i] : 0.0;
+            dd[u] = i < n ? delta[i] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + u * stride;
+            if (i < n) {
+                const double vn = yy[u] / t;
+                const double dn = fabs(vn - vv[u]);
+                s = fmax(s, fabs(dn - dd[u]));
+                v[i] = vn;
+                delta[i] = dn;
+            }
+        }
     }
     const double m = block_max<kThreads>(s, red);
     if (threadIdx.x == 0)
@@ -200,13 +312,29 @@ unsigned grid_for(int64_t n, int64_t cap)
 
 int64_t spmv_blocks(int64_t n) { return (n + kSpmvRows - 1) / kSpmvRows; }
 
-hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
-                       const float *val, int64_t n, const double *v, double *y,
-                       double *partial, StopCtl ctl, bool use_ctl, hipStream_t s)
+bool spmv_staged(int64_t n, int64_t nnz) { return nnz <= kStagedMaxAvg * n; }
+
+int64_t spmv_partials(int64_t n, int64_t nnz)
 {
-    hipLaunchKernelGGL(spmv_kernel, dim3((unsigned)spmv_blocks(n)),
-                       dim3(kThreads), 0, s, row_ptr, col, val, n, v, y, partial,
-                       ctl, use_ctl ? 1 : 0);
+    return spmv_staged(n, nnz) ? (n + kStagedRows - 1) / kStagedRows : spmv_blocks(n);
+}
+
+hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
+                       const float *val, int64_t n, int64_t nnz, const double *v,
+                       double *y, double *partial, StopCtl ctl, bool use_ctl,
+                       hipStream_t s)
+{
+    if (spmv_staged(n, nnz)) {
+        const int64_t tiles = (n + kStagedRows - 1) / kStagedRows;
+        const int64_t per = (tiles + kXcds - 1) / kXcds;
+        hipLaunchKernelGGL(spmv_staged_kernel, dim3((unsigned)(per * kXcds)), dim3(kThreads),
+                           0, s, row_ptr, col, val, n, tiles, per, v, y, partial, ctl,
+                           use_ctl ? 1 : 0);
+    } else {
+        hipLaunchKernelGGL(spmv_kernel, dim3((unsigned)spmv_blocks(n)),
+                           dim3(kThreads), 0, s, row_ptr, col, val, n, v, y, partial,
+                           ctl, use_ctl ? 1 : 0);
+    }
     return hipGetLastError();
 }
 

@@ -242,6 +242,37 @@ def test_knn_csr_full_size_converge(g, orc, knn8d):
                  vg, out.km, w.k)
 
 
+def test_knn_csr_full_size_local_order(g, orc, knn8d):
+    """knn8d at n = 2,000,000 with the graph built on the GPU in the Morton
+    numbering of the points (the staged product, gathers near the row):
+    to convergence against the oracle on that same graph, and the graph
+    itself equal to the workload's k-d tree graph relabelled."""
+    w = knn8d
+    print(f"gpu: knn8d n={w.n} local numbering", flush=True)
+    rp, col, val, perm = g.gpic_knn_graph_local(_t(w.X), 32, 1.0)
+    perm = perm.cpu().numpy()
+    rph, colh, valh = rp.cpu().numpy(), col.cpu().numpy(), val.cpu().numpy()
+    import scipy.sparse as sp
+    S = sp.csr_matrix((w.val, w.col, w.row_ptr), shape=(w.n, w.n))[perm][:, perm].tocsr()
+    S.sort_indices()
+    assert np.array_equal(rph, S.indptr) and np.array_equal(colh, S.indices)
+    assert np.all(np.abs(valh - S.data) <= np.spacing(S.data))
+    del S
+    out = g.pic_csr(rp, col, val, w.k, "converge", 1000, w.eps)
+    wr, dr, v0r, _ = orc.degree_normalize_csr(rph, colh, valh)
+    ref = orc.power_iterate_csr(rph, colh, wr, v0r, "converge", 1000, w.eps)
+    mu = stop_margin(ref.stats, w.eps, ref.iterations)
+    print(f"  iterations gpu={out.pi.iterations} oracle={ref.iterations} "
+          f"margin={mu:.3g}", flush=True)
+    np.testing.assert_allclose(out.degree.cpu().numpy(), dr, rtol=1e-12)
+    assert ref.converged and out.pi.converged
+    assert out.pi.iterations == ref.iterations
+    vg = out.pi.v.cpu().numpy()
+    assert rel_l1(vg, ref.v) <= 1e-4
+    check_labels(orc, f"knn8d csr local n={w.n}", ref.v,
+                 orc.kmeans1d(ref.v, w.k, "dc").labels, vg, out.km, w.k)
+
+
 def test_moons_full_size_cosine(g, orc):
     """Two moons, n = 45,000, cosine affinity (dense W of 8.1 GB), at most 3
     updates with eps = 1e-5 / n: degrees, stop and v against the oracle."""

@@ -565,6 +565,76 @@ def test_csr_column_blocked_parity(g, orc, sort_rows, band):
     np.testing.assert_allclose(v.cpu().numpy(), refc.v, rtol=1e-9)
 
 
+@pytest.mark.parametrize("n,long_rows", [(3001, 0), (4100, 3), (700, 200)])
+def test_csr_staged_product_edges(g, n, long_rows):
+    """The staged CSR product (tiles of 256 rows, entries staged 2,048 per
+    round): tile and round edges, empty rows, rows longer than a round
+    (5,000 entries: a thread's sum carried across rounds), and a mean
+    above 64 entries per row (the 16-lane row-wise product) when the long
+    rows dominate: against the float64 product of the same float32 W."""
+    import scipy.sparse as sp
+    rng = np.random.default_rng(n + long_rows)
+    lens = rng.integers(0, 40, size=n)
+    lens[rng.choice(n, 5, replace=False)] = 0                 # empty rows
+    lens[:long_rows] = 5000 if n > 5000 else n - 1
+    rows = np.repeat(np.arange(n), lens)
+    cols = np.concatenate([np.sort(rng.choice(n, size=m, replace=False)) for m in lens])
+    W = sp.csr_matrix((rng.uniform(0.0, 1.0, size=rows.size).astype(np.float32),
+                       (rows, cols)), shape=(n, n))
+    W.sort_indices()
+    rp, col, val = W.indptr.astype(np.int64), W.indices.astype(np.int32), W.data
+    v = rng.uniform(0.5, 1.5, size=n)
+    print(f"staged csr n={n} nnz={col.size} mean={col.size / n:.1f}", flush=True)
+    y = g.gpic_matvec_csr(_t(rp), _t(col), _t(val), _t(v)).cpu().numpy()
+    np.testing.assert_allclose(y, W.astype(np.float64) @ v, rtol=1e-12, atol=0)
+
+
+def _relabel(rp, col, val, perm):
+    """The graph with node p standing for node perm[p] of the input."""
+    import scipy.sparse as sp
+    n = rp.size - 1
+    S = sp.csr_matrix((val, col, rp), shape=(n, n))
+    P = S[perm][:, perm].tocsr()
+    P.sort_indices()
+    return P.indptr.astype(np.int64), P.indices.astype(np.int32), P.data
+
+
+def test_knn_graph_local_numbering(g, orc):
+    """The kNN graph numbered in the Morton order of the points is the
+    oracle's brute-force graph relabelled by the returned permutation: the
+    same rows, columns and weights (n = 60,000 of the kNN workload's
+    generator, k = 32)."""
+    import workloads
+    w = workloads.make("knn8d", n=60000)
+    print(f"knn graph local n={w.n}", flush=True)
+    rp, col, val, perm = g.gpic_knn_graph_local(_t(w.X), 32, 1.0)
+    torch.cuda.synchronize()
+    perm = perm.cpu().numpy()
+    assert np.array_equal(np.sort(perm), np.arange(w.n))
+    rpo, colo, valo = _relabel(*orc.knn_graph(w.X, 32, 1.0), perm)
+    assert np.array_equal(rp.cpu().numpy(), rpo)
+    assert np.array_equal(col.cpu().numpy(), colo)
+    vg = val.cpu().numpy()
+    assert np.all(np.abs(vg - valo) <= np.spacing(valo))
+
+
+def test_knn_csr_local_order_matches_original(g):
+    """Power iteration over the Morton-numbered graph gives the original
+    graph's v permuted (up to summation order), and stops at the same
+    update."""
+    import workloads
+    w = workloads.make("knn8d", n=50000)
+    X = _t(w.X)
+    rp, col, val = g.gpic_knn_graph(X, 32, 1.0)
+    rpl, coll, vall, perm = g.gpic_knn_graph_local(X, 32, 1.0)
+    a = g.pic_csr(rp, col, val, w.k, "converge", 1000, w.eps)
+    b = g.pic_csr(rpl, coll, vall, w.k, "converge", 1000, w.eps)
+    assert a.pi.iterations == b.pi.iterations and a.pi.converged and b.pi.converged
+    va = a.pi.v.cpu().numpy()
+    vb = b.pi.v.cpu().numpy()
+    np.testing.assert_allclose(vb, va[perm.cpu().numpy()], rtol=1e-10)
+
+
 def _check_knn(g, orc, X, k, sigma):
     rp, col, val = g.gpic_knn_graph(_t(X), k, sigma)
     torch.cuda.synchronize()
