@@ -14,7 +14,13 @@ object is for the dominant kernel (the dense product), timed with HIP events
 on the library's stream, and also as a fraction of the plain read stream
 the device reaches over the same buffer in the same run (read_stream);
 cpu_baseline is the float64 oracle on a bounded sample of the same workload
-on the host cores.
+on the host cores (host described in cpu_baseline.host).
+
+The same line carries the other workloads' figures under "workloads" (the
+small dense blobs and rings, the fused operator on 64-D blobs, the CSR
+path on the 2M-node kNN graph built on the GPU), each with its own
+roofline object for its dominant kernel and its own oracle baseline;
+--workload NAME prints one such workload as a line of its own.
 """
 from __future__ import annotations
 
@@ -59,6 +65,34 @@ def measured_traffic(path: str = TRAFFIC_FILE, source: str = "gemv.hip",
     return t.get("bytes_per_launch")
 
 
+def host_info(threads_used: int) -> dict:
+    """CPU model, sockets, physical cores and logical CPUs of this host, and
+    the threads the oracle ran with."""
+    model, sockets, cores = None, set(), set()
+    phys = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                k, _, v = line.partition(":")
+                k, v = k.strip(), v.strip()
+                if k == "model name" and model is None:
+                    model = v
+                elif k == "physical id":
+                    phys = v
+                    sockets.add(v)
+                elif k == "core id":
+                    cores.add((phys, v))
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        avail = os.cpu_count()
+    return {"cpu_model": model, "sockets": len(sockets) or None,
+            "physical_cores": len(cores) or None, "logical_cpus": os.cpu_count(),
+            "cpus_available_to_process": avail, "threads_used": threads_used}
+
+
 def cpu_baseline(w, n_sample, T):
     """The oracle on the first n_sample points of the same workload."""
     import oracle
@@ -73,7 +107,7 @@ def cpu_baseline(w, n_sample, T):
     t3 = time.perf_counter()
     gbs = T * 4.0 * n_sample * n_sample / (t2 - t1) / 1e9
     return {"value": round(gbs, 3), "unit": "GB/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "host": host_info(oracle.num_threads()),
             "sample": (f"first {n_sample} of the {w.n} points" if n_sample < w.n
                        else f"the whole workload ({w.n} points)")
                       + f", dense W (float64 in the oracle, counted at 4 B/entry "
@@ -97,9 +131,11 @@ def main():
     ap.add_argument("--no-converge", action="store_true")
     ap.add_argument("--no-sym", action="store_true",
                     help="skip the symmetric-storage figures of the headline line")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the other workloads' figures of the headline line")
     ap.add_argument("--workload", default="blobs16d",
                     choices=["blobs16d", "blobs16d_sym", "blobs16d_host", "blobs64d", "knn8d",
-                             "knn8d_rcm", "rings2d", "blobs2d", "moons", "circles3"],
+                             "knn8d_random", "rings2d", "blobs2d", "moons", "circles3"],
                     help="blobs16d is the headline line; the others measure the "
                          "fused, CSR, small dense and cosine (the paper's "
                          "Experiment I shapes) paths")
@@ -264,6 +300,21 @@ def main():
         log(f"bench: copy reference {copy_ref}")
         del src, dst
 
+    others = None
+    if not args.no_workloads:
+        # the other workloads' figures (bounded: a few steps each)
+        others = {}
+        for key, name, st, wu in (("blobs2d_c1", "blobs2d", 5, 2), ("rings2d_c2", "rings2d", 3, 1),
+                                  ("fused_c4", "blobs64d", 2, 1), ("csr_c5", "knn8d", 3, 1)):
+            log(f"bench: workload {name} ...")
+            w2 = make_workload(name)
+            others[key] = measure_path(g, torch, w2, st, wu, cpu=not args.no_cpu_baseline)
+            log(f"bench: {name} e2e {others[key]['e2e_ms']} ms, "
+                f"{others[key]['ms_per_update']} ms/update, roofline frac "
+                f"{others[key]['roofline']['frac']}")
+            del w2
+            torch.cuda.empty_cache()
+
     traffic = measured_traffic()
     line = {
         "metric": "power-iteration GB/s of W streamed (% HBM peak); end-to-end "
@@ -277,7 +328,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64",
+        "dtype": DTYPE,
         "data": "synthetic",
         "config": {"workload": f"blobs16d: n={n}, d={d}, 10 Dirichlet(5) Gaussian "
                                f"blobs, sigma=median pair distance, dense float32 W, "
@@ -300,6 +351,7 @@ def main():
         "symmetric_storage": sym,
         "cpu_baseline": cpu,
         "copy_reference": copy_ref,
+        "workloads": others,
     }
     print(json.dumps(line), flush=True)
 
@@ -401,7 +453,7 @@ def sym_workload(args):
             "value": round(T * stored / (pi_ms * 1e-3) / 1e9, 2), "unit": "GB/s",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
             "ms_per_step": round(r["ms_step"], 4), "higher_is_better": True,
-            "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+            "scaling": "weak", "vs_baseline": None, "dtype": DTYPE, "data": "synthetic",
             "config": {"workload": f"blobs16d: n={n}, d={w.d}, packed upper tiles of A "
                                    f"({stored / 1e9:.2f} GB), T={T}, k={k}", "n": n,
                        "storage": "f32 symmetric tiles", "accumulate": "f64"},
@@ -450,7 +502,7 @@ def host_workload(args):
     line = {"metric": "blobs16d with W in host memory: power-iteration GB/s of W streamed "
                       "over PCIe", "value": round(T * wbytes / t / 1e9, 2), "unit": "GB/s",
             "n_gpus": 1, "steps": T, "warmup": 1, "ms_per_step": round(t * 1e3 / T, 3),
-            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": DTYPE,
             "data": "synthetic",
             "config": {"workload": f"blobs16d: n={n}, dense float32 W ({wbytes / 1e9:.1f} GB) "
                                    "in pinned host memory, two 64 MiB device panels",
@@ -466,45 +518,123 @@ PAPER_GPIC_S = {("moons", 15000): 3.99, ("circles3", 15000): 4.03,
                 ("moons", 45000): 45.07, ("circles3", 45000): 45.90}
 
 
-def other_workload(args):
-    """Fused (blobs64d), CSR (knn8d) and small dense workloads: one JSON line
-    with the path's own rate; not the headline line."""
-    import torch
-    import paper_1604_02700_amd as g
-    import workloads
+DTYPE = "f32 storage, f64 arithmetic"
+FUSED_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_traffic_blobs64d_n200000.json")
+CSR_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmv_staged_traffic_knn8d_n2000000.json")
 
+
+def _events(torch, stream, fn, reps):
+    """Average time of `reps` back-to-back calls between one event pair on
+    the library's stream (ms)."""
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    fn()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def knn8d_points(n=None):
+    """The kNN workload's points (the generator alone: the graph is built
+    on the GPU by the library)."""
+    import workloads
+    n = n or 2000000
+    X, y = workloads.blobs_equal(n=n, d=8, k=50, seed=5)
+    return workloads.Workload("knn8d", X, y, np.float32(1.0), 1e-5 / n, 50, "converge",
+                              1000, "csr", 5)
+
+
+def oracle_baseline(w, graph=None):
+    """The oracle on a bounded sample of the same workload, in the unit of
+    the GPU figure it stands beside."""
+    import oracle
+    th = oracle.num_threads()
+    base = {"cores": th, "kind": "oracle", "host": host_info(th)}
+    if w.path in ("dense", "cosine"):
+        reps = 3 if w.n <= 2000 else 1
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            A = oracle.affinity(w.X, w.sigma) if w.path == "dense" else oracle.affinity_cosine(w.X)
+            W, deg, v0, _ = oracle.degree_normalize(A, copy=False)
+            t1 = time.perf_counter()
+            pi = oracle.power_iterate_dense(W, v0, w.mode, w.max_iter, w.eps)
+            t2 = time.perf_counter()
+            oracle.kmeans1d(pi.v, w.k)
+            t3 = time.perf_counter()
+            ts.append((t1 - t0, t2 - t1, t3 - t2))
+        ta, tp, tk = (float(np.median([t[i] for t in ts])) for i in range(3))
+        return {**base, "value": round(pi.iterations * 4.0 * w.n * w.n / tp / 1e9, 3),
+                "unit": "GB/s", "sample": f"the whole workload ({w.n} points, "
+                f"{pi.iterations} updates), affinity to k-means"
+                + (f", median of {reps} runs" if reps > 1 else ""),
+                "e2e_s": round(ta + tp + tk, 4),
+                "phases_s": {"affinity_normalise": round(ta, 4), "power_iteration": round(tp, 4),
+                             "kmeans": round(tk, 4)}}
+    if w.path == "fused":
+        # one product's rows are independent: 1,000 evenly spaced rows,
+        # scaled to the whole sweep
+        m = 1000
+        rows = (np.arange(m, dtype=np.int64) * w.n) // m
+        v = np.full(w.n, 1.0 / w.n)
+        t0 = time.perf_counter()
+        oracle.matvec_onthefly_rows(w.X, w.sigma, np.ones(w.n), v, rows)
+        t = (time.perf_counter() - t0) * w.n / m
+        return {**base, "value": round(2.0 * w.n * w.n * w.d / t / 1e12, 5), "unit": "TFLOP/s",
+                "sample": f"{m} evenly spaced rows of one on-the-fly product (every pair's "
+                          f"affinity recomputed in float64), scaled by n / {m} to a sweep",
+                "s_per_sweep_estimate": round(t, 3)}
+    if w.path == "csr":
+        rp, col, val = graph
+        T = 5
+        t0 = time.perf_counter()
+        wn, deg, v0, _ = oracle.degree_normalize_csr(rp, col, val)
+        t1 = time.perf_counter()
+        oracle.power_iterate_csr(rp, col, wn, v0, "fixed", T)
+        t2 = time.perf_counter()
+        nnz = col.shape[0]
+        b = 8.0 * nnz + 8.0 * (w.n + 1) + 16.0 * w.n
+        return {**base, "value": round(T * b / (t2 - t1) / 1e9, 3), "unit": "GB/s",
+                "sample": f"{T} updates of the power iteration over the whole graph "
+                          f"({w.n} nodes, {nnz} entries), bytes counted as on the GPU",
+                "s_per_update": round((t2 - t1) / T, 4), "normalise_s": round(t1 - t0, 4)}
+    return None
+
+
+def measure_path(g, torch, w, steps, warmup, cpu=True, graph_numbering="local"):
+    """One workload through its path: end-to-end steps, the power-iteration
+    loop alone, the dominant kernel against its roofline, and (optionally)
+    the oracle beside it.  Returns a dict."""
     dev = torch.device("cuda:0")
-    cache = os.path.join(ROOT, ".cache")
-    log(f"bench: building workload {args.workload} (the kNN graph takes minutes "
-        f"on the host for knn8d)")
-    w = workloads.make(args.workload, n=args.wn, cache_dir=cache)
-    log(f"bench: workload {w.name} n={w.n} d={w.d} path={w.path} mode={w.mode}")
     stream = torch.cuda.current_stream(dev)
     X = torch.from_numpy(w.X).to(dev)
-    # the cosine workloads keep the paper's cap of 3 updates
-    T = w.max_iter if (w.mode == "fixed" or w.path == "cosine") else 1000
-    extra = {}
+    T = w.max_iter
+    info = {"workload": w.name, "n": w.n, "d": w.d, "path": w.path, "mode": w.mode,
+            "T_or_cap": T, "k": w.k}
+    graph = None
     if w.path == "csr":
-        rp = torch.from_numpy(w.row_ptr).to(dev)
-        col = torch.from_numpy(w.col).to(dev)
-        val0 = torch.from_numpy(w.val).to(dev)
+        # the input graph built on the GPU (exact 32-NN, union, Gaussian
+        # weights); "local": nodes numbered in the points' Morton order
+        build = (lambda: g.gpic_knn_graph_local(X, 32, 1.0)) if graph_numbering == "local" \
+            else (lambda: g.gpic_knn_graph(X, 32, 1.0) + (None,))
+        build()
+        torch.cuda.synchronize()
+        tg = time.perf_counter()
+        rp, col, val0, perm = build()
+        torch.cuda.synchronize()
+        info["graph_build_gpu_s"] = round(time.perf_counter() - tg, 4)
+        info["graph_numbering"] = ("Morton order of the points" if graph_numbering == "local"
+                                   else "the generator's point order")
         nnz = int(val0.numel())
-        extra["nnz"] = nnz
-        if w.name.startswith("knn8d") and w.name == "knn8d":
-            # the same input graph built on the GPU (exact kNN, k = 32)
-            g.gpic_knn_graph(X, 32, 1.0)
-            torch.cuda.synchronize()
-            tg = time.perf_counter()
-            grp, gcol, gval = g.gpic_knn_graph(X, 32, 1.0)
-            torch.cuda.synchronize()
-            extra["graph_build_gpu_s"] = round(time.perf_counter() - tg, 4)
-            extra["graph_equal_to_input"] = bool(torch.equal(grp, rp) and torch.equal(gcol, col))
-            del grp, gcol, gval
-            log(f"bench: kNN graph on the GPU in {extra['graph_build_gpu_s']} s")
+        info["nnz"] = nnz
+        graph = (rp, col, val0)
 
         def step():
-            val = val0.clone()
-            return g.pic_csr(rp, col, val, w.k, w.mode, T, w.eps)
+            return g.pic_csr(rp, col, val0.clone(), w.k, w.mode, T, w.eps)
     elif w.path == "fused":
         def step():
             return g.pic_fused(X, w.sigma, w.k, w.mode, T, w.eps)
@@ -519,19 +649,21 @@ def other_workload(args):
         def step():
             return g.pic_dense(X, w.sigma, w.k, w.mode, T, w.eps, A=A)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
+    times = []
+    for _ in range(steps):
+        t0 = time.perf_counter()
         out = step()
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - t0)
     it = out.pi.iterations
     # the power-iteration loop alone, from the same start
     v = out.v0.clone()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    roof = {}
     if w.path == "csr":
         valn = val0.clone()
         valn, _, _, _ = g.gpic_degree_normalize_csr(rp, col, valn)
@@ -541,8 +673,21 @@ def other_workload(args):
         torch.cuda.synchronize()
         pi_ms = e0.elapsed_time(e1)
         bytes_it = 8.0 * nnz + 8.0 * (w.n + 1) + 16.0 * w.n
-        rate = {"unit": "GB/s", "value": it * bytes_it / (pi_ms * 1e-3) / 1e9,
-                "bytes_per_update": bytes_it, "bound": "hbm", "peak": HBM_PEAK_GBS}
+        rate = {"value": it * bytes_it / (pi_ms * 1e-3) / 1e9, "unit": "GB/s",
+                "bytes_per_update": bytes_it}
+        yv = torch.empty_like(v)
+        kms = _events(torch, stream, lambda: g.gpic_matvec_csr(rp, col, valn, v, yv), 20)
+        staged = nnz <= 64 * w.n
+        kernel = ("spmv_staged_kernel" if staged else "spmv_kernel")
+        traffic = measured_traffic(CSR_TRAFFIC_FILE, "power.hip", "power_hip_sha") \
+            if (staged and graph_numbering == "local" and w.n == 2000000) else None
+        roof = {"bound": "hbm", "kernel": kernel, "achieved": bytes_it / (kms * 1e-3) / 1e9,
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": traffic,
+                "avg_launch_ms": kms, "bytes_per_launch": bytes_it}
+        if graph_numbering != "local":
+            roof["note"] = ("gpic_matvec_csr has no column-blocked copy: on a random "
+                            "numbering the power iteration's blocked product is faster "
+                            "than this kernel (ms_per_update)")
     elif w.path == "fused":
         e0.record(stream)
         g.gpic_power_iterate_fused(X, w.sigma, out.degree, v, None, "fixed", it,
@@ -551,12 +696,11 @@ def other_workload(args):
         torch.cuda.synchronize()
         pi_ms = e0.elapsed_time(e1)
         # algorithmic: the operator's 2 n^2 d flop per sweep (every ordered
-        # pair), whatever the kernel evaluates
+        # pair), whatever the kernel evaluates; executed: up to 2^19 points
+        # each pair once in row groups of 256 (group R covers the columns
+        # from its own first row on), three fp16 part products per
+        # coordinate, coordinates padded to 32-coordinate chunks
         flops = 2.0 * w.n * w.n * w.d
-        # evaluated: up to 2^19 points each pair once, in row groups of 256
-        # (group R covers the columns from its own first row on), else every
-        # ordered pair; three fp16 part products per coordinate, coordinates
-        # padded to 32-coordinate chunks
         G = 256
         if w.n <= (1 << 19):
             groups = (w.n + G - 1) // G
@@ -566,13 +710,22 @@ def other_workload(args):
             pairs = float(w.n) * w.n
             kernel = "affinity_mfma_kernel (kApply)"
         exec_flops = 3 * 2.0 * pairs * 32 * ((w.d + 31) // 32)
-        rate = {"unit": "TFLOP/s", "value": it * flops / (pi_ms * 1e-3) / 1e12,
-                "flops_per_sweep": flops, "bound": "mfma", "kernel": kernel,
+        ms_upd = pi_ms / max(it, 1)
+        rate = {"value": flops / (ms_upd * 1e-3) / 1e12, "unit": "TFLOP/s",
+                "flops_per_sweep": flops}
+        traffic = measured_traffic(FUSED_TRAFFIC_FILE, "affinity.hip", "affinity_hip_sha") \
+            if w.n == 200000 else None
+        roof = {"bound": "mfma", "kernel": kernel,
+                "achieved": flops / (ms_upd * 1e-3) / 1e12,
+                "peak": FP16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s", "traffic": traffic,
+                "avg_launch_ms": ms_upd, "flops_per_launch": flops,
+                "flops_note": "algorithmic 2 n^2 d per product (the Gram contraction of every "
+                              "ordered pair) over the dense fp16 matrix-core peak (the Gram "
+                              "runs on fp16 split operands); launch time = one update of the "
+                              "loop (product + reduce + tau/update)",
                 "pairs_evaluated_per_sweep": pairs,
-                "fp16_mfma_flops_per_sweep": exec_flops,
-                "fp16_mfma_tflops": round(it * exec_flops / (pi_ms * 1e-3) / 1e12, 2),
-                "peak": FP16_MFMA_PEAK_TFLOPS}
-        rate["frac_override"] = rate["fp16_mfma_tflops"] / FP16_MFMA_PEAK_TFLOPS
+                "fp16_mfma_flops_executed_per_sweep": exec_flops,
+                "fp16_mfma_tflops_executed": round(exec_flops / (ms_upd * 1e-3) / 1e12, 2)}
     else:
         W = A
         e0.record(stream)
@@ -581,29 +734,58 @@ def other_workload(args):
         torch.cuda.synchronize()
         pi_ms = e0.elapsed_time(e1)
         bytes_it = 4.0 * w.n * w.n
-        rate = {"unit": "GB/s", "value": it * bytes_it / (pi_ms * 1e-3) / 1e9,
-                "bytes_per_update": bytes_it, "bound": "hbm", "peak": HBM_PEAK_GBS}
+        rate = {"value": it * bytes_it / (pi_ms * 1e-3) / 1e9, "unit": "GB/s",
+                "bytes_per_update": bytes_it}
+        yv = torch.empty(w.n, dtype=torch.float64, device=dev)
+        kms = _events(torch, stream, lambda: g.gpic_matvec_dense(W, v, yv, n=w.n), 20)
+        alg = bytes_it + 16.0 * w.n
+        roof = {"bound": "hbm", "kernel": "gemv_kernel", "achieved": alg / (kms * 1e-3) / 1e9,
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None, "avg_launch_ms": kms,
+                "bytes_per_launch": alg}
     rate["value"] = round(rate["value"], 3)
-    # fused: the fraction of the fp16 matrix-core peak the executed part
-    # products reach; otherwise the rate against its own peak
-    frac = rate.pop("frac_override", rate["value"] / rate["peak"])
-    rate["frac"] = round(frac, 4)
-    line = {"metric": f"{w.name}: power-iteration rate ({w.path} operator); "
-                      f"end-to-end PIC seconds",
-            "value": rate["value"], "unit": rate["unit"], "n_gpus": 1,
-            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
-            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": "f64", "data": "synthetic",
-            "config": {"workload": w.name, "n": w.n, "d": w.d, "path": w.path,
-                       "mode": w.mode, "T_or_cap": T, "k": w.k, **extra},
-            "iterations": it, "converged": out.pi.converged,
-            "pi_ms": round(pi_ms, 4), "ms_per_update": round(pi_ms / max(it, 1), 5),
-            "rate": rate}
+    roof["achieved"] = round(roof["achieved"], 3)
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["avg_launch_ms"] = round(roof["avg_launch_ms"], 5)
+    res = {"config": info, "steps": steps, "warmup": warmup,
+           "e2e_ms": round(1e3 * float(np.median(times)), 4), "e2e_statistic": "median",
+           "iterations": it, "converged": out.pi.converged, "pi_ms": round(pi_ms, 4),
+           "ms_per_update": round(pi_ms / max(it, 1), 5), "rate": rate, "roofline": roof}
     paper = PAPER_GPIC_S.get((w.name, w.n))
     if paper is not None:
         # the paper's own GPIC time for this shape (another machine: context)
-        line["paper_context"] = {"gpic_s": paper, "hardware": "Tesla K40m",
-                                 "source": "Table 2", "e2e_s_here": round(ms / 1e3, 5)}
+        res["paper_context"] = {"gpic_s": paper, "hardware": "Tesla K40m",
+                                "source": "Table 2", "e2e_s_here": round(res["e2e_ms"] / 1e3, 5)}
+    if cpu:
+        host_graph = None
+        if graph is not None:
+            host_graph = tuple(t.cpu().numpy() for t in graph)
+        log(f"bench: oracle baseline for {w.name} ...")
+        res["cpu_baseline"] = oracle_baseline(w, host_graph)
+    return res
+
+
+def make_workload(name, n=None):
+    import workloads
+    if name in ("knn8d", "knn8d_random"):
+        return knn8d_points(n)
+    return workloads.make(name, n=n)
+
+
+def other_workload(args):
+    """One non-headline workload as a JSON line of its own."""
+    import torch
+    import paper_1604_02700_amd as g
+
+    w = make_workload(args.workload, args.wn)
+    log(f"bench: workload {args.workload} n={w.n} d={w.d} path={w.path} mode={w.mode}")
+    r = measure_path(g, torch, w, args.steps, args.warmup, cpu=not args.no_cpu_baseline,
+                     graph_numbering="random" if args.workload == "knn8d_random" else "local")
+    line = {"metric": f"{args.workload}: power-iteration rate ({w.path} operator); "
+                      f"end-to-end PIC seconds",
+            "value": r["rate"]["value"], "unit": r["rate"]["unit"], "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": r["e2e_ms"],
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": DTYPE, "data": "synthetic", **r}
     print(json.dumps(line), flush=True)
 
 
