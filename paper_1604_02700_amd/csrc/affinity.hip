@@ -554,40 +554,79 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
                 // column 16 q + 4 g + r over the wave's 16 RB rows: reduce-
                 // scatter over the 16 lanes of a lane group (m = 8, 4), then
                 // add the 4 lanes that share the column (m = 2, 1); lane m
-                // ends with r = 2 b3 + b2 (b = the bits of m)
+                // ends with r = 2 b3 + b2 (b = the bits of m).  The lane
+                // exchanges are data-parallel moves (a row rotation for
+                // m = 8, a swizzle for m = 4, quad permutations for m = 2,
+                // 1) on the two halves of the float64, not LDS permutes.
+                auto xch = [&](double x, int kind) {
+                    const long long b = __double_as_longlong(x);
+                    int lo = (int)(b & 0xffffffffll), hi = (int)(b >> 32);
+                    if (kind == 8) {
+                        lo = __builtin_amdgcn_mov_dpp(lo, 0x128, 0xf, 0xf, false);
+                        hi = __builtin_amdgcn_mov_dpp(hi, 0x128, 0xf, 0xf, false);
+                    } else if (kind == 4) {
+                        lo = __builtin_amdgcn_ds_swizzle(lo, 0x101f);
+                        hi = __builtin_amdgcn_ds_swizzle(hi, 0x101f);
+                    } else if (kind == 2) {
+                        lo = __builtin_amdgcn_mov_dpp(lo, 0x4e, 0xf, 0xf, false);
+                        hi = __builtin_amdgcn_mov_dpp(hi, 0x4e, 0xf, 0xf, false);
+                    } else {
+                        lo = __builtin_amdgcn_mov_dpp(lo, 0xb1, 0xf, 0xf, false);
+                        hi = __builtin_amdgcn_mov_dpp(hi, 0xb1, 0xf, 0xf, false);
+                    }
+                    return __longlong_as_double(((long long)(unsigned)hi << 32) |
+                                                (long long)(unsigned)lo);
+                };
                 {
                     const bool up = (m & 8) != 0;
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
                         const double send = up ? cq[h] : cq[h + 2];
                         const double keep = up ? cq[h + 2] : cq[h];
-                        cq[h] = keep + __shfl_xor(send, 8, kWave);
+                        cq[h] = keep + xch(send, 8);
                     }
                 }
                 {
                     const bool up = (m & 4) != 0;
                     const double send = up ? cq[0] : cq[1];
                     const double keep = up ? cq[1] : cq[0];
-                    cq[0] = keep + __shfl_xor(send, 4, kWave);
+                    cq[0] = keep + xch(send, 4);
                 }
-                cq[0] += __shfl_xor(cq[0], 2, kWave);
-                cq[0] += __shfl_xor(cq[0], 1, kWave);
-                if ((m & 3) == 0)
-                    cred[buf][wave][16 * q + 4 * g + 2 * ((m >> 3) & 1) + ((m >> 2) & 1)] =
-                        cq[0];
+                cq[0] += xch(cq[0], 2);
+                cq[0] += xch(cq[0], 1);
+                // the four lanes of a column hold the same sum (float
+                // addition commutes): all write it, so no branch splits the
+                // tile's code and the scheduler can interleave across blocks
+                cred[buf][wave][16 * q + 4 * g + 2 * ((m >> 3) & 1) + ((m >> 2) & 1)] = cq[0];
             }
         };
         floatx4 ca[RB], cb[RB];
+        // interleave each chain's matrix-core products with the previous
+        // block's epilogue so that the vector ALU and the matrix cores work
+        // at the same time within a wave
+        auto interleave = [&]() {
+            if constexpr (kApplyAny) {
+#pragma unroll
+                for (int t = 0; t < 3 * NCH * RB; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+                }
+            }
+        };
         chain(0, ca);
 #pragma unroll
         for (int q = 0; q < kQ; q += 2) {
             if (q + 1 < kQ)
                 chain(q + 1, cb);
             epi(q, ca);
+            if (q + 1 < kQ)
+                interleave();
             if (q + 2 < kQ)
                 chain(q + 2, ca);
             if (q + 1 < kQ)
                 epi(q + 1, cb);
+            if (q + 2 < kQ)
+                interleave();
         }
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
