@@ -697,11 +697,11 @@ def measure_path(g, torch, w, steps, warmup, cpu=True, graph_numbering="local"):
         pi_ms = e0.elapsed_time(e1)
         # algorithmic: the operator's 2 n^2 d flop per sweep (every ordered
         # pair), whatever the kernel evaluates; executed: up to 2^19 points
-        # each pair once in row groups of 256 (group R covers the columns
+        # each pair once in row groups of G (group R covers the columns
         # from its own first row on), three fp16 part products per
         # coordinate, coordinates padded to 32-coordinate chunks
         flops = 2.0 * w.n * w.n * w.d
-        G = 256
+        G = 384 if w.d <= 64 else 256                 # rows per group of the symmetric product
         if w.n <= (1 << 19):
             groups = (w.n + G - 1) // G
             pairs = float(sum(G * (w.n - G * r) for r in range(groups)))

@@ -343,7 +343,7 @@ __global__ __launch_bounds__(kThreads) void fused_sym_reduce_kernel(
 // When A or W is written (W = 4, RB = 1), the wave's 16 x TC tile goes
 // through LDS and is stored as 4 rows x 4 TC contiguous bytes per store.
 constexpr int kChunkRows = 128;               // nominal rows per workgroup (chunking)
-constexpr int kColAlign = 64;                 // chunk and padding granularity
+constexpr int kColAlign = 128;                // chunk and padding granularity (the widest tile)
 
 template <int NCH, int RB, int TC, int MODE, int W>
 __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
@@ -427,8 +427,9 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
     }
 
-    // staging: piece f = slot * TC + col (tiles start at multiples of 64
-    // and end at or before np, so every load is in bounds)
+    // staging: piece f = slot * TC + col (tiles start at multiples of TC,
+    // chunks and row groups at multiples of kColAlign, and np is one too,
+    // so every tile ends at or before np and every load is in bounds)
     constexpr int kPieces = kSlots * TC;
     constexpr int kPer = (kPieces + NT - 1) / NT;
     half8 stage[kPer];
@@ -596,37 +597,21 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
                 cq[0] += xch(cq[0], 1);
                 // the four lanes of a column hold the same sum (float
                 // addition commutes): all write it, so no branch splits the
-                // tile's code and the scheduler can interleave across blocks
+                // tile's code into blocks the scheduler cannot cross
                 cred[buf][wave][16 * q + 4 * g + 2 * ((m >> 3) & 1) + ((m >> 2) & 1)] = cq[0];
             }
         };
         floatx4 ca[RB], cb[RB];
-        // interleave each chain's matrix-core products with the previous
-        // block's epilogue so that the vector ALU and the matrix cores work
-        // at the same time within a wave
-        auto interleave = [&]() {
-            if constexpr (kApplyAny) {
-#pragma unroll
-                for (int t = 0; t < 3 * NCH * RB; ++t) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
-                }
-            }
-        };
         chain(0, ca);
 #pragma unroll
         for (int q = 0; q < kQ; q += 2) {
             if (q + 1 < kQ)
                 chain(q + 1, cb);
             epi(q, ca);
-            if (q + 1 < kQ)
-                interleave();
             if (q + 2 < kQ)
                 chain(q + 2, ca);
             if (q + 1 < kQ)
                 epi(q + 1, cb);
-            if (q + 2 < kQ)
-                interleave();
         }
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
@@ -922,20 +907,33 @@ int nch_for(int d) { return (d + 31) / 32; }
 // and four independent matrix-core chains per wave hide each other's
 // latency; measured 14.9 ms per product at n = 200,000, d = 64, against
 // 16.4 with 128 rows); the symmetric product, which also keeps column sums
-// and v of its rows, takes two blocks per wave (256 rows) to stay within
-// 256 registers; the sweeps that write A or W take one block per wave and
-// 4 waves (their bound is the stores).
+// and v of its rows, takes three blocks per wave (384 rows) with 128-column
+// tiles up to 64 coordinates (n = 200,000, d = 64: 9.1 ms per product
+// against 10.6 with two blocks and 64-column tiles; four blocks spill) and
+// two blocks with 32-column tiles above (three spill there); the sweeps
+// that write A or W take one block per wave and 4 waves (their bound is
+// the stores).
 constexpr bool sums_rows(int mode)
 {
     return mode == kApply || mode == kDegree || mode == kApplySym;
 }
-constexpr int rb_for(int mode) { return mode == kApplySym ? 2 : (sums_rows(mode) ? 4 : 1); }
-constexpr int waves_for(int mode) { return sums_rows(mode) ? 8 : 4; }
-constexpr int64_t rows_per_group(int mode) { return 16 * rb_for(mode) * waves_for(mode); }
-
-int64_t row_groups(int64_t n, int mode)
+constexpr int rb_for(int mode, int nch)
 {
-    return (n + rows_per_group(mode) - 1) / rows_per_group(mode);
+    return mode == kApplySym ? (nch <= 2 ? 3 : 2) : (sums_rows(mode) ? 4 : 1);
+}
+constexpr int waves_for(int mode) { return sums_rows(mode) ? 8 : 4; }
+constexpr int tc_for(int mode, int nch)
+{
+    return (mode == kApplySym && nch <= 2) ? 128 : (nch <= 2 ? 64 : 32);
+}
+constexpr int64_t rows_per_group(int mode, int nch)
+{
+    return 16 * rb_for(mode, nch) * waves_for(mode);
+}
+
+int64_t row_groups(int64_t n, int mode, int nch)
+{
+    return (n + rows_per_group(mode, nch) - 1) / rows_per_group(mode, nch);
 }
 
 // Column chunks: enough workgroups to fill the chip when rows are few.
@@ -962,14 +960,22 @@ int64_t padded_points(int64_t n) { return (n + kColAlign - 1) / kColAlign * kCol
 // partial sums take about n^2 / 64 bytes (4.3 GB at the limit).  Above it
 // the product sums whole rows.
 constexpr int64_t kFusedSymMaxN = 1 << 19;
-constexpr int64_t kSymGroupRows = rows_per_group(kApplySym);
 
 bool fused_sym(int64_t n, int d) { return use_mfma(d) && n <= kFusedSymMaxN; }
 
+// Column partial sums of the symmetric product for row groups of G rows:
+// the smaller G (256 rows, above 64 coordinates) needs the most entries,
+// so the workspace is sized for it whatever d the product gets.
+int64_t colpart_entries_for(int64_t n, int64_t G)
+{
+    const int64_t groups = (n + G - 1) / G;
+    return colpart_offset(groups - 1, n, G);
+}
 int64_t colpart_entries(int64_t n)
 {
-    const int64_t groups = (n + kSymGroupRows - 1) / kSymGroupRows;
-    return colpart_offset(groups - 1, n, kSymGroupRows);
+    const int64_t a = colpart_entries_for(n, rows_per_group(kApplySym, 1));
+    const int64_t b = colpart_entries_for(n, rows_per_group(kApplySym, kMaxNch));
+    return a > b ? a : b;
 }
 
 // Column chunks of the symmetric product: kMaxChunks chunks, so that the
@@ -1032,10 +1038,11 @@ void launch_engine(const Ws &w, int64_t n, int64_t chunk_cols, int nchunks, floa
                    double *part, double *partial, StopCtl ctl, int use_ctl, hipStream_t s,
                    double *colpart = nullptr)
 {
-    constexpr int RB = rb_for(MODE);
+    constexpr int RB = rb_for(MODE, NCH);
     constexpr int W = waves_for(MODE);
-    constexpr int TC = (NCH <= 2) ? 64 : 32;
-    const dim3 grid((unsigned)row_groups(n, MODE), (unsigned)nchunks);
+    constexpr int TC = tc_for(MODE, NCH);
+    static_assert(kColAlign % TC == 0, "tiles start and end on the padding grain");
+    const dim3 grid((unsigned)row_groups(n, MODE, NCH), (unsigned)nchunks);
     hipLaunchKernelGGL((affinity_mfma_kernel<NCH, RB, TC, MODE, W>), grid, dim3(W * 64), 0,
                        s, w.xh, padded_points(n), w.cn, w.gam, w.sc, w.mr, n, chunk_cols, A,
                        lda, v, degree_in, out, part, colpart, partial, ctl, use_ctl);
@@ -1180,7 +1187,7 @@ int64_t fused_blocks(int64_t n, int d)
     chunking(n, &chunk_cols, &nchunks);
     if (nchunks > 1)
         return (n + kThreads - 1) / kThreads;        // chunk_reduce workgroups
-    return row_groups(n, kApply);                    // tile workgroups
+    return row_groups(n, kApply, nch_for(d));        // tile workgroups
 }
 
 hipError_t launch_affinity(const float *X, int64_t n, int d, float c, float *A,
@@ -1254,9 +1261,10 @@ hipError_t launch_fused_apply(const float *X, int64_t n, int d, float c,
     default: GPIC_MFMA(4); break;
     }
 #undef GPIC_MFMA
+    const int64_t G = rows_per_group(kApplySym, nch_for(d));
     hipLaunchKernelGGL(fused_sym_reduce_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, s, w.part, nchunks, chunk_cols, colpart, n,
-                       kSymGroupRows, degree, y, partial, ctl, uc);
+                       dim3(kThreads), 0, s, w.part, nchunks, chunk_cols, colpart, n, G, degree,
+                       y, partial, ctl, uc);
     return hipGetLastError();
 }
 

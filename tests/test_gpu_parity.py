@@ -440,12 +440,14 @@ def test_fused_parity(g, orc, n, d):
 
 
 @pytest.mark.parametrize("n,d", [(255, 16), (256, 20), (257, 64), (513, 100),
-                                 (2050, 33), (4099, 16)])
+                                 (2050, 33), (4099, 16), (383, 16), (385, 64),
+                                 (769, 33), (1025, 128)])
 def test_fused_symmetric_edges(g, orc, n, d):
-    """The fused operator evaluates each pair once (256-point row groups:
-    row sums for the group, column sums for later groups): sizes around the
-    group and chunk edges, every coordinate-chunk count (d = 16, 20, 33,
-    64, 100), one product against the oracle's on-the-fly rows."""
+    """The fused operator evaluates each pair once (row groups of 384
+    points up to 64 coordinates, 256 above: row sums for the group, column
+    sums for later groups; 128- or 32-column tiles): sizes around the group,
+    tile and chunk edges, every coordinate-chunk count (d = 16, 20, 33, 64,
+    100, 128), one product against the oracle's on-the-fly rows."""
     X = _pts(n, d, 50 + d, scale=1.2)
     sigma = np.float32(np.sqrt(d))
     deg, v0, nz = g.gpic_degree_fused(_t(X), sigma)
