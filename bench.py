@@ -778,6 +778,20 @@ def other_workload(args):
 
     w = make_workload(args.workload, args.wn)
     log(f"bench: workload {args.workload} n={w.n} d={w.d} path={w.path} mode={w.mode}")
+    copy_ref = None
+    if args.copy_ref_gib > 0:
+        # a plain copy of known size in the same process: the reference
+        # that scales the HBM traffic counters of a profiling run
+        dev = torch.device("cuda:0")
+        m = int(args.copy_ref_gib * (1 << 30)) // 4
+        src = torch.ones(m, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        copy_ref = {"bytes_read": 4 * m, "bytes_written": 4 * m, "copies": 3}
+        del src, dst
+        torch.cuda.empty_cache()
     r = measure_path(g, torch, w, args.steps, args.warmup, cpu=not args.no_cpu_baseline,
                      graph_numbering="random" if args.workload == "knn8d_random" else "local")
     line = {"metric": f"{args.workload}: power-iteration rate ({w.path} operator); "
@@ -786,6 +800,8 @@ def other_workload(args):
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": r["e2e_ms"],
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": DTYPE, "data": "synthetic", **r}
+    if copy_ref is not None:
+        line["copy_reference"] = copy_ref
     print(json.dumps(line), flush=True)
 
 
