@@ -43,8 +43,9 @@
 //            sym.hip); only column tiles at or right of the row's block are
 //            computed, and the storage's tile count nb comes in place of lda.
 //   kApplySym: the fused product with each pair evaluated once (A = A^T):
-//            a workgroup's 256 rows take the columns from their own first
-//            row on; the row sums go to its rows, and for columns past its
+//            a workgroup's rows (384 up to 64 coordinates, 256 above) take
+//            the columns from their own first row on; the row sums go to its
+//            rows, and for columns past its
 //            rows A_ij v_i also goes to column sums that a second kernel
 //            adds to the later rows (fused_sym_reduce_kernel).  With v = 1
 //            and no division it is the degree sweep of that same A.
