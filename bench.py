@@ -46,9 +46,36 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def code_text(text: str) -> str:
+    """C++ source with its comments removed and every run of whitespace
+    made one space: what the compiler sees, so that an edit of a comment
+    does not disown counter figures taken on the same kernel."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            out.append(" ")
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash(source: str = "gemv.hip") -> str:
-    with open(os.path.join(ROOT, "paper_1604_02700_amd", "csrc", source), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of a kernel source's code (comments and layout excluded)."""
+    with open(os.path.join(ROOT, "paper_1604_02700_amd", "csrc", source)) as f:
+        return hashlib.sha256(code_text(f.read()).encode()).hexdigest()[:16]
 
 
 def measured_traffic(path: str = TRAFFIC_FILE, source: str = "gemv.hip",
