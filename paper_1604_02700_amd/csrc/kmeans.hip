@@ -251,20 +251,22 @@ constexpr int kFLarge = 8;
 constexpr int64_t kFLargeFrom = (int64_t)1 << 18;
 constexpr int kMaxLevels = 16;
 constexpr int kShortScan = 64;        // longer ranges go to the work queue
-// candidates per queued part and samples evaluated per pass over it: F = 8
-// (large n) shares each candidate read among all 8 samples; F = 64 (small
-// n) keeps more, smaller work items, since the grid would otherwise be
-// thin at the first levels (measured: n = 50,000, k = 10: 0.98 ms against
-// 1.35 ms with the F = 8 setting)
+// candidates per queued part and samples evaluated per pass over it: two
+// samples per wave keep four times as many waves in flight as one wave
+// for all eight, which the long, few parts of the first levels need
+// (measured, n = 2M, k = 50: groups of 8, 4, 2, 1 samples: 22.5, 20.4,
+// 19.8, 22.2 ms; parts of 512 or 2,048 candidates: slower); for F = 64
+// (n = 50,000, k = 10: 0.98 ms against 1.35 ms with the F = 8 setting of
+// that time)
 template <int F> constexpr int chunk_for() { return F == kFLarge ? 1024 : 512; }
-template <int F> constexpr int group_for() { return F == kFLarge ? 8 : 2; }
+template <int F> constexpr int group_for() { return 2; }
 constexpr int kMinChunk = 512;
 
 // Sample f of interval [lo, hi] (m = hi - lo + 1 rows): every row if m <= F,
 // else lo + (f + 1)(m + 1) / (F + 1) - 1 (evaluated as (f + 1) a +
 // (f + 1) b / (F + 1) with m + 1 = (F + 1) a + b); -1 if there is none.
 template <int F>
-__device__ __forceinline__ int32_t sample_row(int32_t lo, int32_t hi, int f)
+__host__ __device__ __forceinline__ int32_t sample_row(int32_t lo, int32_t hi, int f)
 {
     const uint32_t m = (uint32_t)(hi - lo + 1);
     if (m <= (uint32_t)F)
@@ -272,33 +274,6 @@ __device__ __forceinline__ int32_t sample_row(int32_t lo, int32_t hi, int f)
     const uint32_t a = (m + 1) / (F + 1), b = (m + 1) % (F + 1);
     const uint32_t f1 = (uint32_t)(f + 1);
     return lo + (int32_t)(f1 * a + (f1 * b) / (F + 1)) - 1;
-}
-
-// Interval of node q at level L (digits of q in base F + 1, most significant
-// first, choose the gap between samples); false if the node does not exist.
-template <int F>
-__device__ __forceinline__ bool fary_node(int32_t n, int L, uint32_t q, int32_t &lo,
-                                          int32_t &hi)
-{
-    int dig[kMaxLevels];
-    for (int l = 0; l < L; ++l) {
-        dig[l] = (int)(q % (F + 1));
-        q /= (F + 1);
-    }
-    lo = 0;
-    hi = n - 1;
-    for (int l = L - 1; l >= 0; --l) {
-        if (hi - lo + 1 <= F)
-            return false;                     // a leaf interval has no gaps
-        const int c = dig[l];
-        const int32_t nlo = (c == 0) ? lo : sample_row<F>(lo, hi, c - 1) + 1;
-        const int32_t nhi = (c == F) ? hi : sample_row<F>(lo, hi, c) - 1;
-        lo = nlo;
-        hi = nhi;
-        if (lo > hi)
-            return false;
-    }
-    return true;
 }
 
 // Leftmost-argmin merge of (value, index) pairs.
@@ -378,41 +353,197 @@ struct LevelQueue {
     int64_t cap;
 };
 
-// One recursion level: a thread per (node, sample); the F threads of a
-// node sit in one wave (F divides 64).  Sample 0 of a node whose range is
-// long reserves the node's parts (the order of appends does not matter:
-// every row's minimum is order-independent); otherwise, or when the queue
-// is full, every sample thread scans its own row.  Item 0 clears the other
-// pair of counters, whose level has finished.
+// Number of samples of interval [lo, hi] (m > F rows) at or before row r:
+// sample f sits at lo - 1 + floor((f + 1)(m + 1) / (F + 1)), so the count
+// is the largest c <= F with floor(c (m + 1) / (F + 1)) <= r - lo + 1;
+// a float64 estimate is corrected against the exact sample rows.
 template <int F>
-__global__ __launch_bounds__(kThreads) void fary_level_kernel(
+__device__ __forceinline__ int samples_upto(int32_t lo, int32_t hi, int32_t r)
+{
+    const double x = (double)(r - lo + 1), m1 = (double)(hi - lo + 2);
+    int c = (int)((x + 1.0) * (double)(F + 1) / m1) - 1;
+    c = c < 0 ? 0 : (c > F ? F : c);
+    while (c < F && sample_row<F>(lo, hi, c) <= r)
+        ++c;
+    while (c > 0 && sample_row<F>(lo, hi, c - 1) > r)
+        --c;
+    return c;
+}
+
+// The recursion's shape does not depend on the values: which rows are the
+// samples of which level, and the interval each belongs to, follow from n
+// and F alone.  It is laid out once per call as one list per level of
+// (row, interval, last sample row of the interval, first-sample flag) in
+// ascending row order, so each layer's level kernels read a row's interval
+// instead of deriving it.
+struct RowEntry {
+    int32_t r, lo, hi, rl;               // rl: last sample row; bit 31: first sample
+};
+constexpr int32_t kFirstSample = (int32_t)0x80000000;
+
+// A thread per row: the level at which the row is a sample and its entry
+// (the row descends the recursion, gap by gap, until it is a sample), and
+// its rank among the rows of its block at that level.
+template <int F>
+__global__ __launch_bounds__(kThreads) void row_level_kernel(
+    int32_t n, int levels, RowEntry *__restrict__ ent, int32_t *__restrict__ lr,
+    int32_t *__restrict__ bh)
+{
+    __shared__ int32_t wl[kThreads / kWave][kMaxLevels];
+    const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int32_t r = (int32_t)(item < n ? item : -1);
+    int lev = -1;
+    RowEntry e{r, 0, n - 1, 0};
+    if (r >= 0) {
+        int32_t lo = 0, hi = n - 1;
+        for (int l = 0; l < levels; ++l) {
+            if (hi - lo + 1 <= F) {
+                lev = l;                                     // every row a sample
+                e = RowEntry{r, lo, hi, hi | (r == lo ? kFirstSample : 0)};
+                break;
+            }
+            const int c = samples_upto<F>(lo, hi, r);
+            if (c > 0 && sample_row<F>(lo, hi, c - 1) == r) {
+                lev = l;
+                const int32_t rl = sample_row<F>(lo, hi, F - 1);
+                e = RowEntry{r, lo, hi, rl | (c == 1 ? kFirstSample : 0)};
+                break;
+            }
+            const int32_t nlo = (c == 0) ? lo : sample_row<F>(lo, hi, c - 1) + 1;
+            const int32_t nhi = (c == F) ? hi : sample_row<F>(lo, hi, c) - 1;
+            lo = nlo;
+            hi = nhi;
+        }
+    }
+    // rank within the block among rows of the same level (ballots per level)
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+    int rank = 0;
+    for (int l = 0; l < levels; ++l) {
+        const unsigned long long m = __ballot(lev == l);
+        if (lev == l)
+            rank = __popcll(m & below);
+        if (lane == 0)
+            wl[w][l] = __popcll(m);
+    }
+    __syncthreads();
+    if (lev >= 0) {
+        for (int u = 0; u < w; ++u)
+            rank += wl[u][lev];
+        ent[r] = e;
+        lr[r] = (lev << 24) | rank;                          // rank < 256
+    } else if (r >= 0) {
+        lr[r] = -1;                                          // not reached for n <= 2^30
+    }
+    if (threadIdx.x < levels) {
+        int32_t t = 0;
+        for (int u = 0; u < kThreads / kWave; ++u)
+            t += wl[u][threadIdx.x];
+        bh[(int64_t)blockIdx.x * kMaxLevels + threadIdx.x] = t;
+    }
+}
+
+// One workgroup: per level, exclusive scan of the block counts, plus the
+// level's base (the levels' lists are stored one after another); base[l]
+// for l <= levels.
+__global__ __launch_bounds__(1024) void level_scan_kernel(
+    int32_t *__restrict__ bh, int64_t nb, int levels, int32_t *__restrict__ base)
+{
+    __shared__ int32_t ts[1024];
+    __shared__ int32_t tot[kMaxLevels + 1];
+    const int64_t per = (nb + 1023) / 1024;
+    const int64_t b0 = (int64_t)threadIdx.x * per;
+    for (int l = 0; l < levels; ++l) {
+        int32_t t = 0;
+        for (int64_t b = b0; b < b0 + per && b < nb; ++b)
+            t += bh[b * kMaxLevels + l];
+        ts[threadIdx.x] = t;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int32_t run = 0;
+            for (int u = 0; u < 1024; ++u) {
+                const int32_t x = ts[u];
+                ts[u] = run;
+                run += x;
+            }
+            tot[l] = run;
+        }
+        __syncthreads();
+        int32_t run = ts[threadIdx.x];
+        for (int64_t b = b0; b < b0 + per && b < nb; ++b) {
+            const int32_t x = bh[b * kMaxLevels + l];
+            bh[b * kMaxLevels + l] = run;
+            run += x;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        int32_t run = 0;
+        for (int l = 0; l < levels; ++l) {
+            base[l] = run;
+            run += tot[l];
+        }
+        base[levels] = run;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void level_scatter_kernel(
+    int32_t n, const RowEntry *__restrict__ ent, const int32_t *__restrict__ lr,
+    const int32_t *__restrict__ bh, const int32_t *__restrict__ base,
+    RowEntry *__restrict__ list)
+{
+    const int64_t r = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (r >= n)
+        return;
+    const int32_t x = lr[r];
+    if (x < 0)
+        return;
+    const int l = x >> 24;
+    const int64_t pos = (int64_t)base[l] + bh[(int64_t)blockIdx.x * kMaxLevels + l] +
+                        (x & 0xffffff);
+    if (pos < n)
+        list[pos] = ent[r];
+}
+
+// One level of a layer, a thread per sample row of the level (in row
+// order).  A node whose range is at most kShortScan long has each sample
+// scan its own row; a longer one is queued by its first sample, and its
+// other samples leave it to the queue; if the queue has no room the first
+// sample scans every sample row of the node itself.  Item 0 clears the
+// other pair of counters, whose level has finished.
+template <int F>
+__global__ __launch_bounds__(kThreads) void fary_rows_kernel(
     const double *__restrict__ S1, const double *__restrict__ S2,
     const int32_t *__restrict__ run, const double *__restrict__ Dprev,
-    double *__restrict__ Dcur, int32_t *__restrict__ opt, int32_t n, int L,
-    int64_t items, LevelQueue Q, int g)
+    double *__restrict__ Dcur, int32_t *__restrict__ opt, int32_t n,
+    const RowEntry *__restrict__ list, const int32_t *__restrict__ base, int L,
+    LevelQueue Q, int g)
 {
-    static_assert(kWave % F == 0, "a node's samples share a wave");
     const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (item == 0) {
         Q.qlen[(g + 1) & 1] = 0ull;
         Q.qlen[2 + ((g + 1) & 1)] = 0ull;
     }
-    const int f = (int)(item % F);
-    int32_t lo = 0, hi = -1, r = -1, alo = 1, ohi = 0;
-    bool has = item < items && fary_node<F>(n, L, (uint32_t)(item / F), lo, hi);
+    const int64_t b0 = base[L];
+    const int64_t cnt = ((int64_t)base[L + 1] < n ? (int64_t)base[L + 1] : n) - b0;
+    const bool has = item < cnt;
+    int32_t r = -1, lo = 0, hi = -1, rl = 0, alo = 1, ohi = 0;
+    bool first = false;
     int64_t len = 0;
     if (has) {
-        r = sample_row<F>(lo, hi, f);
+        const RowEntry e = list[b0 + item];
+        r = e.r;
+        lo = e.lo;
+        hi = e.hi;
+        first = (e.rl & kFirstSample) != 0;
+        rl = e.rl & ~kFirstSample;
         interval_bounds(opt, n, lo, hi, alo, ohi);
-        const int32_t rlast = (hi - lo + 1 <= F) ? hi : sample_row<F>(lo, hi, F - 1);
-        len = (int64_t)(ohi < rlast ? ohi : rlast) - alo + 1;
+        len = (int64_t)(ohi < rl ? ohi : rl) - alo + 1;
     }
-    // the node's leader (sample 0) reserves its parts
-    const int lane = threadIdx.x % kWave;
-    const int leader = lane - f;
+    const bool lead = has && first && len > kShortScan;
     int64_t e0 = 0, C = 0;
     int ok = 0;
-    if (has && f == 0 && len > kShortScan) {
+    if (lead) {
         C = (len + chunk_for<F>() - 1) / chunk_for<F>();
         e0 = (int64_t)atomicAdd(&Q.qlen[g & 1], (unsigned long long)C);
         ok = e0 + C <= Q.cap;
@@ -424,12 +555,12 @@ __global__ __launch_bounds__(kThreads) void fary_level_kernel(
             }
         } else {
             // no room left (only if split points were far from monotone):
-            // void the reserved slots below the capacity; the samples scan
+            // void the reserved slots below the capacity
             for (int64_t e = e0; e < e0 + C && e < Q.cap; ++e)
                 Q.part[e] = QueuePart{-1, 0, 0, -1, 0, 0, 0, 0};
         }
     }
-    const bool queued = __shfl(ok, leader, kWave) != 0;
+    const int lane = threadIdx.x % kWave;
     const int32_t aend = alo + (int32_t)len - 1;    // end of the longest sample range
     if (ok && C <= kWave) {
         for (int64_t p = 0; p < C; ++p) {
@@ -453,12 +584,23 @@ __global__ __launch_bounds__(kThreads) void fary_level_kernel(
             Q.part[qe0 + p] = QueuePart{qlo, qhi, plo, phi, qalo, qohi, (int32_t)qe0, 0};
         }
     }
-    if (r < 0 || queued)
+    if (!has)
         return;
-    double best = INFINITY;
-    int64_t arg = INT64_MAX;
-    scan_range(S1, S2, run, Dprev, r, alo, ohi < r ? ohi : r, 1, best, arg);
-    store_result(Dcur, opt, r, best, arg, alo);
+    if (len <= kShortScan) {
+        double best = INFINITY;
+        int64_t arg = INT64_MAX;
+        scan_range(S1, S2, run, Dprev, r, alo, ohi < r ? ohi : r, 1, best, arg);
+        store_result(Dcur, opt, r, best, arg, alo);
+    } else if (lead && !ok) {
+        const int ns = (hi - lo + 1 < F) ? hi - lo + 1 : F;
+        for (int f = 0; f < ns; ++f) {
+            const int32_t q = sample_row<F>(lo, hi, f);
+            double best = INFINITY;
+            int64_t arg = INT64_MAX;
+            scan_range(S1, S2, run, Dprev, q, alo, ohi < q ? ohi : q, 1, best, arg);
+            store_result(Dcur, opt, q, best, arg, alo);
+        }
+    }
 }
 
 // The level's queued parts: a wave per (part, group of kGroup samples);
@@ -630,9 +772,12 @@ __global__ __launch_bounds__(kThreads) void labels_kernel(
 
 inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
+unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
+
 struct KmLayout {
     size_t keyA, keyB, idxA, idxB, hist, hsum, sv, run, t1, t2, S1, S2, Da, Db, opt,
-        qpart, qnparts, qheads, qbest, qarg, qlen, sc, first, costs, total;
+        qpart, qnparts, qheads, qbest, qarg, qlen, sc, first, costs, ent, lr, bh, lbase,
+        list, total;
 };
 
 // Queue slots per level.  With monotone split points the interval ranges
@@ -678,11 +823,14 @@ KmLayout layout(int64_t n, int32_t k)
     L.sc = take(sizeof(KmScalars));
     L.first = take((size_t)(k + 1) * 8);
     L.costs = take((size_t)k * 8);
+    L.ent = take(n * sizeof(RowEntry));
+    L.lr = take(n * 4);
+    L.bh = take((size_t)blocks_for(n) * kMaxLevels * 4);
+    L.lbase = take((kMaxLevels + 1) * 4);
+    L.list = take(n * sizeof(RowEntry));
     L.total = o;
     return L;
 }
-
-unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
 } // namespace
 
@@ -757,30 +905,99 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     if (levels > kMaxLevels)
         return hipErrorInvalidValue;               // not reachable for n <= 2^30
     double *Dprev = Da, *Dcur = Db;
-    int g = 0;                                     // levels run so far
-    for (int c = 1; c < ke; ++c) {
-        int32_t *oc = opt + (int64_t)c * n;
-        int64_t nodes = 1;
-        for (int Lv = 0; Lv < levels; ++Lv, nodes *= (F + 1), ++g) {
-            const int64_t items = nodes * F;
-            const dim3 grid((unsigned)((items + kThreads - 1) / kThreads));
-            if (F == kFSmall) {
-                hipLaunchKernelGGL(fary_level_kernel<kFSmall>, grid, dim3(kThreads), 0, s,
-                                   S1, S2, run, Dprev, Dcur, oc, (int32_t)n, Lv, items, Q, g);
-                hipLaunchKernelGGL(fary_queue_kernel<kFSmall>, dim3(2048), dim3(kThreads), 0,
-                                   s, S1, S2, run, Dprev, Dcur, oc, Q, g);
-                hipLaunchKernelGGL(fary_merge_kernel<kFSmall>, dim3(512), dim3(kThreads), 0,
-                                   s, Dcur, oc, Q, g);
-            } else {
-                hipLaunchKernelGGL(fary_level_kernel<kFLarge>, grid, dim3(kThreads), 0, s,
-                                   S1, S2, run, Dprev, Dcur, oc, (int32_t)n, Lv, items, Q, g);
-                hipLaunchKernelGGL(fary_queue_kernel<kFLarge>, dim3(2048), dim3(kThreads), 0,
-                                   s, S1, S2, run, Dprev, Dcur, oc, Q, g);
-                hipLaunchKernelGGL(fary_merge_kernel<kFLarge>, dim3(512), dim3(kThreads), 0,
-                                   s, Dcur, oc, Q, g);
+    if (ke > 1) {
+        // samples per level, from the interval sizes alone (each level's
+        // intervals take at most a few distinct sizes)
+        int64_t count[kMaxLevels] = {};
+        {
+            int64_t sz[64], mult[64];
+            int ns = 1;
+            sz[0] = n;
+            mult[0] = 1;
+            int64_t total = 0;
+            for (int Lv = 0; Lv < levels; ++Lv) {
+                int64_t nsz[64], nmult[64];
+                int nn = 0;
+                auto add = [&](int64_t m, int64_t c) {
+                    if (m <= 0)
+                        return true;
+                    for (int u = 0; u < nn; ++u)
+                        if (nsz[u] == m) {
+                            nmult[u] += c;
+                            return true;
+                        }
+                    if (nn == 64)
+                        return false;
+                    nsz[nn] = m;
+                    nmult[nn++] = c;
+                    return true;
+                };
+                for (int u = 0; u < ns; ++u) {
+                    const int64_t m = sz[u], c = mult[u];
+                    if (m <= F) {
+                        count[Lv] += m * c;
+                        continue;
+                    }
+                    count[Lv] += (int64_t)F * c;
+                    int32_t prev = -1;
+                    for (int f = 0; f <= F; ++f) {
+                        const int32_t sr = (f < F)
+                            ? (F == kFSmall ? sample_row<kFSmall>(0, (int32_t)m - 1, f)
+                                            : sample_row<kFLarge>(0, (int32_t)m - 1, f))
+                            : (int32_t)m;
+                        if (!add(sr - prev - 1, c))
+                            return hipErrorInvalidValue;
+                        prev = sr;
+                    }
+                }
+                total += count[Lv];
+                ns = nn;
+                for (int u = 0; u < nn; ++u) {
+                    sz[u] = nsz[u];
+                    mult[u] = nmult[u];
+                }
             }
+            if (total != n || ns != 0)
+                return hipErrorInvalidValue;       // the recursion does not cover every row
         }
-        double *tmp = Dprev; Dprev = Dcur; Dcur = tmp;
+        RowEntry *ent = (RowEntry *)(w + L.ent), *list = (RowEntry *)(w + L.list);
+        int32_t *lr = (int32_t *)(w + L.lr), *bh = (int32_t *)(w + L.bh);
+        int32_t *lbase = (int32_t *)(w + L.lbase);
+        if (F == kFSmall)
+            hipLaunchKernelGGL(row_level_kernel<kFSmall>, dim3(blocks_for(n)), dim3(kThreads),
+                               0, s, (int32_t)n, levels, ent, lr, bh);
+        else
+            hipLaunchKernelGGL(row_level_kernel<kFLarge>, dim3(blocks_for(n)), dim3(kThreads),
+                               0, s, (int32_t)n, levels, ent, lr, bh);
+        hipLaunchKernelGGL(level_scan_kernel, dim3(1), dim3(1024), 0, s, bh,
+                           (int64_t)blocks_for(n), levels, lbase);
+        hipLaunchKernelGGL(level_scatter_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
+                           (int32_t)n, ent, lr, bh, lbase, list);
+        int g = 0;                                 // levels run so far
+        for (int c = 1; c < ke; ++c) {
+            int32_t *oc = opt + (int64_t)c * n;
+            for (int Lv = 0; Lv < levels; ++Lv, ++g) {
+                const dim3 grid(blocks_for(count[Lv] > 0 ? count[Lv] : 1));
+                if (F == kFSmall) {
+                    hipLaunchKernelGGL(fary_rows_kernel<kFSmall>, grid, dim3(kThreads), 0, s,
+                                       S1, S2, run, Dprev, Dcur, oc, (int32_t)n, list, lbase,
+                                       Lv, Q, g);
+                    hipLaunchKernelGGL(fary_queue_kernel<kFSmall>, dim3(2048), dim3(kThreads),
+                                       0, s, S1, S2, run, Dprev, Dcur, oc, Q, g);
+                    hipLaunchKernelGGL(fary_merge_kernel<kFSmall>, dim3(512), dim3(kThreads),
+                                       0, s, Dcur, oc, Q, g);
+                } else {
+                    hipLaunchKernelGGL(fary_rows_kernel<kFLarge>, grid, dim3(kThreads), 0, s,
+                                       S1, S2, run, Dprev, Dcur, oc, (int32_t)n, list, lbase,
+                                       Lv, Q, g);
+                    hipLaunchKernelGGL(fary_queue_kernel<kFLarge>, dim3(2048), dim3(kThreads),
+                                       0, s, S1, S2, run, Dprev, Dcur, oc, Q, g);
+                    hipLaunchKernelGGL(fary_merge_kernel<kFLarge>, dim3(512), dim3(kThreads),
+                                       0, s, Dcur, oc, Q, g);
+                }
+            }
+            double *tmp = Dprev; Dprev = Dcur; Dcur = tmp;
+        }
     }
     GPIC_TRY(hipGetLastError());
 
