@@ -308,14 +308,52 @@ __device__ __forceinline__ void scan_range(const double *__restrict__ S1,
     }
 }
 
+// The value of lane (lane xor K): data-parallel moves for K = 1, 2, 8
+// (quad permutations, a rotation by 8 within a row of 16), swizzles for
+// K = 4, 16, a permute for K = 32.
+template <int K>
+__device__ __forceinline__ int lane_xor(int x)
+{
+    if (K == 1)
+        return __builtin_amdgcn_mov_dpp(x, 0xb1, 0xf, 0xf, false);
+    if (K == 2)
+        return __builtin_amdgcn_mov_dpp(x, 0x4e, 0xf, 0xf, false);
+    if (K == 4)
+        return __builtin_amdgcn_ds_swizzle(x, 0x101f);
+    if (K == 8)
+        return __builtin_amdgcn_mov_dpp(x, 0x128, 0xf, 0xf, false);
+    if (K == 16)
+        return __builtin_amdgcn_ds_swizzle(x, 0x401f);
+    return __shfl_xor(x, 32, kWave);
+}
+
+template <int K>
+__device__ __forceinline__ void argmin_step(double &best, int32_t &arg)
+{
+    const long long bb = __double_as_longlong(best);
+    const int lo = lane_xor<K>((int)(bb & 0xffffffffll));
+    const int hi = lane_xor<K>((int)(bb >> 32));
+    const double ob = __longlong_as_double(((long long)(unsigned)hi << 32) |
+                                           (long long)(unsigned)lo);
+    const int32_t oa = lane_xor<K>(arg);
+    if (ob < best || (ob == best && oa < arg)) {
+        best = ob;
+        arg = oa;
+    }
+}
+
+// Leftmost minimum of (value, index) over the wave, in every lane (an
+// index of INT64_MAX, no candidate, travels as INT32_MAX).
 __device__ __forceinline__ void wave_argmin(double &best, int64_t &arg)
 {
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        const double ob = __shfl_xor(best, o, kWave);
-        const long long oa = __shfl_xor((long long)arg, o, kWave);
-        amin_merge(best, arg, ob, (int64_t)oa);
-    }
+    int32_t a = (arg == INT64_MAX) ? INT32_MAX : (int32_t)arg;
+    argmin_step<32>(best, a);
+    argmin_step<16>(best, a);
+    argmin_step<8>(best, a);
+    argmin_step<4>(best, a);
+    argmin_step<2>(best, a);
+    argmin_step<1>(best, a);
+    arg = (a == INT32_MAX) ? INT64_MAX : (int64_t)a;
 }
 
 // Candidate bounds of interval [lo, hi]: [alo, ohi]; row r takes j <= r.
