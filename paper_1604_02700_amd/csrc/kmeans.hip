@@ -158,12 +158,13 @@ __global__ void scan_tiles_kernel(double *__restrict__ t1, double *__restrict__ 
     }
 }
 
-// S1[i+1], S2[i+1] = tile offset + in-tile running sums (each thread walks
-// its kItems elements after an exclusive scan of the thread totals).
+// SS[i+1] = (S1[i+1], S2[i+1]) = tile offset + in-tile running sums (each
+// thread walks its kItems elements after an exclusive scan of the thread
+// totals); the two sums of a position sit together, one 16-byte load.
 __global__ __launch_bounds__(kThreads) void prefix_kernel(
     const double *__restrict__ sv, int64_t n, const KmScalars *__restrict__ sc,
     const double *__restrict__ o1, const double *__restrict__ o2,
-    double *__restrict__ S1, double *__restrict__ S2)
+    double2 *__restrict__ SS)
 {
     __shared__ double a1[kThreads], a2[kThreads];
     const double mu = sc->mean;
@@ -198,34 +199,41 @@ __global__ __launch_bounds__(kThreads) void prefix_kernel(
             const double u = sv[i] - mu;
             r1 += u;
             r2 += u * u;
-            S1[i + 1] = r1;
-            S2[i + 1] = r2;
+            SS[i + 1] = double2{r1, r2};
         }
     }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        S1[0] = 0.0;
-        S2[0] = 0.0;
-    }
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        SS[0] = double2{0.0, 0.0};
 }
 
-__device__ __forceinline__ double seg_cost(const double *__restrict__ S1,
-                                           const double *__restrict__ S2,
-                                           int64_t j, int64_t i)
+// cost(j, i) from the prefix sums at j and i + 1
+__device__ __forceinline__ double seg_cost(double2 a, double2 e, int64_t j, int64_t i)
 {
     const double m = (double)(i - j + 1);
-    const double s1 = S1[i + 1] - S1[j];
-    const double s2 = S2[i + 1] - S2[j];
+    const double s1 = e.x - a.x;
+    const double s2 = e.y - a.y;
     const double c = s2 - s1 * s1 / m;
     return c > 0.0 ? c : 0.0;
 }
 
+// A layer's values as its successor reads them: E[j] = D(j - 1) where j
+// starts a run of equal values, +infinity where it does not (a split there
+// would separate equal values), so a candidate needs no separate flag.
+__device__ __forceinline__ void store_next(double *__restrict__ E,
+                                           const int32_t *__restrict__ run, int64_t n,
+                                           int64_t r, double d)
+{
+    if (r + 1 < n)
+        E[r + 1] = run[r + 1] ? d : INFINITY;
+}
+
 __global__ __launch_bounds__(kThreads) void first_layer_kernel(
-    const double *__restrict__ S1, const double *__restrict__ S2, int64_t n,
-    double *__restrict__ D, unsigned long long *__restrict__ qlen)
+    const double2 *__restrict__ SS, const int32_t *__restrict__ run, int64_t n,
+    double *__restrict__ E, unsigned long long *__restrict__ qlen)
 {
     const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (i < n)
-        D[i] = seg_cost(S1, S2, 0, i);
+        store_next(E, run, n, i, seg_cost(SS[0], SS[i + 1], 0, i));
     if (i < 4)
         qlen[i] = 0ull;                 // the recursion's part and row counters
 }
@@ -286,21 +294,19 @@ __device__ __forceinline__ void amin_merge(double &b, int64_t &a, double ob,
     }
 }
 
-// Scan split points j = from, from + stride, ... <= ahi for row r, keeping
-// the leftmost minimum of Dprev[j-1] + cost(j, r) over run starts.  Every
-// candidate is evaluated without branching so successive loads overlap.
-__device__ __forceinline__ void scan_range(const double *__restrict__ S1,
-                                           const double *__restrict__ S2,
-                                           const int32_t *__restrict__ run,
-                                           const double *__restrict__ Dprev,
-                                           int64_t r, int64_t from, int64_t ahi,
-                                           int64_t stride, double &best,
+// Scan split points j = from .. ahi for row r, keeping the leftmost
+// minimum of D(j - 1) + cost(j, r) over run starts (E[j] is +infinity
+// elsewhere, and so is the sum).  Every candidate is evaluated without
+// branching so successive loads overlap.
+__device__ __forceinline__ void scan_range(const double2 *__restrict__ SS,
+                                           const double *__restrict__ Ep, int64_t r,
+                                           int64_t from, int64_t ahi, double &best,
                                            int64_t &arg)
 {
+    const double2 e = SS[r + 1];
 #pragma unroll 4
-    for (int64_t j = from; j <= ahi; j += stride) {
-        const double cst = Dprev[j - 1] + seg_cost(S1, S2, j, r);
-        const double c = run[j] ? cst : INFINITY;
+    for (int64_t j = from; j <= ahi; ++j) {
+        const double c = Ep[j] + seg_cost(SS[j], e, j, r);
         if (c < best) {
             best = c;
             arg = j;
@@ -366,11 +372,12 @@ __device__ __forceinline__ void interval_bounds(const int32_t *__restrict__ opt,
     alo = olo < 1 ? 1 : olo;
 }
 
-__device__ __forceinline__ void store_result(double *__restrict__ Dcur,
+__device__ __forceinline__ void store_result(double *__restrict__ Ec,
+                                             const int32_t *__restrict__ run, int64_t n,
                                              int32_t *__restrict__ opt, int64_t r,
                                              double best, int64_t arg, int64_t alo)
 {
-    Dcur[r] = best;
+    store_next(Ec, run, n, r, best);
     opt[r] = (int32_t)((arg == INT64_MAX) ? alo : arg);
 }
 
@@ -551,10 +558,9 @@ __global__ __launch_bounds__(kThreads) void level_scatter_kernel(
 // other pair of counters, whose level has finished.
 template <int F>
 __global__ __launch_bounds__(kThreads) void fary_rows_kernel(
-    const double *__restrict__ S1, const double *__restrict__ S2,
-    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
-    double *__restrict__ Dcur, int32_t *__restrict__ opt, int32_t n,
-    const RowEntry *__restrict__ list, const int32_t *__restrict__ base, int L,
+    const double2 *__restrict__ SS, const int32_t *__restrict__ run,
+    const double *__restrict__ Ep, double *__restrict__ Ec, int32_t *__restrict__ opt,
+    int32_t n, const RowEntry *__restrict__ list, const int32_t *__restrict__ base, int L,
     LevelQueue Q, int g)
 {
     const int64_t item = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -627,16 +633,16 @@ __global__ __launch_bounds__(kThreads) void fary_rows_kernel(
     if (len <= kShortScan) {
         double best = INFINITY;
         int64_t arg = INT64_MAX;
-        scan_range(S1, S2, run, Dprev, r, alo, ohi < r ? ohi : r, 1, best, arg);
-        store_result(Dcur, opt, r, best, arg, alo);
+        scan_range(SS, Ep, r, alo, ohi < r ? ohi : r, best, arg);
+        store_result(Ec, run, n, opt, r, best, arg, alo);
     } else if (lead && !ok) {
         const int ns = (hi - lo + 1 < F) ? hi - lo + 1 : F;
         for (int f = 0; f < ns; ++f) {
             const int32_t q = sample_row<F>(lo, hi, f);
             double best = INFINITY;
             int64_t arg = INT64_MAX;
-            scan_range(S1, S2, run, Dprev, q, alo, ohi < q ? ohi : q, 1, best, arg);
-            store_result(Dcur, opt, q, best, arg, alo);
+            scan_range(SS, Ep, q, alo, ohi < q ? ohi : q, best, arg);
+            store_result(Ec, run, n, opt, q, best, arg, alo);
         }
     }
 }
@@ -647,9 +653,9 @@ __global__ __launch_bounds__(kThreads) void fary_rows_kernel(
 // the part leaves each sample's minimum for fary_merge_kernel.
 template <int F>
 __global__ __launch_bounds__(kThreads) void fary_queue_kernel(
-    const double *__restrict__ S1, const double *__restrict__ S2,
-    const int32_t *__restrict__ run, const double *__restrict__ Dprev,
-    double *__restrict__ Dcur, int32_t *__restrict__ opt, LevelQueue Q, int g)
+    const double2 *__restrict__ SS, const int32_t *__restrict__ run,
+    const double *__restrict__ Ep, double *__restrict__ Ec, int32_t *__restrict__ opt,
+    int32_t n, LevelQueue Q, int g)
 {
     constexpr int kGroup = group_for<F>();
     constexpr int kGroups = (F + kGroup - 1) / kGroup;
@@ -676,24 +682,24 @@ __global__ __launch_bounds__(kThreads) void fary_queue_kernel(
             for (int u = 0; u < kGroup; ++u) {
                 rr[u] = (g0 + u < ns) ? (int64_t)sample_row<F>(q.lo, q.hi, g0 + u) : -1;
                 lim[u] = (rr[u] < q.ohi) ? rr[u] : q.ohi;
-                s1e[u] = (rr[u] >= 0) ? S1[rr[u] + 1] : 0.0;
-                s2e[u] = (rr[u] >= 0) ? S2[rr[u] + 1] : 0.0;
+                const double2 e = (rr[u] >= 0) ? SS[rr[u] + 1] : double2{0.0, 0.0};
+                s1e[u] = e.x;
+                s2e[u] = e.y;
                 best[u] = INFINITY;
                 arg[u] = INT64_MAX;
             }
             for (int64_t j = (int64_t)q.plo + lane; j <= q.phi; j += kWave) {
-                const double dp = Dprev[j - 1];
-                const double a1 = S1[j], a2 = S2[j];
-                const bool st = run[j] != 0;
+                const double dp = Ep[j];
+                const double2 a = SS[j];
+                const double a1 = a.x, a2 = a.y;
 #pragma unroll
                 for (int u = 0; u < kGroup; ++u) {
-                    // the cost of seg_cost(S1, S2, j, rr[u]), term by term
+                    // seg_cost(SS[j], SS[rr[u] + 1], j, rr[u]), term by term
                     const double mm = (double)(rr[u] - j + 1);
                     const double s1 = s1e[u] - a1;
                     const double s2 = s2e[u] - a2;
                     const double c0 = s2 - s1 * s1 / mm;
-                    const double cst = dp + (c0 > 0.0 ? c0 : 0.0);
-                    const double c = st ? cst : INFINITY;
+                    const double c = dp + (c0 > 0.0 ? c0 : 0.0);
                     if (j <= lim[u] && c < best[u]) {
                         best[u] = c;
                         arg[u] = j;
@@ -707,7 +713,7 @@ __global__ __launch_bounds__(kThreads) void fary_queue_kernel(
                 wave_argmin(best[u], arg[u]);
                 if (lane == 0) {
                     if (single) {
-                        store_result(Dcur, opt, rr[u], best[u], arg[u], q.alo);
+                        store_result(Ec, run, n, opt, rr[u], best[u], arg[u], q.alo);
                     } else {
                         Q.pbest[e * F + g0 + u] = best[u];
                         Q.parg[e * F + g0 + u] =
@@ -723,7 +729,8 @@ __global__ __launch_bounds__(kThreads) void fary_queue_kernel(
 // parts' minima in an order-independent leftmost minimum.
 template <int F>
 __global__ __launch_bounds__(kThreads) void fary_merge_kernel(
-    double *__restrict__ Dcur, int32_t *__restrict__ opt, LevelQueue Q, int g)
+    double *__restrict__ Ec, const int32_t *__restrict__ run, int32_t n,
+    int32_t *__restrict__ opt, LevelQueue Q, int g)
 {
     const int64_t nh = (int64_t)Q.qlen[2 + (g & 1)];
     const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
@@ -747,7 +754,7 @@ __global__ __launch_bounds__(kThreads) void fary_merge_kernel(
             }
             wave_argmin(best, arg);
             if (lane == 0)
-                store_result(Dcur, opt, sample_row<F>(q.lo, q.hi, f), best, arg, q.alo);
+                store_result(Ec, run, n, opt, sample_row<F>(q.lo, q.hi, f), best, arg, q.alo);
         }
     }
 }
@@ -813,7 +820,7 @@ inline size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 unsigned blocks_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
 struct KmLayout {
-    size_t keyA, keyB, idxA, idxB, hist, hsum, sv, run, t1, t2, S1, S2, Da, Db, opt,
+    size_t keyA, keyB, idxA, idxB, hist, hsum, sv, run, t1, t2, SS, Ea, Eb, opt,
         qpart, qnparts, qheads, qbest, qarg, qlen, sc, first, costs, ent, lr, bh, lbase,
         list, total;
 };
@@ -846,10 +853,9 @@ KmLayout layout(int64_t n, int32_t k)
     L.run = take(n * 4);
     L.t1 = take(nt * 8);
     L.t2 = take(nt * 8);
-    L.S1 = take((n + 1) * 8);
-    L.S2 = take((n + 1) * 8);
-    L.Da = take(n * 8);
-    L.Db = take(n * 8);
+    L.SS = take((n + 1) * 16);
+    L.Ea = take(n * 8);
+    L.Eb = take(n * 8);
     L.opt = take((size_t)k * n * 4);
     const size_t cap = (size_t)queue_cap(n);
     L.qpart = take(cap * sizeof(QueuePart));
@@ -894,8 +900,8 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     double *sv = (double *)(w + L.sv);
     int32_t *run = (int32_t *)(w + L.run);
     double *t1 = (double *)(w + L.t1), *t2 = (double *)(w + L.t2);
-    double *S1 = (double *)(w + L.S1), *S2 = (double *)(w + L.S2);
-    double *Da = (double *)(w + L.Da), *Db = (double *)(w + L.Db);
+    double2 *SS = (double2 *)(w + L.SS);
+    double *Ea = (double *)(w + L.Ea), *Eb = (double *)(w + L.Eb);
     int32_t *opt = (int32_t *)(w + L.opt);
     LevelQueue Q;
     Q.part = (QueuePart *)(w + L.qpart);
@@ -924,7 +930,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
                        sv, n, sc, t1, t2);
     hipLaunchKernelGGL(scan_tiles_kernel, dim3(1), dim3(64), 0, s, t1, t2, nt);
     hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)nt), dim3(kThreads), 0, s, sv,
-                       n, sc, t1, t2, S1, S2);
+                       n, sc, t1, t2, SS);
     GPIC_TRY(hipGetLastError());
     KmScalars hsc{};
     GPIC_TRY(hipMemcpyAsync(&hsc, sc, sizeof(hsc), hipMemcpyDeviceToHost, s));
@@ -934,7 +940,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
 
     // 3. layers
     hipLaunchKernelGGL(first_layer_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s,
-                       S1, S2, n, Da, Q.qlen);
+                       SS, run, n, Ea, Q.qlen);
     const int F = fary_f(n);
     // levels of the F-ary recursion: until every interval has <= F rows
     int levels = 1;
@@ -942,7 +948,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
         ++levels;
     if (levels > kMaxLevels)
         return hipErrorInvalidValue;               // not reachable for n <= 2^30
-    double *Dprev = Da, *Dcur = Db;
+    double *Ep = Ea, *Ec = Eb;
     if (ke > 1) {
         // samples per level, from the interval sizes alone (each level's
         // intervals take at most a few distinct sizes)
@@ -1018,23 +1024,23 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
                 const dim3 grid(blocks_for(count[Lv] > 0 ? count[Lv] : 1));
                 if (F == kFSmall) {
                     hipLaunchKernelGGL(fary_rows_kernel<kFSmall>, grid, dim3(kThreads), 0, s,
-                                       S1, S2, run, Dprev, Dcur, oc, (int32_t)n, list, lbase,
+                                       SS, run, Ep, Ec, oc, (int32_t)n, list, lbase,
                                        Lv, Q, g);
                     hipLaunchKernelGGL(fary_queue_kernel<kFSmall>, dim3(2048), dim3(kThreads),
-                                       0, s, S1, S2, run, Dprev, Dcur, oc, Q, g);
+                                       0, s, SS, run, Ep, Ec, oc, (int32_t)n, Q, g);
                     hipLaunchKernelGGL(fary_merge_kernel<kFSmall>, dim3(512), dim3(kThreads),
-                                       0, s, Dcur, oc, Q, g);
+                                       0, s, Ec, run, (int32_t)n, oc, Q, g);
                 } else {
                     hipLaunchKernelGGL(fary_rows_kernel<kFLarge>, grid, dim3(kThreads), 0, s,
-                                       S1, S2, run, Dprev, Dcur, oc, (int32_t)n, list, lbase,
+                                       SS, run, Ep, Ec, oc, (int32_t)n, list, lbase,
                                        Lv, Q, g);
                     hipLaunchKernelGGL(fary_queue_kernel<kFLarge>, dim3(2048), dim3(kThreads),
-                                       0, s, S1, S2, run, Dprev, Dcur, oc, Q, g);
+                                       0, s, SS, run, Ep, Ec, oc, (int32_t)n, Q, g);
                     hipLaunchKernelGGL(fary_merge_kernel<kFLarge>, dim3(512), dim3(kThreads),
-                                       0, s, Dcur, oc, Q, g);
+                                       0, s, Ec, run, (int32_t)n, oc, Q, g);
                 }
             }
-            double *tmp = Dprev; Dprev = Dcur; Dcur = tmp;
+            double *tmp = Ep; Ep = Ec; Ec = tmp;
         }
     }
     GPIC_TRY(hipGetLastError());
