@@ -725,37 +725,55 @@ __global__ __launch_bounds__(kThreads) void fary_queue_kernel(
     }
 }
 
-// Intervals with several parts: a wave per (interval, sample) merges the
-// parts' minima in an order-independent leftmost minimum.
+// Intervals with several parts: the parts' minima of each (interval,
+// sample) merged in an order-independent leftmost minimum, by a wave, or
+// by a whole workgroup at the first levels (few intervals with thousands
+// of parts each; `whole` is uniform over the launch).
 template <int F>
 __global__ __launch_bounds__(kThreads) void fary_merge_kernel(
     double *__restrict__ Ec, const int32_t *__restrict__ run, int32_t n,
-    int32_t *__restrict__ opt, LevelQueue Q, int g)
+    int32_t *__restrict__ opt, LevelQueue Q, int g, int whole)
 {
+    __shared__ double wb[kThreads / kWave];
+    __shared__ int64_t wa[kThreads / kWave];
     const int64_t nh = (int64_t)Q.qlen[2 + (g & 1)];
-    const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
-    const int lane = threadIdx.x % kWave;
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    const int64_t t0 = whole ? (int64_t)blockIdx.x
+                             : (int64_t)blockIdx.x * (kThreads / kWave) + w;
+    const int64_t step = whole ? (int64_t)gridDim.x : (int64_t)gridDim.x * (kThreads / kWave);
+    const int p0 = whole ? (int)threadIdx.x : lane;
+    const int pstep = whole ? kThreads : kWave;
     // work item t: interval t / F, sample t % F
-    for (int64_t t = (int64_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
-         t < nh * F; t += waves) {
+    for (int64_t t = t0; t < nh * F; t += step) {
         const int64_t head = Q.heads[t / F];
         const int f = (int)(t % F);
         const QueuePart q = Q.part[head];
         const int C = Q.nparts[head];
         const int m = q.hi - q.lo + 1;
         const int ns = m < F ? m : F;
-        if (f < ns) {
-            double best = INFINITY;
-            int64_t arg = INT64_MAX;
-            for (int p = lane; p < C; p += kWave) {
-                const int32_t a = Q.parg[(head + p) * F + f];
-                amin_merge(best, arg, Q.pbest[(head + p) * F + f],
-                           a == INT32_MAX ? INT64_MAX : (int64_t)a);
-            }
-            wave_argmin(best, arg);
-            if (lane == 0)
-                store_result(Ec, run, n, opt, sample_row<F>(q.lo, q.hi, f), best, arg, q.alo);
+        if (f >= ns)
+            continue;                                   // uniform per item
+        double best = INFINITY;
+        int64_t arg = INT64_MAX;
+        for (int p = p0; p < C; p += pstep) {
+            const int32_t a = Q.parg[(head + p) * F + f];
+            amin_merge(best, arg, Q.pbest[(head + p) * F + f],
+                       a == INT32_MAX ? INT64_MAX : (int64_t)a);
         }
+        wave_argmin(best, arg);
+        if (whole) {
+            if (lane == 0) {
+                wb[w] = best;
+                wa[w] = arg;
+            }
+            __syncthreads();
+            if (threadIdx.x == 0)
+                for (int u = 1; u < kThreads / kWave; ++u)
+                    amin_merge(best, arg, wb[u], wa[u]);
+            __syncthreads();
+        }
+        if (threadIdx.x % (whole ? kThreads : kWave) == 0)
+            store_result(Ec, run, n, opt, sample_row<F>(q.lo, q.hi, f), best, arg, q.alo);
     }
 }
 
@@ -1022,6 +1040,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
             int32_t *oc = opt + (int64_t)c * n;
             for (int Lv = 0; Lv < levels; ++Lv, ++g) {
                 const dim3 grid(blocks_for(count[Lv] > 0 ? count[Lv] : 1));
+                const int whole = count[Lv] <= 512;    // few intervals, many parts each
                 if (F == kFSmall) {
                     hipLaunchKernelGGL(fary_rows_kernel<kFSmall>, grid, dim3(kThreads), 0, s,
                                        SS, run, Ep, Ec, oc, (int32_t)n, list, lbase,
@@ -1029,7 +1048,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
                     hipLaunchKernelGGL(fary_queue_kernel<kFSmall>, dim3(2048), dim3(kThreads),
                                        0, s, SS, run, Ep, Ec, oc, (int32_t)n, Q, g);
                     hipLaunchKernelGGL(fary_merge_kernel<kFSmall>, dim3(512), dim3(kThreads),
-                                       0, s, Ec, run, (int32_t)n, oc, Q, g);
+                                       0, s, Ec, run, (int32_t)n, oc, Q, g, whole);
                 } else {
                     hipLaunchKernelGGL(fary_rows_kernel<kFLarge>, grid, dim3(kThreads), 0, s,
                                        SS, run, Ep, Ec, oc, (int32_t)n, list, lbase,
@@ -1037,7 +1056,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
                     hipLaunchKernelGGL(fary_queue_kernel<kFLarge>, dim3(2048), dim3(kThreads),
                                        0, s, SS, run, Ep, Ec, oc, (int32_t)n, Q, g);
                     hipLaunchKernelGGL(fary_merge_kernel<kFLarge>, dim3(512), dim3(kThreads),
-                                       0, s, Ec, run, (int32_t)n, oc, Q, g);
+                                       0, s, Ec, run, (int32_t)n, oc, Q, g, whole);
                 }
             }
             double *tmp = Ep; Ep = Ec; Ec = tmp;
