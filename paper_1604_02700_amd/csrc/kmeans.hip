@@ -84,6 +84,27 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     }
 }
 
+// Inclusive scan of (x1, x2) over the NT threads of a block (Hillis-Steele
+// steps in LDS, a fixed order); a1, a2 must hold NT doubles each.
+template <int NT>
+__device__ __forceinline__ void block_scan2(double &x1, double &x2, double *a1, double *a2)
+{
+    const int t = threadIdx.x;
+    a1[t] = x1;
+    a2[t] = x2;
+    __syncthreads();
+    for (int off = 1; off < NT; off <<= 1) {
+        const double y1 = t >= off ? a1[t - off] : 0.0;
+        const double y2 = t >= off ? a2[t - off] : 0.0;
+        __syncthreads();
+        x1 += y1;
+        x2 += y2;
+        a1[t] = x1;
+        a2[t] = x2;
+        __syncthreads();
+    }
+}
+
 struct KmScalars {
     double mean;
     double distinct;
@@ -125,36 +146,42 @@ __global__ __launch_bounds__(kThreads) void tile_moments_kernel(
             s2 += u * u;
         }
     }
-    // thread totals in thread order: serial over the block's 256 totals
+    // the block's total: the last element of the scan of the thread totals
     __shared__ double a1[kThreads], a2[kThreads];
-    a1[threadIdx.x] = s1;
-    a2[threadIdx.x] = s2;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        double x1 = 0.0, x2 = 0.0;
-        for (int t = 0; t < kThreads; ++t) {
-            x1 += a1[t];
-            x2 += a2[t];
-        }
-        t1[blockIdx.x] = x1;
-        t2[blockIdx.x] = x2;
+    block_scan2<kThreads>(s1, s2, a1, a2);
+    if (threadIdx.x == kThreads - 1) {
+        t1[blockIdx.x] = s1;
+        t2[blockIdx.x] = s2;
     }
     (void)red;
 }
 
-// Exclusive scan of the tile totals (serial: there are few tiles).
-__global__ void scan_tiles_kernel(double *__restrict__ t1, double *__restrict__ t2,
-                                  int64_t nt)
+// Exclusive scan of the tile totals by one workgroup: each thread sums a
+// contiguous run of tiles, the runs' totals are scanned across the block,
+// then each thread walks its run again.
+constexpr int kScanThreads = 1024;
+__global__ __launch_bounds__(kScanThreads) void scan_tiles_kernel(
+    double *__restrict__ t1, double *__restrict__ t2, int64_t nt)
 {
-    if (threadIdx.x != 0)
-        return;
-    double r1 = 0.0, r2 = 0.0;
-    for (int64_t b = 0; b < nt; ++b) {
-        const double x1 = t1[b], x2 = t2[b];
+    __shared__ double a1[kScanThreads], a2[kScanThreads];
+    const int64_t per = (nt + kScanThreads - 1) / kScanThreads;
+    const int64_t b0 = (int64_t)threadIdx.x * per;
+    const int64_t b1 = (b0 + per < nt) ? b0 + per : nt;
+    double x1 = 0.0, x2 = 0.0;
+    for (int64_t b = b0; b < b1; ++b) {
+        x1 += t1[b];
+        x2 += t2[b];
+    }
+    double i1 = x1, i2 = x2;
+    block_scan2<kScanThreads>(i1, i2, a1, a2);
+    double r1 = threadIdx.x > 0 ? a1[threadIdx.x - 1] : 0.0;
+    double r2 = threadIdx.x > 0 ? a2[threadIdx.x - 1] : 0.0;
+    for (int64_t b = b0; b < b1; ++b) {
+        const double y1 = t1[b], y2 = t2[b];
         t1[b] = r1;
         t2[b] = r2;
-        r1 += x1;
-        r2 += x2;
+        r1 += y1;
+        r2 += y2;
     }
 }
 
@@ -178,21 +205,12 @@ __global__ __launch_bounds__(kThreads) void prefix_kernel(
             s2 += u * u;
         }
     }
-    a1[threadIdx.x] = s1;
-    a2[threadIdx.x] = s2;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        double r1 = o1[blockIdx.x], r2 = o2[blockIdx.x];
-        for (int t = 0; t < kThreads; ++t) {
-            const double x1 = a1[t], x2 = a2[t];
-            a1[t] = r1;
-            a2[t] = r2;
-            r1 += x1;
-            r2 += x2;
-        }
-    }
-    __syncthreads();
-    double r1 = a1[threadIdx.x], r2 = a2[threadIdx.x];
+    // exclusive offset of this thread: the tile's offset plus the scan of
+    // the earlier threads' totals
+    double i1 = s1, i2 = s2;
+    block_scan2<kThreads>(i1, i2, a1, a2);
+    double r1 = o1[blockIdx.x] + (threadIdx.x > 0 ? a1[threadIdx.x - 1] : 0.0);
+    double r2 = o2[blockIdx.x] + (threadIdx.x > 0 ? a2[threadIdx.x - 1] : 0.0);
     for (int it = 0; it < kItems; ++it) {
         const int64_t i = b + it;
         if (i < n) {
@@ -794,21 +812,24 @@ __global__ void backtrack_kernel(const int32_t *__restrict__ opt, int64_t n,
 
 // One workgroup per cluster: mean (sum in a fixed order / count) and the
 // sum of squared deviations from it.
-__global__ __launch_bounds__(kThreads) void cluster_stats_kernel(
+constexpr int kStatThreads = 1024;
+__global__ __launch_bounds__(kStatThreads) void cluster_stats_kernel(
     const double *__restrict__ sv, const int64_t *__restrict__ first,
     double *__restrict__ centroids, double *__restrict__ costs)
 {
-    __shared__ double red[kThreads / kWave];
+    __shared__ double red[kStatThreads / kWave];
     const int c = blockIdx.x;
     const int64_t b = first[c], e = first[c + 1];
     double s = 0.0;
-    for (int64_t p = b + threadIdx.x; p < e; p += kThreads)
+#pragma unroll 4
+    for (int64_t p = b + threadIdx.x; p < e; p += kStatThreads)
         s += sv[p];
-    const double mu = block_sum<kThreads>(s, red) / (double)(e - b);
+    const double mu = block_sum<kStatThreads>(s, red) / (double)(e - b);
     double q = 0.0;
-    for (int64_t p = b + threadIdx.x; p < e; p += kThreads)
+#pragma unroll 4
+    for (int64_t p = b + threadIdx.x; p < e; p += kStatThreads)
         q += (sv[p] - mu) * (sv[p] - mu);
-    const double tq = block_sum<kThreads>(q, red);
+    const double tq = block_sum<kStatThreads>(q, red);
     if (threadIdx.x == 0) {
         centroids[c] = mu;
         costs[c] = tq;
@@ -946,7 +967,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
     hipLaunchKernelGGL(totals_kernel, dim3(1), dim3(1024), 0, s, t1, t2, nt, n, sc);
     hipLaunchKernelGGL(tile_moments_kernel, dim3((unsigned)nt), dim3(kThreads), 0, s,
                        sv, n, sc, t1, t2);
-    hipLaunchKernelGGL(scan_tiles_kernel, dim3(1), dim3(64), 0, s, t1, t2, nt);
+    hipLaunchKernelGGL(scan_tiles_kernel, dim3(1), dim3(kScanThreads), 0, s, t1, t2, nt);
     hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)nt), dim3(kThreads), 0, s, sv,
                        n, sc, t1, t2, SS);
     GPIC_TRY(hipGetLastError());
@@ -1066,7 +1087,7 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
 
     // 4. boundaries, cluster statistics, labels
     hipLaunchKernelGGL(backtrack_kernel, dim3(1), dim3(64), 0, s, opt, n, ke, first);
-    hipLaunchKernelGGL(cluster_stats_kernel, dim3((unsigned)ke), dim3(kThreads), 0, s,
+    hipLaunchKernelGGL(cluster_stats_kernel, dim3((unsigned)ke), dim3(kStatThreads), 0, s,
                        sv, first, centroids, costs);
     hipLaunchKernelGGL(labels_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, idxA,
                        n, first, ke, labels);
