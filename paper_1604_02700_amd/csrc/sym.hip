@@ -16,14 +16,20 @@
 // [0, n)^2 by 0 with a select (never a multiply by a mask) before it is
 // used, so such padding cannot reach a sum.
 //
-// One workgroup per tile.  Tile (I, J) gives the row sums A_IJ v_J to the
-// rows of block I and, when I < J, the column sums A_IJ^T v_I to the rows
-// of block J (A_JI = A_IJ^T), into part[(I nb + J) 256 + r] and
-// part[(J nb + I) 256 + c].  A second launch adds, for every row i of
-// block I, the nb partials part[(I nb + K) 256 + i - 256 I] (four slices
-// of K summed in ascending order, then added in slice order), divides by
-// d_i and writes per-workgroup partial sums of |y_i| for the L1 norm.
-// Every sum runs in a fixed order: bitwise reproducible.
+// One workgroup per super-tile of 2 x 2 tiles: super-tile (R, S), R <= S,
+// covers the blocks 2R, 2R + 1 (rows) and 2S, 2S + 1 (columns), and takes
+// its stored tiles one after another.  Tile (I, J) gives the row sums
+// A_IJ v_J to the rows of block I and, when I < J, the column sums
+// A_IJ^T v_I to the rows of block J (A_JI = A_IJ^T); the workgroup adds
+// them per row in LDS (tiles in the order (2R, 2S), (2R, 2S + 1),
+// (2R + 1, 2S), (2R + 1, 2S + 1)) and writes 512 sums for the rows of
+// super-row R to part[(R ns + S) 512 + .] and, when R < S, 512 for those of
+// super-row S to part[(S ns + R) 512 + .] -- half the partial sums of one
+// workgroup per tile.  A second launch adds, for every row i, the ns
+// partials of its super-row (four slices summed in ascending order, then
+// added in slice order), divides by d_i and writes per-workgroup partial
+// sums of |y_i| for the L1 norm.  Every sum runs in a fixed order: bitwise
+// reproducible.
 #include "common.h"
 
 namespace gpic {
@@ -32,6 +38,7 @@ namespace {
 constexpr int kTile = 256;                 // tile edge (indices per block)
 constexpr int kThreads = 256;              // four waves; a thread covers 32 rows x 8 columns
 constexpr int64_t kTileEntries = (int64_t)kTile * kTile;
+constexpr int kSuper = 2 * kTile;          // rows (and columns) of a super-tile
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
@@ -40,8 +47,9 @@ __device__ __host__ __forceinline__ int64_t tile_start(int64_t I, int64_t nb)
     return I * nb - I * (I - 1) / 2;
 }
 
-// (I, J) of the t-th stored tile: I from the quadratic formula, corrected
-// by at most a step either way against rounding.
+// (I, J) of the t-th pair I <= J in the order (0,0), (0,1), .., (0,nb-1),
+// (1,1), ..: I from the quadratic formula, corrected by at most a step
+// either way against rounding.
 __device__ __forceinline__ void tile_of(int64_t t, int64_t nb, int64_t *I, int64_t *J)
 {
     const double b = (double)(2 * nb + 1);
@@ -71,8 +79,9 @@ __device__ __forceinline__ void tile_of(int64_t t, int64_t nb, int64_t *I, int64
 // workgroups per compute unit.
 template <bool EDGE>
 __device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I, int64_t J,
-                                         int64_t n, int64_t nb, const double *__restrict__ v,
-                                         double (*cred)[kTile], double *__restrict__ part)
+                                         int64_t n, const double *__restrict__ v,
+                                         double (*cred)[kTile], double *__restrict__ racc_l,
+                                         double *__restrict__ cacc_l)
 {
     const int tid = threadIdx.x;
     const int tx = tid & 31;
@@ -91,7 +100,6 @@ __device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I,
     for (int c = 0; c < 8; ++c)
         cacc[c] = 0.0;
     const floatx4 *base = reinterpret_cast<const floatx4 *>(T) + (8 * ty) * (kTile / 4) + tx;
-    double *prow = part + (I * nb + J) * kTile;
 #pragma unroll 1
     for (int p = 0; p < 4; ++p) {
         double racc[8];
@@ -134,7 +142,7 @@ __device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I,
         rs = rs + __shfl_xor(rs, 1, kWave);
         if ((tx & 3) == 0) {
             const int r = 4 * ((tx >> 4) & 1) + 2 * ((tx >> 3) & 1) + ((tx >> 2) & 1);
-            prow[64 * p + 8 * ty + r] = rs;
+            racc_l[64 * p + 8 * ty + r] += rs;       // this lane's slot in every tile
         }
     }
     if (I == J)
@@ -155,7 +163,8 @@ __device__ __forceinline__ void sym_tile(const float *__restrict__ T, int64_t I,
     __syncthreads();
     // ... then over the four waves, in wave order
     const double s = ((cred[0][tid] + cred[1][tid]) + cred[2][tid]) + cred[3][tid];
-    part[((J * nb + I) * kTile) + tid] = s;
+    cacc_l[tid] += s;
+    __syncthreads();                             // cred is reused by the next tile
 }
 
 __global__ __launch_bounds__(kThreads) void sym_gemv_kernel(
@@ -163,25 +172,47 @@ __global__ __launch_bounds__(kThreads) void sym_gemv_kernel(
     double *__restrict__ part, StopCtl ctl, int use_ctl)
 {
     __shared__ double cred[kThreads / kWave][kTile];
+    __shared__ double acc[4][kTile];              // rows of blocks 2R, 2R+1, 2S, 2S+1
     if (use_ctl) {
         if (blockIdx.x == 0 && threadIdx.x == 0)
             *ctl.cur_stat = 0.0;
         if (stop_reached(ctl))
             return;
     }
-    int64_t I, J;
-    tile_of((int64_t)blockIdx.x, nb, &I, &J);
-    const float *T = As + (tile_start(I, nb) + (J - I)) * kTileEntries;
-    const bool edge = (kTile * (J + 1) > n);     // J >= I: the last block column
-    if (edge)
-        sym_tile<true>(T, I, J, n, nb, v, cred, part);
-    else
-        sym_tile<false>(T, I, J, n, nb, v, cred, part);
+    const int64_t ns = (nb + 1) / 2;
+    int64_t R, S;
+    tile_of((int64_t)blockIdx.x, ns, &R, &S);
+    for (int q = 0; q < 4; ++q)
+        acc[q][threadIdx.x] = 0.0;
+    __syncthreads();
+    // the stored tiles of the super-tile, in a fixed order; on the diagonal
+    // (R = S) the tile (2R + 1, 2R) is not stored, and the column sums of
+    // (2R, 2R + 1) go to block 2R + 1, whose rows sit in acc[1]
+#pragma unroll 1
+    for (int u = 0; u < 4; ++u) {
+        const int64_t I = 2 * R + (u >> 1), J = 2 * S + (u & 1);
+        if (I >= nb || J >= nb || I > J)
+            continue;                            // uniform over the workgroup
+        const float *T = As + (tile_start(I, nb) + (J - I)) * kTileEntries;
+        double *ra = acc[u >> 1];
+        double *ca = (R == S) ? acc[1] : acc[2 + (u & 1)];
+        if (kTile * (J + 1) > n)                 // J >= I: the last block column
+            sym_tile<true>(T, I, J, n, v, cred, ra, ca);
+        else
+            sym_tile<false>(T, I, J, n, v, cred, ra, ca);
+    }
+    __syncthreads();
+    for (int q = 0; q < 2; ++q)
+        part[(R * ns + S) * kSuper + q * kTile + threadIdx.x] = acc[q][threadIdx.x];
+    if (R < S)
+        for (int q = 0; q < 2; ++q)
+            part[(S * ns + R) * kSuper + q * kTile + threadIdx.x] = acc[2 + q][threadIdx.x];
 }
 
-// y_i = (sum over K of part[(I nb + K) 256 + r]) / d_i; one workgroup of
-// 4 x 256 threads per block of 256 rows: slice s sums K = s, s + 4, ..
-// (eight loads in flight), then the four slices are added in slice order.
+// y_i = (sum over K of part[(R ns + K) 512 + 256 (I - 2R) + r]) / d_i for
+// row i = 256 I + r of super-row R = I / 2; one workgroup of 4 x 256
+// threads per block of 256 rows: slice s sums K = s, s + 4, .. (eight loads
+// in flight), then the four slices are added in slice order.
 constexpr int kSlices = 4;
 
 __global__ __launch_bounds__(kThreads * kSlices) void sym_finalize_kernel(
@@ -196,20 +227,21 @@ __global__ __launch_bounds__(kThreads * kSlices) void sym_finalize_kernel(
     const int r = threadIdx.x % kThreads;
     const int sidx = threadIdx.x / kThreads;
     const int64_t I = blockIdx.x;
-    const double *p = part + I * nb * kTile + r;
+    const int64_t ns = (nb + 1) / 2;
+    const double *p = part + (I / 2) * ns * kSuper + (I % 2) * kTile + r;
     double s = 0.0;
     int64_t K = sidx;
-    for (; K + 7 * kSlices < nb; K += 8 * kSlices) {
+    for (; K + 7 * kSlices < ns; K += 8 * kSlices) {
         double x[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            x[u] = p[(K + u * kSlices) * kTile];
+            x[u] = p[(K + u * kSlices) * kSuper];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
             s += x[u];
     }
-    for (; K < nb; K += kSlices)
-        s += p[K * kTile];
+    for (; K < ns; K += kSlices)
+        s += p[K * kSuper];
     sl[sidx][r] = s;
     __syncthreads();
     const int64_t i = kTile * I + r;
@@ -243,8 +275,8 @@ size_t sym_storage_bytes(int64_t n)
 
 size_t sym_part_bytes(int64_t n)
 {
-    const int64_t nb = sym_blocks(n);
-    return (size_t)(nb * nb * kTile) * sizeof(double);
+    const int64_t ns = (sym_blocks(n) + 1) / 2;
+    return (size_t)(ns * ns * kSuper) * sizeof(double);
 }
 
 hipError_t launch_sym_gemv(const float *As, int64_t n, const double *degree,
@@ -252,7 +284,8 @@ hipError_t launch_sym_gemv(const float *As, int64_t n, const double *degree,
                            StopCtl ctl, bool use_ctl, hipStream_t s)
 {
     const int64_t nb = sym_blocks(n);
-    hipLaunchKernelGGL(sym_gemv_kernel, dim3((unsigned)(nb * (nb + 1) / 2)), dim3(kThreads),
+    const int64_t ns = (nb + 1) / 2;
+    hipLaunchKernelGGL(sym_gemv_kernel, dim3((unsigned)(ns * (ns + 1) / 2)), dim3(kThreads),
                        0, s, As, n, nb, v, part, ctl, use_ctl ? 1 : 0);
     hipLaunchKernelGGL(sym_finalize_kernel, dim3((unsigned)nb), dim3(kThreads * kSlices), 0,
                        s, part,
