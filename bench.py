@@ -436,9 +436,7 @@ def measure_sym(g, w, X, T, k, steps, warmup, gemv_reps, converge):
     b.record(stream)
     torch.cuda.synchronize()
     prod_ms = a.elapsed_time(b) / gemv_reps
-    nb = (n + 255) // 256
-    part_bytes = 2.0 * 8 * nb * nb * 256          # partial sums written and read back
-    alg = stored + part_bytes + 24.0 * n           # tiles once, partials, v, d, y
+    alg = stored + 24.0 * n                        # the stored tiles once, v, d, y
     conv = None
     if converge:
         out = g.pic_sym(X, w.sigma, k, "converge", 1000, w.eps, As=As)
