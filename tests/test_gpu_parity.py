@@ -386,10 +386,15 @@ def test_pic_cosine_parity(g, orc, name):
                                      (4097, 10, True), (4225, 20, True),
                                      (4291, 7, False), (50000, 10, False),
                                      (20000, 50, True), (274626, 30, False),
-                                     (500000, 50, False)])
+                                     (500000, 50, False), (262143, 20, False),
+                                     (262144, 20, False), (531440, 30, False),
+                                     (531441, 30, True), (300001, 200, True)])
 def test_kmeans1d_parity(g, orc, n, k, dup):
-    """Sizes straddle the recursion's level counts (64 rows per interval and
-    65 children: n = 64 / 65, 4225 / 4291, 274625 / 274626)."""
+    """Sizes straddle the recursion's level counts (F = 64 below 2^18 rows:
+    n = 64 / 65, 4225 / 4291; F = 8 from 2^18 = 262,144: 9^6 = 531,441 adds
+    a level), the switch between the two (262,143 / 262,144), and fewer
+    distinct values than k (300,001 values rounded to about 100 integers,
+    k = 200)."""
     rng = np.random.default_rng(n + k)
     m = max(1, min(k, n))
     centres = np.sort(rng.uniform(0, 100, size=m))
