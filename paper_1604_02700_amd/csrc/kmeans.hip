@@ -8,7 +8,7 @@
 //      stable scatter with in-wave ranks from ballots;
 //   2. run starts of equal values (a cluster never splits equal values),
 //      their count, the mean, and float64 prefix sums S1, S2 of the centred
-//      values u = v_sorted - mean;
+//      values u = v_sorted - mean (stored as (S1, S2) pairs);
 //   3. dynamic programme over layers c = 1..k_eff-1:
 //        D_c(i) = min_{j <= i, j starts a run} D_{c-1}(j-1) + cost(j, i),
 //        cost(j, i) = max(0, (S2[i+1]-S2[j]) - (S1[i+1]-S1[j])^2 / (i-j+1)),
@@ -270,8 +270,10 @@ __global__ __launch_bounds__(kThreads) void first_layer_kernel(
 // All samples of an interval share its candidates, so an interval whose
 // range is long is queued as parts of candidates, and one wave per (part,
 // group of samples) reads each candidate once and evaluates it for the
-// group's samples; short ranges are scanned by a thread per sample.
-// Node digits and sample rows use 32-bit arithmetic (n <= 2^30).
+// group's samples; short ranges are scanned by a thread per sample.  The
+// recursion's shape (which rows are the samples of which interval at which
+// level) depends on n and F only and is laid out once per call as per-level
+// row lists.  Sample rows use 32-bit arithmetic (n <= 2^30).
 constexpr int kFSmall = 64;
 constexpr int kFLarge = 8;
 constexpr int64_t kFLargeFrom = (int64_t)1 << 18;
