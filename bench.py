@@ -377,9 +377,10 @@ def main():
         "read_stream": read_stream,
         "symmetric_storage": sym,
         "cpu_baseline": cpu,
-        "copy_reference": copy_ref,
         "workloads": others,
     }
+    if copy_ref is not None:
+        line["copy_reference"] = copy_ref          # only in counter-scaling runs
     print(json.dumps(line), flush=True)
 
 
