@@ -759,12 +759,20 @@ def test_sym_affinity_equals_dense(g, n, d):
     assert int(nz.item()) == 0
 
 
-@pytest.mark.parametrize("n", [2, 255, 256, 257, 700, 2050])
+@pytest.mark.parametrize("n", [2, 255, 256, 257, 511, 512, 513, 700, 768, 769, 1025, 1281,
+                               2050])
 def test_sym_matvec_stage_isolation(g, n):
     """y = D^-1 (A v) from the stored float32 tiles: only summation order
-    differs from a float64 product with the unpacked matrix."""
+    differs from a float64 product with the unpacked matrix.  Sizes cover
+    one block, a ragged last block, and an even and odd number of 256-row
+    blocks (the product takes 2 x 2 super-tiles; with an odd count the last
+    super-row holds one block).  The storage is filled with NaN before the
+    affinity writes it, so padding entries outside [0, n)^2 hold NaN and
+    must never reach a sum."""
     X = _pts(n, 3, 60 + n)
-    As, deg, v0, _ = g.gpic_affinity_sym(_t(X), 0.9)
+    As0 = torch.full((g.sym_bytes(n) // 4,), float("nan"), dtype=torch.float32,
+                     device=torch.device("cuda:0"))
+    As, deg, v0, _ = g.gpic_affinity_sym(_t(X), 0.9, As=As0)
     rng = np.random.default_rng(n)
     v = rng.random(n)
     y = g.gpic_matvec_sym(As, n, deg, _t(v)).cpu().numpy()
