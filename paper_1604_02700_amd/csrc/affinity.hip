@@ -321,10 +321,11 @@ __global__ __launch_bounds__(kThreads) void fused_sym_reduce_kernel(
 // ------------------------------------------------------------------ MFMA
 
 // Workgroup: W waves, each owning RB blocks of 16 rows; columns [c0, c1)
-// of its chunk in tiles of TC staged through double-buffered LDS.  A tile
-// holds, per (chunk, part, lane group) slot, TC consecutive half8 pieces:
-// xs[buf][slot * TC + col].  Every staged tile feeds 16 W RB rows, so the
-// operand traffic from L2 per pair of points is 4 d / (16 W RB) bytes.
+// of its chunk in tiles of TC staged through double-buffered LDS while the
+// previous tile is computed.  A tile holds, per (chunk, part, lane group) slot, TC
+// consecutive half8 pieces: xs[buf][slot * TC + col].  Every staged tile
+// feeds 16 W RB rows, so the operand traffic from L2 per pair of points is
+// 4 d / (16 W RB) bytes.
 //
 // v_mfma_f32_16x16x32_f16 operand layout (lane l, g = l / 16, m = l % 16;
 // checked on the device):
@@ -332,17 +333,29 @@ __global__ __launch_bounds__(kThreads) void fused_sym_reduce_kernel(
 //   B operand : column m,   k = 8 g .. 8 g + 7
 //   result    : rows 4 g + r (r = 0..3), column m
 // The A operand carries tile columns 16 q + m and the B operand the wave's
-// rows i, so lane (m, g) ends with row i and columns 16 q + 4 g + r.  Each
-// 32-coordinate chunk takes three products (hi.hi, lo.hi, hi.lo) into one
-// float32 accumulator, which leaves D = x'_i.x'_j (each point in its own
-// scale), and two fused multiply-adds give
+// rows i, so lane (m, g) ends with row i and columns 16 q + 4 g + r: a
+// row's sum is in-lane until the end.  The symmetric product (kApplySym),
+// which also sums columns, swaps the two (the per-lane operand layouts
+// coincide, so the same registers serve): lane (m, g) ends with rows
+// 16 rb + 4 g + r and column 16 q + m, a column's sum over the wave's rows
+// is in-lane plus one sum over the four lane groups, and the row sums stay
+// spread over the 16 lanes m until the end.  Each 32-coordinate chunk takes
+// three products (hi.hi, lo.hi, hi.lo) into one float32 accumulator, which
+// leaves D = x'_i.x'_j (each point in its own scale), and two fused
+// multiply-adds give
 //   c dist2 = sc_j (mr_i D + gam_j) + cn_i
 // (row values in registers, column values staged with the tile);
-// exp2(-c dist2) is clamped to [0, 1], which equals clamping c dist2 at 0.  The matrix-core chain of one 16-column block is issued before the
-// epilogue of the previous block, so the matrix cores and the vector ALUs
-// work at the same time.
+// exp2(-c dist2) is clamped to [0, 1], which equals clamping c dist2 at 0.
+// The matrix-core chain of one 16-column block is issued before the
+// epilogue of the previous block, except in the symmetric product up to 64
+// coordinates, which runs each block's chain and then its epilogue (the
+// compiler then needs fewer registers for the three row blocks; measured
+// 4 % faster at n = 200,000, d = 64 and 13 % at d = 16).
 // When A or W is written (W = 4, RB = 1), the wave's 16 x TC tile goes
 // through LDS and is stored as 4 rows x 4 TC contiguous bytes per store.
+// s_waitcnt operand: outstanding vector memory operations 0, the other
+// counters at their maximum (no wait)
+constexpr int kWaitVm0 = 0x0F70;
 constexpr int kChunkRows = 128;               // nominal rows per workgroup (chunking)
 constexpr int kColAlign = 128;                // chunk and padding granularity (the widest tile)
 
@@ -359,6 +372,17 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     constexpr int NT = W * 64;
     constexpr bool kApplyAny = (MODE == kApply || MODE == kApplySym);
     constexpr bool kSymA = (MODE == kApplySym);
+    // kApplySym swaps the operands' roles (rows as A, columns as B), so lane
+    // (m, g) ends with rows 16 rb + 4 g + r and tile column 16 q + m: a
+    // column's sum over the wave's rows is in-lane over (rb, r) plus one
+    // sum over the four lane groups, and the row sums stay spread over the
+    // 16 lanes m until the end
+    constexpr bool kSwap = kSymA;
+    constexpr int kRV = kSwap ? 4 : 1;           // row values per row block
+    // kSwap up to 64 coordinates: one block at a time (its chain, then its
+    // epilogue); otherwise the next block's chain is issued before the
+    // current block's epilogue
+    constexpr bool kSeq = kSwap && NCH <= 2;
     constexpr int64_t kGroupRows = (int64_t)W * 16 * RB;
     constexpr int kSlots = NCH * 8;              // (chunk, part, lane group)
     constexpr int kQ = TC / 16;                  // 16-column blocks per tile
@@ -407,8 +431,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     }
     // B operands: this lane's rows, hi and lo of every chunk
     half8 bh[RB][NCH], bl[RB][NCH];
-    float cni[RB], mri[RB], rs[RB];
-    __shared__ double vrow[kSymA ? kGroupRows : 1];
+    float cni[RB][kRV], mri[RB][kRV], rs[RB];
+    double vi[kSwap ? RB : 1][kRV];              // kSwap: v of the lane's rows
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int64_t i = wrow0 + 16 * rb + m;
@@ -418,8 +442,19 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
             bh[rb][ch] = xh[((int64_t)(ch * 2 + 0) * 4 + g) * np + ic];
             bl[rb][ch] = xh[((int64_t)(ch * 2 + 1) * 4 + g) * np + ic];
         }
-        cni[rb] = cn[ic];
-        mri[rb] = mr[ic];
+        if (kSwap) {
+#pragma unroll
+            for (int r = 0; r < kRV; ++r) {
+                const int64_t i2 = wrow0 + 16 * rb + 4 * g + r;
+                const int64_t ic2 = i2 < n ? i2 : n - 1;
+                cni[rb][r] = cn[ic2];
+                mri[rb][r] = mr[ic2];
+                vi[rb % (kSwap ? RB : 1)][r] = (i2 < n) ? (v != nullptr ? v[i2] : 1.0) : 0.0;
+            }
+        } else {
+            cni[rb][0] = cn[ic];
+            mri[rb][0] = mr[ic];
+        }
         rs[rb] = 0.0f;
 
         if (MODE == kStoreW) {
@@ -431,17 +466,32 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
     // staging: piece f = slot * TC + col (tiles start at multiples of TC,
     // chunks and row groups at multiples of kColAlign, and np is one too,
     // so every tile ends at or before np and every load is in bounds)
+    // In the symmetric product the operand pieces go from memory straight
+    // into LDS (a wave's 64 pieces are 1 KB of consecutive LDS; kPieces is
+    // a multiple of 256, so whether a wave has a piece is uniform over it),
+    // which frees the staging registers for its row values; the other
+    // sweeps stage them in registers (measured: as fast or faster there,
+    // and the sweeps that write A or W would otherwise wait for their
+    // stores at every tile).  The column values go through registers.
     constexpr int kPieces = kSlots * TC;
     constexpr int kPer = (kPieces + NT - 1) / NT;
-    half8 stage[kPer];
+    static_assert(kPieces % kWave == 0, "whole waves of pieces");
+    constexpr bool kDirect = kSymA;
+    half8 stage[kDirect ? 1 : kPer];
     float gstage = 0.0f, sstage = 0.0f;
     double vstage = 0.0;
-    auto fetch = [&](int64_t jt) {
+    auto fetch = [&](int64_t jt, int buf) {
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
             const int f = threadIdx.x + u * NT;
-            if (kPieces % NT == 0 || f < kPieces)
-                stage[u] = xh[(int64_t)(f / TC) * np + jt + (f % TC)];
+            if (!kDirect && (kPieces % NT == 0 || f < kPieces))
+                stage[u % (kDirect ? 1 : kPer)] = xh[(int64_t)(f / TC) * np + jt + (f % TC)];
+            if (kDirect && (kPieces % NT == 0 || f < kPieces)) {
+                const int fw = f - lane;                 // the wave's first piece
+                __builtin_amdgcn_global_load_lds(
+                    (const void *)(xh + (int64_t)(f / TC) * np + jt + (f % TC)),
+                    (__attribute__((address_space(3))) void *)(&xs[buf][fw]), 16, 0, 0);
+            }
         }
         if (threadIdx.x < TC) {
             gstage = gam[jt + threadIdx.x];
@@ -453,11 +503,16 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
     };
     auto commit = [&](int buf) {
+        if (kDirect) {
+            // the pieces' loads into LDS complete before the barrier that follows
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        } else {
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int f = threadIdx.x + u * NT;
-            if (kPieces % NT == 0 || f < kPieces)
-                xs[buf][f] = stage[u];
+            for (int u = 0; u < kPer; ++u) {
+                const int f = threadIdx.x + u * NT;
+                if (kPieces % NT == 0 || f < kPieces)
+                    xs[buf][f] = stage[u % (kDirect ? 1 : kPer)];
+            }
         }
         if (threadIdx.x < TC) {
             gs[buf][threadIdx.x] = gstage;
@@ -467,17 +522,15 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
     };
 
-    // two float64 accumulators per row block (even and odd q), added at the end
-    double acc[RB][2];
+    // two float64 accumulators per row block (even and odd q), added at the
+    // end; kSwap: one per row of the lane (rb, r)
+    constexpr int kAcc = kSwap ? 4 : 2;
+    double acc[RB][kAcc];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
-        acc[rb][0] = acc[rb][1] = 0.0;
-    if (kSymA) {
-        // v of the workgroup's rows for the column sums (read after the
-        // barrier that follows the first staged tile)
-        for (int t = threadIdx.x; t < kGroupRows; t += NT)
-            vrow[t] = (grow0 + t < n) ? (v != nullptr ? v[grow0 + t] : 1.0) : 0.0;
-    }
+#pragma unroll
+        for (int u = 0; u < kAcc; ++u)
+            acc[rb][u] = 0.0;
 
     auto tile = [&](int buf, int64_t jt, auto masked, auto offdiag) {
         constexpr bool kMask = decltype(masked)::value;
@@ -493,126 +546,145 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
                 const half8 al = xs[buf][((ch * 2 + 1) * 4 + g) * TC + 16 * q + m];
                 // the row blocks' chains are independent: interleaved, no
                 // product waits for the one before it
+                // (the operands' layouts per lane coincide: swapping them
+                // transposes the 16 x 16 result)
+                auto mm = [&](const half8 &col, const half8 &row, const floatx4 &acc4) {
+                    return kSwap ? __builtin_amdgcn_mfma_f32_16x16x32_f16(row, col, acc4, 0, 0, 0)
+                                 : __builtin_amdgcn_mfma_f32_16x16x32_f16(col, row, acc4, 0, 0, 0);
+                };
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
-                    cc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[rb][ch], cc[rb],
-                                                                    0, 0, 0);
+                    cc[rb] = mm(ah, bh[rb][ch], cc[rb]);
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
-                    cc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh[rb][ch], cc[rb],
-                                                                    0, 0, 0);
+                    cc[rb] = mm(al, bh[rb][ch], cc[rb]);
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
-                    cc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[rb][ch], cc[rb],
-                                                                    0, 0, 0);
+                    cc[rb] = mm(ah, bl[rb][ch], cc[rb]);
             }
         };
         // ... and its epilogue
-        auto epi = [&](int q, const floatx4 (&cc)[RB]) {
-            double cq[4] = {0.0, 0.0, 0.0, 0.0};     // kOff: column sums
-            const floatx4 gj = *reinterpret_cast<const floatx4 *>(&gs[buf][16 * q + 4 * g]);
-            const floatx4 sj = *reinterpret_cast<const floatx4 *>(&ss[buf][16 * q + 4 * g]);
+        auto epi_swap = [&](int q, const floatx4 (&cc)[RB]) {
+            // lane (m, g): tile column 16 q + m, rows 16 rb + 4 g + r
+            const int jl = 16 * q + m;
+            const float gj = gs[buf][jl], sj = ss[buf][jl];
+            const double vj = vs[buf][jl];
+            // kMask: j == i  <=>  (jt - wrow0) + jl - 4 g == 16 rb + r, in
+            // 32 bits (the offset clamped far outside the tile's range)
+            int key = 0;
+            bool colbad = false;
+            if (kMask) {
+                const int64_t dj = jt - wrow0;
+                const int dk = (int)(dj < -(1 << 20) ? -(1 << 20) : (dj > (1 << 20) ? (1 << 20) : dj));
+                key = dk + jl - 4 * g;
+                colbad = (int64_t)jl >= c1 - jt;     // j >= c1
+            }
+            double cq = 0.0;                         // kOff: the column's sum
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) {
-                const int64_t i = wrow0 + 16 * rb + m;
-                float a[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    a[r] = __builtin_amdgcn_fmed3f(
-                        exp2_fast(-fmaf(fmaf(cc[rb][r], mri[rb], gj[r]), sj[r], cni[rb])),
+                for (int r = 0; r < 4; ++r) {
+                    float a = __builtin_amdgcn_fmed3f(
+                        exp2_fast(-fmaf(fmaf(cc[rb][r], mri[rb][r % kRV], gj), sj,
+                                        cni[rb][r % kRV])),
                         0.0f, 1.0f);
-                const int64_t j0 = jt + 16 * q + 4 * g;    // this lane's columns
-                if (kMask) {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        if (j0 + r == i || j0 + r >= c1)
-                            a[r] = 0.0f;
-                }
-                if (kWrites) {
-                    float *ow = ot[wave] + m * kOutStride + 16 * q + 4 * g;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        ow[r] = (MODE == kStoreW) ? a[r] * rs[rb] : a[r];
-                }
-                if (MODE == kStore || MODE == kDegree) {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        acc[rb][q & 1] += (double)a[r];
-                } else if (kApplyAny) {
-                    const double *vp = vs[buf] + 16 * q + 4 * g;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        acc[rb][kSymA ? 0 : (q & 1)] =
-                            fma((double)a[r], vp[r], acc[rb][kSymA ? 0 : (q & 1)]);
-                }
-                if (kOff) {
-                    const double vi = vrow[wave * 16 * RB + 16 * rb + m];
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        cq[r] = fma((double)a[r], vi, cq[r]);
+                    if (kMask && (key == 16 * rb + r || colbad))
+                        a = 0.0f;
+                    acc[rb][r % kAcc] = fma((double)a, vj, acc[rb][r % kAcc]);
+                    if (kOff)
+                        cq = fma((double)a, vi[rb % (kSwap ? RB : 1)][r % kRV], cq);
                 }
             }
             if (kOff) {
-                // column 16 q + 4 g + r over the wave's 16 RB rows: reduce-
-                // scatter over the 16 lanes of a lane group (m = 8, 4), then
-                // add the 4 lanes that share the column (m = 2, 1); lane m
-                // ends with r = 2 b3 + b2 (b = the bits of m).  The lane
-                // exchanges are data-parallel moves (a row rotation for
-                // m = 8, a swizzle for m = 4, quad permutations for m = 2,
-                // 1) on the two halves of the float64, not LDS permutes.
-                auto xch = [&](double x, int kind) {
+                // add the four lane groups (rows 4 g + r): swap the upper and
+                // lower 32 lanes, then odd and even rows of 16 lanes, on the
+                // two halves of the float64; every lane ends with the same
+                // sum (each addition takes the lower group's value first)
+                auto sumx = [&](double x, bool half32) {
                     const long long b = __double_as_longlong(x);
-                    int lo = (int)(b & 0xffffffffll), hi = (int)(b >> 32);
-                    if (kind == 8) {
-                        lo = __builtin_amdgcn_mov_dpp(lo, 0x128, 0xf, 0xf, false);
-                        hi = __builtin_amdgcn_mov_dpp(hi, 0x128, 0xf, 0xf, false);
-                    } else if (kind == 4) {
-                        lo = __builtin_amdgcn_ds_swizzle(lo, 0x101f);
-                        hi = __builtin_amdgcn_ds_swizzle(hi, 0x101f);
-                    } else if (kind == 2) {
-                        lo = __builtin_amdgcn_mov_dpp(lo, 0x4e, 0xf, 0xf, false);
-                        hi = __builtin_amdgcn_mov_dpp(hi, 0x4e, 0xf, 0xf, false);
+                    const unsigned lo = (unsigned)(b & 0xffffffffll);
+                    const unsigned hi = (unsigned)((unsigned long long)b >> 32);
+                    unsigned l0, l1, h0, h1;
+                    if (half32) {
+                        const auto pl = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+                        const auto ph = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+                        l0 = pl[0]; l1 = pl[1]; h0 = ph[0]; h1 = ph[1];
                     } else {
-                        lo = __builtin_amdgcn_mov_dpp(lo, 0xb1, 0xf, 0xf, false);
-                        hi = __builtin_amdgcn_mov_dpp(hi, 0xb1, 0xf, 0xf, false);
+                        const auto pl = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+                        const auto ph = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+                        l0 = pl[0]; l1 = pl[1]; h0 = ph[0]; h1 = ph[1];
                     }
-                    return __longlong_as_double(((long long)(unsigned)hi << 32) |
-                                                (long long)(unsigned)lo);
+                    const double x0 = __longlong_as_double((long long)(((unsigned long long)h0 << 32) | l0));
+                    const double x1 = __longlong_as_double((long long)(((unsigned long long)h1 << 32) | l1));
+                    return x0 + x1;
                 };
-                {
-                    const bool up = (m & 8) != 0;
+                cq = sumx(cq, true);
+                cq = sumx(cq, false);
+                cred[buf][wave][jl] = cq;
+            }
+        };
+        auto epi = [&](int q, const floatx4 (&cc)[RB]) {
+            if constexpr (kSwap) {
+                epi_swap(q, cc);
+            } else {
+                const floatx4 gj = *reinterpret_cast<const floatx4 *>(&gs[buf][16 * q + 4 * g]);
+                const floatx4 sj = *reinterpret_cast<const floatx4 *>(&ss[buf][16 * q + 4 * g]);
 #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const double send = up ? cq[h] : cq[h + 2];
-                        const double keep = up ? cq[h + 2] : cq[h];
-                        cq[h] = keep + xch(send, 8);
+                for (int rb = 0; rb < RB; ++rb) {
+                    const int64_t i = wrow0 + 16 * rb + m;
+                    float a[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        a[r] = __builtin_amdgcn_fmed3f(
+                            exp2_fast(-fmaf(fmaf(cc[rb][r], mri[rb][0], gj[r]), sj[r],
+                                            cni[rb][0])),
+                            0.0f, 1.0f);
+                    const int64_t j0 = jt + 16 * q + 4 * g;    // this lane's columns
+                    if (kMask) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (j0 + r == i || j0 + r >= c1)
+                                a[r] = 0.0f;
+                    }
+                    if (kWrites) {
+                        float *ow = ot[wave] + m * kOutStride + 16 * q + 4 * g;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            ow[r] = (MODE == kStoreW) ? a[r] * rs[rb] : a[r];
+                    }
+                    if (MODE == kStore || MODE == kDegree) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            acc[rb][q & 1] += (double)a[r];
+                    } else if (kApplyAny) {
+                        const double *vp = vs[buf] + 16 * q + 4 * g;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            acc[rb][q & 1] = fma((double)a[r], vp[r], acc[rb][q & 1]);
                     }
                 }
-                {
-                    const bool up = (m & 4) != 0;
-                    const double send = up ? cq[0] : cq[1];
-                    const double keep = up ? cq[1] : cq[0];
-                    cq[0] = keep + xch(send, 4);
-                }
-                cq[0] += xch(cq[0], 2);
-                cq[0] += xch(cq[0], 1);
-                // the four lanes of a column hold the same sum (float
-                // addition commutes): all write it, so no branch splits the
-                // tile's code into blocks the scheduler cannot cross
-                cred[buf][wave][16 * q + 4 * g + 2 * ((m >> 3) & 1) + ((m >> 2) & 1)] = cq[0];
             }
         };
         floatx4 ca[RB], cb[RB];
-        chain(0, ca);
+        if constexpr (kSeq) {
+            // one block at a time: the chain, then its epilogue
 #pragma unroll
-        for (int q = 0; q < kQ; q += 2) {
-            if (q + 1 < kQ)
-                chain(q + 1, cb);
-            epi(q, ca);
-            if (q + 2 < kQ)
-                chain(q + 2, ca);
-            if (q + 1 < kQ)
-                epi(q + 1, cb);
+            for (int q = 0; q < kQ; ++q) {
+                chain(q, ca);
+                epi(q, ca);
+            }
+        } else {
+            chain(0, ca);
+#pragma unroll
+            for (int q = 0; q < kQ; q += 2) {
+                if (q + 1 < kQ)
+                    chain(q + 1, cb);
+                epi(q, ca);
+                if (q + 2 < kQ)
+                    chain(q + 2, ca);
+                if (q + 1 < kQ)
+                    epi(q + 1, cb);
+            }
         }
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
@@ -645,14 +717,14 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
 
     const int64_t ntiles = (c1 - c0 + TC - 1) / TC;
     const int64_t rlo = wrow0, rhi = wrow0 + 16 * RB;   // this wave's rows
-    fetch(c0);
+    fetch(c0, 0);
     commit(0);
     __syncthreads();
     for (int64_t t = 0; t < ntiles; ++t) {
         const int buf = (int)(t & 1);
         const int64_t jt = c0 + t * TC;
         if (t + 1 < ntiles)
-            fetch(jt + TC);                          // in flight during compute
+            fetch(jt + TC, buf ^ 1);                 // in flight during compute
         const bool diag = (rlo < jt + TC) && (jt < rhi);
         const bool tail = jt + TC > c1;
         const bool off = kSymA && jt >= grow1;
@@ -668,8 +740,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         }
         if (t + 1 < ntiles) {
             // the barrier ending the previous iteration ordered every wave's
-            // reads of buffer buf ^ 1 before this write; this one orders the
-            // write before the next tile's reads
+            // reads of buffer buf ^ 1 before this tile's loads into it; this
+            // one orders them before the next tile's reads
             commit(buf ^ 1);
             __syncthreads();
         } else if (kSymA) {
@@ -693,14 +765,30 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         return;
     double yabs = 0.0;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const int64_t i = wrow0 + 16 * rb + m;
-        double s = acc[rb][0] + acc[rb][1];
-        // the four lanes sharing a row (g = 0..3) hold disjoint columns
-        s += __shfl_xor(s, 16, kWave);
-        s += __shfl_xor(s, 32, kWave);
-        if (g != 0 || i >= n)
-            continue;
+    for (int rb = 0; rb < RB * kRV; ++rb) {
+        int64_t i;
+        double s;
+        if (kSwap) {
+            // row 16 rb + 4 g + r: the 16 lanes m of its lane group hold
+            // disjoint columns
+            const int b = rb / kRV, r = rb % kRV;
+            i = wrow0 + 16 * b + 4 * g + r;
+            s = acc[b][r % kAcc];
+            s += __shfl_xor(s, 8, kWave);
+            s += __shfl_xor(s, 4, kWave);
+            s += __shfl_xor(s, 2, kWave);
+            s += __shfl_xor(s, 1, kWave);
+            if (m != 0 || i >= n)
+                continue;
+        } else {
+            i = wrow0 + 16 * rb + m;
+            s = acc[rb][0] + acc[rb][1 % kAcc];
+            // the four lanes sharing a row (g = 0..3) hold disjoint columns
+            s += __shfl_xor(s, 16, kWave);
+            s += __shfl_xor(s, 32, kWave);
+            if (g != 0 || i >= n)
+                continue;
+        }
         if (part != nullptr) {
             // chunk partial, reduced in chunk order by chunk_reduce_kernel
             part[(int64_t)blockIdx.y * n + i] = s;
