@@ -322,10 +322,10 @@ __global__ __launch_bounds__(kThreads) void fused_sym_reduce_kernel(
 
 // Workgroup: W waves, each owning RB blocks of 16 rows; columns [c0, c1)
 // of its chunk in tiles of TC staged through double-buffered LDS while the
-// previous tile is computed.  A tile holds, per (chunk, part, lane group) slot, TC
-// consecutive half8 pieces: xs[buf][slot * TC + col].  Every staged tile
-// feeds 16 W RB rows, so the operand traffic from L2 per pair of points is
-// 4 d / (16 W RB) bytes.
+// previous tile is computed.  A tile holds, per (chunk, part, lane group)
+// slot, TC consecutive half8 pieces: xs[buf][slot * TC + col].  Every
+// staged tile feeds 16 W RB rows, so the operand traffic from L2 per pair
+// of points is 4 d / (16 W RB) bytes.
 //
 // v_mfma_f32_16x16x32_f16 operand layout (lane l, g = l / 16, m = l % 16;
 // checked on the device):
@@ -429,7 +429,8 @@ __global__ __launch_bounds__(W * 64) void affinity_mfma_kernel(
         if (c0 >= c1)
             return;                                  // uniform over the workgroup
     }
-    // B operands: this lane's rows, hi and lo of every chunk
+    // row operands (B; A in the symmetric product): this lane's rows, hi
+    // and lo of every chunk
     half8 bh[RB][NCH], bl[RB][NCH];
     float cni[RB][kRV], mri[RB][kRV], rs[RB];
     double vi[kSwap ? RB : 1][kRV];              // kSwap: v of the lane's rows
