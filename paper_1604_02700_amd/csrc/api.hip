@@ -82,9 +82,12 @@ gpic_status hip_fail(hipError_t e, const char *where)
 size_t start_ws(int64_t n) { return al(start_vector_ws(n)); }
 size_t aff_ws(int64_t n) { return al(affinity_ws(n)); }
 
+// [ctl][statistic ring][|y| partials nb][y n][delta n], and for the
+// one-launch dense update (small n) a second partials and y buffer
 size_t pi_ws(int64_t n, int64_t nb)
 {
-    return kCtlBytes + al(kRing * 8) + al((size_t)nb * 8) + 2 * al((size_t)n * 8);
+    const size_t pipe = gemv_pipe_applies(n) ? al((size_t)nb * 8) + al((size_t)n * 8) : 0;
+    return kCtlBytes + al(kRing * 8) + al((size_t)nb * 8) + 2 * al((size_t)n * 8) + pipe;
 }
 
 int64_t fused_nb_bound(int64_t n) { return (n + 7) / 8; }
@@ -227,6 +230,15 @@ struct Product {
     virtual int64_t blocks() const = 0;
     virtual hipError_t launch(const double *v, double *y, double *partial,
                               StopCtl ctl, hipStream_t s) const = 0;
+    // one launch per update (the previous iteration's tau and update, then
+    // this iteration's product), where the operator offers it
+    virtual bool pipelined() const { return false; }
+    virtual hipError_t launch_pipe(double *, double *, const double *, const double *,
+                                   double *, double *, bool, bool, double *, StopCtl,
+                                   hipStream_t) const
+    {
+        return hipErrorNotSupported;
+    }
 };
 
 struct DenseProduct : Product {
@@ -237,6 +249,15 @@ struct DenseProduct : Product {
                       hipStream_t s) const override
     {
         return launch_gemv(W, n, ldw, v, y, partial, ctl, true, s);
+    }
+    bool pipelined() const override { return gemv_pipe_applies(n); }
+    hipError_t launch_pipe(double *v, double *delta, const double *y_prev,
+                           const double *part_prev, double *y_cur, double *part_cur,
+                           bool update, bool product, double *zero_slot, StopCtl ctl,
+                           hipStream_t s) const override
+    {
+        return launch_gemv_pipe(W, n, ldw, v, delta, y_prev, part_prev, y_cur, part_cur, update,
+                                product, zero_slot, ctl, s);
     }
 };
 
@@ -373,6 +394,12 @@ gpic_status run_power_iteration(const Product &op, int64_t n,
     double *y = reinterpret_cast<double *>(w + o);
     o += al((size_t)n * 8);
     double *delta = delta_user ? delta_user : reinterpret_cast<double *>(w + o);
+    o += al((size_t)n * 8);
+    const bool pipe = op.pipelined();
+    double *partial2 = pipe ? reinterpret_cast<double *>(w + o) : nullptr;
+    if (pipe)
+        o += al((size_t)op.blocks() * 8);
+    double *y2 = pipe ? reinterpret_cast<double *>(w + o) : nullptr;
 
     res->iterations = 0;
     res->converged = 0;
@@ -389,9 +416,30 @@ gpic_status run_power_iteration(const Product &op, int64_t n,
     const int64_t T = p->max_iter;
     int64_t t = 0;
     bool stopped = false;
+    // one launch per update: launch u takes iteration u - 1's tau and update
+    // (statistic u - 1, skipped once statistic u - 2 met eps) and, for u < T,
+    // iteration u's product; the partials and y alternate between two
+    // buffers by the parity of u
+    double *pbuf[2] = {partial, partial2};
+    double *ybuf[2] = {y, y2};
+    auto launch_u = [&](int64_t u) {
+        StopCtl ctl;
+        ctl.prev_stat = (conv && u >= 2) ? ring + ((u - 2) % kRing) : nullptr;
+        ctl.cur_stat = (u >= 1) ? ring + ((u - 1) % kRing) : nullptr;
+        ctl.eps = eps;
+        ctl.err = err;
+        const bool prod = u < T;
+        return op.launch_pipe(v, delta, ybuf[(u + 1) & 1], pbuf[(u + 1) & 1], ybuf[u & 1],
+                              pbuf[u & 1], u >= 1, prod, prod ? ring + (u % kRing) : nullptr,
+                              ctl, s);
+    };
+    if (pipe && T > 0)
+        CHECK_HIP(launch_u(0), "product");
     while (t < T && !stopped) {
         const int64_t te = (t + chunk < T) ? t + chunk : T;
-        for (int64_t u = t; u < te; ++u) {
+        for (int64_t u = t; u < te && pipe; ++u)
+            CHECK_HIP(launch_u(u + 1), "update and product");
+        for (int64_t u = t; u < te && !pipe; ++u) {
             StopCtl ctl;
             ctl.prev_stat = (conv && u > 0) ? ring + ((u - 1) % kRing) : nullptr;
             ctl.cur_stat = ring + (u % kRing);

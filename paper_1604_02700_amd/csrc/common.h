@@ -181,6 +181,14 @@ hipError_t launch_gemv(const float *W, int64_t n, int64_t ldw, const double *v,
 hipError_t launch_gemv_panel(const float *W, int64_t m, int64_t n, int64_t ldw,
                              const double *v, double *y, double *partial, StopCtl ctl,
                              bool use_ctl, hipStream_t s);
+// One launch per update of the dense loop for n <= a small bound (launch u:
+// iteration u - 1's tau and update of the workgroup's rows, then iteration
+// u's product with v formed on the fly; same values as the two-launch loop)
+bool gemv_pipe_applies(int64_t n);
+hipError_t launch_gemv_pipe(const float *W, int64_t n, int64_t ldw, double *v, double *delta,
+                            const double *y_prev, const double *part_prev, double *y_cur,
+                            double *part_cur, bool update, bool product, double *zero_slot,
+                            StopCtl ctl, hipStream_t s);
 // CSR product: up to 64 entries per row on average, the staged product
 // (tiles of 256 rows, entries staged in LDS by all lanes, a thread per row
 // summing in entry order), else 16 lanes per row; spmv_partials(n, nnz)

@@ -13,7 +13,9 @@
 // are combined with an integer atomic max on the bit pattern of the
 // non-negative float64, which is order-free and therefore deterministic).
 // Up to 16,384 rows, tau and the update share one launch, in which every
-// workgroup forms tau itself in the same order (so the same bits).
+// workgroup forms tau itself in the same order (so the same bits); up to
+// 2,048 rows of a dense W, they also share it with the next product
+// (update.hip), one launch per update.
 #include "common.h"
 
 namespace gpic {

@@ -846,10 +846,14 @@ def _host_copy(W, n):
     return Wh
 
 
-@pytest.mark.parametrize("n,rows", [(1003, 12), (3000, 64), (4099, None)])
+@pytest.mark.parametrize("n,rows", [(1003, 12), (2048, None), (2049, 16), (3000, 64),
+                                    (4099, None)])
 def test_dense_host_equals_device(g, n, rows):
     """W streamed from pinned host memory in row panels gives bitwise the
-    device-resident path's v, statistics and stop update."""
+    device-resident path's v, statistics and stop update.  Up to n = 2,048
+    the device path runs one launch per update (the previous iteration's tau
+    and update fused with the next product), the host path two: the same
+    values either way."""
     import workloads
     w = workloads.make("blobs16d", n=n)
     W, deg, v0, _ = g.gpic_affinity_normalized(_t(w.X), w.sigma)
