@@ -12,7 +12,7 @@
 // ascending block order), update (grid-wide; block maxima of the statistic
 // are combined with an integer atomic max on the bit pattern of the
 // non-negative float64, which is order-free and therefore deterministic).
-// Up to 16,384 rows, tau and the update share one launch, in which every
+// Up to 65,536 rows, tau and the update share one launch, in which every
 // workgroup forms tau itself in the same order (so the same bits); up to
 // 2,048 rows of a dense W, they also share it with the next product
 // (update.hip), one launch per update.
@@ -25,7 +25,7 @@ constexpr int kThreads = 256;
 constexpr int kSpmvLanes = 16;      // lanes per CSR row
 constexpr int kSpmvRows = 32;       // rows per workgroup of the CSR product
 constexpr int kSpmvUnroll = 4;      // independent gathers in flight per lane
-constexpr int64_t kTauUpdateMaxN = 16384;   // one launch for tau and the update
+constexpr int64_t kTauUpdateMaxN = 65536;   // one launch for tau and the update
 constexpr int kStagedRows = 256;    // rows per tile of the staged CSR product
 constexpr int kStageK = 24;         // entries per thread per round of the staged product
 constexpr int kStage = kStageK * kThreads;   // entries staged in LDS per round (48 KB)
@@ -185,6 +185,27 @@ __global__ __launch_bounds__(kThreads) void spmv_staged_kernel(
         partial[tile] = t;
 }
 
+// Lane t of a 1,024-thread workgroup: the sum of partial[t], partial[t +
+// 1024], ... in that order, eight loads in flight at a time.
+__device__ __forceinline__ double lane_partial_sum(const double *__restrict__ partial,
+                                                   int64_t nb)
+{
+    double s = 0.0;
+    int64_t b = threadIdx.x;
+    for (; b + 7 * 1024 < nb; b += 8 * 1024) {
+        double x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            x[u] = partial[b + u * 1024];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            s += x[u];
+    }
+    for (; b < nb; b += 1024)
+        s += partial[b];
+    return s;
+}
+
 // tau = sum of the block partials, by one workgroup in a fixed order.
 __global__ __launch_bounds__(1024) void reduce_tau_kernel(
     const double *__restrict__ partial, int64_t nb, double *__restrict__ tau,
@@ -193,10 +214,7 @@ __global__ __launch_bounds__(1024) void reduce_tau_kernel(
     __shared__ double red[1024 / kWave];
     if (stop_reached(ctl))
         return;
-    double s = 0.0;
-    for (int64_t b = threadIdx.x; b < nb; b += 1024)
-        s += partial[b];
-    const double t = block_sum<1024>(s, red);
+    const double t = block_sum<1024>(lane_partial_sum(partial, nb), red);
     if (threadIdx.x == 0) {
         *tau = t;
         if (!(t > 0.0) || !isfinite(t))
@@ -257,10 +275,7 @@ __global__ __launch_bounds__(1024) void tau_update_kernel(
     __shared__ double red[1024 / kWave];
     if (stop_reached(ctl))
         return;
-    double s = 0.0;
-    for (int64_t b = threadIdx.x; b < nb; b += 1024)
-        s += partial[b];
-    const double t = block_sum<1024>(s, red);
+    const double t = block_sum<1024>(lane_partial_sum(partial, nb), red);
     const bool bad = !(t > 0.0) || !isfinite(t);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         *tau = t;
