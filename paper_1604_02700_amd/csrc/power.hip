@@ -223,20 +223,28 @@ __global__ __launch_bounds__(1024) void reduce_tau_kernel(
 }
 
 // v <- y / tau, delta <- |v_new - v_old|, statistic = max |delta_new - delta|.
-__global__ __launch_bounds__(kThreads) void update_kernel(
+// Few large workgroups: each adds its maximum to the statistic with one
+// same-address atomic, and those serialise (about 12 ns each), so at most
+// kUpdateBlocks of them.  At n = 2M the update kernel with 2,048
+// workgroups of 256 threads cost 292 us per update of the CSR loop, 256 of
+// 1,024 threads 278 (128-512 workgroups, 2-16 rows per step: 278-334).
+constexpr int kUpdateThreads = 1024;
+constexpr int kUpdateRows = 4;              // rows per thread per step, loads all in flight
+constexpr int64_t kUpdateBlocks = 256;
+__global__ __launch_bounds__(kUpdateThreads) void update_kernel(
     const double *__restrict__ y, const double *__restrict__ tau,
     double *__restrict__ v, double *__restrict__ delta, int64_t n, StopCtl ctl)
 {
-    __shared__ double red[kThreads / kWave];
+    __shared__ double red[kUpdateThreads / kWave];
     if (stop_reached(ctl))
         return;
     const double t = *tau;
     double s = 0.0;
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    // four rows per thread per step, their loads all in flight (the max
-    // is order-free, so the result does not depend on the grouping)
-    constexpr int U = 4;
-    for (int64_t i0 = (int64_t)blockIdx.x * kThreads + threadIdx.x; i0 < n;
+    const int64_t stride = (int64_t)gridDim.x * kUpdateThreads;
+    // kUpdateRows rows per thread per step (the max is order-free, so the
+    // result does not depend on the grouping)
+    constexpr int U = kUpdateRows;
+    for (int64_t i0 = (int64_t)blockIdx.x * kUpdateThreads + threadIdx.x; i0 < n;
          i0 += U * stride) {
         double yy[U], vv[U], dd[U];
 #pragma unroll
@@ -258,7 +266,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(
             }
         }
     }
-    const double m = block_max<kThreads>(s, red);
+    const double m = block_max<kUpdateThreads>(s, red);
     if (threadIdx.x == 0)
         atomicMax(reinterpret_cast<unsigned long long *>(ctl.cur_stat),
                   (unsigned long long)__double_as_longlong(m));
@@ -377,8 +385,10 @@ hipError_t launch_tau_update(const double *partial, int64_t nb, double *tau,
 hipError_t launch_update(const double *y, const double *tau, double *v,
                          double *delta, int64_t n, StopCtl ctl, hipStream_t s)
 {
-    hipLaunchKernelGGL(update_kernel, dim3(grid_for(n, 2048)), dim3(kThreads), 0,
-                       s, y, tau, v, delta, n, ctl);
+    int64_t b = (n + (int64_t)kUpdateThreads * kUpdateRows - 1) / ((int64_t)kUpdateThreads * kUpdateRows);
+    b = b < 1 ? 1 : (b > kUpdateBlocks ? kUpdateBlocks : b);
+    hipLaunchKernelGGL(update_kernel, dim3((unsigned)b), dim3(kUpdateThreads), 0, s, y, tau, v,
+                       delta, n, ctl);
     return hipGetLastError();
 }
 
