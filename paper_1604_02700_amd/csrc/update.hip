@@ -2,9 +2,11 @@
 // Reduction and Norm steps of Algorithm 2's loop and its stop test, with
 // the update equation of section "Power Iteration Clustering: An
 // Overview"): launch u of a run does iteration u - 1's tau and update and
-// iteration u's product y = W v.  Its product is gemv_kernel's (4 rows per
-// 512-thread workgroup, the same loads, multiply-adds and reductions), so
-// its |y| partials are gemv_blocks(n) of them, as the two-launch loop's.
+// iteration u's product y = W v.  Its product takes gemv_kernel's rows and
+// threads (4 rows per 512-thread workgroup) and its multiply-adds and
+// reductions in the same order, so its y and its gemv_blocks(n) |y|
+// partials are the two-launch loop's (up to 2,048 columns a thread has one
+// column group, so there are no loads to run ahead).
 #include "common.h"
 
 namespace gpic {
