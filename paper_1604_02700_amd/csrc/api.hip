@@ -446,14 +446,8 @@ gpic_status run_power_iteration(const Product &op, int64_t n,
             ctl.eps = eps;
             ctl.err = err;
             CHECK_HIP(op.launch(v, y, partial, ctl, s), "product");
-            if (tau_update_fused(n)) {
-                CHECK_HIP(launch_tau_update(partial, op.blocks(), tau, y, v, delta, n, ctl,
-                                            s),
-                          "tau and update");
-            } else {
-                CHECK_HIP(launch_reduce_tau(partial, op.blocks(), tau, ctl, s), "tau");
-                CHECK_HIP(launch_update(y, tau, v, delta, n, ctl, s), "update");
-            }
+            CHECK_HIP(launch_tau_update(partial, op.blocks(), tau, y, v, delta, n, ctl, s),
+                      "tau and update");
         }
         const int64_t m = te - t;
         const int64_t a = t % kRing;

@@ -199,13 +199,8 @@ hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
                        const float *val, int64_t n, int64_t nnz, const double *v,
                        double *y, double *partial, StopCtl ctl, bool use_ctl,
                        hipStream_t s);
-hipError_t launch_reduce_tau(const double *partial, int64_t nb, double *tau,
-                             StopCtl ctl, hipStream_t s);
-hipError_t launch_update(const double *y, const double *tau, double *v,
-                         double *delta, int64_t n, StopCtl ctl, hipStream_t s);
-// tau and the update in one launch (bitwise the same results); used for
-// n up to tau_update_fused's bound, where launches dominate
-bool tau_update_fused(int64_t n);
+// tau and the update in one launch (every workgroup forms tau itself in
+// one fixed order, so all hold the same bits)
 hipError_t launch_tau_update(const double *partial, int64_t nb, double *tau,
                              const double *y, double *v, double *delta, int64_t n,
                              StopCtl ctl, hipStream_t s);

@@ -7,15 +7,13 @@
 // An Overview"; the Multiply, Reduction and Norm steps of Algorithm 2's loop
 // and its stop test).
 //
-// One update is three launches on the caller's stream: product (writes y and
-// per-block partial sums of |y_i|), tau (one workgroup sums the partials in
-// ascending block order), update (grid-wide; block maxima of the statistic
-// are combined with an integer atomic max on the bit pattern of the
-// non-negative float64, which is order-free and therefore deterministic).
-// Up to 65,536 rows, tau and the update share one launch, in which every
-// workgroup forms tau itself in the same order (so the same bits); up to
-// 2,048 rows of a dense W, they also share it with the next product
-// (update.hip), one launch per update.
+// One update is two launches on the caller's stream: the product (writes y
+// and per-block partial sums of |y_i|), then tau and the update in one
+// launch (every workgroup sums the partials itself in one fixed order, so
+// all hold the same tau; block maxima of the statistic are combined with an
+// integer atomic max on the bit pattern of the non-negative float64, which
+// is order-free and therefore deterministic).  Up to 2,048 rows of a dense
+// W they share one launch with the next product (update.hip).
 #include "common.h"
 
 namespace gpic {
@@ -25,7 +23,6 @@ constexpr int kThreads = 256;
 constexpr int kSpmvLanes = 16;      // lanes per CSR row
 constexpr int kSpmvRows = 32;       // rows per workgroup of the CSR product
 constexpr int kSpmvUnroll = 4;      // independent gathers in flight per lane
-constexpr int64_t kTauUpdateMaxN = 65536;   // one launch for tau and the update
 constexpr int kStagedRows = 256;    // rows per tile of the staged CSR product
 constexpr int kStageK = 24;         // entries per thread per round of the staged product
 constexpr int kStage = kStageK * kThreads;   // entries staged in LDS per round (48 KB)
@@ -206,75 +203,20 @@ __device__ __forceinline__ double lane_partial_sum(const double *__restrict__ pa
     return s;
 }
 
-// tau = sum of the block partials, by one workgroup in a fixed order.
-__global__ __launch_bounds__(1024) void reduce_tau_kernel(
-    const double *__restrict__ partial, int64_t nb, double *__restrict__ tau,
-    StopCtl ctl)
-{
-    __shared__ double red[1024 / kWave];
-    if (stop_reached(ctl))
-        return;
-    const double t = block_sum<1024>(lane_partial_sum(partial, nb), red);
-    if (threadIdx.x == 0) {
-        *tau = t;
-        if (!(t > 0.0) || !isfinite(t))
-            *ctl.err = 1;
-    }
-}
-
-// v <- y / tau, delta <- |v_new - v_old|, statistic = max |delta_new - delta|.
-// Few large workgroups: each adds its maximum to the statistic with one
-// same-address atomic, and those serialise (about 12 ns each), so at most
-// kUpdateBlocks of them.  At n = 2M the update kernel with 2,048
-// workgroups of 256 threads cost 292 us per update of the CSR loop, 256 of
-// 1,024 threads 278 (128-512 workgroups, 2-16 rows per step: 278-334).
-constexpr int kUpdateThreads = 1024;
-constexpr int kUpdateRows = 4;              // rows per thread per step, loads all in flight
+// tau and the update in one launch: every workgroup forms tau from the
+// partials in the same fixed order (lane t of 1,024 sums partial[t],
+// partial[t + 1024], ... in that order, then the block sum: the same bits
+// everywhere), then updates its rows: v <- y / tau, delta <- |v_new -
+// v_old|, statistic = max |delta_new - delta|, kUpdateRows rows per thread
+// per step with their loads in flight (the maximum is order-free).  Each
+// workgroup adds its maximum to the statistic with one same-address
+// atomic, and those serialise (about 12 ns each), so at most kUpdateBlocks
+// workgroups: at n = 2M an update grid of 2,048 workgroups of 256 threads
+// cost 292 us per update of the CSR loop, 256 of 1,024 threads 278
+// (128-512 workgroups, 2-16 rows per step: 278-334), and tau in the same
+// launch instead of a one-workgroup launch of its own 275.
+constexpr int kUpdateRows = 4;              // rows per thread per step
 constexpr int64_t kUpdateBlocks = 256;
-__global__ __launch_bounds__(kUpdateThreads) void update_kernel(
-    const double *__restrict__ y, const double *__restrict__ tau,
-    double *__restrict__ v, double *__restrict__ delta, int64_t n, StopCtl ctl)
-{
-    __shared__ double red[kUpdateThreads / kWave];
-    if (stop_reached(ctl))
-        return;
-    const double t = *tau;
-    double s = 0.0;
-    const int64_t stride = (int64_t)gridDim.x * kUpdateThreads;
-    // kUpdateRows rows per thread per step (the max is order-free, so the
-    // result does not depend on the grouping)
-    constexpr int U = kUpdateRows;
-    for (int64_t i0 = (int64_t)blockIdx.x * kUpdateThreads + threadIdx.x; i0 < n;
-         i0 += U * stride) {
-        double yy[U], vv[U], dd[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t i = i0 + u * stride;
-            yy[u] = i < n ? y[i] : 0.0;
-            vv[u] = i < n ? v[i] : 0.0;
-            dd[u] = i < n ? delta[i] : 0.0;
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t i = i0 + u * stride;
-            if (i < n) {
-                const double vn = yy[u] / t;
-                const double dn = fabs(vn - vv[u]);
-                s = fmax(s, fabs(dn - dd[u]));
-                v[i] = vn;
-                delta[i] = dn;
-            }
-        }
-    }
-    const double m = block_max<kUpdateThreads>(s, red);
-    if (threadIdx.x == 0)
-        atomicMax(reinterpret_cast<unsigned long long *>(ctl.cur_stat),
-                  (unsigned long long)__double_as_longlong(m));
-}
-
-// Both steps in one launch for small n: every workgroup forms tau from the
-// partials exactly as reduce_tau_kernel does (same order, so the same
-// bits), then updates its rows.
 __global__ __launch_bounds__(1024) void tau_update_kernel(
     const double *__restrict__ partial, int64_t nb, double *__restrict__ tau,
     const double *__restrict__ y, double *__restrict__ v, double *__restrict__ delta,
@@ -294,12 +236,27 @@ __global__ __launch_bounds__(1024) void tau_update_kernel(
         return;                                     // uniform: t is the same everywhere
     double m = 0.0;
     const int64_t stride = (int64_t)gridDim.x * 1024;
-    for (int64_t i = (int64_t)blockIdx.x * 1024 + threadIdx.x; i < n; i += stride) {
-        const double vn = y[i] / t;
-        const double dn = fabs(vn - v[i]);
-        m = fmax(m, fabs(dn - delta[i]));
-        v[i] = vn;
-        delta[i] = dn;
+    constexpr int U = kUpdateRows;
+    for (int64_t i0 = (int64_t)blockIdx.x * 1024 + threadIdx.x; i0 < n; i0 += U * stride) {
+        double yy[U], vv[U], dd[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + u * stride;
+            yy[u] = i < n ? y[i] : 0.0;
+            vv[u] = i < n ? v[i] : 0.0;
+            dd[u] = i < n ? delta[i] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + u * stride;
+            if (i < n) {
+                const double vn = yy[u] / t;
+                const double dn = fabs(vn - vv[u]);
+                m = fmax(m, fabs(dn - dd[u]));
+                v[i] = vn;
+                delta[i] = dn;
+            }
+        }
     }
     m = block_max<1024>(m, red);
     if (threadIdx.x == 0)
@@ -363,32 +320,14 @@ hipError_t launch_spmv(const int64_t *row_ptr, const int32_t *col,
     return hipGetLastError();
 }
 
-hipError_t launch_reduce_tau(const double *partial, int64_t nb, double *tau,
-                             StopCtl ctl, hipStream_t s)
-{
-    hipLaunchKernelGGL(reduce_tau_kernel, dim3(1), dim3(1024), 0, s, partial, nb,
-                       tau, ctl);
-    return hipGetLastError();
-}
-
-bool tau_update_fused(int64_t n) { return n <= kTauUpdateMaxN; }
-
 hipError_t launch_tau_update(const double *partial, int64_t nb, double *tau,
                              const double *y, double *v, double *delta, int64_t n,
                              StopCtl ctl, hipStream_t s)
 {
-    hipLaunchKernelGGL(tau_update_kernel, dim3((unsigned)((n + 1023) / 1024)), dim3(1024),
-                       0, s, partial, nb, tau, y, v, delta, n, ctl);
-    return hipGetLastError();
-}
-
-hipError_t launch_update(const double *y, const double *tau, double *v,
-                         double *delta, int64_t n, StopCtl ctl, hipStream_t s)
-{
-    int64_t b = (n + (int64_t)kUpdateThreads * kUpdateRows - 1) / ((int64_t)kUpdateThreads * kUpdateRows);
+    int64_t b = (n + 1023) / 1024;
     b = b < 1 ? 1 : (b > kUpdateBlocks ? kUpdateBlocks : b);
-    hipLaunchKernelGGL(update_kernel, dim3((unsigned)b), dim3(kUpdateThreads), 0, s, y, tau, v,
-                       delta, n, ctl);
+    hipLaunchKernelGGL(tau_update_kernel, dim3((unsigned)b), dim3(1024), 0, s, partial, nb, tau,
+                       y, v, delta, n, ctl);
     return hipGetLastError();
 }
 
