@@ -240,7 +240,7 @@ int64_t csr_blocked_partials(int64_t n);
 // Builds the copy in ws; synchronises.  *usable_host = 0 (nothing built)
 // when a row's columns are not ascending, fewer than a quarter of the
 // entries lie more than 2^17 columns from the diagonal, or a block holds
-// >= 2^31 entries.
+// >= 2^30 entries.
 hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
                              const float *val, int64_t n, int64_t nnz, void *ws,
                              CsrBlocked *out, hipStream_t s, int *usable_host);

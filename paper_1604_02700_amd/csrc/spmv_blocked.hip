@@ -15,7 +15,8 @@
 // LDS before a thread per row adds them (spmv_blocked_staged_kernel).
 //
 // The copy needs every row's columns in ascending order (checked on the
-// device) and at most 32 blocks (n <= 2^23), and it is made only when at
+// device), at most 32 blocks (n <= 2^23) and fewer than 2^30 entries in
+// each block (their positions are int32), and it is made only when at
 // least a quarter of the entries lie more than 2^17 columns from the
 // diagonal (a numbering with locality already suits the row-wise kernel,
 // which is used otherwise).  Results differ from the row-wise kernel only in the order of
@@ -32,6 +33,9 @@ constexpr int kLanes = 16;               // lanes per row in the copy
 constexpr int kUnroll = 4;               // gathers in flight per lane
 constexpr int kScanTile = 4096;          // elements per scan tile (16 per thread)
 constexpr int64_t kFar = (int64_t)1 << 17;   // "far" from the diagonal
+// entries per block below which the block's int32 positions, and the
+// products' position arithmetic past them, stay in range
+constexpr int64_t kMaxBlockEntries = (int64_t)1 << 30;
 
 int64_t al(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
@@ -51,9 +55,10 @@ __global__ __launch_bounds__(kThreads) void block_count_kernel(
         int64_t p = row_ptr[i];
         int32_t prev = -1;
         bool unsorted = false;
+        bool huge = false;
         for (int b = 0; b < nb; ++b) {
             const int64_t lim = (int64_t)(b + 1) << kColShift;
-            int32_t c = 0;
+            int64_t c = 0;
             while (p < e) {
                 const int32_t cp = col[p];
                 if ((int64_t)cp >= lim)
@@ -64,9 +69,12 @@ __global__ __launch_bounds__(kThreads) void block_count_kernel(
                 ++c;
                 ++p;
             }
-            counts[(int64_t)b * n + i] = c;
+            huge = huge || c >= kMaxBlockEntries;     // repeated columns
+            counts[(int64_t)b * n + i] = (int32_t)(c < kMaxBlockEntries ? c : 0);
         }
-        if (p < e || unsorted)        // leftover entries: columns out of order
+        // leftover entries (columns out of order), or a row segment that
+        // alone reaches the block limit: no copy
+        if (p < e || unsorted || huge)
             flags[0] = 1;
     }
 #pragma unroll
@@ -188,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void block_scatter_kernel(
 }
 
 // base[b] = first entry of block b; rpb[b][i] = offs[b][i] - base[b],
-// rpb[b][n] = entries in block b.  Flags a block of 2^31 entries or more.
+// rpb[b][n] = entries in block b.  Flags a block of 2^30 entries or more.
 __global__ __launch_bounds__(kThreads) void block_rows_kernel(
     const int64_t *__restrict__ offs, int64_t n, int nb, int64_t nnz,
     int64_t *__restrict__ base, int32_t *__restrict__ rpb, int *__restrict__ flags)
@@ -204,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void block_rows_kernel(
         base[b] = b0;
         if (b + 1 == nb)
             base[nb] = nnz;
-        if (b1 - b0 > (int64_t)INT32_MAX)
+        if (b1 - b0 >= kMaxBlockEntries)
             flags[0] = 1;
     }
     const int64_t o = (i < n) ? offs[b * n + i] : b1;
@@ -457,7 +465,7 @@ hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
             hipSuccess ||
         (e = hipStreamSynchronize(s)) != hipSuccess)
         return e;
-    if (bad)                             // a block of 2^31 entries or more
+    if (bad)                             // a block of 2^30 entries or more
         return hipSuccess;
     *usable_host = 1;
     // rows are sorted: every entry lands in its block's range

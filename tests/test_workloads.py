@@ -49,3 +49,14 @@ def test_knn_graph_small():
     M = sp.csr_matrix((val, col, rp), shape=(n, n))
     assert abs(M - M.T).max() == 0
     assert val.dtype == np.float32 and np.all(val > 0) and np.all(val <= 1)
+
+
+def test_random_kout_graph():
+    rp, col, val = workloads.random_kout_graph(300, 7, 3)
+    assert rp.dtype == np.int64 and col.dtype == np.int32 and val.dtype == np.float32
+    assert np.array_equal(rp, np.arange(301) * 7) and col.shape == val.shape == (2100,)
+    assert np.all(col >= 0) and np.all(col < 300)
+    assert np.all(np.diff(col.reshape(300, 7), axis=1) >= 0)      # rows sorted
+    assert np.all(val >= 0.1) and np.all(val < 1.0)
+    again = workloads.random_kout_graph(300, 7, 3)
+    assert all(np.array_equal(a, b) for a, b in zip((rp, col, val), again))

@@ -26,7 +26,7 @@ import numpy as np
 
 __all__ = [
     "Workload", "WORKLOADS", "make", "blobs_uniform_centres", "rings", "two_moons",
-    "blobs_dirichlet", "blobs_equal", "knn_graph", "sha256_of",
+    "blobs_dirichlet", "blobs_equal", "knn_graph", "random_kout_graph", "sha256_of",
     "split_equal", "split_dirichlet", "median_pair_distance_sigma",
 ]
 
@@ -227,6 +227,23 @@ def knn_graph(X: np.ndarray, knn: int = 32, sigma: float = 1.0,
     col = S.indices.astype(np.int32)
     val = S.data.astype(np.float32)
     return row_ptr, col, val
+
+
+def random_kout_graph(m: int, k: int, seed: int):
+    """A CSR graph of m nodes with exactly k stored entries per row.
+
+    Row i holds k columns drawn uniformly from [0, m) with replacement
+    (repeats kept, so a row's columns are non-decreasing rather than
+    strictly increasing) and sorted, with float32 weights drawn uniformly
+    from [0.1, 1).  No locality: a row's neighbours lie anywhere.  Draw
+    order: the columns row by row, then the weights.  Returns
+    (row_ptr int64 [m+1], col int32 [m k], val float32 [m k]).
+    """
+    rng = np.random.default_rng(seed)
+    col = np.sort(rng.integers(0, m, size=(m, k), dtype=np.int64), axis=1)
+    val = rng.uniform(0.1, 1.0, size=m * k).astype(np.float32)
+    row_ptr = np.arange(m + 1, dtype=np.int64) * k
+    return row_ptr, col.reshape(-1).astype(np.int32), val
 
 
 # name -> (builder, description); builders take (seed, n_override)
