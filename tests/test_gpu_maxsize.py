@@ -16,6 +16,8 @@
   oracle runs on G0 and the GPU's first copy times B must match it to
   rounding, and since every copy's rows sit in the same relative place,
   every copy must hold the same bits.
+* 1-D k-means at its documented maximum, n = 2^30 values, k = 2: the
+  split against a brute force over every split point.
 """
 import numpy as np
 import pytest
@@ -160,3 +162,89 @@ def test_csr_past_2_31_entries(g, orc, form, m, k, B):
     np.testing.assert_allclose(out.stats * B, ref.stats, rtol=1e-6, atol=1e-18)
     del rp, col, val, deg, v0, v
     torch.cuda.empty_cache()
+
+
+# --------------------------------------------------------------- k-means
+def _mixture_quantiles(n, seed):
+    """n sorted values: evenly spaced quantiles of a mixture of two
+    overlapping uniform distributions (60 % on [-3, 1], 40 % on [0, 3]),
+    each shifted by a seeded fraction of its spacing, then merged; a k = 2
+    optimum sits inside the overlap.  No sort of random values at n = 2^30."""
+    rng = np.random.default_rng(seed)
+    na = int(0.6 * n)
+    parts = []
+    for m, lo, hi in ((na, -3.0, 1.0), (n - na, 0.0, 3.0)):
+        u = np.arange(m, dtype=np.float64)
+        u += rng.uniform(0.25, 0.75)
+        u *= (hi - lo) / m
+        u += lo
+        parts.append(u)
+    v = np.concatenate(parts)
+    del parts, u
+    v.sort(kind="stable")                   # two sorted runs: a merge
+    return v
+
+
+def _split_cost(vs, s):
+    """Within-cluster sum of squares of vs[:s] and vs[s:] (sorted vs),
+    each side centred on its own mean; numpy's pairwise sums."""
+    tot = 0.0
+    for part in (vs[:s], vs[s:]):
+        tot += float(np.sum(np.square(part - part.mean())))
+    return tot
+
+
+def _best_split(vs, chunk=1 << 25):
+    """Brute force over all n - 1 split points with centred float64 prefix
+    sums (left size j: S2_j - S1_j^2 / j, the right side alike)."""
+    n = vs.size
+    u = vs - vs.mean()
+    S1 = np.cumsum(u)
+    np.square(u, out=u)
+    S2 = np.cumsum(u, out=u)
+    t1, t2 = S1[-1], S2[-1]
+    best, arg = np.inf, -1
+    for a in range(1, n, chunk):
+        e = min(n, a + chunk)
+        j = np.arange(a, e, dtype=np.float64)
+        s1, s2 = S1[a - 1:e - 1], S2[a - 1:e - 1]
+        c = s2 - s1 * s1 / j
+        c += (t2 - s2) - np.square(t1 - s1) / (n - j)
+        i = int(np.argmin(c))
+        if c[i] < best:
+            best, arg = float(c[i]), a + i
+    return arg
+
+
+def test_kmeans1d_at_2_30_values(g):
+    """The documented maximum n = 2^30, k = 2: the values in an affine
+    permutation of their sorted order, so the GPU sorts them.  Its clusters
+    must be contiguous in value, its split as good as the best of all
+    2^30 - 1 split points (both costs recomputed with pairwise sums, to
+    1e-9), its reported cost and centroids those of its own split."""
+    n = 1 << 30
+    print(f"gpu: kmeans1d n={n} k=2", flush=True)
+    vs = _mixture_quantiles(n, 21)
+    assert np.all(np.diff(vs[:: 1 << 20]) >= 0)
+    perm_a, perm_b = 0x9E3779B1, 12345             # odd: a bijection modulo 2^30
+    vsg = _t(vs)
+    idx = (torch.arange(n, dtype=torch.int64, device=DEV) * perm_a + perm_b) % n
+    v = vsg[idx]
+    del vsg, idx
+    torch.cuda.empty_cache()
+    km = g.gpic_kmeans1d(v, 2)
+    assert km.k_eff == 2
+    lab = km.labels
+    a = int((lab == 0).sum().item())
+    lo_max = float(torch.where(lab == 0, v, torch.full_like(v, -np.inf)).max().item())
+    hi_min = float(torch.where(lab == 1, v, torch.full_like(v, np.inf)).min().item())
+    assert 0 < a < n and lo_max < hi_min and lo_max == vs[a - 1] and hi_min == vs[a]
+    cent = km.centroids.cpu().numpy()
+    del v, lab, km.labels
+    torch.cuda.empty_cache()
+    b = _best_split(vs)
+    ca, cb = _split_cost(vs, a), _split_cost(vs, b)
+    print(f"  split gpu={a} brute force={b} cost {ca:.12e} vs {cb:.12e}", flush=True)
+    assert abs(ca - cb) <= 1e-9 * cb
+    assert km.cost == pytest.approx(ca, rel=1e-9)
+    np.testing.assert_allclose(cent, [vs[:a].mean(), vs[a:].mean()], rtol=1e-9)
