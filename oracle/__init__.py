@@ -83,6 +83,8 @@ def _declare(lib):
     lib.orc_affinity_cosine_rows.argtypes = [p, i64, i32, i64, i64, p]
     lib.orc_knn_graph.argtypes = [p, i64, i32, i32, f64, p, p, p]
     lib.orc_knn_graph.restype = i64
+    lib.orc_knn_rows.argtypes = [p, i64, i32, i32, f64, p, i64, p, p, p]
+    lib.orc_knn_rows.restype = i32
     lib.orc_degree_rows.argtypes = [p, i64, i32, f64, p, i64, p]
     lib.orc_degree_normalize.argtypes = [p, i64, p, p]
     lib.orc_degree_normalize.restype = i64
@@ -296,6 +298,25 @@ def knn_graph(X, k, sigma):
     if nnz < 0:
         raise ValueError("k must be in [1, n-1]")
     return rp, col[:nnz].copy(), val[:nnz].copy()
+
+
+def knn_rows(X, k, sigma, rows):
+    """The k nearest neighbours of the listed points, in order (self
+    excluded, ties to the smaller index), as the kNN graph defines them:
+    (nbr int64 [m, k], squared distances float64 [m, k], weights float32
+    [m, k])."""
+    X = _f32(X)
+    n, d = X.shape
+    r = np.ascontiguousarray(rows, dtype=np.int64)
+    m = r.shape[0]
+    nbr = np.empty((m, int(k)), dtype=np.int64)
+    d2 = np.empty((m, int(k)))
+    w = np.empty((m, int(k)), dtype=np.float32)
+    st = _L().orc_knn_rows(_ptr(X), n, d, int(k), float(np.float32(sigma)), _ptr(r), m,
+                           _ptr(nbr), _ptr(d2), _ptr(w))
+    if st != 0:
+        raise ValueError("k must be in [1, n-1] and rows in [0, n)")
+    return nbr, d2, w
 
 
 def kmeans1d(v, k, method="auto") -> KMeansResult:

@@ -35,6 +35,8 @@
  *                          input: exact k nearest neighbours, union
  *                          symmetrised, Gaussian weights (not in the paper;
  *                          the input of its method in graph form).
+ *   orc_knn_rows           the same neighbour lists and weights for listed
+ *                          points only.
  *   orc_kmeans1d           "k-means of v" (Algorithm 1, last step), read as
  *                          the exact minimum within-cluster sum of squares
  *                          partition of the scalars v_i (plain O(k n^2)
@@ -594,12 +596,35 @@ static double sq_dist(const float *X, int32_t d, int64_t i, int64_t j)
     return s;
 }
 
-/* Exact k-nearest-neighbour graph: N(i) = the k points j != i with the
- * smallest (||x_i - x_j||^2, j) (squared distance summed over coordinates
- * in order; ties to the smaller index); edge {i, j} if j in N(i) or i in
- * N(j); weight exp(-||x_i - x_j||^2 / (2 sigma^2)) in float64, rounded once
- * to float32; rows sorted by column.  row_ptr [n+1]; col and val hold up to
- * 2 n k entries.  Returns nnz, or -1 if k is not in [1, n-1]. */
+/* N(i): the k points j != i with the smallest (||x_i - x_j||^2, j), in that
+ * order (squared distance summed over coordinates in order; ties to the
+ * smaller index), into bj[0..k) with their squared distances in bd. */
+static void knn_of(const float *X, int64_t n, int32_t d, int32_t k, int64_t i, double *bd,
+                   int64_t *bj)
+{
+    int32_t m = 0;                               /* kept so far, sorted by (dist, j) */
+    for (int64_t j = 0; j < n; ++j) {
+        if (j == i)
+            continue;
+        double dj = sq_dist(X, d, i, j);
+        if (m == k && !(dj < bd[k - 1]))
+            continue;                            /* j > kept indices: ties lose */
+        int32_t p = (m < k) ? m++ : k - 1;
+        while (p > 0 && dj < bd[p - 1]) {
+            bd[p] = bd[p - 1];
+            bj[p] = bj[p - 1];
+            --p;
+        }
+        bd[p] = dj;
+        bj[p] = j;
+    }
+}
+
+/* Exact k-nearest-neighbour graph: N(i) as in knn_of; edge {i, j} if j in
+ * N(i) or i in N(j); weight exp(-||x_i - x_j||^2 / (2 sigma^2)) in float64,
+ * rounded once to float32; rows sorted by column.  row_ptr [n+1]; col and
+ * val hold up to 2 n k entries.  Returns nnz, or -1 if k is not in
+ * [1, n-1]. */
 int64_t orc_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, double sigma,
                       int64_t *row_ptr, int32_t *col, float *val)
 {
@@ -612,22 +637,7 @@ int64_t orc_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, double si
         int64_t *bj = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
 #pragma omp for schedule(static)
         for (int64_t i = 0; i < n; ++i) {
-            int32_t m = 0;                       /* kept so far, sorted by (dist, j) */
-            for (int64_t j = 0; j < n; ++j) {
-                if (j == i)
-                    continue;
-                double dj = sq_dist(X, d, i, j);
-                if (m == k && !(dj < bd[k - 1]))
-                    continue;                    /* j > kept indices: ties lose */
-                int32_t p = (m < k) ? m++ : k - 1;
-                while (p > 0 && dj < bd[p - 1]) {
-                    bd[p] = bd[p - 1];
-                    bj[p] = bj[p - 1];
-                    --p;
-                }
-                bd[p] = dj;
-                bj[p] = j;
-            }
+            knn_of(X, n, d, k, i, bd, bj);
             for (int32_t t = 0; t < k; ++t) {
                 e[(2 * i) * (int64_t)k + 2 * t].row = i;
                 e[(2 * i) * (int64_t)k + 2 * t].col = bj[t];
@@ -656,4 +666,28 @@ int64_t orc_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, double si
         row_ptr[i + 1] += row_ptr[i];
     free(e);
     return nnz;
+}
+
+/* N(i) of the listed points alone (the graph's neighbour lists one by one,
+ * for sampled checks of graphs too large to build here): for row t,
+ * nbr[t k + s] = the s-th nearest of point rows[t] as in knn_of, d2 its
+ * squared distance and w its weight exp(-d2 / (2 sigma^2)) rounded once to
+ * float32.  Returns 0, or -1 if k is not in [1, n-1] or a row is out of
+ * range. */
+int32_t orc_knn_rows(const float *X, int64_t n, int32_t d, int32_t k, double sigma,
+                     const int64_t *rows, int64_t m, int64_t *nbr, double *d2, float *w)
+{
+    if (k < 1 || (int64_t)k > n - 1)
+        return -1;
+    for (int64_t t = 0; t < m; ++t)
+        if (rows[t] < 0 || rows[t] >= n)
+            return -1;
+    const double two_sigma2 = 2.0 * sigma * sigma;
+#pragma omp parallel for schedule(dynamic)
+    for (int64_t t = 0; t < m; ++t) {
+        knn_of(X, n, d, k, rows[t], d2 + t * k, nbr + t * k);
+        for (int32_t s = 0; s < k; ++s)
+            w[t * k + s] = (float)exp(-d2[t * k + s] / two_sigma2);
+    }
+    return 0;
 }

@@ -48,6 +48,8 @@ int32_t orc_kmeans1d(const double *v, int64_t n, int32_t k, int32_t method, int3
                      double *centroids, int32_t *k_eff, double *cost_out);
 int64_t orc_knn_graph(const float *X, int64_t n, int32_t d, int32_t k, double sigma,
                       int64_t *row_ptr, int32_t *col, float *val);
+int32_t orc_knn_rows(const float *X, int64_t n, int32_t d, int32_t k, double sigma,
+                     const int64_t *rows, int64_t m, int64_t *nbr, double *d2, float *w);
 
 static int failures = 0;
 
@@ -207,6 +209,26 @@ static void run_sparse(int64_t n, int32_t d, int32_t k)
                 found |= (col[q] == (int32_t)i && val[q] == val[p]);
             EXPECT(found, "edge (%lld, %d) without its mirror", (long long)i, j);
         }
+    }
+    {                                            /* the neighbour lists alone */
+        const int64_t rows[3] = {0, n / 2, n - 1};
+        int64_t *nb = xmalloc((size_t)(3 * k) * sizeof(int64_t));
+        double *d2 = xmalloc((size_t)(3 * k) * sizeof(double));
+        float *wk = xmalloc((size_t)(3 * k) * sizeof(float));
+        EXPECT(orc_knn_rows(X, n, d, k, 1.0, rows, 3, nb, d2, wk) == 0, "knn rows");
+        for (int t = 0; t < 3; ++t)
+            for (int32_t s = 0; s < k; ++s) {
+                int found = 0;                   /* each neighbour is in the row */
+                for (int64_t q = rp[rows[t]]; q < rp[rows[t] + 1]; ++q)
+                    found |= (col[q] == (int32_t)nb[t * k + s] && val[q] == wk[t * k + s]);
+                EXPECT(found, "neighbour %d of row %lld missing", s, (long long)rows[t]);
+                EXPECT(s == 0 || d2[t * k + s - 1] <= d2[t * k + s], "neighbours not ordered");
+            }
+        const int64_t bad[1] = {n};
+        EXPECT(orc_knn_rows(X, n, d, k, 1.0, bad, 1, nb, d2, wk) == -1, "row out of range");
+        free(wk);
+        free(d2);
+        free(nb);
     }
     double *a = xmalloc((size_t)nnz * sizeof(double));
     double *w = xmalloc((size_t)nnz * sizeof(double));

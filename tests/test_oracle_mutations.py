@@ -57,6 +57,7 @@ def _pin_suite(orc):
         ("brute_gauss", lambda: pins.test_brute_force_fifty_digits(orc, 8, 2, "gauss")),
         ("knn_ckdtree", lambda: pins.test_knn_graph_matches_ckdtree(orc)),
         ("knn_ties", lambda: pins.test_knn_graph_ties_and_structure(orc)),
+        ("knn_rows", lambda: pins.test_knn_rows_matches_ckdtree(orc)),
         ("brute_cosine", lambda: pins.test_brute_force_fifty_digits(orc, 7, 3, "cosine")),
         ("row_sums_v0", lambda: pins.test_rows_of_W_sum_to_one_and_v0(orc)),
         ("zero_degree", lambda: pins.test_zero_degree_row_is_counted(orc)),

@@ -507,6 +507,32 @@ def test_knn_graph_matches_ckdtree(orc):
     np.testing.assert_allclose(val, S.data.astype(np.float32), rtol=2e-7)
 
 
+def test_knn_rows_matches_ckdtree(orc):
+    """The neighbour lists of listed points alone equal scipy's k-d tree
+    query (a library kNN routine): same points in the same order, squared
+    distances to rounding, Gaussian weights; and on an integer lattice the
+    ties go to the smaller index (corner point 0: 1 and 12 at distance 1,
+    13 at sqrt 2, then 2 before 24 at distance 2)."""
+    from scipy.spatial import cKDTree
+    n, d, k, sigma = 2000, 8, 12, np.float32(0.9)
+    X = _pts(n, d, 73)
+    rows = np.array([0, 1, 777, 1998, 1999], dtype=np.int64)
+    nbr, d2, w = orc.knn_rows(X, k, sigma, rows)
+    P = X.astype(np.float64)
+    dist, nb = cKDTree(P).query(P[rows], k=k + 1)
+    assert np.all(nb[:, 0] == rows)
+    assert np.array_equal(nbr, nb[:, 1:])
+    np.testing.assert_allclose(d2, dist[:, 1:] ** 2, rtol=1e-12)
+    np.testing.assert_allclose(w, np.exp(-dist[:, 1:] ** 2 / (2.0 * float(sigma) ** 2)),
+                               rtol=2e-7)
+    g = np.arange(12, dtype=np.float32)
+    L = np.stack(np.meshgrid(g, g), axis=-1).reshape(-1, 2)
+    nbr, d2, _ = orc.knn_rows(L, 4, 1.0, [0])
+    assert list(nbr[0]) == [1, 12, 13, 2] and list(d2[0]) == [1.0, 1.0, 2.0, 4.0]
+    with pytest.raises(ValueError):
+        orc.knn_rows(L, 4, 1.0, [144])
+
+
 def test_knn_graph_ties_and_structure(orc):
     """Integer lattice points (many exact distance ties): ties go to the
     smaller index; the graph is symmetric with equal weights both ways, has
