@@ -16,6 +16,9 @@
   oracle runs on G0 and the GPU's first copy times B must match it to
   rounding, and since every copy's rows sit in the same relative place,
   every copy must hold the same bits.
+* The kNN graph builder with room for more than 2^31 entries (n = 17M,
+  k = 64): structure and mirror symmetry over the whole graph, sampled rows
+  against the oracle's neighbour lists.
 * 1-D k-means at its documented maximum, n = 2^30 values, k = 2: the
   split against a brute force over every split point.
 """
@@ -161,6 +164,88 @@ def test_csr_past_2_31_entries(g, orc, form, m, k, B):
     np.testing.assert_allclose(v[:m].cpu().numpy() * B, ref.v, rtol=1e-9)
     np.testing.assert_allclose(out.stats * B, ref.stats, rtol=1e-6, atol=1e-18)
     del rp, col, val, deg, v0, v
+    torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------- kNN graph
+def _mix64(x):
+    """A 64-bit mixing step on int64 tensors (wrapping arithmetic)."""
+    x = x ^ (x >> 31)
+    x = x * 0x7FB5D329728EA185
+    x = x ^ (x >> 27)
+    x = x * 0x2545F4914F6CDD1D
+    return x ^ (x >> 33)
+
+
+def _mirror_fingerprints(rp, col, val, chunk=1 << 27):
+    """Wrapping sums of a hash of (min(i, j), max(i, j), weight bits) over
+    the stored entries with i < j and over those with i > j: equal when
+    every edge is stored both ways with the same weight."""
+    nnz = col.numel()
+    lo_sum = torch.zeros((), dtype=torch.int64, device=DEV)
+    hi_sum = torch.zeros((), dtype=torch.int64, device=DEV)
+    bounds = rp[1:].contiguous()
+    for s in range(0, nnz, chunk):
+        p = torch.arange(s, min(nnz, s + chunk), dtype=torch.int64, device=DEV)
+        r = torch.searchsorted(bounds, p, right=True)
+        c = col[s:s + p.numel()].to(torch.int64)
+        wb = val[s:s + p.numel()].view(torch.int32).to(torch.int64)
+        h = _mix64(torch.minimum(r, c) * 0x100000001B3 + torch.maximum(r, c)
+                   + (wb << 40))
+        lo_sum += torch.where(r < c, h, torch.zeros_like(h)).sum()
+        hi_sum += torch.where(r > c, h, torch.zeros_like(h)).sum()
+        assert not bool((r == c).any())                      # no self loops
+    return int(lo_sum.item()), int(hi_sum.item())
+
+
+def test_knn_graph_past_2_31_entries(g, orc):
+    """n = 17,000,000 8-D points, k = 64: room for 2 n k > 2^31 entries.
+    Whole graph: rows sorted, at least k entries each, no self loops, every
+    edge stored both ways with one weight (hash fingerprints).  Sampled
+    rows against the oracle's neighbour lists: each of a row's k nearest
+    is in the row with its weight, and a sampled entry that is not among
+    them has the row's point among its own k nearest."""
+    import workloads
+    n, k, sigma = 17_000_000, 64, 1.0
+    assert 2 * n * k > 1 << 31 and 2 * n * k < 1 << 32
+    X, _ = workloads.blobs_equal(n=n, d=8, k=50, seed=31)
+    print(f"gpu: knn graph n={n} d=8 k={k}", flush=True)
+    rp, col, val = g.gpic_knn_graph(_t(X), k, sigma)
+    torch.cuda.empty_cache()
+    nnz = col.numel()
+    print(f"  nnz={nnz}", flush=True)
+    assert int(rp[0].item()) == 0 and int(rp[-1].item()) == nnz
+    assert n * k <= nnz <= 2 * n * k
+    assert int((rp[1:] - rp[:-1]).min().item()) >= k
+    starts = torch.zeros(nnz, dtype=torch.bool, device=DEV)
+    starts[rp[:-1]] = True
+    up = col[1:] > col[:-1]
+    assert bool((up | starts[1:]).all())                     # rows strictly sorted
+    del starts, up
+    lo, hi = _mirror_fingerprints(rp, col, val)
+    assert lo == hi
+    rows = np.concatenate([[0, 1, n // 2, n - 1],
+                           np.random.default_rng(4).choice(n, 4, replace=False)])
+    nbr, d2, w = orc.knn_rows(X, k, sigma, rows)
+    rph = rp.cpu().numpy()
+    extra = []
+    for t, i in enumerate(rows):
+        c = col[rph[i]:rph[i + 1]].cpu().numpy()
+        v = val[rph[i]:rph[i + 1]].cpu().numpy()
+        pos = np.searchsorted(c, nbr[t])
+        assert np.all(pos < c.size) and np.array_equal(c[pos], nbr[t])
+        assert np.all(np.abs(v[pos] - w[t]) <= np.spacing(w[t]))
+        rest = np.setdiff1d(c, nbr[t])
+        for j in rest[[0, rest.size // 2, -1]] if rest.size else []:
+            extra.append((int(i), int(j), float(v[np.searchsorted(c, j)])))
+    if extra:
+        nb2, _, w2 = orc.knn_rows(X, k, sigma, [j for _, j, _ in extra])
+        for (i, j, wij), nj, wj in zip(extra, nb2, w2):
+            hit = np.nonzero(nj == i)[0]
+            assert hit.size == 1, f"entry ({i}, {j}) without i among j's nearest"
+            assert abs(wij - wj[hit[0]]) <= np.spacing(wj[hit[0]])
+    print(f"  sampled rows {len(rows)}, reverse entries checked {len(extra)}", flush=True)
+    del rp, col, val
     torch.cuda.empty_cache()
 
 
