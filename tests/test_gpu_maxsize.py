@@ -6,6 +6,9 @@
   invariants over a few updates.
 * Symmetric storage of the same points (entries past 2^31 in the packed
   tiles): sampled rows of one product against the oracle.
+* The fused operator at the largest n that evaluates each pair once
+  (2^19, d = 64): W 1 = 1 over the whole vector, sampled rows against the
+  oracle.
 * CSR graphs with more than 2^31 stored entries, one for each product
   form (staged: up to 64 entries per row on average; row-wise: more;
   column-blocked: sorted rows, no locality, n <= 2^23).  Each graph is B
@@ -108,6 +111,39 @@ def test_sym_past_2_31_entries(g, orc, big_blobs):
     yr = orc.matvec_onthefly_rows(w.X, w.sigma, dfull, vr, rows)
     np.testing.assert_allclose(y[rows], yr, rtol=1e-5)
     del As
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------- fused operator
+def test_fused_pair_once_at_2_19(g, orc):
+    """The fused operator's largest size that evaluates each pair once,
+    n = 2^19 points of 64 dimensions (4.3 GB of column partial sums):
+    sampled degrees and one product against the oracle's rows, and over
+    the whole vector W 1 = 1 to 1e-12 (the degrees are the row sums of the
+    same symmetric A the product uses, each pair's term shared by its row
+    and its column)."""
+    import workloads
+    n = 1 << 19
+    X, _ = workloads.blobs_equal(n=n, d=64, k=20, seed=17)
+    sigma = np.float32(4.0)
+    print(f"gpu: fused pair-once n={n} d=64", flush=True)
+    Xg = _t(X)
+    deg, v0, nz = g.gpic_degree_fused(Xg, sigma)
+    ones = torch.ones(n, dtype=torch.float64, device=DEV)
+    y1 = g.gpic_matvec_fused(Xg, sigma, deg, ones).cpu().numpy()
+    np.testing.assert_allclose(y1, 1.0, rtol=1e-12)
+    rng = np.random.default_rng(6)
+    rows = np.unique(np.concatenate([[0, 1, 383, 384, n // 2, n - 385, n - 384, n - 2, n - 1],
+                                     rng.choice(n, 12, replace=False)])).astype(np.int64)
+    dr = orc.degree_rows(X, sigma, rows)
+    np.testing.assert_allclose(deg.cpu().numpy()[rows], dr, rtol=1e-4)
+    vr = rng.uniform(0.5, 1.5, size=n)
+    y = g.gpic_matvec_fused(Xg, sigma, deg, _t(vr)).cpu().numpy()
+    dfull = np.zeros(n)
+    dfull[rows] = dr
+    yr = orc.matvec_onthefly_rows(X, sigma, dfull, vr, rows)
+    np.testing.assert_allclose(y[rows], yr, rtol=1e-4)
+    del Xg, deg, v0, ones
     torch.cuda.empty_cache()
 
 
