@@ -609,7 +609,7 @@ def oracle_baseline(w, graph=None):
     th = oracle.num_threads()
     base = {"cores": th, "kind": "oracle", "host": host_info(th)}
     if w.path in ("dense", "cosine"):
-        reps = 3 if w.n <= 2000 else 1
+        reps = 3 if w.n <= 10000 else 1          # the two small configurations
         ts = []
         for _ in range(reps):
             t0 = time.perf_counter()
