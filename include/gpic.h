@@ -389,7 +389,15 @@ gpic_status gpic_power_iterate_fused(const float *X, int64_t n, int32_t d,
                                      gpic_pi_result *res, void *stream);
 
 /* The same loop over a CSR W (values already normalised by
- * gpic_degree_normalize_csr).  ws: gpic_workspace_bytes(GPIC_OP_PI_CSR, n, nnz, 0). */
+ * gpic_degree_normalize_csr).  ws: gpic_workspace_bytes(GPIC_OP_PI_CSR, n, nnz, 0).
+ * For 2^18 < n <= 2^23 the workspace also holds a column-blocked copy of W
+ * (about 8 bytes per stored entry plus per-block row offsets and sums),
+ * made once per call and used when every row's columns are ascending, at
+ * least a quarter of the entries lie more than 2^17 columns from the
+ * diagonal and each block of 2^18 columns holds fewer than 2^30 entries;
+ * the iterates then differ from the row-wise product's only in the order
+ * of the float64 sums.  Building the copy synchronises the stream once
+ * more. */
 gpic_status gpic_power_iterate_csr(const int64_t *row_ptr, const int32_t *col,
                                    const float *val, int64_t n, int64_t nnz,
                                    const gpic_pi_params *params, double *v,
