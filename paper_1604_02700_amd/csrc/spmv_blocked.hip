@@ -39,49 +39,95 @@ constexpr int64_t kMaxBlockEntries = (int64_t)1 << 30;
 
 int64_t al(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
-// Per row: entries per column block (counts[b * n + i]), the order check
-// (flags[0]) and the number of entries more than 2^17 columns away from
-// the diagonal (far[0], an integer sum: a row-wise product is cache
-// friendly when few entries are far).
-__global__ __launch_bounds__(kThreads) void block_count_kernel(
+// Whether the copy is worth making, before any per-block work: the order
+// check (flags[0]: a row's columns not ascending) and the number of
+// entries more than 2^17 columns from the diagonal (far[0], an integer
+// sum: a row-wise product is cache friendly when few entries are far).
+// kLanes lanes per row read its columns coalesced; grid-stride over rows,
+// one count per workgroup into part[], added up by far_total_kernel (no
+// same-address atomics: they serialise).
+constexpr int kScanBlocks = 8192;
+__global__ __launch_bounds__(kThreads) void far_scan_kernel(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, int64_t n,
-    int nb, int32_t *__restrict__ counts, int *__restrict__ flags,
-    unsigned long long *__restrict__ far)
+    int *__restrict__ flags, unsigned long long *__restrict__ part)
 {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    __shared__ unsigned long long red[kThreads / kWave];
+    const int sl = threadIdx.x % kLanes;
+    constexpr int rows_per_block = kThreads / kLanes;
     unsigned long long nfar = 0;
-    if (i < n) {
-        const int64_t e = row_ptr[i + 1];
-        int64_t p = row_ptr[i];
-        int32_t prev = -1;
-        bool unsorted = false;
-        bool huge = false;
-        for (int b = 0; b < nb; ++b) {
-            const int64_t lim = (int64_t)(b + 1) << kColShift;
-            int64_t c = 0;
-            while (p < e) {
-                const int32_t cp = col[p];
-                if ((int64_t)cp >= lim)
-                    break;
-                unsorted = unsorted || cp < prev;
-                nfar += ((int64_t)cp - i > kFar || i - (int64_t)cp > kFar) ? 1u : 0u;
-                prev = cp;
-                ++c;
-                ++p;
-            }
-            huge = huge || c >= kMaxBlockEntries;     // repeated columns
-            counts[(int64_t)b * n + i] = (int32_t)(c < kMaxBlockEntries ? c : 0);
+    bool unsorted = false;
+    for (int64_t i = (int64_t)blockIdx.x * rows_per_block + threadIdx.x / kLanes; i < n;
+         i += (int64_t)gridDim.x * rows_per_block) {
+        const int64_t b = row_ptr[i], e = row_ptr[i + 1];
+        for (int64_t p = b + sl; p < e; p += kLanes) {
+            const int64_t c = col[p];
+            nfar += (c - i > kFar || i - c > kFar) ? 1u : 0u;
+            unsorted = unsorted || (p > b && col[p - 1] > c);
         }
-        // leftover entries (columns out of order), or a row segment that
-        // alone reaches the block limit: no copy
-        if (p < e || unsorted || huge)
-            flags[0] = 1;
     }
+    if (unsorted)
+        flags[0] = 1;
 #pragma unroll
     for (int o = kWave / 2; o > 0; o >>= 1)
         nfar += __shfl_xor(nfar, o, kWave);
-    if ((threadIdx.x % kWave) == 0 && nfar != 0)
-        atomicAdd(far, nfar);
+    if ((threadIdx.x % kWave) == 0)
+        red[threadIdx.x / kWave] = nfar;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t = 0;
+        for (int w = 0; w < kThreads / kWave; ++w)
+            t += red[w];
+        part[blockIdx.x] = t;
+    }
+}
+
+// far[0] = the sum of the m workgroup counts (one workgroup).
+__global__ __launch_bounds__(kThreads) void far_total_kernel(
+    const unsigned long long *__restrict__ part, int m, unsigned long long *__restrict__ far)
+{
+    __shared__ unsigned long long red[kThreads / kWave];
+    unsigned long long t = 0;
+    for (int b = threadIdx.x; b < m; b += kThreads)
+        t += part[b];
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1)
+        t += __shfl_xor(t, o, kWave);
+    if ((threadIdx.x % kWave) == 0)
+        red[threadIdx.x / kWave] = t;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long u = 0;
+        for (int w = 0; w < kThreads / kWave; ++w)
+            u += red[w];
+        far[0] = u;
+    }
+}
+
+// Per row: entries per column block (counts[b * n + i]) once the copy is
+// to be made (rows ascending); flags[0] when a row segment alone reaches
+// the block limit (repeated columns).
+__global__ __launch_bounds__(kThreads) void block_count_kernel(
+    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, int64_t n,
+    int nb, int32_t *__restrict__ counts, int *__restrict__ flags)
+{
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= n)
+        return;
+    const int64_t e = row_ptr[i + 1];
+    int64_t p = row_ptr[i];
+    bool huge = false;
+    for (int b = 0; b < nb; ++b) {
+        const int64_t lim = (int64_t)(b + 1) << kColShift;
+        int64_t c = 0;
+        while (p < e && (int64_t)col[p] < lim) {
+            ++c;
+            ++p;
+        }
+        huge = huge || c >= kMaxBlockEntries;
+        counts[(int64_t)b * n + i] = (int32_t)(c < kMaxBlockEntries ? c : 0);
+    }
+    if (p < e || huge)                 // leftover entries (out of order), or too many
+        flags[0] = 1;
 }
 
 // Exclusive scan of counts (block-major) into int64 offsets: tile sums,
@@ -429,9 +475,16 @@ hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
 
     unsigned long long *far = reinterpret_cast<unsigned long long *>(w + 64);
     const unsigned rows_grid = (unsigned)((n + kThreads - 1) / kThreads);
+    const int64_t scan_rows = kThreads / kLanes;
+    const unsigned scan_grid =
+        (unsigned)std::min<int64_t>((n + scan_rows - 1) / scan_rows, kScanBlocks);
+    // the workgroup counts go in the counts buffer, unused until the copy is made
+    unsigned long long *far_part = reinterpret_cast<unsigned long long *>(counts);
     hipLaunchKernelGGL(clear_flags_kernel, dim3(1), dim3(1), 0, s, flags, far);
-    hipLaunchKernelGGL(block_count_kernel, dim3(rows_grid), dim3(kThreads), 0, s, row_ptr,
-                       col, n, (int)nb, counts, flags, far);
+    hipLaunchKernelGGL(far_scan_kernel, dim3(scan_grid), dim3(kThreads), 0, s, row_ptr, col,
+                       n, flags, far_part);
+    hipLaunchKernelGGL(far_total_kernel, dim3(1), dim3(kThreads), 0, s,
+                       (const unsigned long long *)far_part, (int)scan_grid, far);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
@@ -450,6 +503,10 @@ hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
     *usable_host = 0;
     if (h.flag || 4 * h.far < (unsigned long long)nnz)
         return hipSuccess;
+    hipLaunchKernelGGL(block_count_kernel, dim3(rows_grid), dim3(kThreads), 0, s, row_ptr,
+                       col, n, (int)nb, counts, flags);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
     hipLaunchKernelGGL(scan_tile_sums_kernel, dim3((unsigned)ntiles), dim3(kThreads), 0, s,
                        counts, m, tsum);
     hipLaunchKernelGGL(scan_tile_offsets_kernel, dim3(1), dim3(1024), 0, s, tsum, ntiles);
