@@ -797,6 +797,63 @@ __global__ __launch_bounds__(kThreads) void fary_merge_kernel(
     }
 }
 
+// The last layer: the backtrack reads its split point at row n - 1 only,
+// so that row's leftmost argmin over every candidate j in [1, n - 1] is
+// found by one scan instead of the layer's recursion (the same candidates,
+// cost expression and tie rule as a row's own scan).  Workgroup b scans a
+// contiguous chunk (each lane in ascending j, strict improvement), leaving
+// its leftmost minimum in pbest[b], parg[b].
+constexpr int kLastBlocks = 256;
+__global__ __launch_bounds__(kThreads) void last_row_kernel(
+    const double2 *__restrict__ SS, const double *__restrict__ Ep, int64_t n,
+    double *__restrict__ pbest, int32_t *__restrict__ parg)
+{
+    __shared__ double wb[kThreads / kWave];
+    __shared__ int64_t wa[kThreads / kWave];
+    const int64_t r = n - 1;
+    const double2 e = SS[r + 1];
+    const int64_t per = (n - 1 + gridDim.x - 1) / gridDim.x;
+    const int64_t j0 = 1 + (int64_t)blockIdx.x * per;
+    const int64_t j1 = (j0 + per - 1 < r) ? j0 + per - 1 : r;
+    double best = INFINITY;
+    int64_t arg = INT64_MAX;
+    for (int64_t j = j0 + threadIdx.x; j <= j1; j += kThreads) {
+        const double c = Ep[j] + seg_cost(SS[j], e, j, r);
+        if (c < best) {
+            best = c;
+            arg = j;
+        }
+    }
+    wave_argmin(best, arg);
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    if (lane == 0) {
+        wb[w] = best;
+        wa[w] = arg;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int u = 1; u < kThreads / kWave; ++u)
+            amin_merge(best, arg, wb[u], wa[u]);
+        pbest[blockIdx.x] = best;
+        parg[blockIdx.x] = (arg == INT64_MAX) ? INT32_MAX : (int32_t)arg;
+    }
+}
+
+// The chunks' minima merged (order-independent leftmost minimum) into the
+// last layer's split point at row n - 1.
+__global__ __launch_bounds__(kWave) void last_row_merge_kernel(
+    const double *__restrict__ pbest, const int32_t *__restrict__ parg, int nb, int64_t n,
+    int32_t *__restrict__ opt)
+{
+    double best = INFINITY;
+    int64_t arg = INT64_MAX;
+    for (int b = threadIdx.x; b < nb; b += kWave)
+        amin_merge(best, arg, pbest[b], parg[b] == INT32_MAX ? INT64_MAX : (int64_t)parg[b]);
+    wave_argmin(best, arg);
+    if (threadIdx.x == 0)
+        opt[n - 1] = (int32_t)((arg == INT64_MAX) ? 1 : arg);
+}
+
 __global__ void backtrack_kernel(const int32_t *__restrict__ opt, int64_t n,
                                  int ke, int64_t *__restrict__ first)
 {
@@ -1061,6 +1118,17 @@ hipError_t run_kmeans1d(const double *v, int64_t n, int32_t k, int32_t *labels,
         int g = 0;                                 // levels run so far
         for (int c = 1; c < ke; ++c) {
             int32_t *oc = opt + (int64_t)c * n;
+            if (c == ke - 1) {
+                // only row n - 1 of the last layer is read
+                const int64_t want = (n - 1 + kThreads - 1) / kThreads;
+                const int nbl = (int)(want < kLastBlocks ? want : kLastBlocks);
+                hipLaunchKernelGGL(last_row_kernel, dim3(nbl), dim3(kThreads), 0, s, SS, Ep,
+                                   n, Q.pbest, Q.parg);
+                hipLaunchKernelGGL(last_row_merge_kernel, dim3(1), dim3(kWave), 0, s,
+                                   (const double *)Q.pbest, (const int32_t *)Q.parg, nbl, n,
+                                   oc);
+                break;
+            }
             for (int Lv = 0; Lv < levels; ++Lv, ++g) {
                 const dim3 grid(blocks_for(count[Lv] > 0 ? count[Lv] : 1));
                 const int whole = count[Lv] <= 512;    // few intervals, many parts each
