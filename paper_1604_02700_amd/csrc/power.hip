@@ -156,13 +156,13 @@ __global__ __launch_bounds__(kThreads) void spmv_staged_kernel(
         if (r0 + kStage < e1)
             load(r0 + kStage);                       // in flight during the sums
         const int64_t r1 = (r0 + kStage < e1) ? r0 + kStage : e1;
-        // the row's slice of this round, clamped in 64 bits: a row outside
-        // the round gives a = z (rows may lie far from the round in a tile
-        // of more than 2^31 entries)
+        // the row's slice of this round, clamped in 64 bits before it is
+        // narrowed: a row outside the round gets the empty slice (rows may
+        // lie far from the round in a tile of more than 2^31 entries)
         const int64_t lo = (rs > r0) ? rs : r0;
         const int64_t hi = (re < r1) ? re : r1;
-        const int a = (int)(lo - r0);
-        const int z = (hi > lo) ? (int)(hi - r0) : a;
+        const int a = (hi > lo) ? (int)(lo - r0) : 0;
+        const int z = (hi > lo) ? (int)(hi - r0) : 0;
         int p = a;
         for (; p + 4 <= z; p += 4) {
             double q[4];

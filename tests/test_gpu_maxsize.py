@@ -6,6 +6,8 @@
   invariants over a few updates.
 * Symmetric storage of the same points (entries past 2^31 in the packed
   tiles): sampled rows of one product against the oracle.
+* One tile of the staged CSR product with more than 2^31 entries (an
+  exact row sum).
 * The fused operator at the largest n that evaluates each pair once
   (2^19, d = 64): W 1 = 1 over the whole vector, sampled rows against the
   oracle.
@@ -111,6 +113,32 @@ def test_sym_past_2_31_entries(g, orc, big_blobs):
     yr = orc.matvec_onthefly_rows(w.X, w.sigma, dfull, vr, rows)
     np.testing.assert_allclose(y[rows], yr, rtol=1e-5)
     del As
+    torch.cuda.empty_cache()
+
+
+def test_csr_staged_tile_past_2_31_entries(g):
+    """One 256-row tile of the staged product holding more than 2^31
+    entries: row 256 holds 2^31 + 100 entries of weight 1 (columns cycling
+    over all nodes), the other rows of its tile and of the graph none, and
+    v = 1, so y at that row is exactly its entry count and 0 elsewhere.
+    The rows after it in the tile lie more than 2^31 entries past the
+    early rounds, the case whose round bounds must be clamped in 64 bits
+    before they are narrowed.  (A mean of 64 entries per row at most keeps
+    the staged product: n = 2^25 + 2^20.)"""
+    n = (1 << 25) + (1 << 20)
+    big = (1 << 31) + 100
+    assert big <= 64 * n
+    print(f"gpu: staged tile with {big} entries in one row, n={n}", flush=True)
+    rp = torch.zeros(n + 1, dtype=torch.int64, device=DEV)
+    rp[257:] = big
+    col = (torch.arange(big, dtype=torch.int64, device=DEV) % n).to(torch.int32)
+    val = torch.ones(big, dtype=torch.float32, device=DEV)
+    v = torch.ones(n, dtype=torch.float64, device=DEV)
+    y = g.gpic_matvec_csr(rp, col, val, v)
+    assert float(y[256].item()) == float(big)
+    y[256] = 0.0
+    assert float(y.abs().max().item()) == 0.0
+    del rp, col, val, v, y
     torch.cuda.empty_cache()
 
 
