@@ -381,6 +381,7 @@ def test_pic_cosine_parity(g, orc, name):
 
 # ------------------------------------------------------------------ k-means
 @pytest.mark.parametrize("n,k,dup", [(1, 1, False), (2, 2, False), (5, 3, False),
+                                     (9, 9, False), (40, 39, False),
                                      (64, 8, False), (65, 8, False), (66, 8, True),
                                      (1000, 4, False), (4097, 10, False),
                                      (4097, 10, True), (4225, 20, True),
@@ -392,9 +393,10 @@ def test_pic_cosine_parity(g, orc, name):
 def test_kmeans1d_parity(g, orc, n, k, dup):
     """Sizes straddle the recursion's level counts (F = 64 below 2^18 rows:
     n = 64 / 65, 4225 / 4291; F = 8 from 2^18 = 262,144: 9^6 = 531,441 adds
-    a level), the switch between the two (262,143 / 262,144), and fewer
+    a level), the switch between the two (262,143 / 262,144), fewer
     distinct values than k (300,001 values rounded to about 100 integers,
-    k = 200)."""
+    k = 200), and k = n or n - 1 (the last layer's one row has a single
+    split point, or two, with a finite cost)."""
     rng = np.random.default_rng(n + k)
     m = max(1, min(k, n))
     centres = np.sort(rng.uniform(0, 100, size=m))
