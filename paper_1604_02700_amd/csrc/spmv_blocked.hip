@@ -186,14 +186,21 @@ __global__ __launch_bounds__(kThreads) void scan_apply_kernel(
     const int32_t *__restrict__ counts, int64_t m, const int64_t *__restrict__ toff,
     int64_t *__restrict__ offs)
 {
-    // thread t owns 16 consecutive elements of the tile
-    __shared__ int64_t part[kThreads];
+    // the tile goes through LDS both ways, so that the loads of counts and
+    // the stores of offsets are coalesced; thread t scans its kItems
+    // consecutive counts (rows padded by one slot against bank conflicts)
     constexpr int per = kScanTile / kThreads;
-    const int64_t x0 = (int64_t)blockIdx.x * kScanTile + threadIdx.x * per;
+    constexpr int pitch = per + 1;
+    __shared__ int32_t cin[kThreads * pitch];
+    __shared__ int64_t out[kThreads * pitch];
+    __shared__ int64_t part[kThreads];
+    const int64_t b0 = (int64_t)blockIdx.x * kScanTile;
+    for (int e = threadIdx.x; e < kScanTile; e += kThreads)
+        cin[(e / per) * pitch + e % per] = (b0 + e < m) ? counts[b0 + e] : 0;
+    __syncthreads();
     int64_t s = 0;
     for (int k = 0; k < per; ++k)
-        if (x0 + k < m)
-            s += counts[x0 + k];
+        s += cin[threadIdx.x * pitch + k];
     part[threadIdx.x] = s;
     __syncthreads();
     for (int o = 1; o < kThreads; o <<= 1) {
@@ -203,11 +210,14 @@ __global__ __launch_bounds__(kThreads) void scan_apply_kernel(
         __syncthreads();
     }
     int64_t run = toff[blockIdx.x] + part[threadIdx.x] - s;
-    for (int k = 0; k < per; ++k)
-        if (x0 + k < m) {
-            offs[x0 + k] = run;
-            run += counts[x0 + k];
-        }
+    for (int k = 0; k < per; ++k) {
+        out[threadIdx.x * pitch + k] = run;
+        run += cin[threadIdx.x * pitch + k];
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kScanTile; e += kThreads)
+        if (b0 + e < m)
+            offs[b0 + e] = out[(e / per) * pitch + e % per];
 }
 
 // Scatter every row's entries into its blocks: 16 lanes per row; entry p
