@@ -103,30 +103,59 @@ __global__ __launch_bounds__(kThreads) void far_total_kernel(
     }
 }
 
+// First entry of column block b in row [s0, e) (rows ascending): the
+// first q with col[q] >= b 2^18, e for b = nb.
+__device__ __forceinline__ int64_t block_start(const int32_t *__restrict__ col, int64_t s0,
+                                               int64_t e, int b, int nb)
+{
+    if (b >= nb)
+        return e;
+    const int32_t lim = (int32_t)((int64_t)b << kColShift);
+    int64_t lo = s0, hi = e;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (col[mid] < lim)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// kLanes lanes per row: the row's block starts (a binary search each,
+// b = lane, lane + kLanes, ...) into LDS, bnd[g][b] for b = 0 .. nb.
+constexpr int kRowsPerBlock = kThreads / kLanes;
+__device__ __forceinline__ void row_block_starts(const int32_t *__restrict__ col, int64_t s0,
+                                                 int64_t e, bool live, int nb, int sl,
+                                                 int64_t *bnd)
+{
+    for (int b = sl; b <= nb; b += kLanes)
+        bnd[b] = live ? block_start(col, s0, e, b, nb) : 0;
+}
+
 // Per row: entries per column block (counts[b * n + i]) once the copy is
-// to be made (rows ascending); flags[0] when a row segment alone reaches
-// the block limit (repeated columns).
+// to be made (rows ascending), from the row's block starts; flags[0] when a
+// row segment alone reaches the block limit (repeated columns).
 __global__ __launch_bounds__(kThreads) void block_count_kernel(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, int64_t n,
     int nb, int32_t *__restrict__ counts, int *__restrict__ flags)
 {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i >= n)
+    __shared__ int64_t bnd[kRowsPerBlock][kMaxBlocks + 1];
+    const int g = threadIdx.x / kLanes, sl = threadIdx.x % kLanes;
+    const int64_t i = (int64_t)blockIdx.x * kRowsPerBlock + g;
+    const bool live = i < n;
+    const int64_t s0 = live ? row_ptr[i] : 0, e = live ? row_ptr[i + 1] : 0;
+    row_block_starts(col, s0, e, live, nb, sl, bnd[g]);
+    __syncthreads();
+    if (!live)
         return;
-    const int64_t e = row_ptr[i + 1];
-    int64_t p = row_ptr[i];
     bool huge = false;
-    for (int b = 0; b < nb; ++b) {
-        const int64_t lim = (int64_t)(b + 1) << kColShift;
-        int64_t c = 0;
-        while (p < e && (int64_t)col[p] < lim) {
-            ++c;
-            ++p;
-        }
-        huge = huge || c >= kMaxBlockEntries;
+    for (int b = sl; b < nb; b += kLanes) {
+        const int64_t c = bnd[g][b + 1] - bnd[g][b];
+        huge = huge || c >= kMaxBlockEntries;     // repeated columns
         counts[(int64_t)b * n + i] = (int32_t)(c < kMaxBlockEntries ? c : 0);
     }
-    if (p < e || huge)                 // leftover entries (out of order), or too many
+    if (huge)
         flags[0] = 1;
 }
 
@@ -220,32 +249,26 @@ __global__ __launch_bounds__(kThreads) void scan_apply_kernel(
             offs[b0 + e] = out[(e / per) * pitch + e % per];
 }
 
-// Scatter every row's entries into its blocks: 16 lanes per row; entry p
-// of block b goes to offs[b][i] + (p - first entry of block b in the row),
-// the first entry found by binary search in the sorted row.
+// Scatter every row's entries into its blocks: kLanes lanes per row; entry
+// p of block b goes to offs[b][i] + (p - the row's first entry of block b).
 __global__ __launch_bounds__(kThreads) void block_scatter_kernel(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
-    const float *__restrict__ val, int64_t n, const int64_t *__restrict__ offs,
+    const float *__restrict__ val, int64_t n, int nb, const int64_t *__restrict__ offs,
     int32_t *__restrict__ colb, float *__restrict__ valb)
 {
-    const int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / kLanes;
-    const int sl = threadIdx.x % kLanes;
-    if (i >= n)
+    __shared__ int64_t bnd[kRowsPerBlock][kMaxBlocks + 1];
+    const int g = threadIdx.x / kLanes, sl = threadIdx.x % kLanes;
+    const int64_t i = (int64_t)blockIdx.x * kRowsPerBlock + g;
+    const bool live = i < n;
+    const int64_t s0 = live ? row_ptr[i] : 0, e = live ? row_ptr[i + 1] : 0;
+    row_block_starts(col, s0, e, live, nb, sl, bnd[g]);
+    __syncthreads();
+    if (!live)
         return;
-    const int64_t s0 = row_ptr[i], e = row_ptr[i + 1];
     for (int64_t p = s0 + sl; p < e; p += kLanes) {
         const int32_t c = col[p];
         const int b = c >> kColShift;
-        const int32_t lim = (int32_t)((int64_t)b << kColShift);
-        int64_t lo = s0, hi = p;          // first q in [s0, p] with col[q] >= lim
-        while (lo < hi) {
-            const int64_t mid = lo + (hi - lo) / 2;
-            if (col[mid] < lim)
-                lo = mid + 1;
-            else
-                hi = mid;
-        }
-        const int64_t dst = offs[(int64_t)b * n + i] + (p - lo);
+        const int64_t dst = offs[(int64_t)b * n + i] + (p - bnd[g][b]);
         colb[dst] = c;
         valb[dst] = val[p];
     }
@@ -484,7 +507,6 @@ hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
     int64_t *offs = reinterpret_cast<int64_t *>(B.ypart);      // reused below
 
     unsigned long long *far = reinterpret_cast<unsigned long long *>(w + 64);
-    const unsigned rows_grid = (unsigned)((n + kThreads - 1) / kThreads);
     const int64_t scan_rows = kThreads / kLanes;
     const unsigned scan_grid =
         (unsigned)std::min<int64_t>((n + scan_rows - 1) / scan_rows, kScanBlocks);
@@ -513,7 +535,8 @@ hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
     *usable_host = 0;
     if (h.flag || 4 * h.far < (unsigned long long)nnz)
         return hipSuccess;
-    hipLaunchKernelGGL(block_count_kernel, dim3(rows_grid), dim3(kThreads), 0, s, row_ptr,
+    const unsigned group_grid = (unsigned)((n + kRowsPerBlock - 1) / kRowsPerBlock);
+    hipLaunchKernelGGL(block_count_kernel, dim3(group_grid), dim3(kThreads), 0, s, row_ptr,
                        col, n, (int)nb, counts, flags);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
@@ -536,9 +559,8 @@ hipError_t build_csr_blocked(const int64_t *row_ptr, const int32_t *col,
         return hipSuccess;
     *usable_host = 1;
     // rows are sorted: every entry lands in its block's range
-    hipLaunchKernelGGL(block_scatter_kernel,
-                       dim3((unsigned)((n * kLanes + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, s, row_ptr, col, val, n, offs, B.colb, B.valb);
+    hipLaunchKernelGGL(block_scatter_kernel, dim3(group_grid), dim3(kThreads), 0, s, row_ptr,
+                       col, val, n, (int)nb, offs, B.colb, B.valb);
     *out = B;
     return hipGetLastError();
 }
